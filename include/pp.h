@@ -1,0 +1,205 @@
+/*
+ * pp.h -- C ABI of the pattern/connectivity-pruned 3x3 convolution library
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The method is the one of Niu et al., "Towards Real-Time DNN Inference on
+ * Mobile Platforms with Model Pruning and Compiler Optimization":
+ *   - pattern pruning keeps a fixed subset of the 9 taps of every 3x3 kernel,
+ *     chosen from a small pattern library; connectivity pruning removes whole
+ *     (out-channel, in-channel) kernels (Sec. 2, structured pruning);
+ *   - the pruned weights are stored in a compact format with no zero weights
+ *     and no per-weight indices (Sec. 3, "sparse model storage"), with the
+ *     filters reordered so that filters of the same or similar patterns sit
+ *     together and the weights compacted along the kernel direction (Sec. 3,
+ *     "matrix reorder");
+ *   - a convolution is fused with its bias and activation (Sec. 3, "DSL
+ *     related optimization": conv + BN + activation fused into one layer).
+ *
+ * Conventions for every call:
+ *   - All calls return pp_status; 0 is success, negative values are errors.
+ *     No call aborts, throws or prints.  pp_last_error() gives a detail
+ *     string for the calling thread's most recent error.
+ *   - The caller owns every buffer.  The library allocates no device memory
+ *     and keeps no global state beyond its loaded GPU code.
+ *   - Device work is enqueued asynchronously on the caller's HIP stream
+ *     (hipStream_t passed as void*, NULL = default stream).  Nothing
+ *     synchronises; a device fault surfaces at the caller's next sync.
+ *   - Every argument is validated on the host before any device work is
+ *     enqueued.  A call that returns an error has enqueued nothing.
+ *   - Activations are NCHW, contiguous, fp32 or bf16 (pp_dtype).
+ */
+#ifndef PP_H_
+#define PP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PP_OK = 0,
+  PP_EINVAL = -1,        /* bad argument: NULL pointer, out-of-range value     */
+  PP_ESIZE = -2,         /* a buffer is smaller than required                  */
+  PP_EBLOB = -3,         /* packed blob is malformed or inconsistent           */
+  PP_EUNSUPPORTED = -4,  /* valid request the GPU kernels do not implement     */
+  PP_EHIP = -5           /* the HIP runtime reported an error at launch        */
+} pp_status;
+
+typedef enum { PP_F32 = 0, PP_BF16 = 1 } pp_dtype;
+
+/* flags of pp_conv2d_fwd / pp_net_op */
+enum { PP_RELU = 1u };
+
+/* Shape and storage of one pruned 3x3 layer. */
+typedef struct {
+  int32_t c_out;     /* output channels (filters), 1..65535                 */
+  int32_t c_in;      /* input channels, 1..65535                            */
+  int32_t stride;    /* 1..16 (the GPU kernels run 1 and 2)                 */
+  int32_t pad;       /* zero padding on every side, 0..16                   */
+  int32_t dilation;  /* 1..16 (the GPU kernels run 1 and 2)                 */
+  int32_t wdtype;    /* pp_dtype of the stored weights                      */
+} pp_layer_desc;
+
+/*
+ * pp_pack -- pattern projection + compact storage + filter reorder (Sec. 2
+ * structured pruning; Sec. 3 "sparse model storage" and "matrix reorder").
+ * Host-only, pure and deterministic: equal inputs give equal bytes.
+ *
+ *   d           layer description (c_out, c_in, stride, pad, dilation, wdtype)
+ *   w           host fp32 [c_out][c_in][3][3] dense weights.  Taps outside a
+ *               kernel's pattern and kernels with conn = 0 are dropped, even
+ *               when nonzero; zero weights inside a kept pattern are stored.
+ *   bias        host fp32 [c_out], or NULL for zeros
+ *   pattern_id  host u8 [c_out][c_in]: index into lib_masks; read only where
+ *               conn = 1
+ *   conn        host u8 [c_out][c_in]: 1 = kernel kept, 0 = pruned (other
+ *               values are an error)
+ *   lib_masks   host u16 [n_patterns]: 9-bit tap masks, bit t = tap
+ *               (ky, kx) with t = 3*ky + kx; each must be in 1..511
+ *   n_patterns  1..255
+ *   out         host buffer for the blob, or NULL to query the size
+ *   inout_bytes in: capacity of out; out: bytes required / written
+ *
+ * Errors: PP_EINVAL (NULL pointer other than bias/out, ranges, conn not 0/1,
+ * pattern id >= n_patterns where conn = 1, bad mask), PP_ESIZE (capacity too
+ * small; *inout_bytes then holds the required size).
+ *
+ * Blob layout "PPK1" (little-endian, each section 64-byte aligned, padding
+ * zero):
+ *   header  u32[24]: magic 0x314B5050, version | wdtype<<16, c_out, c_in,
+ *           stride, pad, dilation, n_patterns, group (=8), n_groups,
+ *           n_kept, n_wt, off_masks, off_perm, off_codes, off_woff, off_w,
+ *           off_bias, total_bytes, 0 x 5
+ *   masks   u16[n_patterns]
+ *   perm    u32[n_groups*8]: packed slot -> original filter, 0xFFFFFFFF for
+ *           padding slots; n_groups = ceil(c_out/8)
+ *   codes   u8[n_groups][c_in][8]: pattern id of kernel (perm[8g+s], c) or
+ *           0xFF when pruned
+ *   woff    u32[n_groups*c_in + 1]: index in w of the first weight of entry
+ *           (g, c)
+ *   w       fp32 or bf16 [n_wt]: for g, c, slot ascending, kept kernels only,
+ *           the pattern's taps in ascending tap order (bf16: each kernel
+ *           padded to an even element count with a zero)
+ *   bias    fp32[n_groups*8] in packed slot order
+ * Filter order: kept-kernel count descending, then pattern histogram
+ * (count of pattern 0, 1, ... each descending), then filter index.
+ */
+pp_status pp_pack(const pp_layer_desc* d, const float* w, const float* bias,
+                  const uint8_t* pattern_id, const uint8_t* conn,
+                  const uint16_t* lib_masks, int32_t n_patterns,
+                  void* out, size_t* inout_bytes);
+
+/*
+ * pp_blob_info -- validate a host copy of a blob and return its description.
+ * Any output pointer may be NULL.  Errors: PP_EINVAL (blob NULL), PP_EBLOB
+ * (bad magic/version, sizes or offsets inconsistent with `bytes`, woff not
+ * monotone, a code >= n_patterns, a perm entry out of range).
+ */
+pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
+                       int32_t* n_kept, int64_t* n_wt);
+
+/*
+ * pp_conv2d_fwd -- y = act(conv3x3_pruned(x) + bias) for one packed layer.
+ *   h_blob, blob_bytes  host copy of the blob (its header is read here, so no
+ *                       device-to-host copy is needed)
+ *   d_blob              the same bytes in device memory, 256-byte aligned
+ *   x                   device [n][c_in][h][w] in act_dtype
+ *   y                   device [n][c_out][h_out][w_out] in act_dtype,
+ *                       h_out = (h + 2 pad - 2 dilation - 1)/stride + 1;
+ *                       must not overlap x
+ *   flags               PP_RELU
+ * Output channels are in the original filter order.  Accumulation is fp32
+ * in a fixed order, so repeated calls give bitwise-identical results.
+ * Errors: PP_EINVAL, PP_EBLOB, PP_EUNSUPPORTED (stride or dilation outside
+ * {1,2}, pad > 2*dilation, weight dtype not the activation dtype, h_out or
+ * w_out < 1), PP_EHIP.
+ */
+pp_status pp_conv2d_fwd(const void* h_blob, size_t blob_bytes, const void* d_blob,
+                        const void* x, void* y, int32_t n, int32_t h, int32_t w,
+                        int32_t act_dtype, uint32_t flags, void* hip_stream);
+
+/* pp_conv2d_out_size -- h_out, w_out of a packed layer for an h x w input. */
+pp_status pp_conv2d_out_size(const void* h_blob, size_t blob_bytes, int32_t h, int32_t w,
+                             int32_t* h_out, int32_t* w_out);
+
+/* ------------------------------------------------------------------------
+ * Network execution: an ordered op list over activation slots, the flat
+ * layer-wise representation of a model (Sec. 3, "DSL related optimization":
+ * each layer one entry, conv fused with its activation).
+ * Slot 0 is the network input x, slot 1 the output y, slots 2..15 live in
+ * the caller's workspace.
+ * ---------------------------------------------------------------------- */
+typedef enum {
+  PP_OP_CONV_PP = 0,     /* pruned 3x3 conv: h_blob/blob_bytes/d_blob          */
+  PP_OP_CONV_DENSE = 1,  /* dense k x k conv, stride 1: k, pad, c_in, c_out,   */
+                         /* d_w [c_out][c_in][k][k], d_b fp32 [c_out]          */
+  PP_OP_DECONV = 2,      /* transposed conv: k, stride, pad, c_in, c_out,      */
+                         /* d_w [c_in][c_out][k][k], d_b fp32 [c_out]          */
+  PP_OP_MAXPOOL2 = 3,    /* 2x2 max pool, stride 2 (floor)                     */
+  PP_OP_UPSAMPLE2 = 4,   /* nearest-neighbour x2                               */
+  PP_OP_PIXSHUF2 = 5,    /* PixelShuffle(2): out[c,2h+i,2w+j] = in[4c+2i+j,h,w] */
+  PP_OP_ADD = 6          /* dst = src + src2 (same shape)                      */
+} pp_op_kind;
+
+#define PP_MAX_SLOTS 16
+
+typedef struct {
+  int32_t kind;              /* pp_op_kind                                      */
+  int32_t src, src2, dst;    /* slots; dst must differ from src and src2        */
+  uint32_t flags;            /* PP_RELU (conv / deconv ops)                     */
+  int32_t k, stride, pad, dilation, c_in, c_out;   /* dense conv / deconv       */
+  const void* h_blob;        /* PP_OP_CONV_PP: host blob                        */
+  size_t blob_bytes;
+  const void* d_blob;        /* PP_OP_CONV_PP: device blob                      */
+  const void* d_w;           /* dense ops: device weights in the act dtype      */
+  const float* d_b;          /* dense ops: device fp32 bias, or NULL            */
+} pp_net_op;
+
+/*
+ * pp_net_workspace -- bytes of workspace pp_net_fwd needs for this op list
+ * and input shape, and the output shape (any output pointer may be NULL).
+ * Errors: PP_EINVAL (bad op, slot or shape chain), PP_EBLOB.
+ */
+pp_status pp_net_workspace(const pp_net_op* ops, int32_t n_ops, int32_t n, int32_t c,
+                           int32_t h, int32_t w, int32_t act_dtype, size_t* bytes,
+                           int32_t* out_c, int32_t* out_h, int32_t* out_w);
+
+/*
+ * pp_net_fwd -- run the op list on the stream, one launch per op, no host
+ * synchronisation.  x is device [n][c][h][w]; y receives slot 1 (shape from
+ * pp_net_workspace).  Errors: as pp_net_workspace, PP_ESIZE (ws_bytes too
+ * small), PP_EUNSUPPORTED, PP_EHIP.
+ */
+pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void* x, void* y,
+                     int32_t n, int32_t c, int32_t h, int32_t w, int32_t act_dtype,
+                     void* workspace, size_t ws_bytes, void* hip_stream);
+
+const char* pp_status_str(pp_status s);
+const char* pp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PP_H_ */

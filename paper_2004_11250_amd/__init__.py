@@ -1,0 +1,285 @@
+"""Pattern/connectivity-pruned 3x3 convolution on AMD Instinct MI355X.
+
+Thin ctypes binding over ``libppconv.so`` (C ABI declared in
+``include/pp.h``).  Every step of the computation runs in the library's HIP
+kernels; this module only marshals arguments.  PyTorch provides device memory
+and the current HIP stream.
+
+The library is loaded on first use; if it has not been built the call raises
+``RuntimeError`` (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libppconv.so")
+
+PP_OK, PP_EINVAL, PP_ESIZE, PP_EBLOB, PP_EUNSUPPORTED, PP_EHIP = 0, -1, -2, -3, -4, -5
+PP_F32, PP_BF16 = 0, 1
+PP_RELU = 1
+(OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
+
+# exported symbols declared in include/pp.h
+SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_out_size", "pp_net_workspace",
+           "pp_net_fwd", "pp_status_str", "pp_last_error")
+
+
+class PPError(RuntimeError):
+    def __init__(self, status, where, detail):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("c_out", ctypes.c_int32), ("c_in", ctypes.c_int32), ("stride", ctypes.c_int32),
+                ("pad", ctypes.c_int32), ("dilation", ctypes.c_int32), ("wdtype", ctypes.c_int32)]
+
+
+class NetOp(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("src", ctypes.c_int32), ("src2", ctypes.c_int32),
+                ("dst", ctypes.c_int32), ("flags", ctypes.c_uint32), ("k", ctypes.c_int32),
+                ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("dilation", ctypes.c_int32),
+                ("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32), ("h_blob", ctypes.c_void_p),
+                ("blob_bytes", ctypes.c_size_t), ("d_blob", ctypes.c_void_p), ("d_w", ctypes.c_void_p),
+                ("d_b", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load (once) and return the ctypes handle of libppconv.so."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -m paper_2004_11250_amd.build` "
+                           "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    vp, sz, i32, u32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_uint32
+    lib.pp_pack.argtypes = [ctypes.POINTER(LayerDesc), vp, vp, vp, vp, vp, i32, vp, ctypes.POINTER(sz)]
+    lib.pp_blob_info.argtypes = [vp, sz, ctypes.POINTER(LayerDesc), ctypes.POINTER(i32),
+                                 ctypes.POINTER(ctypes.c_int64)]
+    lib.pp_conv2d_fwd.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp]
+    lib.pp_conv2d_out_size.argtypes = [vp, sz, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.pp_net_workspace.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
+                                     ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.pp_net_fwd.argtypes = [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp]
+    lib.pp_status_str.argtypes = [i32]
+    lib.pp_status_str.restype = ctypes.c_char_p
+    lib.pp_last_error.argtypes = []
+    lib.pp_last_error.restype = ctypes.c_char_p
+    for name in ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_out_size", "pp_net_workspace",
+                 "pp_net_fwd"):
+        getattr(lib, name).restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(status, where):
+    if status != PP_OK:
+        lib = load_library()
+        raise PPError(status, where, lib.pp_last_error().decode())
+
+
+def _ptr(a) -> int:
+    return a.ctypes.data if isinstance(a, np.ndarray) else int(a)
+
+
+# ---------------------------------------------------------------------------
+# packing (host only)
+# ---------------------------------------------------------------------------
+
+def pack(w, b, pattern_id, conn, lib_masks, stride=1, pad=1, dilation=1, wdtype=PP_F32) -> np.ndarray:
+    """pp_pack: dense fp32 weights + pattern ids + connectivity -> PPK1 blob (uint8 array)."""
+    lib = load_library()
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    c_out, c_in = w.shape[:2]
+    pid = np.ascontiguousarray(pattern_id, dtype=np.uint8)
+    conn = np.ascontiguousarray(conn, dtype=np.uint8)
+    masks = np.ascontiguousarray(lib_masks, dtype=np.uint16)
+    bias = None if b is None else np.ascontiguousarray(b, dtype=np.float32)
+    d = LayerDesc(c_out, c_in, stride, pad, dilation, wdtype)
+    n = ctypes.c_size_t(0)
+    args = (ctypes.byref(d), _ptr(w), None if bias is None else _ptr(bias), _ptr(pid), _ptr(conn), _ptr(masks),
+            len(masks))
+    _check(lib.pp_pack(*args, None, ctypes.byref(n)), "pp_pack(size)")
+    out = np.zeros(n.value, dtype=np.uint8)
+    _check(lib.pp_pack(*args, _ptr(out), ctypes.byref(n)), "pp_pack")
+    return out
+
+
+def blob_info(blob) -> dict:
+    lib = load_library()
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    d = LayerDesc()
+    nk = ctypes.c_int32(0)
+    nw = ctypes.c_int64(0)
+    _check(lib.pp_blob_info(_ptr(blob), blob.nbytes, ctypes.byref(d), ctypes.byref(nk), ctypes.byref(nw)),
+           "pp_blob_info")
+    return dict(c_out=d.c_out, c_in=d.c_in, stride=d.stride, pad=d.pad, dilation=d.dilation, wdtype=d.wdtype,
+                n_kept=nk.value, n_wt=nw.value)
+
+
+def out_size(blob, h, w):
+    lib = load_library()
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    ho, wo = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib.pp_conv2d_out_size(_ptr(blob), blob.nbytes, h, w, ctypes.byref(ho), ctypes.byref(wo)),
+           "pp_conv2d_out_size")
+    return ho.value, wo.value
+
+
+# ---------------------------------------------------------------------------
+# device execution (torch tensors for memory and streams)
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return PP_F32
+    if t.dtype == torch.bfloat16:
+        return PP_BF16
+    raise TypeError(f"activations must be float32 or bfloat16, got {t.dtype}")
+
+
+def _stream_ptr(stream=None) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+class PackedLayer:
+    """A packed layer: host copy (for header parsing) + device copy."""
+
+    def __init__(self, blob: np.ndarray, device="cuda"):
+        torch = _torch()
+        self.h_blob = np.ascontiguousarray(blob, dtype=np.uint8)
+        self.info = blob_info(self.h_blob)
+        self.d_blob = torch.from_numpy(self.h_blob.copy()).to(device)
+        if self.d_blob.data_ptr() % 256:
+            raise RuntimeError("device blob allocation is not 256-byte aligned")
+
+    @classmethod
+    def from_weights(cls, w, b, pattern_id, conn, lib_masks, stride=1, pad=1, dilation=1, wdtype=PP_F32,
+                     device="cuda"):
+        return cls(pack(w, b, pattern_id, conn, lib_masks, stride, pad, dilation, wdtype), device)
+
+
+def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None):
+    """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None)."""
+    torch = _torch()
+    lib = load_library()
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous NCHW")
+    n, c, h, w = x.shape
+    if c != layer.info["c_in"]:
+        raise ValueError(f"x has {c} channels, the layer expects {layer.info['c_in']}")
+    ho, wo = out_size(layer.h_blob, h, w)
+    shape = (n, layer.info["c_out"], ho, wo)
+    if out is None:
+        out = torch.empty(shape, dtype=x.dtype, device=x.device)
+    elif tuple(out.shape) != shape or out.dtype != x.dtype or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous {x.dtype} tensor of shape {shape}")
+    st = lib.pp_conv2d_fwd(_ptr(layer.h_blob), layer.h_blob.nbytes, layer.d_blob.data_ptr(), x.data_ptr(),
+                           out.data_ptr(), n, h, w, _dtype_code(x), PP_RELU if relu else 0, _stream_ptr(stream))
+    _check(st, "pp_conv2d_fwd")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# networks: a flat op list over activation slots (pp_net_fwd)
+# ---------------------------------------------------------------------------
+
+def _bf16_bits(a: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round to nearest even (offline weight prep)."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return (((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF).astype(np.uint16)
+
+
+class Net:
+    """A network ready for pp_net_fwd: packed pruned layers and dense weights
+    resident on the device, plus the op array.
+
+    ``spec`` is a dict with ``ops`` (list of op dicts: op in conv3 / conv /
+    deconv / maxpool2 / up2 / pshuf2 / add, src/src2/dst slots, shapes and
+    flags) and ``params`` the matching list of weight dicts (conv3: w, b, pid,
+    conn, lib; conv/deconv: w, b)."""
+
+    _KIND = {"conv3": OP_CONV_PP, "conv": OP_CONV_DENSE, "deconv": OP_DECONV, "maxpool2": OP_MAXPOOL2,
+             "up2": OP_UPSAMPLE2, "pshuf2": OP_PIXSHUF2, "add": OP_ADD}
+
+    def __init__(self, ops, params, dtype="f32", device="cuda"):
+        torch = _torch()
+        self.dtype = dtype
+        self.wd = PP_BF16 if dtype == "bf16" else PP_F32
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.layers = []     # keeps device buffers alive
+        arr = (NetOp * len(ops))()
+        for i, (op, prm) in enumerate(zip(ops, params)):
+            kind = self._KIND[op["op"]]
+            e = arr[i]
+            e.kind = kind
+            e.src, e.dst = op["src"], op["dst"]
+            e.src2 = op.get("src2", 0)
+            e.flags = PP_RELU if op.get("relu") else 0
+            if kind == OP_CONV_PP:
+                L = PackedLayer.from_weights(prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"],
+                                             op["stride"], op["pad"], op["dil"], self.wd, device)
+                self.layers.append(L)
+                e.h_blob = L.h_blob.ctypes.data
+                e.blob_bytes = L.h_blob.nbytes
+                e.d_blob = L.d_blob.data_ptr()
+            elif kind in (OP_CONV_DENSE, OP_DECONV):
+                w = np.ascontiguousarray(prm["w"], dtype=np.float32)
+                if self.wd == PP_BF16:
+                    dw = torch.from_numpy(_bf16_bits(w).view(np.int16)).to(device)
+                else:
+                    dw = torch.from_numpy(w).to(device)
+                db = torch.from_numpy(np.ascontiguousarray(prm["b"], dtype=np.float32)).to(device)
+                self.layers.append((dw, db))
+                e.k, e.stride, e.pad, e.dilation = op["k"], op["stride"], op["pad"], op.get("dil", 1)
+                e.c_in, e.c_out = op["c_in"], op["c_out"]
+                e.d_w = dw.data_ptr()
+                e.d_b = db.data_ptr()
+        self.ops = arr
+        self.n_ops = len(ops)
+        self._ws = None
+
+    def plan(self, n, c, h, w):
+        lib = load_library()
+        nb = ctypes.c_size_t(0)
+        oc, oh, ow = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
+        _check(lib.pp_net_workspace(self.ops, self.n_ops, n, c, h, w, self.wd, ctypes.byref(nb), ctypes.byref(oc),
+                                    ctypes.byref(oh), ctypes.byref(ow)), "pp_net_workspace")
+        return nb.value, (n, oc.value, oh.value, ow.value)
+
+    def forward(self, x, out=None, workspace=None, stream=None):
+        torch = _torch()
+        lib = load_library()
+        if x.dtype != self.tdtype or not x.is_contiguous():
+            raise ValueError("x must be contiguous and of the net's dtype")
+        n, c, h, w = x.shape
+        nbytes, oshape = self.plan(n, c, h, w)
+        if workspace is None:
+            if self._ws is None or self._ws.numel() < nbytes:
+                self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=x.device)
+            workspace = self._ws
+        if workspace.numel() < nbytes:
+            raise ValueError(f"workspace needs {nbytes} bytes")
+        if out is None:
+            out = torch.empty(oshape, dtype=x.dtype, device=x.device)
+        elif tuple(out.shape) != tuple(oshape) or out.dtype != x.dtype or not out.is_contiguous():
+            raise ValueError(f"out must be a contiguous {x.dtype} tensor of shape {oshape}")
+        _check(lib.pp_net_fwd(self.ops, self.n_ops, x.data_ptr(), out.data_ptr(), n, c, h, w, self.wd,
+                              workspace.data_ptr(), workspace.numel(), _stream_ptr(stream)), "pp_net_fwd")
+        return out

@@ -1,0 +1,128 @@
+// api_conv.cpp -- pp_conv2d_fwd / pp_conv2d_out_size: host validation and
+// dispatch of the pruned 3x3 convolution (pattern + connectivity pruning,
+// Sec. 2; conv fused with bias and activation, Sec. 3).
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <string>
+
+#include "api_internal.hpp"
+#include "conv_pp.hpp"
+#include "ppk1.hpp"
+
+namespace pp {
+
+static const uint16_t kCanon8Masks[8] = {0x03A, 0x0B2, 0x0B8, 0x09A, 0x01B, 0x036, 0x0D8, 0x1B0};
+
+int library_kind(const BlobView& v) {
+  if (v.n_patterns == 8) {
+    bool same = true;
+    for (int p = 0; p < 8; ++p) {
+      uint16_t m;
+      std::memcpy(&m, v.masks + p, 2);
+      same = same && m == kCanon8Masks[p];
+    }
+    if (same) return kLibCanon8;
+  }
+  if (v.n_patterns == 1) {
+    uint16_t m;
+    std::memcpy(&m, v.masks, 2);
+    if (m == 0x1FF) return kLibDense9;
+  }
+  return kLibGeneric;
+}
+
+static int out_dim(int in, int pad, int dil, int stride) { return (in + 2 * pad - 2 * dil - 1) / stride + 1; }
+
+pp_status conv_check(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, int* ho, int* wo) {
+  if (n < 1 || h < 1 || w < 1) return fail(PP_EINVAL, "n, h, w must be >= 1");
+  if (act_dtype != PP_F32 && act_dtype != PP_BF16) return fail(PP_EINVAL, "bad activation dtype");
+  if (v.stride != 1 && v.stride != 2) return fail(PP_EUNSUPPORTED, "stride must be 1 or 2");
+  if (v.dil != 1 && v.dil != 2) return fail(PP_EUNSUPPORTED, "dilation must be 1 or 2");
+  if (v.pad > 2 * v.dil) return fail(PP_EUNSUPPORTED, "pad larger than the kernel extent");
+  if (v.wdtype != act_dtype) return fail(PP_EUNSUPPORTED, "weight dtype must equal activation dtype");
+  const long hn = h + 2L * v.pad - 2L * v.dil - 1, wn = w + 2L * v.pad - 2L * v.dil - 1;
+  if (hn < 0 || wn < 0) return fail(PP_EUNSUPPORTED, "input smaller than the dilated kernel");
+  if (static_cast<long long>(n) * v.c_in * h * w > (1LL << 40) ||
+      static_cast<long long>(n) * v.c_out * h * w > (1LL << 40))
+    return fail(PP_EINVAL, "tensor too large");
+  *ho = out_dim(h, v.pad, v.dil, v.stride);
+  *wo = out_dim(w, v.pad, v.dil, v.stride);
+  return PP_OK;
+}
+
+pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
+                       int32_t w, int32_t act_dtype, uint32_t flags, hipStream_t st) {
+  int ho = 0, wo = 0;
+  pp_status s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
+  if (s != PP_OK) return s;
+  if (!d_blob || !x || !y) return fail(PP_EINVAL, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_blob) % 256) return fail(PP_EINVAL, "device blob must be 256-byte aligned");
+  const size_t esz = act_dtype == PP_BF16 ? 2 : 4;
+  if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % esz)
+    return fail(PP_EINVAL, "activation pointers misaligned");
+  const uint8_t* xb = static_cast<const uint8_t*>(x);
+  const uint8_t* yb = static_cast<const uint8_t*>(y);
+  const size_t xbytes = static_cast<size_t>(n) * v.c_in * h * w * esz;
+  const size_t ybytes = static_cast<size_t>(n) * v.c_out * ho * wo * esz;
+  if (xb < yb + ybytes && yb < xb + xbytes) return fail(PP_EINVAL, "x and y overlap");
+  if (flags & ~static_cast<uint32_t>(PP_RELU)) return fail(PP_EINVAL, "unknown flags");
+
+  ConvParams p;
+  p.blob = static_cast<const uint8_t*>(d_blob);
+  p.x = x;
+  p.y = y;
+  p.n = n;
+  p.h = h;
+  p.w = w;
+  p.ho = ho;
+  p.wo = wo;
+  p.c_in = v.c_in;
+  p.c_out = v.c_out;
+  p.pad = v.pad;
+  p.stride = v.stride;
+  p.dil = v.dil;
+  p.n_groups = v.n_groups;
+  p.off_codes = v.off_codes;
+  p.off_woff = v.off_woff;
+  p.off_w = v.off_w;
+  p.off_bias = v.off_bias;
+  p.off_perm = v.off_perm;
+  p.off_masks = v.off_masks;
+  p.n_wt = static_cast<uint32_t>(v.n_wt);
+  p.n_patterns = v.n_patterns;
+  p.flags = flags;
+  const int lib = library_kind(v);
+  const ConvPlan plan = plan_conv(p, lib);
+  hipError_t e = launch_conv(lib, plan, p, act_dtype == PP_BF16, st);
+  if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
+  return PP_OK;
+}
+
+}  // namespace pp
+
+using namespace pp;
+
+extern "C" pp_status pp_conv2d_out_size(const void* h_blob, size_t blob_bytes, int32_t h, int32_t w,
+                                        int32_t* h_out, int32_t* w_out) {
+  clear_error();
+  BlobView v;
+  pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
+  if (s != PP_OK) return s;
+  if (h < 1 || w < 1) return fail(PP_EINVAL, "h, w must be >= 1");
+  const long hn = h + 2L * v.pad - 2L * v.dil - 1, wn = w + 2L * v.pad - 2L * v.dil - 1;
+  if (hn < 0 || wn < 0) return fail(PP_EINVAL, "input smaller than the dilated kernel");
+  if (h_out) *h_out = static_cast<int32_t>(hn / v.stride + 1);
+  if (w_out) *w_out = static_cast<int32_t>(wn / v.stride + 1);
+  return PP_OK;
+}
+
+extern "C" pp_status pp_conv2d_fwd(const void* h_blob, size_t blob_bytes, const void* d_blob, const void* x,
+                                   void* y, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
+                                   void* hip_stream) {
+  clear_error();
+  BlobView v;
+  pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
+  if (s != PP_OK) return s;
+  return conv_enqueue(v, d_blob, x, y, n, h, w, act_dtype, flags, static_cast<hipStream_t>(hip_stream));
+}

@@ -1,0 +1,224 @@
+// net.cpp -- pp_net_workspace / pp_net_fwd: run a flat op list (one entry
+// per fused layer, the layer-wise representation of Sec. 3) on one stream.
+// Slot 0 is the input, slot 1 the output, slots 2.. live in the caller's
+// workspace at fixed 256-byte-aligned offsets.  Validation of the whole list
+// happens before the first launch.
+#include <hip/hip_runtime.h>
+
+#include <string>
+#include <vector>
+
+#include "api_internal.hpp"
+#include "dense.hpp"
+#include "ppk1.hpp"
+
+namespace pp {
+namespace {
+
+struct Shape {
+  int c = 0, h = 0, w = 0;
+  bool defined = false;
+};
+
+struct Plan {
+  std::vector<Shape> in, in2, out;
+  std::vector<BlobView> views;
+  size_t slot_bytes[PP_MAX_SLOTS] = {};
+  size_t slot_off[PP_MAX_SLOTS] = {};
+  size_t ws_bytes = 0;
+  Shape final_shape;
+};
+
+pp_status bad(int i, const std::string& msg) { return fail(PP_EINVAL, "op " + std::to_string(i) + ": " + msg); }
+
+pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w, int act, Plan* pl) {
+  if (!ops || n_ops < 1) return fail(PP_EINVAL, "empty op list");
+  if (n < 1 || c < 1 || h < 1 || w < 1) return fail(PP_EINVAL, "bad input shape");
+  if (act != PP_F32 && act != PP_BF16) return fail(PP_EINVAL, "bad activation dtype");
+  const size_t esz = act == PP_BF16 ? 2 : 4;
+  Shape slots[PP_MAX_SLOTS];
+  slots[0] = Shape{c, h, w, true};
+  pl->in.resize(n_ops);
+  pl->in2.resize(n_ops);
+  pl->out.resize(n_ops);
+  pl->views.resize(n_ops);
+  std::vector<Shape> writes1;
+  for (int i = 0; i < n_ops; ++i) {
+    const pp_net_op& op = ops[i];
+    if (op.src < 0 || op.src >= PP_MAX_SLOTS || op.dst < 1 || op.dst >= PP_MAX_SLOTS) return bad(i, "slot out of range");
+    if (op.dst == op.src) return bad(i, "dst equals src");
+    if (!slots[op.src].defined) return bad(i, "src slot not written yet");
+    const Shape s = slots[op.src];
+    Shape o;
+    switch (op.kind) {
+      case PP_OP_CONV_PP: {
+        pp_status st = parse_blob(op.h_blob, op.blob_bytes, &pl->views[i], /*full=*/false);
+        if (st != PP_OK) return st;
+        if (!op.d_blob) return bad(i, "d_blob is NULL");
+        const BlobView& v = pl->views[i];
+        if (v.c_in != s.c) return bad(i, "input channels do not match the blob");
+        if (op.flags & ~static_cast<uint32_t>(PP_RELU)) return bad(i, "unknown flags");
+        int ho = 0, wo = 0;
+        st = conv_check(v, n, s.h, s.w, act, &ho, &wo);
+        if (st != PP_OK) return st;
+        o = Shape{v.c_out, ho, wo, true};
+        break;
+      }
+      case PP_OP_CONV_DENSE: {
+        if (op.k != 1 && op.k != 3 && op.k != 9) return fail(PP_EUNSUPPORTED, "dense conv: k must be 1, 3 or 9");
+        if (op.stride != 1 || op.dilation != 1) return fail(PP_EUNSUPPORTED, "dense conv: stride and dilation 1 only");
+        if (op.pad < 0 || op.pad > op.k) return bad(i, "bad pad");
+        if (op.c_in != s.c || op.c_out < 1) return bad(i, "channel mismatch");
+        if (!op.d_w) return bad(i, "d_w is NULL");
+        const int ho = s.h + 2 * op.pad - op.k + 1, wo = s.w + 2 * op.pad - op.k + 1;
+        if (ho < 1 || wo < 1) return bad(i, "input smaller than the kernel");
+        o = Shape{op.c_out, ho, wo, true};
+        break;
+      }
+      case PP_OP_DECONV: {
+        if (op.k != 4 || op.stride != 2 || op.pad != 1)
+          return fail(PP_EUNSUPPORTED, "transposed conv: kernel 4, stride 2, pad 1 only");
+        if (op.c_in != s.c || op.c_out < 1) return bad(i, "channel mismatch");
+        if (!op.d_w) return bad(i, "d_w is NULL");
+        o = Shape{op.c_out, 2 * s.h, 2 * s.w, true};
+        break;
+      }
+      case PP_OP_MAXPOOL2:
+        if (s.h < 2 || s.w < 2) return bad(i, "maxpool input smaller than 2x2");
+        o = Shape{s.c, s.h / 2, s.w / 2, true};
+        break;
+      case PP_OP_UPSAMPLE2:
+        o = Shape{s.c, 2 * s.h, 2 * s.w, true};
+        break;
+      case PP_OP_PIXSHUF2:
+        if (s.c % 4) return bad(i, "pixel shuffle needs a multiple of 4 channels");
+        o = Shape{s.c / 4, 2 * s.h, 2 * s.w, true};
+        break;
+      case PP_OP_ADD: {
+        if (op.src2 < 0 || op.src2 >= PP_MAX_SLOTS || !slots[op.src2].defined) return bad(i, "src2 not written yet");
+        if (op.dst == op.src2) return bad(i, "dst equals src2");
+        const Shape s2 = slots[op.src2];
+        if (s2.c != s.c || s2.h != s.h || s2.w != s.w) return bad(i, "add operands differ in shape");
+        pl->in2[i] = s2;
+        o = s;
+        break;
+      }
+      default:
+        return bad(i, "unknown op kind");
+    }
+    const double elems = static_cast<double>(n) * o.c * o.h * o.w;
+    if (elems > static_cast<double>(1LL << 40)) return bad(i, "activation too large");
+    pl->in[i] = s;
+    pl->out[i] = o;
+    slots[op.dst] = o;
+    const size_t bytes = static_cast<size_t>(n) * o.c * o.h * o.w * esz;
+    if (bytes > pl->slot_bytes[op.dst]) pl->slot_bytes[op.dst] = bytes;
+    if (op.dst == 1) writes1.push_back(o);
+  }
+  if (!slots[1].defined) return fail(PP_EINVAL, "no op writes the output slot 1");
+  for (const Shape& s : writes1)
+    if (s.c != slots[1].c || s.h != slots[1].h || s.w != slots[1].w)
+      return fail(PP_EINVAL, "slot 1 is written with different shapes");
+  pl->final_shape = slots[1];
+  size_t off = 0;
+  for (int sl = 2; sl < PP_MAX_SLOTS; ++sl) {
+    pl->slot_off[sl] = off;
+    off += (pl->slot_bytes[sl] + 255) / 256 * 256;
+  }
+  pl->ws_bytes = off;
+  return PP_OK;
+}
+
+}  // namespace
+}  // namespace pp
+
+using namespace pp;
+
+extern "C" pp_status pp_net_workspace(const pp_net_op* ops, int32_t n_ops, int32_t n, int32_t c, int32_t h, int32_t w,
+                                      int32_t act_dtype, size_t* bytes, int32_t* out_c, int32_t* out_h,
+                                      int32_t* out_w) {
+  clear_error();
+  Plan pl;
+  pp_status st = make_plan(ops, n_ops, n, c, h, w, act_dtype, &pl);
+  if (st != PP_OK) return st;
+  if (bytes) *bytes = pl.ws_bytes;
+  if (out_c) *out_c = pl.final_shape.c;
+  if (out_h) *out_h = pl.final_shape.h;
+  if (out_w) *out_w = pl.final_shape.w;
+  return PP_OK;
+}
+
+extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void* x, void* y, int32_t n, int32_t c,
+                                int32_t h, int32_t w, int32_t act_dtype, void* workspace, size_t ws_bytes,
+                                void* hip_stream) {
+  clear_error();
+  Plan pl;
+  pp_status st = make_plan(ops, n_ops, n, c, h, w, act_dtype, &pl);
+  if (st != PP_OK) return st;
+  if (!x || !y) return fail(PP_EINVAL, "NULL x or y");
+  if (ws_bytes < pl.ws_bytes) return fail(PP_ESIZE, "workspace smaller than pp_net_workspace");
+  if (pl.ws_bytes && !workspace) return fail(PP_EINVAL, "NULL workspace");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(PP_EINVAL, "workspace must be 256-byte aligned");
+  const bool bf = act_dtype == PP_BF16;
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  auto slot_ptr = [&](int s) -> void* {
+    if (s == 0) return const_cast<void*>(x);
+    if (s == 1) return y;
+    return static_cast<uint8_t*>(workspace) + pl.slot_off[s];
+  };
+  for (int i = 0; i < n_ops; ++i) {
+    const pp_net_op& op = ops[i];
+    const Shape& si = pl.in[i];
+    const Shape& so = pl.out[i];
+    void* dst = slot_ptr(op.dst);
+    const void* src = slot_ptr(op.src);
+    hipError_t e = hipSuccess;
+    switch (op.kind) {
+      case PP_OP_CONV_PP:
+        st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags, stream);
+        if (st != PP_OK) return st;
+        break;
+      case PP_OP_CONV_DENSE:
+      case PP_OP_DECONV: {
+        DenseParams p;
+        p.x = src;
+        p.y = dst;
+        p.wt = op.d_w;
+        p.bias = op.d_b;
+        p.n = n;
+        p.c_in = si.c;
+        p.h = si.h;
+        p.w = si.w;
+        p.c_out = so.c;
+        p.ho = so.h;
+        p.wo = so.w;
+        p.k = op.k;
+        p.stride = op.stride;
+        p.pad = op.pad;
+        p.relu = (op.flags & PP_RELU) ? 1 : 0;
+        e = op.kind == PP_OP_CONV_DENSE ? launch_dense_conv(p, bf, stream) : launch_deconv(p, bf, stream);
+        break;
+      }
+      default: {
+        GlueParams p;
+        p.op = op.kind == PP_OP_MAXPOOL2 ? kGlueMaxPool2
+             : op.kind == PP_OP_UPSAMPLE2 ? kGlueUp2
+             : op.kind == PP_OP_PIXSHUF2 ? kGluePixShuf2 : kGlueAdd;
+        p.x = src;
+        p.x2 = op.kind == PP_OP_ADD ? slot_ptr(op.src2) : nullptr;
+        p.y = dst;
+        p.n = n;
+        p.c_in = si.c;
+        p.h = si.h;
+        p.w = si.w;
+        p.c_out = so.c;
+        p.ho = so.h;
+        p.wo = so.w;
+        e = launch_glue(p, bf, stream);
+        break;
+      }
+    }
+    if (e != hipSuccess) return fail(PP_EHIP, "op " + std::to_string(i) + ": " + hipGetErrorString(e));
+  }
+  return PP_OK;
+}

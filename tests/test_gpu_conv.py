@@ -1,0 +1,199 @@
+"""GPU parity of pp_conv2d_fwd against the CPU oracle (fp64 masked-dense
+direct convolution), element by element, plus bitwise invariants.
+
+Run on an MI355X with ``pytest -m gpu``.  Every case prints its name, seed
+and shape before touching the GPU."""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import bf16 as obf16
+from oracle import conv as oconv
+from tests.tolerance import check
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+pp = pytest.importorskip("paper_2004_11250_amd")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    pp.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _to_dev(x, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(x, np.float32)).cuda()
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def _from_dev(y):
+    torch.cuda.synchronize()
+    return y.float().cpu().numpy().astype(np.float64)
+
+
+def run_layer(L, x, stride=1, pad=1, dil=1, relu=True, dtype="f32", out_channels=None):
+    """GPU result and oracle (result, bound) on the same rounded inputs."""
+    wd = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
+    if dtype == "bf16":
+        x = obf16.round_f32(x)
+        w_or = obf16.round_f32(L["w"])
+    else:
+        w_or = L["w"]
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], stride, pad, dil, wd)
+    y = _from_dev(pp.conv2d_fwd(layer, _to_dev(x, dtype), relu=relu))
+    sel = slice(None) if out_channels is None else out_channels
+    args = (x, w_or[sel], L["b"][sel], L["pid"][sel], L["conn"][sel], L["lib"])
+    ref = oconv.conv3x3_pruned(*args, stride, pad, dil, relu)
+    bound = oconv.conv3x3_bound(*args, stride, pad, dil)
+    return y[:, sel], ref, bound
+
+
+def test_config1_layer():
+    spec = workloads.net_spec(1)
+    op = spec["ops"][0]
+    L = workloads.layer_params(1, 0, op)
+    x = workloads.net_input(1)
+    _say("config 1 layer 16->16 32x32 fp32 relu")
+    y, ref, bound = run_layer(L, x, relu=True)
+    check(y, ref, bound, "f32", "config 1")
+
+
+# (c_out, c_in, h, w, stride, pad, dil, n): sizes the oracle finishes in
+# seconds; they span several tiles and channel chunks and end in ragged tails
+SHAPES = [
+    (16, 16, 32, 32, 1, 1, 1, 1),
+    (19, 13, 23, 29, 1, 1, 1, 2),      # small-map tiling, ragged groups/chunks
+    (24, 21, 57, 61, 1, 1, 1, 1),      # medium-map tiling
+    (12, 10, 101, 131, 1, 1, 1, 1),    # large-map tiling
+    (33, 9, 45, 38, 2, 1, 1, 1),       # stride 2
+    (20, 17, 34, 30, 1, 2, 2, 1),      # dilation 2
+    (9, 11, 41, 27, 2, 2, 2, 1),       # stride 2 + dilation 2
+    (8, 3, 5, 7, 1, 0, 1, 1),          # no padding, tiny map
+    (5, 4, 1, 1, 1, 1, 1, 3),          # 1x1 map
+    (64, 64, 17, 16, 1, 1, 1, 1),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[f"{s[0]}x{s[1]}_{s[2]}x{s[3]}_s{s[4]}p{s[5]}d{s[6]}" for s in SHAPES])
+def test_random_shapes(shape, dtype):
+    c_out, c_in, h, w, s, p, d, n = shape
+    seed = hash(shape) % 10000
+    L = workloads.random_layer(seed, c_out, c_in, keep=0.45)
+    x = workloads.random_input(seed, (n, c_in, h, w))
+    _say("random layer", shape, dtype, "seed", seed)
+    y, ref, bound = run_layer(L, x, s, p, d, relu=bool(seed % 2), dtype=dtype)
+    check(y, ref, bound, dtype, f"{shape} {dtype}")
+
+
+@pytest.mark.parametrize("libname", ["dense9", "generic", "canon8_permuted"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_pattern_libraries(libname, dtype):
+    rng = np.random.default_rng(3)
+    if libname == "dense9":
+        lib = np.array([0x1FF], np.uint16)
+    elif libname == "generic":
+        lib = np.array([0x010, 0x1FF, 0x155, 0x0BA, 0x007, 0x1C0, 0x124, 0x049, 0x03A, 0x111, 0x054], np.uint16)
+    else:   # same masks as the canonical library, different order -> generic path
+        lib = np.array(workloads.CANON8[::-1], np.uint16)
+    L = workloads.random_layer(77, 21, 11, lib=lib, keep=0.6)
+    x = workloads.random_input(77, (2, 11, 29, 35))
+    for (s, p, d) in ((1, 1, 1), (2, 1, 1), (1, 2, 2)):
+        _say("library", libname, dtype, (s, p, d))
+        y, ref, bound = run_layer(L, x, s, p, d, relu=False, dtype=dtype)
+        check(y, ref, bound, dtype, f"{libname} {dtype} {(s, p, d)}")
+
+
+def test_all_kernels_pruned_gives_relu_bias_exactly():
+    L = workloads.random_layer(8, 13, 6)
+    L["conn"][:] = 0
+    x = workloads.random_input(8, (1, 6, 20, 20))
+    for relu in (False, True):
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        y = _from_dev(pp.conv2d_fwd(layer, _to_dev(x, "f32"), relu=relu))
+        b = np.maximum(L["b"], 0) if relu else L["b"]
+        assert np.array_equal(y, np.broadcast_to(b.astype(np.float64)[None, :, None, None], y.shape))
+
+
+def test_empty_filters_and_unused_channels():
+    L = workloads.random_layer(9, 17, 9, keep=0.5)
+    L["conn"][3] = 0           # filter 3: no kept kernel
+    L["conn"][:, 4] = 0        # channel 4: read by no filter
+    x = workloads.random_input(9, (1, 9, 24, 24))
+    y, ref, bound = run_layer(L, x)
+    check(y, ref, bound, "f32", "empty filter")
+    assert np.array_equal(y[:, 3], np.broadcast_to(np.float64(max(L["b"][3], 0)), y[:, 3].shape))
+
+
+def test_determinism_and_invariants():
+    L = workloads.random_layer(10, 24, 16, keep=0.4)
+    x = workloads.random_input(10, (1, 16, 40, 44))
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+    xd = _to_dev(x, "f32")
+    y1 = _from_dev(pp.conv2d_fwd(layer, xd))
+    y2 = _from_dev(pp.conv2d_fwd(layer, xd))
+    assert np.array_equal(y1, y2), "run-to-run results differ"
+    # zero input -> bias, bitwise
+    y0 = _from_dev(pp.conv2d_fwd(layer, torch.zeros_like(xd), relu=True))
+    assert np.array_equal(y0, np.broadcast_to(np.maximum(L["b"], 0).astype(np.float64)[None, :, None, None], y0.shape))
+    # a channel pruned for filter o does not influence it, bitwise
+    c = 5
+    x2 = x.copy()
+    x2[:, c] += 3.0
+    y3 = _from_dev(pp.conv2d_fwd(layer, _to_dev(x2, "f32")))
+    for o in range(24):
+        if not L["conn"][o, c]:
+            assert np.array_equal(y1[:, o], y3[:, o]), o
+    # power-of-two scaling with zero bias is exact
+    L0 = dict(L, b=np.zeros_like(L["b"]))
+    layer0 = pp.PackedLayer.from_weights(L0["w"], L0["b"], L0["pid"], L0["conn"], L0["lib"])
+    ya = _from_dev(pp.conv2d_fwd(layer0, xd))
+    yb = _from_dev(pp.conv2d_fwd(layer0, xd * 4.0))
+    assert np.array_equal(4.0 * ya, yb)
+
+
+def test_filter_order_does_not_change_results():
+    # packing the same filters in a different order moves output channels
+    # only; the per-filter accumulation order is unchanged, so bitwise equal
+    L = workloads.random_layer(11, 20, 12, keep=0.5)
+    x = workloads.random_input(11, (1, 12, 30, 30))
+    perm = np.random.default_rng(0).permutation(20)
+    La = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+    Lb = pp.PackedLayer.from_weights(L["w"][perm], L["b"][perm], L["pid"][perm], L["conn"][perm], L["lib"])
+    xd = _to_dev(x, "f32")
+    ya = _from_dev(pp.conv2d_fwd(La, xd))
+    yb = _from_dev(pp.conv2d_fwd(Lb, xd))
+    assert np.array_equal(ya[:, perm], yb)
+
+
+def _vgg_layers():
+    spec = workloads.net_spec(2)
+    h = spec["h"]
+    out = []
+    for i, op in enumerate(spec["ops"]):
+        if op["op"] == "maxpool2":
+            h //= 2
+        elif op["op"] == "conv3":
+            out.append((i, op, h))
+    return out
+
+
+@pytest.mark.parametrize("idx", range(13))
+def test_vgg16_full_size_layer_sampled(idx):
+    # full-size VGG-16 layer (224x224 input), the launch configuration the
+    # benchmark times; the oracle computes 8 sampled filters completely
+    i, op, h = _vgg_layers()[idx]
+    L = workloads.layer_params(2, i, op)
+    x = workloads.random_input(500 + i, (1, op["c_in"], h, h), 0.0, 1.0)
+    sel = np.sort(np.random.default_rng(i).choice(op["c_out"], size=8, replace=False))
+    _say("vgg16 layer", i, op["c_in"], "->", op["c_out"], f"{h}x{h}")
+    y, ref, bound = run_layer(L, x, relu=True, out_channels=sel)
+    check(y, ref, bound, "f32", f"vgg layer {i}")

@@ -1,0 +1,132 @@
+"""GPU parity of pp_net_fwd on the five evaluated networks at full size.
+
+Teacher-forced check: every op's GPU output is compared with the oracle run
+on that op's GPU input (sampled output channels for the large layers), so
+errors do not compound.  The op outputs come from pp_net_fwd itself, run on
+the op-list prefix that ends with that op.  pp_net_fwd must also equal the
+chain of single-layer calls bitwise."""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import bf16 as obf16
+from oracle import net as onet
+from tests.tolerance import check
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+pp = pytest.importorskip("paper_2004_11250_amd")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    pp.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _input(cfg, dtype):
+    x = workloads.net_input(cfg)
+    if dtype == "bf16":
+        x = obf16.round_f32(x)
+    t = torch.from_numpy(x).cuda()
+    return x, (t.to(torch.bfloat16) if dtype == "bf16" else t)
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.float().cpu().numpy()
+
+
+def _sampled(op, prm, n_keep, seed):
+    """Restrict an op to a subset of its output channels (oracle cost)."""
+    if op["op"] not in ("conv3", "conv", "deconv") or op["c_out"] <= n_keep:
+        return op, prm, slice(None)
+    sel = np.sort(np.random.default_rng(seed).choice(op["c_out"], size=n_keep, replace=False))
+    p = dict(prm)
+    if op["op"] == "deconv":
+        p["w"] = prm["w"][:, sel]
+    else:
+        p["w"] = prm["w"][sel]
+        for k in ("pid", "conn"):
+            if k in prm:
+                p[k] = prm[k][sel]
+    p["b"] = prm["b"][sel]
+    return dict(op, c_out=len(sel)), p, sel
+
+
+def teacher_forced(cfg, dtype, n_keep=6):
+    spec = workloads.net_spec(cfg)
+    params = workloads.net_params(cfg)
+    net = pp.Net(spec["ops"], params, dtype)
+    x_np, x = _input(cfg, dtype)
+    slots = {0: x_np}
+    worst = 0.0
+    for i, (op, prm) in enumerate(zip(spec["ops"], params)):
+        _say(f"cfg {cfg} {dtype} op {i} {op['op']} c_in={op.get('c_in')} c_out={op.get('c_out')}")
+        # pp_net_fwd on the prefix ending at op i, with op i writing slot 1
+        sub = pp.Net.__new__(pp.Net)
+        sub.__dict__.update(net.__dict__)
+        arr = (pp.NetOp * (i + 1))()
+        for j in range(i + 1):
+            arr[j] = net.ops[j]
+        arr[i].dst = 1
+        sub.ops, sub.n_ops, sub._ws = arr, i + 1, None
+        y = _np(sub.forward(x))
+        src = slots[op["src"]]
+        src2 = slots.get(op.get("src2")) if "src2" in op else None
+        sop, sprm, sel = _sampled(op, prm, n_keep, 1000 * cfg + i)
+        ref, bound = onet.run_op(sop, sprm, src, src2, dtype)
+        yi = y[:, sel]
+        if bound is None:
+            # data movement only: must be exact
+            assert np.array_equal(yi, onet.store(ref, dtype)), f"cfg {cfg} op {i}"
+        else:
+            worst = max(worst, check(yi, ref, bound, dtype, f"cfg {cfg} op {i} ({op['op']})"))
+        slots[op["dst"]] = y
+    return worst
+
+
+@pytest.mark.parametrize("cfg,dtype", [(1, "f32"), (2, "f32"), (3, "f32"), (4, "f32"), (4, "bf16"), (5, "f32"),
+                                       (5, "bf16")])
+def test_network_teacher_forced(cfg, dtype):
+    worst = teacher_forced(cfg, dtype)
+    _say(f"cfg {cfg} {dtype}: worst |err|/S = {worst:.3e}")
+
+
+def test_vgg16_net_equals_chained_layer_calls():
+    spec = workloads.net_spec(2)
+    params = workloads.net_params(2)
+    net = pp.Net(spec["ops"], params, "f32")
+    _, x = _input(2, "f32")
+    _say("vgg16 pp_net_fwd vs chained pp_conv2d_fwd + maxpool")
+    y_net = _np(net.forward(x))
+    cur = x
+    li = 0
+    for op, prm in zip(spec["ops"], params):
+        if op["op"] == "conv3":
+            cur = pp.conv2d_fwd(net.layers[li], cur, relu=op["relu"])
+            li += 1
+        else:
+            one = pp.Net([dict(op, src=0, dst=1)], [prm], "f32")
+            cur = one.forward(cur)
+    assert np.array_equal(y_net, _np(cur))
+
+
+def test_vgg16_end_to_end_vs_oracle_chain():
+    # informational bound: the all-oracle chain vs the GPU chain, errors compound
+    spec = workloads.net_spec(2)
+    params = workloads.net_params(2)
+    net = pp.Net(spec["ops"], params, "f32")
+    x_np, x = _input(2, "f32")
+    y = _np(net.forward(x)).astype(np.float64)
+    ref = onet.run_net(spec, params, x_np, "f32").astype(np.float64)
+    rel = np.max(np.abs(y - ref)) / np.max(np.abs(ref))
+    _say(f"vgg16 end-to-end max|err|/max|ref| = {rel:.3e}")
+    assert rel < 1e-4
