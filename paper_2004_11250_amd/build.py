@@ -25,8 +25,12 @@ OBJDIR = os.path.join(PKG, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
+# -structurizecfg-skip-uniform-regions: the pattern dispatch of the pruned
+# conv is a wave-uniform branch tree; left unstructurized it needs no
+# accumulator copies at the joins (the structurized form duplicates them).
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature",
-             "-Xclang", "-packed-fp32-ops", "-Wno-pass-failed", f"-I{INCLUDE}", f"-I{CSRC}"]
+             "-Xclang", "-packed-fp32-ops", "-mllvm", "-structurizecfg-skip-uniform-regions",
+             "-Wno-pass-failed", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
 def _run(cmd):

@@ -25,12 +25,45 @@ struct ConvParams {
   int tiles_x = 0, tiles_y = 0, n_ftiles = 0;   // filled by the launcher
 };
 
-// Which compiled tiling to use for a layer shape.
+// The compiled tilings ("recipes"):
+//   id, R x CC outputs per lane, LW lanes across (64/LW down), WF filter waves
+//   (8 filters each), WS channel-split waves, CPW channels per wave per chunk.
+#define PP_RECIPES(X)        \
+  X(0, 4, 4, 8, 1, 4, 2)     \
+  X(1, 4, 4, 8, 2, 2, 4)     \
+  X(2, 4, 4, 8, 4, 1, 8)     \
+  X(3, 2, 4, 8, 1, 4, 2)     \
+  X(4, 2, 4, 8, 2, 2, 4)     \
+  X(5, 2, 4, 8, 4, 1, 8)     \
+  X(6, 2, 2, 8, 1, 4, 4)     \
+  X(7, 2, 2, 8, 2, 2, 8)     \
+  X(8, 2, 2, 8, 1, 8, 2)     \
+  X(9, 1, 2, 8, 1, 8, 2)     \
+  X(10, 1, 1, 8, 1, 8, 2)    \
+  X(11, 4, 2, 8, 1, 4, 2)    \
+  X(12, 2, 4, 8, 1, 4, 1)    \
+  X(13, 2, 2, 8, 1, 4, 1)
+
+constexpr int kNumRecipes = 14;
+
+struct RecipeInfo {
+  int r, cc, lw, wf, ws, cpw;
+};
+
+// geometry of a recipe, and whether its LDS footprint fits for (stride, dilation)
+RecipeInfo recipe_info(int id);
+bool recipe_fits(int id, int stride, int dil);
+// recipes compiled for a pattern library (the canonical library gets all)
+bool recipe_compiled(int lib, int id);
+
 struct ConvPlan {
   int recipe = 0;
 };
 
 ConvPlan plan_conv(const ConvParams& p, int lib);
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st);
+
+template <int LIB, int S, int D, class TA>
+hipError_t launch_recipe(int id, const ConvParams& p, hipStream_t st);
 
 }  // namespace pp

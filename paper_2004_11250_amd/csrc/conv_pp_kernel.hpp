@@ -1,0 +1,499 @@
+// conv_pp_kernel.hpp -- the pattern/connectivity-pruned 3x3 convolution
+// kernel template for gfx950 (included by the per-library .hip files).
+//
+// One launch computes y = act(conv(x, W_pruned) + b) for a PPK1-packed layer
+// (pattern + connectivity pruning, Sec. 2; compact storage and filter
+// reorder, Sec. 3; conv fused with bias and activation, Sec. 3).
+//
+// Mapping to CDNA4:
+//   * A workgroup owns one spatial output tile of one image and WF slot
+//     groups (8 packed filters each, one group per wave).  Its input halo
+//     tile is staged from HBM into LDS one chunk of CCH = WS*CPW input
+//     channels at a time (coalesced along rows, zero-filled outside the
+//     image) and shared by every filter of the workgroup.
+//   * Lanes are output pixels: each lane owns an R x CC block of outputs for
+//     the 8 filters of its wave, so the 3x3 neighbourhood it needs for one
+//     input channel (the "patch") is read from LDS once and reused by every
+//     kept kernel of that channel.
+//   * Everything that depends on the sparsity structure is wave-uniform: the
+//     per-(group, channel) code word, the weight offset and the weights are
+//     scalar loads into SGPRs, and the pattern selects a code path through a
+//     uniform branch whose tap offsets are compile-time constants.  No lane
+//     ever diverges on the pruning structure.
+//   * Software pipelining: code words for the wave's channels of a chunk are
+//     fetched before the chunk is staged; the weights and the patch of
+//     channel k+1 are in flight while channel k is computed.
+//   * WS waves of a workgroup split each chunk's channels; their partial sums
+//     are combined through LDS by a fixed binary tree, so results are
+//     deterministic.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "conv_pp.hpp"
+
+namespace pp {
+namespace kern {
+
+template <class T>
+__device__ __forceinline__ T sload(const uint8_t* base, uint32_t byte_off) {
+  // 32-bit pieces through the constant address space: uniform addresses
+  // become s_load_dword{,x2,x4} into SGPRs
+  typedef const __attribute__((address_space(4))) uint32_t* cptr;
+  static_assert(sizeof(T) % 4 == 0, "scalar loads move whole dwords");
+  const cptr src = (cptr)(base + byte_off);
+  union {
+    T v;
+    uint32_t u[sizeof(T) / 4];
+  } r;
+#pragma unroll
+  for (int i = 0; i < static_cast<int>(sizeof(T) / 4); ++i) r.u[i] = src[i];
+  return r.v;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+__device__ __forceinline__ float load_act(const float* p, size_t i) { return p[i]; }
+__device__ __forceinline__ float load_act(const uint16_t* p, size_t i) {
+  return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
+}
+__device__ __forceinline__ uint32_t to_bf16_bits(float v) {
+  uint32_t u = __float_as_uint(v);
+  u += 0x7FFFu + ((u >> 16) & 1u);   // round to nearest even (finite values)
+  return u >> 16;
+}
+
+// wait until every outstanding LDS and scalar-memory load has returned
+__device__ __forceinline__ void wait_lgkm() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+constexpr uint32_t kCanon8[8] = {0x03A, 0x0B2, 0x0B8, 0x09A, 0x01B, 0x036, 0x0D8, 0x1B0};
+
+constexpr int nth_tap(uint32_t mask, int n) {
+  for (int t = 0; t < 9; ++t)
+    if ((mask >> t) & 1u) {
+      if (n == 0) return t;
+      --n;
+    }
+  return -1;
+}
+
+// acc[r][q] += w * x(r*S + ky*D, q*S + kx*D) for one tap
+template <int TAP, int S, int D, int R, int CC, int PR, int PC>
+__device__ __forceinline__ void fma_tap(float (&acc)[R][CC], const float (&pt)[PR][PC], float w) {
+  constexpr int ky = TAP / 3, kx = TAP % 3;
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int q = 0; q < CC; ++q) acc[r][q] = __builtin_fmaf(w, pt[r * S + ky * D][q * S + kx * D], acc[r][q]);
+}
+
+template <uint32_t MASK, int S, int D, int R, int CC, int PR, int PC>
+__device__ __forceinline__ void apply4(float (&acc)[R][CC], const float (&pt)[PR][PC], float w0, float w1,
+                                       float w2, float w3) {
+  fma_tap<nth_tap(MASK, 0), S, D>(acc, pt, w0);
+  fma_tap<nth_tap(MASK, 1), S, D>(acc, pt, w1);
+  fma_tap<nth_tap(MASK, 2), S, D>(acc, pt, w2);
+  fma_tap<nth_tap(MASK, 3), S, D>(acc, pt, w3);
+}
+
+template <int S, int D, int R, int CC, int PR, int PC>
+__device__ __forceinline__ void apply_canon8(uint32_t p, float (&acc)[R][CC], const float (&pt)[PR][PC],
+                                             float w0, float w1, float w2, float w3) {
+  switch (p) {
+    case 0: apply4<kCanon8[0], S, D>(acc, pt, w0, w1, w2, w3); break;
+    case 1: apply4<kCanon8[1], S, D>(acc, pt, w0, w1, w2, w3); break;
+    case 2: apply4<kCanon8[2], S, D>(acc, pt, w0, w1, w2, w3); break;
+    case 3: apply4<kCanon8[3], S, D>(acc, pt, w0, w1, w2, w3); break;
+    case 4: apply4<kCanon8[4], S, D>(acc, pt, w0, w1, w2, w3); break;
+    case 5: apply4<kCanon8[5], S, D>(acc, pt, w0, w1, w2, w3); break;
+    case 6: apply4<kCanon8[6], S, D>(acc, pt, w0, w1, w2, w3); break;
+    case 7: apply4<kCanon8[7], S, D>(acc, pt, w0, w1, w2, w3); break;
+    default: break;
+  }
+}
+
+// generic library: taps tested one by one against the runtime mask
+template <int S, int D, int R, int CC, int PR, int PC>
+__device__ __forceinline__ void apply_generic(uint32_t mask, float (&acc)[R][CC], const float (&pt)[PR][PC],
+                                              const uint8_t* blob, uint32_t off_w, uint32_t k, uint32_t n_wt,
+                                              bool bf16w) {
+  uint32_t q = 0;
+  const uint32_t last = n_wt ? n_wt - 1 : 0u;   // clamp: never read past the weights
+#define PP_TAP(T)                                                \
+  if (mask & (1u << T)) {                                        \
+    const uint32_t kq = min(k + q, last);                        \
+    float wv;                                                    \
+    if (bf16w) {                                                 \
+      uint32_t u = sload<uint32_t>(blob, (off_w + 2 * kq) & ~3u); \
+      wv = (kq & 1) ? bf16_hi(u) : bf16_lo(u);                   \
+    } else {                                                     \
+      wv = sload<float>(blob, off_w + 4 * kq);                   \
+    }                                                            \
+    fma_tap<T, S, D>(acc, pt, wv);                               \
+    ++q;                                                         \
+  }
+  PP_TAP(0) PP_TAP(1) PP_TAP(2) PP_TAP(3) PP_TAP(4) PP_TAP(5) PP_TAP(6) PP_TAP(7) PP_TAP(8)
+#undef PP_TAP
+}
+
+// blockIdx -> logical block so that consecutive logical blocks (which share
+// the same input tile) land on the same XCD: the dispatcher sends block b to
+// XCD b % 8, and each XCD has its own L2.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb) {
+  const uint32_t x = b & 7u, local = b >> 3;
+  const uint32_t q0 = nb >> 3, r = nb & 7u, q1 = q0 + (r ? 1u : 0u);
+  return x < r ? x * q1 + local : r * q1 + (x - r) * q0 + local;
+}
+
+// compile-time geometry of one tiling
+template <int S, int D, int R, int CC, int LW, int WF, int WS, int CPW>
+struct Geo {
+  static constexpr int LH = 64 / LW;
+  static constexpr int TH = LH * R, TW = LW * CC;          // output tile
+  static constexpr int PR = (R - 1) * S + 2 * D + 1;       // patch rows
+  static constexpr int PC = (CC - 1) * S + 2 * D + 1;      // patch cols
+  static constexpr int TIH = (TH - 1) * S + 2 * D + 1;     // input tile rows
+  static constexpr int TIW = (TW - 1) * S + 2 * D + 1;     // input tile cols
+  static constexpr int LSTR = (TIW + 3) / 4 * 4;           // LDS row stride (floats)
+  static constexpr int CHSTR = TIH * LSTR;                 // LDS channel stride
+  static constexpr int CCH = WS * CPW;                     // channels per chunk
+  static constexpr int NT = WF * WS * 64;
+  static constexpr int NACC = 8 * R * CC;
+  static constexpr int STAGE = CCH * CHSTR;
+  static constexpr int RED = (WS > 1) ? (WS / 2) * WF * NACC * 64 : 0;
+  static constexpr int LDS_FLOATS = STAGE > RED ? STAGE : RED;
+  static constexpr int STAGE_N = CCH * TIH * TIW;
+  static constexpr int NST = (STAGE_N + NT - 1) / NT;
+  static constexpr int VW = ((CC * S) % 4 == 0) ? 4 : (((CC * S) % 2 == 0) ? 2 : 1);
+  static constexpr int N4 = (VW == 4) ? PC / 4 : 0;
+  static constexpr int N2 = (VW >= 2) ? (PC - 4 * N4) / 2 : 0;
+  static constexpr int N1 = PC - 4 * N4 - 2 * N2;
+  static constexpr bool fits = LDS_FLOATS * 4 <= 64 * 1024 && LW * LH == 64 && (WS & (WS - 1)) == 0;
+};
+
+template <int LIB, int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, class TA>
+__global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
+  using G = Geo<S, D, R, CC, LW, WF, WS, CPW>;
+  constexpr int PR = G::PR, PC = G::PC, TIH = G::TIH, TIW = G::TIW, LSTR = G::LSTR, CHSTR = G::CHSTR;
+  constexpr int CCH = G::CCH, NT = G::NT, NACC = G::NACC, NST = G::NST, STAGE_N = G::STAGE_N;
+  constexpr bool WBF = sizeof(TA) == 2;   // bf16 weights with bf16 activations
+  static_assert(G::fits, "tiling does not fit");
+
+  __shared__ __attribute__((aligned(16))) float lds[G::LDS_FLOATS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wf = wid % WF, wk = wid / WF;
+  const int lx = lane % LW, ly = lane / LW;
+
+  uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int ft = blk % a.n_ftiles;
+  blk /= a.n_ftiles;
+  const int tx = blk % a.tiles_x;
+  blk /= a.tiles_x;
+  const int ty = blk % a.tiles_y;
+  const int img = blk / a.tiles_y;
+
+  const int oy0 = ty * G::TH, ox0 = tx * G::TW;
+  const int iy0 = oy0 * S - a.pad, ix0 = ox0 * S - a.pad;
+  const int grp = ft * WF + wf;               // this wave's slot group
+  const bool has_grp = grp < a.n_groups;      // wave-uniform
+
+  const TA* __restrict__ x = static_cast<const TA*>(a.x) + static_cast<size_t>(img) * a.c_in * a.h * a.w;
+  const uint8_t* blob = a.blob;
+  // this image of x as a buffer resource: loads past its end return 0
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<TA*>(x), static_cast<short>(0),
+      static_cast<int>(static_cast<uint32_t>(a.c_in) * a.h * a.w * sizeof(TA)), 0x00020000);
+
+  float acc[8][R][CC];
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int q = 0; q < CC; ++q) acc[s][r][q] = 0.0f;
+
+  const int lane_off = (ly * R * S) * LSTR + lx * CC * S;
+  // staging coordinates of this lane
+  constexpr int NW = WF * WS;
+  constexpr int NCB = (TIW + 63) / 64;                  // 64-column blocks of a staged row
+  constexpr int RPW = (CCH * TIH + NW - 1) / NW;        // staged rows per wave
+  uint32_t gxs[NCB];
+  bool col_ok[NCB];
+#pragma unroll
+  for (int m = 0; m < NCB; ++m) {
+    const int gx = ix0 + lane + 64 * m;
+    col_ok[m] = lane + 64 * m < TIW && gx >= 0 && gx < a.w;
+    gxs[m] = col_ok[m] ? static_cast<uint32_t>(gx) : 0u;
+  }
+
+  for (int cb = 0; cb < a.c_in; cb += CCH) {
+
+    __syncthreads();   // the previous chunk's LDS reads are done
+    // ---- stage input channels [cb, cb+CCH) of the halo tile into LDS.
+    // Wave w stages rows [w*RPW, (w+1)*RPW) of the CCH x TIH staged rows
+    // (row coordinates are wave-uniform; staged row r sits at LDS offset
+    // r*LSTR); lanes cover the TIW columns.  All global loads of a lane are
+    // issued before its LDS writes.
+    {
+      // opaque copy of the chunk index: keeps the compiler from hoisting the
+      // per-row bounds tests out of the chunk loop (they would pin ~2 SGPRs
+      // per staged row for the whole kernel)
+      int cbo = cb;
+      asm volatile("" : "+s"(cbo));
+      float v[RPW][NCB];
+#pragma unroll
+      for (int k = 0; k < RPW; ++k) {
+        const int row = wid * RPW + k + (cbo - cb);
+        const int ch = row / TIH, i = row % TIH;
+        const int c = cb + ch, gy = iy0 + i;
+        const bool row_ok = row < CCH * TIH && c < a.c_in && gy >= 0 && gy < a.h;   // wave-uniform
+        const uint32_t rbase = (static_cast<uint32_t>(c) * a.h + gy) * static_cast<uint32_t>(a.w);
+#pragma unroll
+        for (int m = 0; m < NCB; ++m) {
+          // out-of-image elements get an offset past the buffer: the load returns 0
+          const uint32_t off = (row_ok && col_ok[m]) ? (rbase + gxs[m]) * sizeof(TA) : 0x80000000u;
+          if (sizeof(TA) == 2)
+            v[k][m] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(xr, off, 0, 0)) << 16);
+          else
+            v[k][m] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0));
+        }
+        // issue each row's load right after its address arithmetic (the
+        // scheduler would otherwise compute all rows' addresses first and
+        // run out of SGPRs)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      float* dst = lds + wid * RPW * LSTR + lane;
+#pragma unroll
+      for (int k = 0; k < RPW; ++k) {
+        if (wid * RPW + k + (cbo - cb) < CCH * TIH) {
+#pragma unroll
+          for (int m = 0; m < NCB; ++m)
+            if (lane + 64 * m < TIW) dst[k * LSTR + 64 * m] = v[k][m];
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- channel loop.  The dispatch code exists once (no unrolling over
+    // channels) to keep the instruction footprint small; latency is hidden
+    // by the other waves of the SIMD.
+    const int cl0 = wk * CPW;
+    const int nch = has_grp ? max(0, min(CPW, a.c_in - (cb + cl0))) : 0;   // wave-uniform
+    // code word and weight offset of the first channel; the loop prefetches
+    // those of the next channel
+    uint32_t e = static_cast<uint32_t>(has_grp ? grp : 0) * a.c_in + min(cb + cl0, a.c_in - 1);
+    uint2 cw_next = sload<uint2>(blob, a.off_codes + 8 * e);
+    uint32_t wo_next = sload<uint32_t>(blob, a.off_woff + 4 * e);
+#pragma unroll 1
+    for (int k = 0; k < nch; ++k) {
+      const uint2 cw = cw_next;
+      const uint32_t wof = min(wo_next, a.n_wt);
+      if (k + 1 < nch) {
+        ++e;
+        cw_next = sload<uint2>(blob, a.off_codes + 8 * e);
+        wo_next = sload<uint32_t>(blob, a.off_woff + 4 * e);
+      }
+      if ((cw.x & cw.y) == 0xFFFFFFFFu) continue;   // no kept kernel in this group-channel
+      // patch: the lane's input neighbourhood for this channel
+      float p[PR][PC];
+      {
+        const float* src = lds + (cl0 + k) * CHSTR + lane_off;
+#pragma unroll
+        for (int r = 0; r < PR; ++r) {
+          const float* row = src + r * LSTR;
+#pragma unroll
+          for (int i = 0; i < G::N4; ++i) {
+            const float4 v = *reinterpret_cast<const float4*>(row + 4 * i);
+            p[r][4 * i] = v.x; p[r][4 * i + 1] = v.y; p[r][4 * i + 2] = v.z; p[r][4 * i + 3] = v.w;
+          }
+#pragma unroll
+          for (int i = 0; i < G::N2; ++i) {
+            const float2 v = *reinterpret_cast<const float2*>(row + 4 * G::N4 + 2 * i);
+            p[r][4 * G::N4 + 2 * i] = v.x; p[r][4 * G::N4 + 2 * i + 1] = v.y;
+          }
+#pragma unroll
+          for (int i = 0; i < G::N1; ++i) p[r][4 * G::N4 + 2 * G::N2 + i] = row[4 * G::N4 + 2 * G::N2 + i];
+        }
+      }
+      if (LIB == kLibCanon8) {
+        // weights of all 8 slots, issued together (kept kernels stored in
+        // slot order, 4 weights each; a pruned slot re-reads its successor's)
+        float4 wv[8];
+        uint32_t kk = wof;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
+          if (WBF) {
+            const uint2 u = sload<uint2>(blob, a.off_w + 2 * min(kk, a.n_wt));
+            wv[s] = make_float4(bf16_lo(u.x), bf16_hi(u.x), bf16_lo(u.y), bf16_hi(u.y));
+          } else {
+            wv[s] = sload<float4>(blob, a.off_w + 4 * min(kk, a.n_wt));
+          }
+          kk += (pid != 0xFFu) ? 4u : 0u;
+        }
+        // materialise all weights here: one wait for the whole group-channel
+        // instead of a load + wait sunk into every dispatch branch
+#pragma unroll
+        for (int s = 0; s < 8; ++s) asm volatile("" ::"s"(wv[s].x), "s"(wv[s].y), "s"(wv[s].z), "s"(wv[s].w));
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
+          apply_canon8<S, D>(pid, acc[s], p, wv[s].x, wv[s].y, wv[s].z, wv[s].w);
+        }
+      } else {
+        uint32_t kk = wof;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
+          if (pid == 0xFFu) continue;
+          if (LIB == kLibDense9) {
+            float w9[9];
+            if (WBF) {
+              const uint32_t kc = min(kk, a.n_wt >= 10 ? a.n_wt - 10 : 0u);
+              const uint4 u = sload<uint4>(blob, a.off_w + 2 * kc);
+              const uint32_t u4 = sload<uint32_t>(blob, a.off_w + 2 * kc + 16);
+              w9[0] = bf16_lo(u.x); w9[1] = bf16_hi(u.x); w9[2] = bf16_lo(u.y); w9[3] = bf16_hi(u.y);
+              w9[4] = bf16_lo(u.z); w9[5] = bf16_hi(u.z); w9[6] = bf16_lo(u.w); w9[7] = bf16_hi(u.w);
+              w9[8] = bf16_lo(u4);
+              kk += 10;
+            } else {
+              const uint32_t kc = min(kk, a.n_wt >= 9 ? a.n_wt - 9 : 0u);
+              const float4 u = sload<float4>(blob, a.off_w + 4 * kc);
+              const float4 v = sload<float4>(blob, a.off_w + 4 * kc + 16);
+              const float z = sload<float>(blob, a.off_w + 4 * kc + 32);
+              w9[0] = u.x; w9[1] = u.y; w9[2] = u.z; w9[3] = u.w;
+              w9[4] = v.x; w9[5] = v.y; w9[6] = v.z; w9[7] = v.w; w9[8] = z;
+              kk += 9;
+            }
+            fma_tap<0, S, D>(acc[s], p, w9[0]);
+            fma_tap<1, S, D>(acc[s], p, w9[1]);
+            fma_tap<2, S, D>(acc[s], p, w9[2]);
+            fma_tap<3, S, D>(acc[s], p, w9[3]);
+            fma_tap<4, S, D>(acc[s], p, w9[4]);
+            fma_tap<5, S, D>(acc[s], p, w9[5]);
+            fma_tap<6, S, D>(acc[s], p, w9[6]);
+            fma_tap<7, S, D>(acc[s], p, w9[7]);
+            fma_tap<8, S, D>(acc[s], p, w9[8]);
+          } else {
+            const uint32_t pc = min(pid, static_cast<uint32_t>(a.n_patterns - 1));
+            const uint32_t mw = sload<uint32_t>(blob, (a.off_masks + 2 * pc) & ~3u);
+            const uint32_t mask = ((pc & 1u) ? (mw >> 16) : mw) & 0x1FFu;
+            apply_generic<S, D>(mask, acc[s], p, blob, a.off_w, kk, a.n_wt, WBF);
+            const uint32_t nt = __builtin_popcount(mask);
+            kk += WBF ? ((nt + 1u) & ~1u) : nt;
+          }
+        }
+      }
+    }
+  }
+
+  // ---- combine the WS channel-split partial sums: fixed binary tree
+  if (WS > 1) {
+#pragma unroll
+    for (int half = WS / 2; half >= 1; half /= 2) {
+      __syncthreads();
+      if (wk >= half && wk < 2 * half) {
+        float* dst = lds + static_cast<size_t>((wk - half) * WF + wf) * NACC * 64 + lane;
+        int i = 0;
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+#pragma unroll
+          for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int q = 0; q < CC; ++q, ++i) dst[i * 64] = acc[s][r][q];
+      }
+      __syncthreads();
+      if (wk < half) {
+        const float* src = lds + static_cast<size_t>(wk * WF + wf) * NACC * 64 + lane;
+        int i = 0;
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+#pragma unroll
+          for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int q = 0; q < CC; ++q, ++i) acc[s][r][q] += src[i * 64];
+      }
+    }
+    if (wk > 0) return;
+  }
+  if (!has_grp) return;
+
+  // ---- epilogue: + bias, activation, store to the original channel order
+  TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  const bool relu = (a.flags & PP_RELU) != 0;
+  const int oxl = ox0 + lx * CC;
+  const bool vec = (CC % 4 == 0) && (a.wo % 4 == 0) &&
+                   (reinterpret_cast<uintptr_t>(a.y) % (4 * sizeof(TA)) == 0);   // aligned vector stores
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
+    const uint32_t o = sload<uint32_t>(blob, a.off_perm + 4 * slot);
+    if (o >= static_cast<uint32_t>(a.c_out)) continue;   // padding slot
+    const float bias = sload<float>(blob, a.off_bias + 4 * slot);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int oy = oy0 + ly * R + r;
+      if (oy >= a.ho) continue;
+      TA* row = y + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
+      float v[CC];
+#pragma unroll
+      for (int q = 0; q < CC; ++q) {
+        v[q] = acc[s][r][q] + bias;
+        if (relu) v[q] = fmaxf(v[q], 0.0f);
+      }
+      if (vec && oxl + CC <= a.wo) {
+#pragma unroll
+        for (int q = 0; q < CC; q += 4) {
+          if (WBF) {
+            uint2 u;
+            u.x = to_bf16_bits(v[q]) | (to_bf16_bits(v[q + 1]) << 16);
+            u.y = to_bf16_bits(v[q + 2]) | (to_bf16_bits(v[q + 3]) << 16);
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(row) + oxl + q) = u;
+          } else {
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(row) + oxl + q) =
+                make_float4(v[q], v[q + 1], v[q + 2], v[q + 3]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < CC; ++q) {
+          if (oxl + q < a.wo) {
+            if (WBF)
+              reinterpret_cast<uint16_t*>(row)[oxl + q] = static_cast<uint16_t>(to_bf16_bits(v[q]));
+            else
+              reinterpret_cast<float*>(row)[oxl + q] = v[q];
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side: one tiling = one Recipe; launch helpers
+// ---------------------------------------------------------------------------
+template <int LIB, int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, class TA>
+hipError_t launch_tiling(ConvParams p, hipStream_t st) {
+  using G = Geo<S, D, R, CC, LW, WF, WS, CPW>;
+  if constexpr (!G::fits) {
+    return hipErrorInvalidConfiguration;
+  } else {
+    p.tiles_x = (p.wo + G::TW - 1) / G::TW;
+    p.tiles_y = (p.ho + G::TH - 1) / G::TH;
+    p.n_ftiles = (p.n_groups + WF - 1) / WF;
+    const size_t nb = static_cast<size_t>(p.n_ftiles) * p.tiles_x * p.tiles_y * p.n;
+    if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((pp_conv3x3_kernel<LIB, S, D, R, CC, LW, WF, WS, CPW, TA>), dim3(static_cast<uint32_t>(nb)),
+                       dim3(WF * WS * 64), 0, st, p);
+    return hipGetLastError();
+  }
+}
+
+}  // namespace kern
+}  // namespace pp

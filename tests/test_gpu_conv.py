@@ -197,3 +197,21 @@ def test_vgg16_full_size_layer_sampled(idx):
     _say("vgg16 layer", i, op["c_in"], "->", op["c_out"], f"{h}x{h}")
     y, ref, bound = run_layer(L, x, relu=True, out_channels=sel)
     check(y, ref, bound, "f32", f"vgg layer {i}")
+
+
+# every compiled tiling, forced through the PP_RECIPE override of the planner
+RECIPES = list(range(14))
+
+
+@pytest.mark.parametrize("recipe", RECIPES)
+def test_every_tiling(recipe, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    for (s, p, d), dtype, shape in (((1, 1, 1), "f32", (19, 21, 37, 45)), ((2, 1, 1), "f32", (17, 9, 41, 50)),
+                                    ((1, 2, 2), "f32", (11, 13, 29, 33)), ((1, 1, 1), "bf16", (24, 17, 33, 70))):
+        c_out, c_in, h, w = shape
+        seed = 40 + recipe
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        _say("recipe", recipe, (s, p, d), dtype, shape)
+        y, ref, bound = run_layer(L, x, s, p, d, relu=True, dtype=dtype)
+        check(y, ref, bound, dtype, f"recipe {recipe} {(s, p, d)} {dtype}")
