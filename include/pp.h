@@ -83,12 +83,13 @@ typedef struct {
  *   inout_bytes in: capacity of out; out: bytes required / written
  *
  * Errors: PP_EINVAL (NULL pointer other than bias/out, ranges, conn not 0/1,
- * pattern id >= n_patterns where conn = 1, bad mask), PP_ESIZE (capacity too
- * small; *inout_bytes then holds the required size).
+ * pattern id >= n_patterns where conn = 1, bad mask, more than 2^24 - 1
+ * stored weights), PP_ESIZE (capacity too small; *inout_bytes then holds the
+ * required size).
  *
  * Blob layout "PPK1" (little-endian, each section 64-byte aligned, padding
  * zero):
- *   header  u32[24]: magic 0x314B5050, version | wdtype<<16, c_out, c_in,
+ *   header  u32[24]: magic 0x314B5050, version (2) | wdtype<<16, c_out, c_in,
  *           stride, pad, dilation, n_patterns, group (=8), n_groups,
  *           n_kept, n_wt, off_masks, off_perm, off_codes, off_woff, off_w,
  *           off_bias, total_bytes, 0 x 5
@@ -97,8 +98,9 @@ typedef struct {
  *           padding slots; n_groups = ceil(c_out/8)
  *   codes   u8[n_groups][c_in][8]: pattern id of kernel (perm[8g+s], c) or
  *           0xFF when pruned
- *   woff    u32[n_groups*c_in + 1]: index in w of the first weight of entry
- *           (g, c)
+ *   woff    u32[n_groups*c_in + 1]: entry (g, c) holds in bits 0..23 the
+ *           index in w of its first weight and in bits 24..31 the mask of its
+ *           kept slots (bit s set = slot s kept); the last entry is n_wt
  *   w       fp32 or bf16 [n_wt]: for g, c, slot ascending, kept kernels only,
  *           the pattern's taps in ascending tap order (bf16: each kernel
  *           padded to an even element count with a zero)

@@ -19,7 +19,10 @@ padding bytes are zero):
                                          (0xFFFFFFFF for padding slots)
   codes    u8[n_groups][c_in][8]         pattern id of kernel (perm[8g+s], c),
                                          0xFF if the kernel is pruned
-  woff     u32[n_groups*c_in + 1]        first weight of entry (g, c)
+  woff     u32[n_groups*c_in + 1]        entry (g, c): bits 0..23 index of its
+                                         first weight, bits 24..31 the mask of
+                                         its kept slots (bit s = slot s kept);
+                                         the last entry is n_wt (< 2^24)
   w        f32 or bf16 [n_wt]            for g, c, s ascending, kept kernels
                                          only: the pattern's taps in ascending
                                          tap order (bf16: padded to an even
@@ -41,7 +44,8 @@ import numpy as np
 from . import bf16 as _bf16
 
 MAGIC = 0x314B5050
-VERSION = 1
+VERSION = 2
+MAX_WT = (1 << 24) - 1
 GROUP = 8
 ALIGN = 64
 HEADER_WORDS = 24
@@ -120,12 +124,14 @@ def pack(w, b, pid, conn, lib, stride=1, pad=1, dil=1, wdtype=WD_F32) -> bytes:
     for g in range(n_groups):
         for c in range(c_in):
             woff.append(len(wvals))
+            kept_mask = 0
             for s in range(GROUP):
                 o = perm[GROUP * g + s]
                 if o == NO_FILTER or not conn[o, c]:
                     continue
                 p = int(pid[o, c])
                 codes[(g * c_in + c) * GROUP + s] = p
+                kept_mask |= 1 << s
                 n_kept += 1
                 taps = [t for t in range(9) if (lib[p] >> t) & 1]
                 vals = [wflat[o, c, t] for t in taps]
@@ -136,8 +142,11 @@ def pack(w, b, pid, conn, lib, stride=1, pad=1, dil=1, wdtype=WD_F32) -> bytes:
                     wvals.extend(bits)
                 else:
                     wvals.extend(float(v) for v in vals)
+            woff[-1] |= kept_mask << 24
     woff.append(len(wvals))
     n_wt = len(wvals)
+    if n_wt > MAX_WT:
+        raise ValueError("layer has too many weights for 24-bit offsets")
 
     off_masks = _align(HEADER_WORDS * 4)
     off_perm = _align(off_masks + 2 * n_p)
@@ -184,7 +193,9 @@ def parse(blob: bytes) -> dict:
     d["perm"] = np.frombuffer(blob, "<u4", slots, off_perm).copy()
     d["codes"] = np.frombuffer(blob, "u1", n_groups * c_in * group, off_codes).reshape(
         n_groups, c_in, group).copy()
-    d["woff"] = np.frombuffer(blob, "<u4", n_groups * c_in + 1, off_woff).copy()
+    woff = np.frombuffer(blob, "<u4", n_groups * c_in + 1, off_woff).copy()
+    d["woff"] = woff & np.uint32(MAX_WT)
+    d["kept_mask"] = (woff >> np.uint32(24)).astype(np.uint8)
     if wdtype == WD_BF16:
         d["w"] = _bf16.bits_to_f32(np.frombuffer(blob, "<u2", n_wt, off_w))
     else:

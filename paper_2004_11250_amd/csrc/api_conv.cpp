@@ -93,7 +93,7 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   p.n_patterns = v.n_patterns;
   p.flags = flags;
   const int lib = library_kind(v);
-  const ConvPlan plan = plan_conv(p, lib);
+  const ConvPlan plan = plan_conv(p, lib, act_dtype == PP_BF16);
   hipError_t e = launch_conv(lib, plan, p, act_dtype == PP_BF16, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;

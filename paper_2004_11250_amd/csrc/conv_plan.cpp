@@ -17,17 +17,24 @@ RecipeInfo recipe_info(int id) {
   return RecipeInfo{0, 0, 0, 0, 0, 0};
 }
 
-// same LDS accounting as the kernel: staged halo tile or reduction buffer
-bool recipe_fits(int id, int s, int d) {
+// same LDS accounting as the kernel (Geo in conv_pp_kernel.hpp): fp32 uses
+// double-buffered DMA staging with 64*NW-float channel regions
+bool recipe_fits(int id, int s, int d, bool bf16) {
   const RecipeInfo r = recipe_info(id);
   if (r.r == 0) return false;
   const int lh = 64 / r.lw;
   const int th = lh * r.r, tw = r.lw * r.cc;
   const int tih = (th - 1) * s + 2 * d + 1, tiw = (tw - 1) * s + 2 * d + 1;
   const int lstr = (tiw + 3) / 4 * 4;
-  const long stage = static_cast<long>(r.ws) * r.cpw * tih * lstr;
+  const int nw = r.wf * r.ws, cch = r.ws * r.cpw;
+  const bool dma = !bf16;
+  const int seg = 64 * nw;
+  const int chstr = dma ? (tih * lstr + seg - 1) / seg * seg : tih * lstr;
+  const long buf = static_cast<long>(cch) * chstr;
   const long red = r.ws > 1 ? static_cast<long>(r.ws / 2) * r.wf * 8 * r.r * r.cc * 64 : 0;
-  return (stage > red ? stage : red) * 4 <= 64 * 1024;
+  const long total = (buf > red ? buf : red) + (dma ? buf : 0);
+  const int loads = cch * (chstr / 64 / nw);
+  return total * 4 <= 64 * 1024 && (!dma || loads <= 60);
 }
 
 bool recipe_compiled(int lib, int id) {
@@ -40,10 +47,10 @@ static int env_recipe() {
   return std::atoi(e);
 }
 
-ConvPlan plan_conv(const ConvParams& p, int lib) {
+ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
   ConvPlan plan;
   const int forced = env_recipe();
-  if (forced >= 0 && forced < kNumRecipes && recipe_compiled(lib, forced) && recipe_fits(forced, p.stride, p.dil)) {
+  if (forced >= 0 && forced < kNumRecipes && recipe_compiled(lib, forced) && recipe_fits(forced, p.stride, p.dil, bf16)) {
     plan.recipe = forced;
     return plan;
   }
@@ -59,7 +66,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib) {
     pref[0] = 8; pref[1] = 13; pref[2] = 13; pref[3] = 13;
   }
   for (int id : pref)
-    if (recipe_compiled(lib, id) && recipe_fits(id, p.stride, p.dil)) {
+    if (recipe_compiled(lib, id) && recipe_fits(id, p.stride, p.dil, bf16)) {
       plan.recipe = id;
       return plan;
     }
@@ -77,7 +84,7 @@ static hipError_t launch_lib(int id, const ConvParams& p, hipStream_t st) {
 }
 
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st) {
-  if (!recipe_compiled(lib, plan.recipe) || !recipe_fits(plan.recipe, p.stride, p.dil))
+  if (!recipe_compiled(lib, plan.recipe) || !recipe_fits(plan.recipe, p.stride, p.dil, bf16_act))
     return hipErrorInvalidConfiguration;
   if (bf16_act) {
     if (lib == kLibCanon8) return launch_lib<kLibCanon8, uint16_t>(plan.recipe, p, st);

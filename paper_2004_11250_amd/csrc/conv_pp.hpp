@@ -28,23 +28,29 @@ struct ConvParams {
 // The compiled tilings ("recipes"):
 //   id, R x CC outputs per lane, LW lanes across (64/LW down), WF filter waves
 //   (8 filters each), WS channel-split waves, CPW channels per wave per chunk.
-#define PP_RECIPES(X)        \
-  X(0, 4, 4, 8, 1, 4, 2)     \
-  X(1, 4, 4, 8, 2, 2, 4)     \
-  X(2, 4, 4, 8, 4, 1, 8)     \
-  X(3, 2, 4, 8, 1, 4, 2)     \
-  X(4, 2, 4, 8, 2, 2, 4)     \
-  X(5, 2, 4, 8, 4, 1, 8)     \
-  X(6, 2, 2, 8, 1, 4, 4)     \
-  X(7, 2, 2, 8, 2, 2, 8)     \
-  X(8, 2, 2, 8, 1, 8, 2)     \
-  X(9, 1, 2, 8, 1, 8, 2)     \
-  X(10, 1, 1, 8, 1, 8, 2)    \
-  X(11, 4, 2, 8, 1, 4, 2)    \
-  X(12, 2, 4, 8, 1, 4, 1)    \
-  X(13, 2, 2, 8, 1, 4, 1)
+#define PP_RECIPES(X)       \
+  X(0, 4, 4, 8, 1, 4, 1)    \
+  X(1, 4, 4, 8, 2, 2, 2)    \
+  X(2, 4, 4, 8, 4, 1, 4)    \
+  X(3, 2, 4, 8, 1, 4, 2)    \
+  X(4, 2, 4, 8, 2, 2, 4)    \
+  X(5, 2, 4, 8, 4, 1, 8)    \
+  X(6, 2, 2, 8, 1, 4, 4)    \
+  X(7, 2, 2, 8, 2, 2, 8)    \
+  X(8, 2, 2, 8, 1, 8, 2)    \
+  X(9, 1, 2, 8, 1, 8, 2)    \
+  X(10, 1, 1, 8, 1, 8, 2)   \
+  X(11, 4, 2, 8, 1, 4, 2)   \
+  X(12, 2, 4, 8, 1, 4, 1)   \
+  X(13, 2, 2, 8, 1, 4, 1)   \
+  X(14, 2, 4, 8, 8, 1, 8)   \
+  X(15, 2, 2, 8, 4, 1, 8)   \
+  X(16, 2, 2, 8, 4, 2, 4)   \
+  X(17, 2, 4, 8, 4, 2, 4)   \
+  X(18, 4, 4, 8, 2, 1, 4)   \
+  X(19, 2, 2, 8, 2, 4, 4)
 
-constexpr int kNumRecipes = 14;
+constexpr int kNumRecipes = 20;
 
 struct RecipeInfo {
   int r, cc, lw, wf, ws, cpw;
@@ -52,7 +58,7 @@ struct RecipeInfo {
 
 // geometry of a recipe, and whether its LDS footprint fits for (stride, dilation)
 RecipeInfo recipe_info(int id);
-bool recipe_fits(int id, int stride, int dil);
+bool recipe_fits(int id, int stride, int dil, bool bf16);
 // recipes compiled for a pattern library (the canonical library gets all)
 bool recipe_compiled(int lib, int id);
 
@@ -60,7 +66,7 @@ struct ConvPlan {
   int recipe = 0;
 };
 
-ConvPlan plan_conv(const ConvParams& p, int lib);
+ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16);
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st);
 
 template <int LIB, int S, int D, class TA>

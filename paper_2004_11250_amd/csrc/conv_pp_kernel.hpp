@@ -69,6 +69,13 @@ __device__ __forceinline__ uint32_t to_bf16_bits(float v) {
 // wait until every outstanding LDS and scalar-memory load has returned
 __device__ __forceinline__ void wait_lgkm() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
+// workgroup barrier for LDS hand-off without a memory fence: the caller has
+// already waited for the LDS writes that matter (its own ds ops complete in
+// order; DMA writes via an explicit vmcnt wait)
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 constexpr uint32_t kCanon8[8] = {0x03A, 0x0B2, 0x0B8, 0x09A, 0x01B, 0x036, 0x0D8, 0x1B0};
 
 constexpr int nth_tap(uint32_t mask, int n) {
@@ -149,7 +156,7 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb) {
 }
 
 // compile-time geometry of one tiling
-template <int S, int D, int R, int CC, int LW, int WF, int WS, int CPW>
+template <int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, bool DMA>
 struct Geo {
   static constexpr int LH = 64 / LW;
   static constexpr int TH = LH * R, TW = LW * CC;          // output tile
@@ -158,31 +165,45 @@ struct Geo {
   static constexpr int TIH = (TH - 1) * S + 2 * D + 1;     // input tile rows
   static constexpr int TIW = (TW - 1) * S + 2 * D + 1;     // input tile cols
   static constexpr int LSTR = (TIW + 3) / 4 * 4;           // LDS row stride (floats)
-  static constexpr int CHSTR = TIH * LSTR;                 // LDS channel stride
+  static constexpr int NW = WF * WS;                       // waves per workgroup
   static constexpr int CCH = WS * CPW;                     // channels per chunk
-  static constexpr int NT = WF * WS * 64;
+  // DMA staging writes whole 64-float segments; a channel's region is padded
+  // so that its NQ segments split evenly over the NW waves
+  static constexpr int SEG = 64 * NW;
+  static constexpr int CHSTR = DMA ? (TIH * LSTR + SEG - 1) / SEG * SEG : TIH * LSTR;
+  static constexpr int NQ = CHSTR / 64;                    // DMA segments per channel
+  static constexpr int NQW = NQ / NW;                      // ... per wave
+  static constexpr int LOADS = CCH * NQW;                  // DMA loads per wave per chunk
   static constexpr int NACC = 8 * R * CC;
-  static constexpr int STAGE = CCH * CHSTR;
+  static constexpr int BUF = CCH * CHSTR;                  // one staged chunk
   static constexpr int RED = (WS > 1) ? (WS / 2) * WF * NACC * 64 : 0;
-  static constexpr int LDS_FLOATS = STAGE > RED ? STAGE : RED;
-  static constexpr int STAGE_N = CCH * TIH * TIW;
-  static constexpr int NST = (STAGE_N + NT - 1) / NT;
+  // lds0 = max(chunk, partial-sum exchange); DMA adds a second chunk buffer
+  static constexpr int LDS_FLOATS = (BUF > RED ? BUF : RED) + (DMA ? BUF : 0);
   static constexpr int VW = ((CC * S) % 4 == 0) ? 4 : (((CC * S) % 2 == 0) ? 2 : 1);
   static constexpr int N4 = (VW == 4) ? PC / 4 : 0;
   static constexpr int N2 = (VW >= 2) ? (PC - 4 * N4) / 2 : 0;
   static constexpr int N1 = PC - 4 * N4 - 2 * N2;
-  static constexpr bool fits = LDS_FLOATS * 4 <= 64 * 1024 && LW * LH == 64 && (WS & (WS - 1)) == 0;
+  static constexpr bool fits = LDS_FLOATS * 4 <= 64 * 1024 && LW * LH == 64 && (WS & (WS - 1)) == 0 &&
+                               (!DMA || LOADS <= 60);
 };
 
 template <int LIB, int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, class TA>
 __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
-  using G = Geo<S, D, R, CC, LW, WF, WS, CPW>;
-  constexpr int PR = G::PR, PC = G::PC, TIH = G::TIH, TIW = G::TIW, LSTR = G::LSTR, CHSTR = G::CHSTR;
-  constexpr int CCH = G::CCH, NT = G::NT, NACC = G::NACC, NST = G::NST, STAGE_N = G::STAGE_N;
   constexpr bool WBF = sizeof(TA) == 2;   // bf16 weights with bf16 activations
+  constexpr bool DMA = !WBF;              // fp32: stage with direct buffer->LDS loads
+  using G = Geo<S, D, R, CC, LW, WF, WS, CPW, DMA>;
+  constexpr int PR = G::PR, PC = G::PC, TIH = G::TIH, TIW = G::TIW, LSTR = G::LSTR, CHSTR = G::CHSTR;
+  constexpr int CCH = G::CCH, NACC = G::NACC, NW = G::NW;
   static_assert(G::fits, "tiling does not fit");
 
-  __shared__ __attribute__((aligned(16))) float lds[G::LDS_FLOATS];
+  // DMA path: two distinct LDS arrays (static buffer selection lets the
+  // compiler see that loads into one never alias reads of the other);
+  // lds0 also holds the single buffer of the register path and the
+  // partial-sum exchange of the split-channel waves.
+  constexpr int LDS0 = G::BUF > G::RED ? G::BUF : G::RED;
+  __shared__ __attribute__((aligned(16))) float lds0[LDS0];
+  __shared__ __attribute__((aligned(16))) float lds1[DMA ? G::BUF : 1];
+  float* const lds = lds0;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -206,9 +227,11 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   const TA* __restrict__ x = static_cast<const TA*>(a.x) + static_cast<size_t>(img) * a.c_in * a.h * a.w;
   const uint8_t* blob = a.blob;
   // this image of x as a buffer resource: loads past its end return 0
+  const uint32_t img_bytes = static_cast<uint32_t>(a.c_in) * a.h * a.w * sizeof(TA);
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<TA*>(x), static_cast<short>(0),
-      static_cast<int>(static_cast<uint32_t>(a.c_in) * a.h * a.w * sizeof(TA)), 0x00020000);
+      const_cast<TA*>(x), static_cast<short>(0), static_cast<int>(img_bytes), 0x00020000);
+  const uint32_t chan_bytes = static_cast<uint32_t>(a.h) * a.w * sizeof(TA);
+  const int n_chunks = (a.c_in + CCH - 1) / CCH;
 
   float acc[8][R][CC];
 #pragma unroll
@@ -219,91 +242,110 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       for (int q = 0; q < CC; ++q) acc[s][r][q] = 0.0f;
 
   const int lane_off = (ly * R * S) * LSTR + lx * CC * S;
-  // staging coordinates of this lane
-  constexpr int NW = WF * WS;
-  constexpr int NCB = (TIW + 63) / 64;                  // 64-column blocks of a staged row
-  constexpr int RPW = (CCH * TIH + NW - 1) / NW;        // staged rows per wave
-  uint32_t gxs[NCB];
-  bool col_ok[NCB];
+
+  // ---- staging (fp32): every wave issues segments m = wid + NW*t of every
+  // channel of a chunk; lane l of segment m stages element q = 64m + l of the
+  // channel's LDS region (row q / LSTR, col q % LSTR).  Its byte offset in
+  // the channel is fixed for the whole kernel; padding and out-of-image
+  // elements get an offset past the buffer, which the hardware returns as 0.
+  uint32_t qoff[DMA ? G::NQW : 1];
+  if constexpr (DMA) {
 #pragma unroll
-  for (int m = 0; m < NCB; ++m) {
-    const int gx = ix0 + lane + 64 * m;
-    col_ok[m] = lane + 64 * m < TIW && gx >= 0 && gx < a.w;
-    gxs[m] = col_ok[m] ? static_cast<uint32_t>(gx) : 0u;
+    for (int t = 0; t < G::NQW; ++t) {
+      const int q = 64 * (wid + NW * t) + lane;
+      const int row = q / LSTR, col = q % LSTR;
+      const int gy = iy0 + row, gx = ix0 + col;
+      const bool ok = row < TIH && col < TIW && gy >= 0 && gy < a.h && gx >= 0 && gx < a.w;
+      qoff[t] = ok ? (static_cast<uint32_t>(gy) * a.w + gx) * 4u : 0x80000000u;
+    }
   }
-
-  for (int cb = 0; cb < a.c_in; cb += CCH) {
-
-    __syncthreads();   // the previous chunk's LDS reads are done
-    // ---- stage input channels [cb, cb+CCH) of the halo tile into LDS.
-    // Wave w stages rows [w*RPW, (w+1)*RPW) of the CCH x TIH staged rows
-    // (row coordinates are wave-uniform; staged row r sits at LDS offset
-    // r*LSTR); lanes cover the TIW columns.  All global loads of a lane are
-    // issued before its LDS writes.
-    {
-      // opaque copy of the chunk index: keeps the compiler from hoisting the
-      // per-row bounds tests out of the chunk loop (they would pin ~2 SGPRs
-      // per staged row for the whole kernel)
-      int cbo = cb;
-      asm volatile("" : "+s"(cbo));
-      float v[RPW][NCB];
+  auto stage_dma = [&](int chunk, float* base) {
+    // launder the LDS base: otherwise the compiler hoists all CCH*NQW
+    // destination addresses out of the chunk loop and spills SGPRs
+    asm volatile("" : "+s"(base));
 #pragma unroll
-      for (int k = 0; k < RPW; ++k) {
-        const int row = wid * RPW + k + (cbo - cb);
-        const int ch = row / TIH, i = row % TIH;
-        const int c = cb + ch, gy = iy0 + i;
-        const bool row_ok = row < CCH * TIH && c < a.c_in && gy >= 0 && gy < a.h;   // wave-uniform
-        const uint32_t rbase = (static_cast<uint32_t>(c) * a.h + gy) * static_cast<uint32_t>(a.w);
+    for (int ch = 0; ch < CCH; ++ch) {
+      // channels past c_in read at offset >= the buffer size: zeros
+      const uint32_t cofs = static_cast<uint32_t>(min(chunk * CCH + ch, a.c_in)) * chan_bytes;
 #pragma unroll
-        for (int m = 0; m < NCB; ++m) {
-          // out-of-image elements get an offset past the buffer: the load returns 0
-          const uint32_t off = (row_ok && col_ok[m]) ? (rbase + gxs[m]) * sizeof(TA) : 0x80000000u;
-          if (sizeof(TA) == 2)
-            v[k][m] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(xr, off, 0, 0)) << 16);
-          else
-            v[k][m] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0));
-        }
-        // issue each row's load right after its address arithmetic (the
-        // scheduler would otherwise compute all rows' addresses first and
-        // run out of SGPRs)
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      float* dst = lds + wid * RPW * LSTR + lane;
-#pragma unroll
-      for (int k = 0; k < RPW; ++k) {
-        if (wid * RPW + k + (cbo - cb) < CCH * TIH) {
-#pragma unroll
-          for (int m = 0; m < NCB; ++m)
-            if (lane + 64 * m < TIW) dst[k * LSTR + 64 * m] = v[k][m];
-        }
+      for (int t = 0; t < G::NQW; ++t) {
+        float* dst = base + ch * CHSTR + 64 * (wid + NW * t);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 4, qoff[t],
+                                                 cofs, 0, 0);
       }
     }
-    __syncthreads();
+  };
 
-    // ---- channel loop.  The dispatch code exists once (no unrolling over
-    // channels) to keep the instruction footprint small; latency is hidden
-    // by the other waves of the SIMD.
+  // ---- staging (bf16): wave w stages rows [w*RPW, (w+1)*RPW) of the chunk's
+  // CCH x TIH rows (wave-uniform row coordinates), lanes cover the columns and
+  // convert to fp32; all loads of a lane are issued before its LDS writes.
+  constexpr int NCB = (TIW + 63) / 64;
+  constexpr int RPW = (CCH * TIH + NW - 1) / NW;
+  auto stage_regs = [&](int cb) {
+    // opaque copy of the chunk index: keeps the compiler from hoisting the
+    // per-row arithmetic out of the chunk loop (it would pin ~2 SGPRs per
+    // staged row for the whole kernel)
+    int cbo = cb;
+    asm volatile("" : "+s"(cbo));
+    float v[RPW][NCB];
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+      const int row = wid * RPW + k + (cbo - cb);
+      const int ch = row / TIH, i = row % TIH;
+      const int c = cb + ch, gy = iy0 + i;
+      const bool row_ok = row < CCH * TIH && c < a.c_in && gy >= 0 && gy < a.h;   // wave-uniform
+      const uint32_t rbase = (static_cast<uint32_t>(c) * a.h + gy) * static_cast<uint32_t>(a.w);
+#pragma unroll
+      for (int m = 0; m < NCB; ++m) {
+        const int gx = ix0 + lane + 64 * m;
+        const bool ok = row_ok && lane + 64 * m < TIW && gx >= 0 && gx < a.w;
+        const uint32_t off = ok ? (rbase + gx) * sizeof(TA) : 0x80000000u;
+        if (sizeof(TA) == 2)
+          v[k][m] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(xr, off, 0, 0)) << 16);
+        else
+          v[k][m] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    float* dst = lds + wid * RPW * LSTR + lane;
+#pragma unroll
+    for (int k = 0; k < RPW; ++k) {
+      if (wid * RPW + k + (cbo - cb) < CCH * TIH) {
+#pragma unroll
+        for (int m = 0; m < NCB; ++m)
+          if (lane + 64 * m < TIW) dst[k * LSTR + 64 * m] = v[k][m];
+      }
+    }
+  };
+
+  // ---- one chunk: every kept kernel of this wave's 8 filters on the wave's
+  // CPW channels of the chunk held in LDS buffer `buf`
+  auto compute_chunk = [&](int cb, const float* base) {
     const int cl0 = wk * CPW;
     const int nch = has_grp ? max(0, min(CPW, a.c_in - (cb + cl0))) : 0;   // wave-uniform
-    // code word and weight offset of the first channel; the loop prefetches
-    // those of the next channel
+    // code word and woff of the first channel; the loop prefetches the next
     uint32_t e = static_cast<uint32_t>(has_grp ? grp : 0) * a.c_in + min(cb + cl0, a.c_in - 1);
     uint2 cw_next = sload<uint2>(blob, a.off_codes + 8 * e);
     uint32_t wo_next = sload<uint32_t>(blob, a.off_woff + 4 * e);
 #pragma unroll 1
     for (int k = 0; k < nch; ++k) {
       const uint2 cw = cw_next;
-      const uint32_t wof = min(wo_next, a.n_wt);
+      const uint32_t wo = wo_next;
       if (k + 1 < nch) {
         ++e;
         cw_next = sload<uint2>(blob, a.off_codes + 8 * e);
         wo_next = sload<uint32_t>(blob, a.off_woff + 4 * e);
       }
-      if ((cw.x & cw.y) == 0xFFFFFFFFu) continue;   // no kept kernel in this group-channel
+      const uint32_t kept = wo >> 24;   // bit s: slot s has a kept kernel
+      if (kept == 0) continue;
+      // first weight of the entry, clamped so that every slot's read stays
+      // inside the weight array (plus the >= 32 bytes that follow it)
+      const uint32_t nk4 = static_cast<uint32_t>(__builtin_popcount(kept)) * 4u;
+      const uint32_t w0 = min(wo & 0xFFFFFFu, a.n_wt - min(a.n_wt, nk4));
       // patch: the lane's input neighbourhood for this channel
       float p[PR][PC];
       {
-        const float* src = lds + (cl0 + k) * CHSTR + lane_off;
+        const float* src = base + (cl0 + k) * CHSTR + lane_off;
 #pragma unroll
         for (int r = 0; r < PR; ++r) {
           const float* row = src + r * LSTR;
@@ -322,20 +364,19 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
         }
       }
       if (LIB == kLibCanon8) {
-        // weights of all 8 slots, issued together (kept kernels stored in
-        // slot order, 4 weights each; a pruned slot re-reads its successor's)
+        // weights of all 8 slots, issued together: slot s reads the kernel at
+        // rank popcount(kept & (2^s - 1)) of the entry (4 weights each)
         float4 wv[8];
-        uint32_t kk = wof;
+        const uint32_t wbyte = a.off_w + (WBF ? 2u : 4u) * w0;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-          const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
+          const uint32_t rank = static_cast<uint32_t>(__builtin_popcount(kept & ((1u << s) - 1u)));
           if (WBF) {
-            const uint2 u = sload<uint2>(blob, a.off_w + 2 * min(kk, a.n_wt));
+            const uint2 u = sload<uint2>(blob, wbyte + 8u * rank);
             wv[s] = make_float4(bf16_lo(u.x), bf16_hi(u.x), bf16_lo(u.y), bf16_hi(u.y));
           } else {
-            wv[s] = sload<float4>(blob, a.off_w + 4 * min(kk, a.n_wt));
+            wv[s] = sload<float4>(blob, wbyte + 16u * rank);
           }
-          kk += (pid != 0xFFu) ? 4u : 0u;
         }
         // materialise all weights here: one wait for the whole group-channel
         // instead of a load + wait sunk into every dispatch branch
@@ -343,15 +384,16 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
         for (int s = 0; s < 8; ++s) asm volatile("" ::"s"(wv[s].x), "s"(wv[s].y), "s"(wv[s].z), "s"(wv[s].w));
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
+          if (!((kept >> s) & 1u)) continue;
           const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
           apply_canon8<S, D>(pid, acc[s], p, wv[s].x, wv[s].y, wv[s].z, wv[s].w);
         }
       } else {
-        uint32_t kk = wof;
+        uint32_t kk = w0;
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
+          if (!((kept >> s) & 1u)) continue;
           const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
-          if (pid == 0xFFu) continue;
           if (LIB == kLibDense9) {
             float w9[9];
             if (WBF) {
@@ -390,6 +432,38 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
           }
         }
       }
+    }
+  };
+
+  if constexpr (DMA) {
+    // double-buffered: chunk j+1 streams into one LDS array while chunk j is
+    // computed from the other; two chunks per trip keep the selection static
+    auto step = [&](int j, float* cur, float* nxt) {
+      if (j + 1 < n_chunks) {
+        stage_dma(j + 1, nxt);
+        // vmcnt counts in order: chunk j's loads are done once only chunk
+        // j+1's LOADS remain outstanding
+        __builtin_amdgcn_s_waitcnt((G::LOADS & 15) | ((G::LOADS >> 4) << 14) | 0x0F70);   // vmcnt(LOADS)
+      } else {
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+      }
+      // plain s_barrier: __syncthreads() would also wait for the next
+      // chunk's loads (vmcnt(0)) and serialise staging with compute
+      lds_barrier();
+      compute_chunk(j * CCH, cur);
+      lds_barrier();
+    };
+    stage_dma(0, lds0);
+    for (int j = 0; j < n_chunks; j += 2) {
+      step(j, lds0, lds1);
+      if (j + 1 < n_chunks) step(j + 1, lds1, lds0);
+    }
+  } else {
+    for (int cb = 0; cb < a.c_in; cb += CCH) {
+      __syncthreads();   // the previous chunk's LDS reads are done
+      stage_regs(cb);
+      __syncthreads();
+      compute_chunk(cb, lds0);
     }
   }
 
@@ -480,7 +554,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
 // ---------------------------------------------------------------------------
 template <int LIB, int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, class TA>
 hipError_t launch_tiling(ConvParams p, hipStream_t st) {
-  using G = Geo<S, D, R, CC, LW, WF, WS, CPW>;
+  using G = Geo<S, D, R, CC, LW, WF, WS, CPW, sizeof(TA) == 4>;
   if constexpr (!G::fits) {
     return hipErrorInvalidConfiguration;
   } else {

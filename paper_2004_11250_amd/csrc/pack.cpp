@@ -57,6 +57,7 @@ pp_status parse_blob(const void* blob, size_t bytes, BlobView* v, bool full) {
   if (ng != (c_out + kGroup - 1) / kGroup) return fail(PP_EBLOB, "bad group count");
   const uint64_t slots = ng * kGroup;
   const uint64_t n_wt = h[H_NWT];
+  if (n_wt > kMaxWt) return fail(PP_EBLOB, "n_wt too large");
   const uint64_t wsz = (wd == PP_BF16) ? 2 : 4;
   const uint64_t total = h[H_TOTAL];
   if (total != bytes) return fail(PP_EBLOB, "total_bytes does not match blob size");
@@ -129,16 +130,19 @@ pp_status parse_blob(const void* blob, size_t bytes, BlobView* v, bool full) {
   for (uint64_t e = 0; e < ng * c_in; ++e) {
     uint32_t wo;
     std::memcpy(&wo, v->woff + e, 4);
-    if (wo != pos) return fail(PP_EBLOB, "woff inconsistent with codes");
+    if ((wo & kMaxWt) != pos) return fail(PP_EBLOB, "woff inconsistent with codes");
     const uint64_t g = e / c_in;
+    uint32_t mask = 0;
     for (int s = 0; s < kGroup; ++s) {
       uint8_t p = v->codes[e * kGroup + s];
       if (p == kPruned) continue;
       if (p >= npat) return fail(PP_EBLOB, "pattern id out of range");
       if (g * kGroup + s >= c_out) return fail(PP_EBLOB, "kernel in a padding slot");
       pos += wper[p];
+      mask |= 1u << s;
       ++kept;
     }
+    if ((wo >> 24) != mask) return fail(PP_EBLOB, "kept-slot mask inconsistent with codes");
   }
   uint32_t wend;
   std::memcpy(&wend, v->woff + ng * c_in, 4);
@@ -221,7 +225,7 @@ extern "C" pp_status pp_pack(const pp_layer_desc* d, const float* w, const float
         }
       }
     }
-  if (n_wt > 0xFFFFFFF0ull) return fail(PP_EINVAL, "layer too large for 32-bit weight offsets");
+  if (n_wt > kMaxWt) return fail(PP_EINVAL, "layer has too many weights for 24-bit offsets");
   const uint64_t wsz = bf ? 2 : 4;
   const size_t off_masks = align_up(kHeaderWords * 4);
   const size_t off_perm = align_up(off_masks + 2 * static_cast<size_t>(n_patterns));
@@ -258,7 +262,8 @@ extern "C" pp_status pp_pack(const pp_layer_desc* d, const float* w, const float
   for (int g = 0; g < ng; ++g)
     for (int c = 0; c < c_in; ++c) {
       const size_t e = static_cast<size_t>(g) * c_in + c;
-      put32(b, off_woff + 4 * e, static_cast<uint32_t>(pos));
+      const uint64_t pos0 = pos;
+      uint32_t kept_mask = 0;
       for (int s = 0; s < kGroup; ++s) {
         uint8_t code = kPruned;
         const int slot = g * kGroup + s;
@@ -281,10 +286,12 @@ extern "C" pp_status pp_pack(const pp_layer_desc* d, const float* w, const float
               ++written;
             }
             pos += wper[p];   // bf16 padding element stays zero
+            kept_mask |= 1u << s;
           }
         }
         codes[e * kGroup + s] = code;
       }
+      put32(b, off_woff + 4 * e, static_cast<uint32_t>(pos0) | (kept_mask << 24));
     }
   put32(b, off_woff + 4 * (static_cast<size_t>(ng) * c_in), static_cast<uint32_t>(pos));
   for (int i = 0; i < slots; ++i) {

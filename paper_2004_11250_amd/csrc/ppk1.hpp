@@ -18,7 +18,8 @@
 namespace pp {
 
 constexpr uint32_t kMagic = 0x314B5050u;   // "PPK1"
-constexpr uint32_t kVersion = 1;
+constexpr uint32_t kVersion = 2;
+constexpr uint32_t kMaxWt = (1u << 24) - 1;   // woff keeps the kept-slot mask in bits 24..31
 constexpr int kGroup = 8;                  // filters per slot group
 constexpr int kAlign = 64;                 // section alignment in bytes
 constexpr int kHeaderWords = 24;

@@ -200,7 +200,7 @@ def test_vgg16_full_size_layer_sampled(idx):
 
 
 # every compiled tiling, forced through the PP_RECIPE override of the planner
-RECIPES = list(range(14))
+RECIPES = list(range(20))
 
 
 @pytest.mark.parametrize("recipe", RECIPES)

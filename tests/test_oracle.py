@@ -303,6 +303,7 @@ def test_pack_golden_small():
     assert list(d["perm"]) == g["perm"]
     assert list(d["codes"].ravel()) == g["codes"]
     assert list(d["woff"]) == g["woff"]
+    assert list(d["kept_mask"]) == g["kept_mask"]
     assert list(d["w"]) == g["w"]
     assert list(d["bias"]) == g["bias"]
     assert d["n_kept"] == g["n_kept"][0] and d["n_wt"] == g["n_wt"][0]
@@ -328,6 +329,10 @@ def test_pack_roundtrip_and_structure():
         kept = L["conn"].sum(axis=1)
         assert all(kept[perm[i]] >= kept[perm[i + 1]] for i in range(c_out - 1))
         assert np.all(np.diff(d["woff"].astype(np.int64)) >= 0)
+        for g in range(d["n_groups"]):
+            for c in range(c_in):
+                m = [s for s in range(8) if d["codes"][g, c, s] != ppk1.PRUNED]
+                assert d["kept_mask"][g * c_in + c] == sum(1 << s for s in m)
 
 
 def test_pack_bf16_odd_tap_padding():
