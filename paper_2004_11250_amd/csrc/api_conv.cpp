@@ -46,6 +46,11 @@ pp_status conv_check(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t
   if (static_cast<long long>(n) * v.c_in * h * w > (1LL << 40) ||
       static_cast<long long>(n) * v.c_out * h * w > (1LL << 40))
     return fail(PP_EINVAL, "tensor too large");
+  // the kernels address one image of x through a buffer resource with byte
+  // offsets below 2^31
+  const long long esz = act_dtype == PP_BF16 ? 2 : 4;
+  if (static_cast<long long>(v.c_in) * h * w * esz >= (1LL << 31))
+    return fail(PP_EUNSUPPORTED, "one input image must be smaller than 2 GiB");
   *ho = out_dim(h, v.pad, v.dil, v.stride);
   *wo = out_dim(w, v.pad, v.dil, v.stride);
   return PP_OK;
@@ -90,6 +95,7 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   p.off_perm = v.off_perm;
   p.off_masks = v.off_masks;
   p.n_wt = static_cast<uint32_t>(v.n_wt);
+  p.blob_bytes = static_cast<uint32_t>(v.total);
   p.n_patterns = v.n_patterns;
   p.flags = flags;
   const int lib = library_kind(v);

@@ -18,8 +18,9 @@ RecipeInfo recipe_info(int id) {
 }
 
 // same LDS accounting as the kernel (Geo in conv_pp_kernel.hpp): fp32 uses
-// double-buffered DMA staging with 64*NW-float channel regions
-bool recipe_fits(int id, int s, int d, bool bf16) {
+// double-buffered DMA staging with 64*NW-float channel regions, and the
+// canonical library also stages its group data (metadata + weights)
+bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
   const RecipeInfo r = recipe_info(id);
   if (r.r == 0) return false;
   const int lh = 64 / r.lw;
@@ -28,13 +29,16 @@ bool recipe_fits(int id, int s, int d, bool bf16) {
   const int lstr = (tiw + 3) / 4 * 4;
   const int nw = r.wf * r.ws, cch = r.ws * r.cpw;
   const bool dma = !bf16;
+  const bool ldsw = dma && lib == kLibCanon8;
   const int seg = 64 * nw;
   const int chstr = dma ? (tih * lstr + seg - 1) / seg * seg : tih * lstr;
-  const long buf = static_cast<long>(cch) * chstr;
+  const int wmax = (cch * 32 + 63) / 64 * 64;
+  const long gdata = ldsw ? static_cast<long>(r.wf) * (64 + wmax) : 0;
+  const long buf = static_cast<long>(cch) * chstr + gdata;
   const long red = r.ws > 1 ? static_cast<long>(r.ws / 2) * r.wf * 8 * r.r * r.cc * 64 : 0;
   const long total = (buf > red ? buf : red) + (dma ? buf : 0);
-  const int loads = cch * (chstr / 64 / nw);
-  return total * 4 <= 64 * 1024 && (!dma || loads <= 60);
+  const int loads = cch * (chstr / 64 / nw) + (ldsw ? 1 + wmax / 64 : 0);
+  return total * 4 <= 160 * 1024 && (!dma || loads <= 60) && cch <= 16;
 }
 
 bool recipe_compiled(int lib, int id) {
@@ -50,7 +54,7 @@ static int env_recipe() {
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
   ConvPlan plan;
   const int forced = env_recipe();
-  if (forced >= 0 && forced < kNumRecipes && recipe_compiled(lib, forced) && recipe_fits(forced, p.stride, p.dil, bf16)) {
+  if (forced >= 0 && forced < kNumRecipes && recipe_compiled(lib, forced) && recipe_fits(forced, p.stride, p.dil, bf16, lib)) {
     plan.recipe = forced;
     return plan;
   }
@@ -66,7 +70,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
     pref[0] = 8; pref[1] = 13; pref[2] = 13; pref[3] = 13;
   }
   for (int id : pref)
-    if (recipe_compiled(lib, id) && recipe_fits(id, p.stride, p.dil, bf16)) {
+    if (recipe_compiled(lib, id) && recipe_fits(id, p.stride, p.dil, bf16, lib)) {
       plan.recipe = id;
       return plan;
     }
@@ -84,7 +88,7 @@ static hipError_t launch_lib(int id, const ConvParams& p, hipStream_t st) {
 }
 
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st) {
-  if (!recipe_compiled(lib, plan.recipe) || !recipe_fits(plan.recipe, p.stride, p.dil, bf16_act))
+  if (!recipe_compiled(lib, plan.recipe) || !recipe_fits(plan.recipe, p.stride, p.dil, bf16_act, lib))
     return hipErrorInvalidConfiguration;
   if (bf16_act) {
     if (lib == kLibCanon8) return launch_lib<kLibCanon8, uint16_t>(plan.recipe, p, st);

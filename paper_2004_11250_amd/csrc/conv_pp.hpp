@@ -19,6 +19,7 @@ struct ConvParams {
   int n = 0, h = 0, w = 0, ho = 0, wo = 0;
   int c_in = 0, c_out = 0, pad = 0, stride = 1, dil = 1, n_groups = 0;
   uint32_t off_codes = 0, off_woff = 0, off_w = 0, off_bias = 0, off_perm = 0, off_masks = 0;
+  uint32_t blob_bytes = 0;  // total bytes of the blob (its buffer resource bound)
   uint32_t n_wt = 0;        // weight elements; every weight offset read from the device is clamped to it
   int n_patterns = 0;
   uint32_t flags = 0;
@@ -58,7 +59,7 @@ struct RecipeInfo {
 
 // geometry of a recipe, and whether its LDS footprint fits for (stride, dilation)
 RecipeInfo recipe_info(int id);
-bool recipe_fits(int id, int stride, int dil, bool bf16);
+bool recipe_fits(int id, int stride, int dil, bool bf16, int lib);
 // recipes compiled for a pattern library (the canonical library gets all)
 bool recipe_compiled(int lib, int id);
 

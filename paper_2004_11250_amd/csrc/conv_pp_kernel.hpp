@@ -156,7 +156,7 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb) {
 }
 
 // compile-time geometry of one tiling
-template <int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, bool DMA>
+template <int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, bool DMA, bool LDSW>
 struct Geo {
   static constexpr int LH = 64 / LW;
   static constexpr int TH = LH * R, TW = LW * CC;          // output tile
@@ -175,7 +175,13 @@ struct Geo {
   static constexpr int NQW = NQ / NW;                      // ... per wave
   static constexpr int LOADS = CCH * NQW;                  // DMA loads per wave per chunk
   static constexpr int NACC = 8 * R * CC;
-  static constexpr int BUF = CCH * CHSTR;                  // one staged chunk
+  // group data staged next to the input (canonical library, fp32): per slot
+  // group 64 dwords of metadata (CCH woff entries, then 2*CCH code dwords at
+  // 32) and up to CCH*8 kernels x 4 weights
+  static constexpr int WMAX = (CCH * 32 + 63) / 64 * 64;
+  static constexpr int GDATA = LDSW ? WF * (64 + WMAX) : 0;
+  static constexpr int GLOADS = 1 + WMAX / 64;             // group-data loads per chunk
+  static constexpr int BUF = CCH * CHSTR + GDATA;          // one staged chunk
   static constexpr int RED = (WS > 1) ? (WS / 2) * WF * NACC * 64 : 0;
   // lds0 = max(chunk, partial-sum exchange); DMA adds a second chunk buffer
   static constexpr int LDS_FLOATS = (BUF > RED ? BUF : RED) + (DMA ? BUF : 0);
@@ -183,15 +189,16 @@ struct Geo {
   static constexpr int N4 = (VW == 4) ? PC / 4 : 0;
   static constexpr int N2 = (VW >= 2) ? (PC - 4 * N4) / 2 : 0;
   static constexpr int N1 = PC - 4 * N4 - 2 * N2;
-  static constexpr bool fits = LDS_FLOATS * 4 <= 64 * 1024 && LW * LH == 64 && (WS & (WS - 1)) == 0 &&
-                               (!DMA || LOADS <= 60);
+  static constexpr bool fits = LDS_FLOATS * 4 <= 160 * 1024 && LW * LH == 64 && (WS & (WS - 1)) == 0 &&
+                               (!DMA || LOADS + (LDSW ? GLOADS : 0) <= 60) && CCH <= 16;
 };
 
 template <int LIB, int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, class TA>
 __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   constexpr bool WBF = sizeof(TA) == 2;   // bf16 weights with bf16 activations
   constexpr bool DMA = !WBF;              // fp32: stage with direct buffer->LDS loads
-  using G = Geo<S, D, R, CC, LW, WF, WS, CPW, DMA>;
+  constexpr bool LDSW = DMA && LIB == kLibCanon8;   // code words + weights staged in LDS too
+  using G = Geo<S, D, R, CC, LW, WF, WS, CPW, DMA, LDSW>;
   constexpr int PR = G::PR, PC = G::PC, TIH = G::TIH, TIW = G::TIW, LSTR = G::LSTR, CHSTR = G::CHSTR;
   constexpr int CCH = G::CCH, NACC = G::NACC, NW = G::NW;
   static_assert(G::fits, "tiling does not fit");
@@ -232,6 +239,10 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       const_cast<TA*>(x), static_cast<short>(0), static_cast<int>(img_bytes), 0x00020000);
   const uint32_t chan_bytes = static_cast<uint32_t>(a.h) * a.w * sizeof(TA);
   const int n_chunks = (a.c_in + CCH - 1) / CCH;
+  // the blob as a buffer resource (group-data staging): reads past its end return 0
+  const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(blob), static_cast<short>(0), static_cast<int>(a.blob_bytes), 0x00020000);
+  const int sgrp = has_grp ? grp : 0;   // clamped group for address arithmetic
 
   float acc[8][R][CC];
 #pragma unroll
@@ -274,6 +285,32 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
                                                  cofs, 0, 0);
       }
     }
+  };
+
+  // ---- group data (canonical library, fp32): wave (wf, 0) copies, for its
+  // slot group and the chunk's CCH channels, the woff entries (lanes 0..CCH-1),
+  // the code words (lanes 32..32+2*CCH-1) and the compact weights from index
+  // wstart on (WMAX dwords) into the group's region after the input chunk.
+  auto stage_group = [&](int chunk, float* base, uint32_t wstart) {
+    float* meta = base + CCH * CHSTR + wf * (64 + G::WMAX);
+    asm volatile("" : "+s"(meta));
+    const uint32_t e0 = static_cast<uint32_t>(sgrp) * a.c_in + chunk * CCH;
+    uint32_t off;
+    if (lane < CCH)
+      off = a.off_woff + 4u * (e0 + lane);
+    else if (lane >= 32 && lane < 32 + 2 * CCH)
+      off = a.off_codes + 8u * (e0 + ((lane - 32) >> 1)) + 4u * ((lane - 32) & 1);
+    else
+      off = 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (__attribute__((address_space(3))) void*)meta, 4, off, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < G::WMAX / 64; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (__attribute__((address_space(3))) void*)(meta + 64 + 64 * i), 4,
+                                               a.off_w + 4u * (wstart + 64u * i + lane), 0, 0, 0);
+  };
+  auto chunk_wstart = [&](int chunk) -> uint32_t {   // first weight of (group, chunk)
+    const uint32_t e0 = static_cast<uint32_t>(sgrp) * a.c_in + min(chunk * CCH, a.c_in - 1);
+    return sload<uint32_t>(blob, a.off_woff + 4u * e0) & 0xFFFFFFu;
   };
 
   // ---- staging (bf16): wave w stages rows [w*RPW, (w+1)*RPW) of the chunk's
@@ -320,6 +357,74 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
 
   // ---- one chunk: every kept kernel of this wave's 8 filters on the wave's
   // CPW channels of the chunk held in LDS buffer `buf`
+  auto load_patch = [&](float(&p)[PR][PC], const float* src) {
+#pragma unroll
+    for (int r = 0; r < PR; ++r) {
+      const float* row = src + r * LSTR;
+#pragma unroll
+      for (int i = 0; i < G::N4; ++i) {
+        const float4 v = *reinterpret_cast<const float4*>(row + 4 * i);
+        p[r][4 * i] = v.x; p[r][4 * i + 1] = v.y; p[r][4 * i + 2] = v.z; p[r][4 * i + 3] = v.w;
+      }
+#pragma unroll
+      for (int i = 0; i < G::N2; ++i) {
+        const float2 v = *reinterpret_cast<const float2*>(row + 4 * G::N4 + 2 * i);
+        p[r][4 * G::N4 + 2 * i] = v.x; p[r][4 * G::N4 + 2 * i + 1] = v.y;
+      }
+#pragma unroll
+      for (int i = 0; i < G::N1; ++i) p[r][4 * G::N4 + 2 * G::N2 + i] = row[4 * G::N4 + 2 * G::N2 + i];
+    }
+  };
+
+  // ---- one chunk, canonical library, fp32: everything the channel loop reads
+  // is in LDS (input patch, code words, woff, weights), so its waits are
+  // in-order LDS waits and the next channel's metadata is prefetched.
+  auto compute_chunk_ldsw = [&](int cb, const float* base, uint32_t wstart) {
+    const int cl0 = wk * CPW;
+    const int nch = has_grp ? max(0, min(CPW, a.c_in - (cb + cl0))) : 0;   // wave-uniform
+    if (nch == 0) return;
+    const uint32_t* meta = reinterpret_cast<const uint32_t*>(base + CCH * CHSTR + wf * (64 + G::WMAX));
+    const float* wbuf = base + CCH * CHSTR + wf * (64 + G::WMAX) + 64;
+    uint32_t m_wo = meta[cl0], m_c0 = meta[32 + 2 * cl0], m_c1 = meta[33 + 2 * cl0];
+#pragma unroll 1
+    for (int k = 0; k < nch; ++k) {
+      const uint32_t wo = __builtin_amdgcn_readfirstlane(m_wo);
+      const uint32_t cx = __builtin_amdgcn_readfirstlane(m_c0), cy = __builtin_amdgcn_readfirstlane(m_c1);
+      if (k + 1 < nch) {
+        m_wo = meta[cl0 + k + 1];
+        m_c0 = meta[32 + 2 * (cl0 + k + 1)];
+        m_c1 = meta[33 + 2 * (cl0 + k + 1)];
+      }
+      const uint32_t kept = wo >> 24;   // bit s: slot s has a kept kernel
+      if (kept == 0) continue;
+      // entry's first weight relative to the staged range, clamped so every
+      // read stays inside the group's weight buffer
+      const uint32_t nk4 = static_cast<uint32_t>(__builtin_popcount(kept)) * 4u;
+      const uint32_t rel = min((wo & 0xFFFFFFu) - wstart, static_cast<uint32_t>(G::WMAX) - nk4);
+      float4 wv[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const uint32_t rank = static_cast<uint32_t>(__builtin_popcount(kept & ((1u << s) - 1u)));
+        if ((kept >> s) & 1u)
+          wv[s] = *reinterpret_cast<const float4*>(wbuf + rel + 4u * rank);
+        else
+          wv[s] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      }
+      float p[PR][PC];
+      load_patch(p, base + (cl0 + k) * CHSTR + lane_off);
+      // one wait for the weights and the patch, then the dispatch
+#pragma unroll
+      for (int s = 0; s < 8; ++s) asm volatile("" ::"v"(wv[s].x), "v"(wv[s].y), "v"(wv[s].z), "v"(wv[s].w));
+      const uint2 cw = make_uint2(cx, cy);
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        if (!((kept >> s) & 1u)) continue;
+        const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
+        apply_canon8<S, D>(pid, acc[s], p, wv[s].x, wv[s].y, wv[s].z, wv[s].w);
+      }
+    }
+  };
+
   auto compute_chunk = [&](int cb, const float* base) {
     const int cl0 = wk * CPW;
     const int nch = has_grp ? max(0, min(CPW, a.c_in - (cb + cl0))) : 0;   // wave-uniform
@@ -344,25 +449,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       const uint32_t w0 = min(wo & 0xFFFFFFu, a.n_wt - min(a.n_wt, nk4));
       // patch: the lane's input neighbourhood for this channel
       float p[PR][PC];
-      {
-        const float* src = base + (cl0 + k) * CHSTR + lane_off;
-#pragma unroll
-        for (int r = 0; r < PR; ++r) {
-          const float* row = src + r * LSTR;
-#pragma unroll
-          for (int i = 0; i < G::N4; ++i) {
-            const float4 v = *reinterpret_cast<const float4*>(row + 4 * i);
-            p[r][4 * i] = v.x; p[r][4 * i + 1] = v.y; p[r][4 * i + 2] = v.z; p[r][4 * i + 3] = v.w;
-          }
-#pragma unroll
-          for (int i = 0; i < G::N2; ++i) {
-            const float2 v = *reinterpret_cast<const float2*>(row + 4 * G::N4 + 2 * i);
-            p[r][4 * G::N4 + 2 * i] = v.x; p[r][4 * G::N4 + 2 * i + 1] = v.y;
-          }
-#pragma unroll
-          for (int i = 0; i < G::N1; ++i) p[r][4 * G::N4 + 2 * G::N2 + i] = row[4 * G::N4 + 2 * G::N2 + i];
-        }
-      }
+      load_patch(p, base + (cl0 + k) * CHSTR + lane_off);
       if (LIB == kLibCanon8) {
         // weights of all 8 slots, issued together: slot s reads the kernel at
         // rank popcount(kept & (2^s - 1)) of the entry (4 weights each)
@@ -438,22 +525,43 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   if constexpr (DMA) {
     // double-buffered: chunk j+1 streams into one LDS array while chunk j is
     // computed from the other; two chunks per trip keep the selection static
+    // first weight of the chunk being computed / staged next (group data)
+    uint32_t ws_cur = 0, ws_nxt = 0;
+    const bool gstager = LDSW && wk == 0;   // this wave stages its group's data
     auto step = [&](int j, float* cur, float* nxt) {
       if (j + 1 < n_chunks) {
         stage_dma(j + 1, nxt);
-        // vmcnt counts in order: chunk j's loads are done once only chunk
-        // j+1's LOADS remain outstanding
-        __builtin_amdgcn_s_waitcnt((G::LOADS & 15) | ((G::LOADS >> 4) << 14) | 0x0F70);   // vmcnt(LOADS)
+        if (gstager) {
+          ws_nxt = chunk_wstart(j + 1);
+          stage_group(j + 1, nxt, ws_nxt);
+          // vmcnt counts in order: chunk j's loads are done once only chunk
+          // j+1's loads remain outstanding
+          constexpr int L = G::LOADS + G::GLOADS;
+          __builtin_amdgcn_s_waitcnt((L & 15) | ((L >> 4) << 14) | 0x0F70);   // vmcnt(L)
+        } else {
+          __builtin_amdgcn_s_waitcnt((G::LOADS & 15) | ((G::LOADS >> 4) << 14) | 0x0F70);   // vmcnt(LOADS)
+        }
       } else {
         __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
       }
       // plain s_barrier: __syncthreads() would also wait for the next
       // chunk's loads (vmcnt(0)) and serialise staging with compute
       lds_barrier();
-      compute_chunk(j * CCH, cur);
+      if constexpr (LDSW) {
+        // every wave of the group needs the staged range's start
+        const uint32_t wsc = wk == 0 ? ws_cur : chunk_wstart(j);
+        compute_chunk_ldsw(j * CCH, cur, wsc);
+      } else {
+        compute_chunk(j * CCH, cur);
+      }
       lds_barrier();
+      ws_cur = ws_nxt;
     };
     stage_dma(0, lds0);
+    if (gstager) {
+      ws_cur = chunk_wstart(0);
+      stage_group(0, lds0, ws_cur);
+    }
     for (int j = 0; j < n_chunks; j += 2) {
       step(j, lds0, lds1);
       if (j + 1 < n_chunks) step(j + 1, lds1, lds0);
@@ -554,7 +662,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
 // ---------------------------------------------------------------------------
 template <int LIB, int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, class TA>
 hipError_t launch_tiling(ConvParams p, hipStream_t st) {
-  using G = Geo<S, D, R, CC, LW, WF, WS, CPW, sizeof(TA) == 4>;
+  using G = Geo<S, D, R, CC, LW, WF, WS, CPW, sizeof(TA) == 4, sizeof(TA) == 4 && LIB == kLibCanon8>;
   if constexpr (!G::fits) {
     return hipErrorInvalidConfiguration;
   } else {
