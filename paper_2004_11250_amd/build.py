@@ -28,9 +28,11 @@ ARCH = "gfx950"
 # -structurizecfg-skip-uniform-regions: the pattern dispatch of the pruned
 # conv is a wave-uniform branch tree; left unstructurized it needs no
 # accumulator copies at the joins (the structurized form duplicates them).
+# -simplifycfg-sink-common=false: otherwise the eight pattern cases, which
+# have the same shape, are merged into one FMA block fed by register copies.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature",
              "-Xclang", "-packed-fp32-ops", "-mllvm", "-structurizecfg-skip-uniform-regions",
-             "-Wno-pass-failed", f"-I{INCLUDE}", f"-I{CSRC}"]
+             "-mllvm", "-simplifycfg-sink-common=false", "-Wno-pass-failed", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
 def _run(cmd):

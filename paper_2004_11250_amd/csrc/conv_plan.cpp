@@ -32,13 +32,12 @@ bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
   const bool ldsw = dma && lib == kLibCanon8;
   const int seg = 64 * nw;
   const int chstr = dma ? (tih * lstr + seg - 1) / seg * seg : tih * lstr;
-  const int wmax = (cch * 32 + 63) / 64 * 64;
-  const long gdata = ldsw ? static_cast<long>(r.wf) * (64 + wmax) : 0;
+  const long gdata = ldsw ? static_cast<long>(r.wf) * cch * 32 : 0;
+  const long meta = ldsw ? 4L * r.wf * 64 : 0;
   const long buf = static_cast<long>(cch) * chstr + gdata;
   const long red = r.ws > 1 ? static_cast<long>(r.ws / 2) * r.wf * 8 * r.r * r.cc * 64 : 0;
-  const long total = (buf > red ? buf : red) + (dma ? buf : 0);
-  const int loads = cch * (chstr / 64 / nw) + (ldsw ? 1 + wmax / 64 : 0);
-  return total * 4 <= 160 * 1024 && (!dma || loads <= 60) && cch <= 16;
+  const long total = (buf > red ? buf : red) + (dma ? buf : 0) + meta;
+  return total * 4 <= 160 * 1024 && cch <= 16 && cch % 2 == 0;
 }
 
 bool recipe_compiled(int lib, int id) {

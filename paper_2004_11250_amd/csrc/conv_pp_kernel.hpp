@@ -175,22 +175,23 @@ struct Geo {
   static constexpr int NQW = NQ / NW;                      // ... per wave
   static constexpr int LOADS = CCH * NQW;                  // DMA loads per wave per chunk
   static constexpr int NACC = 8 * R * CC;
-  // group data staged next to the input (canonical library, fp32): per slot
-  // group 64 dwords of metadata (CCH woff entries, then 2*CCH code dwords at
-  // 32) and up to CCH*8 kernels x 4 weights
-  static constexpr int WMAX = (CCH * 32 + 63) / 64 * 64;
-  static constexpr int GDATA = LDSW ? WF * (64 + WMAX) : 0;
-  static constexpr int GLOADS = 1 + WMAX / 64;             // group-data loads per chunk
+  // canonical library, fp32: next to each staged input chunk, the chunk's
+  // weights of every slot group expanded to a fixed [channel][slot][4] layout
+  // (pruned slots zero); the metadata (CCH woff entries, then 2*CCH code
+  // dwords from index 32) sits in a ring of 4 buffers of 64 dwords per group
+  static constexpr int WEXP = CCH * 32;                    // expanded weights per group
+  static constexpr int GDATA = LDSW ? WF * WEXP : 0;
+  static constexpr int META = LDSW ? 4 * WF * 64 : 0;
   static constexpr int BUF = CCH * CHSTR + GDATA;          // one staged chunk
   static constexpr int RED = (WS > 1) ? (WS / 2) * WF * NACC * 64 : 0;
   // lds0 = max(chunk, partial-sum exchange); DMA adds a second chunk buffer
-  static constexpr int LDS_FLOATS = (BUF > RED ? BUF : RED) + (DMA ? BUF : 0);
+  static constexpr int LDS_FLOATS = (BUF > RED ? BUF : RED) + (DMA ? BUF : 0) + META;
   static constexpr int VW = ((CC * S) % 4 == 0) ? 4 : (((CC * S) % 2 == 0) ? 2 : 1);
   static constexpr int N4 = (VW == 4) ? PC / 4 : 0;
   static constexpr int N2 = (VW >= 2) ? (PC - 4 * N4) / 2 : 0;
   static constexpr int N1 = PC - 4 * N4 - 2 * N2;
   static constexpr bool fits = LDS_FLOATS * 4 <= 160 * 1024 && LW * LH == 64 && (WS & (WS - 1)) == 0 &&
-                               (!DMA || LOADS + (LDSW ? GLOADS : 0) <= 60) && CCH <= 16;
+                               CCH <= 16 && CCH % 2 == 0;
 };
 
 template <int LIB, int S, int D, int R, int CC, int LW, int WF, int WS, int CPW, class TA>
@@ -210,6 +211,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   constexpr int LDS0 = G::BUF > G::RED ? G::BUF : G::RED;
   __shared__ __attribute__((aligned(16))) float lds0[LDS0];
   __shared__ __attribute__((aligned(16))) float lds1[DMA ? G::BUF : 1];
+  __shared__ __attribute__((aligned(16))) uint32_t ldsm[LDSW ? G::META : 1];
   float* const lds = lds0;
 
   const int tid = threadIdx.x;
@@ -287,12 +289,11 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
     }
   };
 
-  // ---- group data (canonical library, fp32): wave (wf, 0) copies, for its
-  // slot group and the chunk's CCH channels, the woff entries (lanes 0..CCH-1),
-  // the code words (lanes 32..32+2*CCH-1) and the compact weights from index
-  // wstart on (WMAX dwords) into the group's region after the input chunk.
-  auto stage_group = [&](int chunk, float* base, uint32_t wstart) {
-    float* meta = base + CCH * CHSTR + wf * (64 + G::WMAX);
+  // ---- group data (canonical library, fp32), staged by wave (wf, 0) for its
+  // slot group.  Metadata of a chunk: woff entries in lanes 0..CCH-1, code
+  // dwords in lanes 32..32+2*CCH-1 of one 64-dword DMA.
+  auto stage_meta = [&](int chunk) {
+    uint32_t* meta = ldsm + ((chunk & 3) * WF + wf) * 64;
     asm volatile("" : "+s"(meta));
     const uint32_t e0 = static_cast<uint32_t>(sgrp) * a.c_in + chunk * CCH;
     uint32_t off;
@@ -303,14 +304,29 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
     else
       off = 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (__attribute__((address_space(3))) void*)meta, 4, off, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < G::WMAX / 64; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (__attribute__((address_space(3))) void*)(meta + 64 + 64 * i), 4,
-                                               a.off_w + 4u * (wstart + 64u * i + lane), 0, 0, 0);
   };
-  auto chunk_wstart = [&](int chunk) -> uint32_t {   // first weight of (group, chunk)
-    const uint32_t e0 = static_cast<uint32_t>(sgrp) * a.c_in + min(chunk * CCH, a.c_in - 1);
-    return sload<uint32_t>(blob, a.off_woff + 4u * e0) & 0xFFFFFFu;
+  // Expanded weights of a chunk (its metadata must already be in LDS): DMA
+  // i covers channels 2i, 2i+1; lane l -> channel 2i + l/32, slot (l/4)%8,
+  // tap l%4.  A kept slot's weights sit at rank popcount(kept & (2^s-1)) of
+  // its channel's entry; pruned slots and channels past c_in load zero.
+  auto stage_wexp = [&](int chunk, float* base) {
+    const uint32_t* meta = ldsm + ((chunk & 3) * WF + wf) * 64;
+    float* wdst = base + CCH * CHSTR + wf * G::WEXP;
+    asm volatile("" : "+s"(wdst));
+    const int s = (lane >> 2) & 7, q = lane & 3;
+    uint32_t wo[CCH / 2];
+#pragma unroll
+    for (int i = 0; i < CCH / 2; ++i) wo[i] = meta[2 * i + (lane >> 5)];
+#pragma unroll
+    for (int i = 0; i < CCH / 2; ++i) {
+      const int c = chunk * CCH + 2 * i + (lane >> 5);
+      const uint32_t kmask = wo[i] >> 24;
+      const uint32_t rank = __builtin_popcount(kmask & ((1u << s) - 1u));
+      const bool ok = c < a.c_in && ((kmask >> s) & 1u);
+      const uint32_t off = ok ? a.off_w + 4u * ((wo[i] & 0xFFFFFFu) + 4u * rank + q) : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (__attribute__((address_space(3))) void*)(wdst + 64 * i), 4,
+                                               off, 0, 0, 0);
+    }
   };
 
   // ---- staging (bf16): wave w stages rows [w*RPW, (w+1)*RPW) of the chunk's
@@ -377,14 +393,15 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   };
 
   // ---- one chunk, canonical library, fp32: everything the channel loop reads
-  // is in LDS (input patch, code words, woff, weights), so its waits are
-  // in-order LDS waits and the next channel's metadata is prefetched.
-  auto compute_chunk_ldsw = [&](int cb, const float* base, uint32_t wstart) {
+  // is in LDS -- input patch, metadata, and the weights at fixed
+  // [channel][slot] positions, read only for kept slots
+  auto compute_chunk_ldsw = [&](int j, const float* base) {
+    const int cb = j * CCH;
     const int cl0 = wk * CPW;
     const int nch = has_grp ? max(0, min(CPW, a.c_in - (cb + cl0))) : 0;   // wave-uniform
     if (nch == 0) return;
-    const uint32_t* meta = reinterpret_cast<const uint32_t*>(base + CCH * CHSTR + wf * (64 + G::WMAX));
-    const float* wbuf = base + CCH * CHSTR + wf * (64 + G::WMAX) + 64;
+    const uint32_t* meta = ldsm + ((j & 3) * WF + wf) * 64;
+    const float* wexp = base + CCH * CHSTR + wf * G::WEXP;
     uint32_t m_wo = meta[cl0], m_c0 = meta[32 + 2 * cl0], m_c1 = meta[33 + 2 * cl0];
 #pragma unroll 1
     for (int k = 0; k < nch; ++k) {
@@ -397,30 +414,15 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       }
       const uint32_t kept = wo >> 24;   // bit s: slot s has a kept kernel
       if (kept == 0) continue;
-      // entry's first weight relative to the staged range, clamped so every
-      // read stays inside the group's weight buffer
-      const uint32_t nk4 = static_cast<uint32_t>(__builtin_popcount(kept)) * 4u;
-      const uint32_t rel = min((wo & 0xFFFFFFu) - wstart, static_cast<uint32_t>(G::WMAX) - nk4);
-      float4 wv[8];
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const uint32_t rank = static_cast<uint32_t>(__builtin_popcount(kept & ((1u << s) - 1u)));
-        if ((kept >> s) & 1u)
-          wv[s] = *reinterpret_cast<const float4*>(wbuf + rel + 4u * rank);
-        else
-          wv[s] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      }
       float p[PR][PC];
       load_patch(p, base + (cl0 + k) * CHSTR + lane_off);
-      // one wait for the weights and the patch, then the dispatch
-#pragma unroll
-      for (int s = 0; s < 8; ++s) asm volatile("" ::"v"(wv[s].x), "v"(wv[s].y), "v"(wv[s].z), "v"(wv[s].w));
-      const uint2 cw = make_uint2(cx, cy);
+      const float4* wc = reinterpret_cast<const float4*>(wexp + (cl0 + k) * 32);
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         if (!((kept >> s) & 1u)) continue;
-        const uint32_t pid = ((s < 4 ? cw.x : cw.y) >> (8 * (s & 3))) & 0xFFu;
-        apply_canon8<S, D>(pid, acc[s], p, wv[s].x, wv[s].y, wv[s].z, wv[s].w);
+        const float4 w = wc[s];
+        const uint32_t pid = ((s < 4 ? cx : cy) >> (8 * (s & 3))) & 0xFFu;
+        apply_canon8<S, D>(pid, acc[s], p, w.x, w.y, w.z, w.w);
       }
     }
   };
@@ -524,44 +526,36 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
 
   if constexpr (DMA) {
     // double-buffered: chunk j+1 streams into one LDS array while chunk j is
-    // computed from the other; two chunks per trip keep the selection static
-    // first weight of the chunk being computed / staged next (group data)
-    uint32_t ws_cur = 0, ws_nxt = 0;
+    // computed from the other (two chunks per trip keep the selection
+    // static).  Step j: wait for everything issued so far (chunk j's input
+    // and group data), one barrier (chunk j visible; chunk j-1 no longer
+    // read), issue chunk j+1 (and the metadata of chunk j+3), compute j.
     const bool gstager = LDSW && wk == 0;   // this wave stages its group's data
-    auto step = [&](int j, float* cur, float* nxt) {
+    if (gstager) {
+      stage_meta(0);
+      if (1 < n_chunks) stage_meta(1);
+      if (2 < n_chunks) stage_meta(2);
+      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): metadata of chunks 0..2
+    }
+    stage_dma(0, lds0);
+    if (gstager) stage_wexp(0, lds0);
+    auto step = [&](int j, const float* cur, float* nxt) {
+      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+      // plain s_barrier: __syncthreads() would make the compiler wait for
+      // memory operations that are intentionally still in flight
+      lds_barrier();
       if (j + 1 < n_chunks) {
         stage_dma(j + 1, nxt);
         if (gstager) {
-          ws_nxt = chunk_wstart(j + 1);
-          stage_group(j + 1, nxt, ws_nxt);
-          // vmcnt counts in order: chunk j's loads are done once only chunk
-          // j+1's loads remain outstanding
-          constexpr int L = G::LOADS + G::GLOADS;
-          __builtin_amdgcn_s_waitcnt((L & 15) | ((L >> 4) << 14) | 0x0F70);   // vmcnt(L)
-        } else {
-          __builtin_amdgcn_s_waitcnt((G::LOADS & 15) | ((G::LOADS >> 4) << 14) | 0x0F70);   // vmcnt(LOADS)
+          stage_wexp(j + 1, nxt);
+          if (j + 3 < n_chunks) stage_meta(j + 3);
         }
-      } else {
-        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
       }
-      // plain s_barrier: __syncthreads() would also wait for the next
-      // chunk's loads (vmcnt(0)) and serialise staging with compute
-      lds_barrier();
-      if constexpr (LDSW) {
-        // every wave of the group needs the staged range's start
-        const uint32_t wsc = wk == 0 ? ws_cur : chunk_wstart(j);
-        compute_chunk_ldsw(j * CCH, cur, wsc);
-      } else {
+      if constexpr (LDSW)
+        compute_chunk_ldsw(j, cur);
+      else
         compute_chunk(j * CCH, cur);
-      }
-      lds_barrier();
-      ws_cur = ws_nxt;
     };
-    stage_dma(0, lds0);
-    if (gstager) {
-      ws_cur = chunk_wstart(0);
-      stage_group(0, lds0, ws_cur);
-    }
     for (int j = 0; j < n_chunks; j += 2) {
       step(j, lds0, lds1);
       if (j + 1 < n_chunks) step(j + 1, lds1, lds0);
