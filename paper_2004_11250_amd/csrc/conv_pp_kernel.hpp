@@ -76,6 +76,14 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// LDS pointers as 32-bit LDS byte addresses and back
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+template <class T>
+__device__ __forceinline__ uint32_t lds_addr(T* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) T*)p));
+}
+__device__ __forceinline__ lds_void_ptr lds_ptr(uint32_t a) { return (lds_void_ptr)(uintptr_t)a; }
+
 constexpr uint32_t kCanon8[8] = {0x03A, 0x0B2, 0x0B8, 0x09A, 0x01B, 0x036, 0x0D8, 0x1B0};
 
 constexpr int nth_tap(uint32_t mask, int n) {
@@ -272,29 +280,29 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       qoff[t] = ok ? (static_cast<uint32_t>(gy) * a.w + gx) * 4u : 0x80000000u;
     }
   }
-  auto stage_dma = [&](int chunk, float* base) {
-    // launder the LDS base: otherwise the compiler hoists all CCH*NQW
-    // destination addresses out of the chunk loop and spills SGPRs
-    asm volatile("" : "+s"(base));
+  auto stage_dma = [&](int chunk, float* base) __attribute__((always_inline)) {
+    // launder the LDS base (as a 32-bit LDS address): otherwise the compiler
+    // hoists all CCH*NQW destination addresses out of the chunk loop and
+    // spills SGPRs
+    uint32_t lb = lds_addr(base);
+    asm volatile("" : "+s"(lb));
 #pragma unroll
     for (int ch = 0; ch < CCH; ++ch) {
       // channels past c_in read at offset >= the buffer size: zeros
       const uint32_t cofs = static_cast<uint32_t>(min(chunk * CCH + ch, a.c_in)) * chan_bytes;
 #pragma unroll
-      for (int t = 0; t < G::NQW; ++t) {
-        float* dst = base + ch * CHSTR + 64 * (wid + NW * t);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (__attribute__((address_space(3))) void*)dst, 4, qoff[t],
-                                                 cofs, 0, 0);
-      }
+      for (int t = 0; t < G::NQW; ++t)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, lds_ptr(lb + 4u * (ch * CHSTR + 64 * (wid + NW * t))), 4,
+                                                 qoff[t], cofs, 0, 0);
     }
   };
 
   // ---- group data (canonical library, fp32), staged by wave (wf, 0) for its
   // slot group.  Metadata of a chunk: woff entries in lanes 0..CCH-1, code
   // dwords in lanes 32..32+2*CCH-1 of one 64-dword DMA.
-  auto stage_meta = [&](int chunk) {
-    uint32_t* meta = ldsm + ((chunk & 3) * WF + wf) * 64;
-    asm volatile("" : "+s"(meta));
+  auto stage_meta = [&](int chunk) __attribute__((always_inline)) {
+    uint32_t mb = lds_addr(ldsm + ((chunk & 3) * WF + wf) * 64);
+    asm volatile("" : "+s"(mb));
     const uint32_t e0 = static_cast<uint32_t>(sgrp) * a.c_in + chunk * CCH;
     uint32_t off;
     if (lane < CCH)
@@ -303,16 +311,16 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       off = a.off_codes + 8u * (e0 + ((lane - 32) >> 1)) + 4u * ((lane - 32) & 1);
     else
       off = 0x80000000u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (__attribute__((address_space(3))) void*)meta, 4, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(br, lds_ptr(mb), 4, off, 0, 0, 0);
   };
   // Expanded weights of a chunk (its metadata must already be in LDS): DMA
   // i covers channels 2i, 2i+1; lane l -> channel 2i + l/32, slot (l/4)%8,
   // tap l%4.  A kept slot's weights sit at rank popcount(kept & (2^s-1)) of
   // its channel's entry; pruned slots and channels past c_in load zero.
-  auto stage_wexp = [&](int chunk, float* base) {
+  auto stage_wexp = [&](int chunk, float* base) __attribute__((always_inline)) {
     const uint32_t* meta = ldsm + ((chunk & 3) * WF + wf) * 64;
-    float* wdst = base + CCH * CHSTR + wf * G::WEXP;
-    asm volatile("" : "+s"(wdst));
+    uint32_t wb = lds_addr(base + CCH * CHSTR + wf * G::WEXP);
+    asm volatile("" : "+s"(wb));
     const int s = (lane >> 2) & 7, q = lane & 3;
     uint32_t wo[CCH / 2];
 #pragma unroll
@@ -324,8 +332,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       const uint32_t rank = __builtin_popcount(kmask & ((1u << s) - 1u));
       const bool ok = c < a.c_in && ((kmask >> s) & 1u);
       const uint32_t off = ok ? a.off_w + 4u * ((wo[i] & 0xFFFFFFu) + 4u * rank + q) : 0x80000000u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(br, (__attribute__((address_space(3))) void*)(wdst + 64 * i), 4,
-                                               off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(br, lds_ptr(wb + 4u * 64 * i), 4, off, 0, 0, 0);
     }
   };
 
@@ -334,7 +341,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   // convert to fp32; all loads of a lane are issued before its LDS writes.
   constexpr int NCB = (TIW + 63) / 64;
   constexpr int RPW = (CCH * TIH + NW - 1) / NW;
-  auto stage_regs = [&](int cb) {
+  auto stage_regs = [&](int cb) __attribute__((always_inline)) {
     // opaque copy of the chunk index: keeps the compiler from hoisting the
     // per-row arithmetic out of the chunk loop (it would pin ~2 SGPRs per
     // staged row for the whole kernel)
@@ -373,7 +380,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
 
   // ---- one chunk: every kept kernel of this wave's 8 filters on the wave's
   // CPW channels of the chunk held in LDS buffer `buf`
-  auto load_patch = [&](float(&p)[PR][PC], const float* src) {
+  auto load_patch = [&](float(&p)[PR][PC], const float* src) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < PR; ++r) {
       const float* row = src + r * LSTR;
@@ -395,7 +402,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   // ---- one chunk, canonical library, fp32: everything the channel loop reads
   // is in LDS -- input patch, metadata, and the weights at fixed
   // [channel][slot] positions, read only for kept slots
-  auto compute_chunk_ldsw = [&](int j, const float* base) {
+  auto compute_chunk_ldsw = [&](int j, const float* base) __attribute__((always_inline)) {
     const int cb = j * CCH;
     const int cl0 = wk * CPW;
     const int nch = has_grp ? max(0, min(CPW, a.c_in - (cb + cl0))) : 0;   // wave-uniform
@@ -427,7 +434,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
     }
   };
 
-  auto compute_chunk = [&](int cb, const float* base) {
+  auto compute_chunk = [&](int cb, const float* base) __attribute__((always_inline)) {
     const int cl0 = wk * CPW;
     const int nch = has_grp ? max(0, min(CPW, a.c_in - (cb + cl0))) : 0;   // wave-uniform
     // code word and woff of the first channel; the loop prefetches the next
@@ -539,7 +546,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
     }
     stage_dma(0, lds0);
     if (gstager) stage_wexp(0, lds0);
-    auto step = [&](int j, const float* cur, float* nxt) {
+    auto step = [&](int j, const float* cur, float* nxt) __attribute__((always_inline)) {
       __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
       // plain s_barrier: __syncthreads() would make the compiler wait for
       // memory operations that are intentionally still in flight
