@@ -81,6 +81,116 @@ def surviving_macs(op, prm, oshape, batch):
     return 0
 
 
+KERNEL_SOURCES = ("conv_pp_kernel.hpp", "conv_pp_inst.hpp", "conv_pp.hpp", "conv_plan.cpp", "conv_pp_c8_s1d1.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pp_conv3x3_vgg16_224x224_b1_traffic.json")
+
+
+def kernel_source_hash():
+    """sha256 over the sources of the pruned-conv kernel and its planner: a
+    stored byte count is valid only for the code it was measured on."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2004_11250_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _kernel_label(name):
+    """Kernel name without 'void ' and without its parameter list."""
+    name = name.replace("void ", "")
+    return name[:name.rfind("(")] if name.endswith(")") else name
+
+
+def summarize_profile(root, cfg=2):
+    """Summarise rocprofv3 CSV output under ``root`` (kt/: --kernel-trace
+    --stats; fetch/, write/: --pmc FETCH_SIZE / WRITE_SIZE of a run with
+    --copy-mib; sq*/: other --pmc passes) for one frame of the network: the
+    dispatches of the first frame are the len(ops) dispatches starting at the
+    first pruned-conv launch.  Writes the traffic JSON read by the benchmark
+    and prints a markdown summary."""
+    import csv
+    import glob
+
+    import workloads
+    spec = workloads.net_spec(cfg)
+    n_ops = len(spec["ops"])
+    shapes = layer_shapes(spec)
+
+    def rows(sub):
+        f = glob.glob(os.path.join(root, sub, "*_counter_collection.csv")) or \
+            glob.glob(os.path.join(root, sub, "*_kernel_trace.csv"))
+        return list(csv.DictReader(open(f[0]))) if f else []
+
+    def by_dispatch(rs):
+        d = {}
+        for r in rs:
+            e = d.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "grid": r.get("Grid_Size") or
+                                                     r.get("Grid_Size_X"), "c": {}})
+            e["dur_ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            if "Counter_Name" in r:
+                e["c"][r["Counter_Name"]] = e["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        return [d[k] for k in sorted(d)]
+
+    def frames(ds):
+        first = next(i for i, e in enumerate(ds) if "pp_conv3x3_kernel" in e["name"])
+        out = []
+        while first + n_ops <= len(ds) and "pp_conv3x3_kernel" in ds[first]["name"]:
+            out.append(ds[first:first + n_ops])
+            first += n_ops
+            if len(out) == 3:
+                break
+        return out
+
+    def calib(ds, counter, mib):
+        # the elementwise copy: the largest grid among the non-library kernels
+        # before the first frame, reads and writes exactly mib MiB
+        first = next(i for i, e in enumerate(ds) if "pp_conv3x3_kernel" in e["name"])
+        cands = [e for e in ds[:first] if "mul" in e["name"].lower() or "elementwise" in e["name"].lower()]
+        e = max(cands, key=lambda e: int(e["grid"]))
+        return mib * 1024.0 / e["c"][counter], e["c"][counter]
+
+    kt = by_dispatch(rows("kt"))
+    fe = by_dispatch(rows("fetch"))
+    wr = by_dispatch(rows("write"))
+    kt_fr, fe_fr, wr_fr = frames(kt), frames(fe), frames(wr)
+    ff, f_raw = calib(fe, "FETCH_SIZE", 256)
+    wf, w_raw = calib(wr, "WRITE_SIZE", 256)
+    sq = {}
+    for sub in sorted(os.listdir(root)):
+        if sub.startswith("sq") and os.path.isdir(os.path.join(root, sub)):
+            for fr in frames(by_dispatch(rows(sub)))[:1]:
+                for i, e in enumerate(fr):
+                    sq.setdefault(i, {}).update(e["c"])
+    lay = []
+    for i, (k, op, ish, osh) in enumerate(shapes):
+        dur = sum(f[i]["dur_ns"] for f in kt_fr) / len(kt_fr) / 1e3
+        fetch = sum(f[i]["c"]["FETCH_SIZE"] for f in fe_fr) / len(fe_fr) * ff * 1024
+        write = sum(f[i]["c"]["WRITE_SIZE"] for f in wr_fr) / len(wr_fr) * wf * 1024
+        lay.append(dict(op=i, kind=op["op"], lib=op.get("lib", ""), c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
+                        kernel=_kernel_label(kt_fr[0][i]["name"]), us=round(dur, 3),
+                        fetch_mb=round(fetch / 1e6, 3), write_mb=round(write / 1e6, 3), sq=sq.get(i, {})))
+    pr = [l for l in lay if l["kind"] == "conv3" and l["lib"] == "canon8"]
+    traffic = dict(kernel_source_sha256=kernel_source_hash(), fetch_factor=round(ff, 4), write_factor=round(wf, 4),
+                   launches=len(pr), bytes_per_frame=int(sum((l["fetch_mb"] + l["write_mb"]) * 1e6 for l in pr)),
+                   us_per_frame=round(sum(l["us"] for l in pr), 3),
+                   layers=[{k: v for k, v in l.items() if k != "sq"} for l in pr])
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(traffic, fh, indent=1)
+    print(f"calibration: 256 MiB elementwise copy reads FETCH_SIZE={f_raw:.0f} KiB (factor {ff:.4f}), "
+          f"WRITE_SIZE={w_raw:.0f} KiB (factor {wf:.4f})\n")
+    sqk = sorted({c for l in lay for c in l["sq"]})
+    print("| op | kind | lib | c_in->c_out | out | kernel | us (trace) | HBM read MB | HBM write MB | " +
+          " | ".join(sqk) + " |")
+    print("|" + "---|" * (9 + len(sqk)))
+    for l in lay:
+        print(f"| {l['op']} | {l['kind']} | {l['lib']} | {l['c_in']}->{l['c_out']} | {l['hw']} | {l['kernel']} | "
+              f"{l['us']} | {l['fetch_mb']} | {l['write_mb']} | " +
+              " | ".join(f"{l['sq'].get(c, 0):.4g}" for c in sqk) + " |")
+    print(f"\npattern-pruned launches per frame: {len(pr)}, {traffic['us_per_frame']} us, "
+          f"{traffic['bytes_per_frame'] / 1e6:.2f} MB HBM traffic")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -91,7 +201,15 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparator")
     ap.add_argument("--layer-steps", type=int, default=100)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="first run one elementwise fp32 copy of this many MiB (reads and writes exactly that "
+                         "much), the reference for scaling hardware byte counters")
+    ap.add_argument("--summarize-profile", metavar="DIR", default=None,
+                    help="summarise rocprofv3 output under DIR (no GPU needed) and exit")
     args = ap.parse_args()
+    if args.summarize_profile:
+        summarize_profile(args.summarize_profile, args.config)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
               file=sys.stderr)
@@ -120,6 +238,14 @@ def main():
     ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
     y = torch.empty(oshape, dtype=tdt, device=dev)
     stream = torch.cuda.current_stream()
+
+    if args.copy_mib > 0:
+        n = args.copy_mib * (1 << 20) // 4
+        ca = torch.rand(n, device=dev)
+        cb = torch.empty_like(ca)
+        torch.mul(ca, 1.0, out=cb)
+        torch.cuda.synchronize()
+        del ca, cb
 
     # ---- whole-frame timing
     for _ in range(args.warmup):
@@ -170,8 +296,14 @@ def main():
     pr_macs = sum(l["surviving_mmac"] for l in pr) * 1e6
     pr_us = sum(l["us"] for l in pr)
     achieved = 2 * pr_macs / (pr_us * 1e-6) / 1e12 if pr_us else 0.0
+    traffic = None
+    if cfg == 2 and dtype == "f32" and os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+        if t.get("kernel_source_sha256") == kernel_source_hash():
+            traffic = t["bytes_per_frame"]
     roofline = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS, unit="TFLOP/s",
-                    frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), traffic=None,
+                    frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), traffic=traffic,
                     kernel="pp_conv3x3_kernel (pattern-pruned layers, summed over the frame)",
                     scalar_fma_peak=PEAK_FP32_SCALAR_FMA_TFLOPS)
 

@@ -59,7 +59,19 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
   }
   const long pix = static_cast<long>(p.ho) * p.wo;
   int pref[4];
-  if (pix >= 100L * 100L) {
+  if (lib == kLibCanon8 && !bf16 && p.stride == 1) {
+    // fp32 canonical library, from timings of every tiling on the VGG-16
+    // layer shapes (MI355X)
+    if (pix >= 160L * 160L) {
+      pref[0] = 17; pref[1] = 16; pref[2] = 4; pref[3] = 13;
+    } else if (pix >= 80L * 80L) {
+      pref[0] = 19; pref[1] = 3; pref[2] = 13; pref[3] = 13;
+    } else if (pix >= 20L * 20L) {
+      pref[0] = 8; pref[1] = 19; pref[2] = 6; pref[3] = 13;
+    } else {
+      pref[0] = 10; pref[1] = 9; pref[2] = 8; pref[3] = 13;
+    }
+  } else if (pix >= 100L * 100L) {
     pref[0] = 0; pref[1] = 3; pref[2] = 12; pref[3] = 13;
   } else if (pix >= 40L * 40L) {
     pref[0] = 3; pref[1] = 12; pref[2] = 13; pref[3] = 13;
