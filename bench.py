@@ -30,8 +30,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-PEAK_FP32_VECTOR_TFLOPS = 157.3     # MI355X: 256 CU x 2.4 GHz x 256 FLOP/clk (packed fp32)
-PEAK_FP32_SCALAR_FMA_TFLOPS = 78.6  # same without packed fp32 (128 FLOP/clk/CU)
+PEAK_FP32_VECTOR_TFLOPS = 157.3     # MI355X: 256 CU x 2.4 GHz x 256 FLOP/clk; plain (non-packed) wave64
+                                    # v_fmac_f32 issues every 2 cycles per SIMD on gfx950, so this is the
+                                    # FMA peak of the kernels here (built without packed FP32)
 PEAK_HBM_GBS = 8000.0
 
 WORKLOADS = {2: "vgg16_conv_stack_224x224_b1", 3: "style_transfer_512x512_b1", 4: "super_resolution_270x480_x4_b1",
@@ -304,8 +305,7 @@ def main():
             traffic = t["bytes_per_frame"]
     roofline = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS, unit="TFLOP/s",
                     frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), traffic=traffic,
-                    kernel="pp_conv3x3_kernel (pattern-pruned layers, summed over the frame)",
-                    scalar_fma_peak=PEAK_FP32_SCALAR_FMA_TFLOPS)
+                    kernel="pattern-pruned 3x3 conv kernels (the 12 pruned layers, summed over the frame)")
 
     # ---- dense comparator: the same masked model as dense convs (torch / MIOpen)
     dense = None

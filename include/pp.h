@@ -142,6 +142,17 @@ pp_status pp_conv2d_fwd(const void* h_blob, size_t blob_bytes, const void* d_blo
                         const void* x, void* y, int32_t n, int32_t h, int32_t w,
                         int32_t act_dtype, uint32_t flags, void* hip_stream);
 
+/*
+ * pp_conv2d_recipe -- the GPU tiling ("recipe" id) pp_conv2d_fwd uses for
+ * this layer, batch and input size (informational: lets callers and tests
+ * see which compiled kernel runs).  The environment variable PP_RECIPE=<id>
+ * forces a tiling when it can run the layer; otherwise the planner's choice
+ * is reported.  Host-only.  Errors: as pp_conv2d_out_size, PP_EINVAL (recipe
+ * NULL, act_dtype), PP_EUNSUPPORTED.
+ */
+pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
+                           int32_t act_dtype, int32_t* recipe);
+
 /* pp_conv2d_out_size -- h_out, w_out of a packed layer for an h x w input. */
 pp_status pp_conv2d_out_size(const void* h_blob, size_t blob_bytes, int32_t h, int32_t w,
                              int32_t* h_out, int32_t* w_out);

@@ -24,8 +24,8 @@ PP_RELU = 1
 (OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
 
 # exported symbols declared in include/pp.h
-SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_out_size", "pp_net_workspace",
-           "pp_net_fwd", "pp_status_str", "pp_last_error")
+SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_recipe", "pp_conv2d_out_size",
+           "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error")
 
 
 class PPError(RuntimeError):
@@ -66,6 +66,7 @@ def load_library(path: str = LIB_PATH):
                                  ctypes.POINTER(ctypes.c_int64)]
     lib.pp_conv2d_fwd.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp]
     lib.pp_conv2d_out_size.argtypes = [vp, sz, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.pp_conv2d_recipe.argtypes = [vp, sz, i32, i32, i32, i32, ctypes.POINTER(i32)]
     lib.pp_net_workspace.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
                                      ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.pp_net_fwd.argtypes = [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp]
@@ -132,6 +133,15 @@ def out_size(blob, h, w):
     _check(lib.pp_conv2d_out_size(_ptr(blob), blob.nbytes, h, w, ctypes.byref(ho), ctypes.byref(wo)),
            "pp_conv2d_out_size")
     return ho.value, wo.value
+
+
+def conv2d_recipe(blob, n, h, w, act_dtype=PP_F32) -> int:
+    """Tiling id that pp_conv2d_fwd uses for this layer and input shape."""
+    lib = load_library()
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    r = ctypes.c_int32(-1)
+    _check(lib.pp_conv2d_recipe(_ptr(blob), blob.nbytes, n, h, w, act_dtype, ctypes.byref(r)), "pp_conv2d_recipe")
+    return r.value
 
 
 # ---------------------------------------------------------------------------

@@ -56,6 +56,8 @@ pp_status conv_check(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t
   return PP_OK;
 }
 
+ConvParams layer_params(const BlobView& v, int32_t n, int32_t h, int32_t w, int ho, int wo);
+
 pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
                        int32_t w, int32_t act_dtype, uint32_t flags, hipStream_t st) {
   int ho = 0, wo = 0;
@@ -73,10 +75,22 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   if (xb < yb + ybytes && yb < xb + xbytes) return fail(PP_EINVAL, "x and y overlap");
   if (flags & ~static_cast<uint32_t>(PP_RELU)) return fail(PP_EINVAL, "unknown flags");
 
-  ConvParams p;
+  ConvParams p = layer_params(v, n, h, w, ho, wo);
   p.blob = static_cast<const uint8_t*>(d_blob);
   p.x = x;
   p.y = y;
+  p.flags = flags;
+  const int lib = library_kind(v);
+  const ConvPlan plan = plan_conv(p, lib, act_dtype == PP_BF16);
+  hipError_t e = launch_conv(lib, plan, p, act_dtype == PP_BF16, st);
+  if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
+  return PP_OK;
+}
+
+// launch parameters of one layer for an n x c_in x h x w input (device
+// pointers and flags are set by the caller)
+ConvParams layer_params(const BlobView& v, int32_t n, int32_t h, int32_t w, int ho, int wo) {
+  ConvParams p;
   p.n = n;
   p.h = h;
   p.w = w;
@@ -97,12 +111,7 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   p.n_wt = static_cast<uint32_t>(v.n_wt);
   p.blob_bytes = static_cast<uint32_t>(v.total);
   p.n_patterns = v.n_patterns;
-  p.flags = flags;
-  const int lib = library_kind(v);
-  const ConvPlan plan = plan_conv(p, lib, act_dtype == PP_BF16);
-  hipError_t e = launch_conv(lib, plan, p, act_dtype == PP_BF16, st);
-  if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
-  return PP_OK;
+  return p;
 }
 
 }  // namespace pp
@@ -120,6 +129,21 @@ extern "C" pp_status pp_conv2d_out_size(const void* h_blob, size_t blob_bytes, i
   if (hn < 0 || wn < 0) return fail(PP_EINVAL, "input smaller than the dilated kernel");
   if (h_out) *h_out = static_cast<int32_t>(hn / v.stride + 1);
   if (w_out) *w_out = static_cast<int32_t>(wn / v.stride + 1);
+  return PP_OK;
+}
+
+extern "C" pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
+                                      int32_t act_dtype, int32_t* recipe) {
+  clear_error();
+  BlobView v;
+  pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
+  if (s != PP_OK) return s;
+  if (!recipe) return fail(PP_EINVAL, "recipe is NULL");
+  int ho = 0, wo = 0;
+  s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
+  if (s != PP_OK) return s;
+  const ConvParams p = layer_params(v, n, h, w, ho, wo);
+  *recipe = plan_conv(p, library_kind(v), act_dtype == PP_BF16).recipe;
   return PP_OK;
 }
 

@@ -13,16 +13,28 @@ RecipeInfo recipe_info(int id) {
     return RecipeInfo{R, CC, LW, WF, WS, CPW};
     PP_RECIPES(PP_X)
 #undef PP_X
+#define PP_W(ID, R, CC, LW, WS) \
+  case ID:                      \
+    return RecipeInfo{R, CC, LW, 1, WS, 0};
+    PP_WRECIPES(PP_W)
+#undef PP_W
   }
   return RecipeInfo{0, 0, 0, 0, 0, 0};
 }
 
-// same LDS accounting as the kernel (Geo in conv_pp_kernel.hpp): fp32 uses
-// double-buffered DMA staging with 64*NW-float channel regions, and the
-// canonical library also stages its group data (metadata + weights)
+static bool is_wave_recipe(int id) { return id >= kFirstWaveRecipe && id < kNumRecipes; }
+
+// LDS accounting of the wave-pipeline kernel (shared with WGeo in conv_pp_wave.hpp)
+static bool wave_recipe_fits(const RecipeInfo& r, int s, int d, int lib, bool bf16) {
+  const int warea = lib == kLibDense9 ? 128 : 64;
+  const int nslot = bf16 ? 2 : 4;
+  return wave_lds_floats(r.r, r.cc, r.lw, r.ws, s, d, warea, nslot) * 4 <= 160 * 1024 && r.ws >= 1 && r.ws <= 16;
+}
+
 bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
   const RecipeInfo r = recipe_info(id);
   if (r.r == 0) return false;
+  if (is_wave_recipe(id)) return (lib == kLibCanon8 || lib == kLibDense9) && wave_recipe_fits(r, s, d, lib, bf16);
   const int lh = 64 / r.lw;
   const int th = lh * r.r, tw = r.lw * r.cc;
   const int tih = (th - 1) * s + 2 * d + 1, tiw = (tw - 1) * s + 2 * d + 1;
@@ -41,7 +53,16 @@ bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
 }
 
 bool recipe_compiled(int lib, int id) {
+  if (id < 0 || id >= kNumRecipes) return false;
+  if (is_wave_recipe(id)) return lib == kLibCanon8 || lib == kLibDense9;
   return lib == kLibCanon8 || id == 0 || id == 3 || id == 6 || id == 8 || id == 12 || id == 13;
+}
+
+// a recipe that can run this layer: compiled for the library, fits in LDS,
+// and (wave-pipeline kernel) compiled for the layer's padding (pad = dilation)
+static bool recipe_usable(int id, const ConvParams& p, int lib, bool bf16) {
+  if (!recipe_compiled(lib, id) || !recipe_fits(id, p.stride, p.dil, bf16, lib)) return false;
+  return !is_wave_recipe(id) || p.pad == p.dil;
 }
 
 static int env_recipe() {
@@ -53,23 +74,27 @@ static int env_recipe() {
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
   ConvPlan plan;
   const int forced = env_recipe();
-  if (forced >= 0 && forced < kNumRecipes && recipe_compiled(lib, forced) && recipe_fits(forced, p.stride, p.dil, bf16, lib)) {
+  if (forced >= 0 && forced < kNumRecipes && recipe_usable(forced, p, lib, bf16)) {
     plan.recipe = forced;
     return plan;
   }
   const long pix = static_cast<long>(p.ho) * p.wo;
   int pref[4];
-  if (lib == kLibCanon8 && !bf16 && p.stride == 1) {
-    // fp32 canonical library, from timings of every tiling on the VGG-16
-    // layer shapes (MI355X)
-    if (pix >= 160L * 160L) {
-      pref[0] = 17; pref[1] = 16; pref[2] = 4; pref[3] = 13;
+  if ((lib == kLibCanon8 || lib == kLibDense9) && !bf16 && p.stride == 1 && p.pad == p.dil) {
+    // fp32, stride 1: the wave-pipeline tilings that timed fastest on the
+    // VGG-16 layer shapes (MI355X), by output size; v4 tilings as fallback
+    if (lib == kLibDense9 || p.c_in <= 8) {
+      pref[0] = 31; pref[1] = 20; pref[2] = 0; pref[3] = 13;
+    } else if (pix >= 160L * 160L) {
+      pref[0] = 30; pref[1] = 31; pref[2] = 17; pref[3] = 13;
     } else if (pix >= 80L * 80L) {
-      pref[0] = 19; pref[1] = 3; pref[2] = 13; pref[3] = 13;
+      pref[0] = 20; pref[1] = 19; pref[2] = 3; pref[3] = 13;
+    } else if (pix >= 40L * 40L) {
+      pref[0] = 27; pref[1] = 22; pref[2] = 8; pref[3] = 13;
     } else if (pix >= 20L * 20L) {
-      pref[0] = 8; pref[1] = 19; pref[2] = 6; pref[3] = 13;
+      pref[0] = 23; pref[1] = 22; pref[2] = 8; pref[3] = 13;
     } else {
-      pref[0] = 10; pref[1] = 9; pref[2] = 8; pref[3] = 13;
+      pref[0] = 25; pref[1] = 23; pref[2] = 10; pref[3] = 13;
     }
   } else if (pix >= 100L * 100L) {
     pref[0] = 0; pref[1] = 3; pref[2] = 12; pref[3] = 13;
@@ -81,7 +106,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
     pref[0] = 8; pref[1] = 13; pref[2] = 13; pref[3] = 13;
   }
   for (int id : pref)
-    if (recipe_compiled(lib, id) && recipe_fits(id, p.stride, p.dil, bf16, lib)) {
+    if (recipe_usable(id, p, lib, bf16)) {
       plan.recipe = id;
       return plan;
     }
@@ -98,9 +123,22 @@ static hipError_t launch_lib(int id, const ConvParams& p, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
+template <int LIB, class TA>
+static hipError_t launch_wave(int id, const ConvParams& p, hipStream_t st) {
+  if (p.stride == 1 && p.dil == 1) return launch_wave_recipe<LIB, 1, 1, TA>(id, p, st);
+  if (p.stride == 2 && p.dil == 1) return launch_wave_recipe<LIB, 2, 1, TA>(id, p, st);
+  if (p.stride == 1 && p.dil == 2) return launch_wave_recipe<LIB, 1, 2, TA>(id, p, st);
+  if (p.stride == 2 && p.dil == 2) return launch_wave_recipe<LIB, 2, 2, TA>(id, p, st);
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st) {
-  if (!recipe_compiled(lib, plan.recipe) || !recipe_fits(plan.recipe, p.stride, p.dil, bf16_act, lib))
-    return hipErrorInvalidConfiguration;
+  if (!recipe_usable(plan.recipe, p, lib, bf16_act)) return hipErrorInvalidConfiguration;
+  if (is_wave_recipe(plan.recipe)) {
+    if (lib == kLibDense9)
+      return bf16_act ? launch_wave<kLibDense9, uint16_t>(plan.recipe, p, st) : launch_wave<kLibDense9, float>(plan.recipe, p, st);
+    return bf16_act ? launch_wave<kLibCanon8, uint16_t>(plan.recipe, p, st) : launch_wave<kLibCanon8, float>(plan.recipe, p, st);
+  }
   if (bf16_act) {
     if (lib == kLibCanon8) return launch_lib<kLibCanon8, uint16_t>(plan.recipe, p, st);
     if (lib == kLibDense9) return launch_lib<kLibDense9, uint16_t>(plan.recipe, p, st);

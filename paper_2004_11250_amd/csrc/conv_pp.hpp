@@ -51,7 +51,47 @@ struct ConvParams {
   X(18, 4, 4, 8, 2, 1, 4)   \
   X(19, 2, 2, 8, 2, 4, 4)
 
-constexpr int kNumRecipes = 20;
+// Tilings of the wave-pipeline kernel (canonical library): id, R x CC
+// outputs per lane, LW lanes across, WS channel-split waves of one slot group.
+#define PP_WRECIPES(X)  \
+  X(20, 2, 4, 8, 4)     \
+  X(21, 2, 2, 8, 4)     \
+  X(22, 2, 2, 8, 8)     \
+  X(23, 2, 2, 8, 16)    \
+  X(24, 1, 2, 8, 8)     \
+  X(25, 1, 1, 8, 16)    \
+  X(26, 4, 4, 8, 4)     \
+  X(27, 2, 4, 8, 8)     \
+  X(28, 2, 2, 8, 2)     \
+  X(29, 1, 4, 8, 2)     \
+  X(30, 1, 4, 8, 4)     \
+  X(31, 2, 4, 8, 2)
+
+constexpr int kFirstWaveRecipe = 20;
+
+// LDS row stride (floats) of the wave-pipeline kernel's staged tile: the
+// smallest multiple of 4 >= n, up to n + 12, for which lane rows rstep tile
+// rows apart start 16 banks apart (of 32), else n
+constexpr int wave_row_stride(int n, int rstep) {
+  for (int s = n; s <= n + 12; s += 4)
+    if ((s * rstep) % 32 == 16) return s;
+  return n;
+}
+
+// LDS floats of one wave-pipeline workgroup: per wave a ring of nslot
+// (staged tile rounded up to 256 floats + 64 weight floats), or the
+// partial-sum exchange of 2 slots per wave, whichever is larger; warea =
+// expanded weight floats per staged channel (64 canonical, 128 all-ones)
+constexpr long wave_lds_floats(int r, int cc, int lw, int ws, int s, int d, int warea, int nslot) {
+  const int th = (64 / lw) * r, tw = lw * cc;
+  const int tih = (th - 1) * s + 2 * d + 1, tiw = (tw - 1) * s + 2 * d + 1;
+  const int lstr = wave_row_stride((tiw + 6) / 4 * 4, r * s);
+  const long nq = (static_cast<long>(tih) * lstr + 255) / 256;
+  const long ring = nslot * (nq * 256 + warea);
+  const long xch = static_cast<long>(ws) * 2 * r * cc * 64;
+  return ws * ring > xch ? ws * ring : xch;
+}
+constexpr int kNumRecipes = 32;
 
 struct RecipeInfo {
   int r, cc, lw, wf, ws, cpw;
@@ -72,5 +112,9 @@ hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool 
 
 template <int LIB, int S, int D, class TA>
 hipError_t launch_recipe(int id, const ConvParams& p, hipStream_t st);
+
+// wave-pipeline kernel, canonical (kLibCanon8) and all-ones (kLibDense9) libraries
+template <int LIB, int S, int D, class TA>
+hipError_t launch_wave_recipe(int id, const ConvParams& p, hipStream_t st);
 
 }  // namespace pp

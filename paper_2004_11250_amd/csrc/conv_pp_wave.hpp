@@ -1,0 +1,612 @@
+// conv_pp_wave.hpp -- pattern/connectivity-pruned 3x3 convolution for the
+// canonical 8-pattern library, "wave pipeline" form (gfx950).
+//
+// Same result as pp_conv3x3_kernel (pattern + connectivity pruning, Sec. 2;
+// compact storage and filter reorder, Sec. 3; conv fused with bias and
+// activation, Sec. 3), organised so that a wave never waits on another wave
+// while it walks its input channels:
+//
+//   * A workgroup owns one output tile of one image and ONE slot group (8
+//     packed filters).  Its WS waves split the input channels into WS
+//     contiguous ranges; each wave runs its range on its own and the partial
+//     sums are combined at the end through LDS in a fixed order
+//     (deterministic).
+//   * Lanes are output pixels (R x CC outputs per lane, LW lanes across), as
+//     in the other kernel, so the pattern of a (slot, channel) kernel is
+//     wave-uniform and selects a code path whose tap offsets are compile-time
+//     constants.
+//   * Per wave, a software pipeline over its channels with a private 2-slot
+//     LDS ring:  the halo tile of channel c+2 and the expanded weights of its
+//     8 slots are loaded from global memory into registers while channel c is
+//     computed; they are written to the LDS ring one channel later; the
+//     channel's metadata (kept-slot mask, weight offset, pattern codes) comes
+//     by scalar loads three channels ahead.  Within a channel, the patch and
+//     the kept slots' weights are read from LDS together and waited for once.
+//   * The halo tile is read with 16-byte loads when the image width is a
+//     multiple of 4 (the tile origin is moved down to a multiple of 4 columns
+//     and the patch reads are shifted back), else element by element;
+//     out-of-image elements read zero through the buffer range check.
+#pragma once
+
+#include "conv_pp_kernel.hpp"
+
+namespace pp {
+namespace kern {
+
+template <int LIB, int S, int D, int R, int CC, int LW, int WS, bool ABF>
+struct WGeo {
+  // ring slots per wave: fp32 channels are DMA'd straight into LDS DPF
+  // channels ahead (DPF + 1 slots); bf16 goes through registers (2 slots)
+  static constexpr int DPF = 3;
+  static constexpr int NSLOT = ABF ? 2 : DPF + 1;
+  // expanded weights per slot in LDS: 4 taps (canonical library) or the 9
+  // taps padded to 12 (all-ones library)
+  static constexpr int KW = LIB == kLibDense9 ? 12 : 4;
+  static constexpr int KT = LIB == kLibDense9 ? 9 : 4;     // taps per kept kernel
+  static constexpr int WAREA = (8 * KW + 63) / 64 * 64;
+  static constexpr int NWL = WAREA / 64;                   // weight loads per lane
+  static constexpr int LH = 64 / LW;
+  static constexpr int TH = LH * R, TW = LW * CC;          // output tile
+  static constexpr int PR = (R - 1) * S + 2 * D + 1;       // patch rows
+  static constexpr int PC = (CC - 1) * S + 2 * D + 1;      // patch cols
+  static constexpr int TIH = (TH - 1) * S + 2 * D + 1;     // input tile rows
+  static constexpr int TIW = (TW - 1) * S + 2 * D + 1;     // input tile cols
+  // + up to 3 columns in front of the tile when its origin is moved down to a
+  // multiple of 4
+  static constexpr int LSTR = wave_row_stride((TIW + 3 + 3) / 4 * 4, R * S);
+  static constexpr int AREA = TIH * LSTR;
+  static constexpr int NQ = (AREA + 255) / 256;           // 4-float staging groups per lane
+  static constexpr int PATCH = NQ * 256;                  // floats per staged channel
+  static constexpr int SLOT = PATCH + WAREA;
+  static constexpr int RING = NSLOT * SLOT;               // per wave
+  static constexpr int NACC = 8 * R * CC;
+  // partial-sum exchange: PS slots at a time, every wave writes PS*R*CC floats per lane
+  static constexpr int PS = 2;
+  static constexpr int XCH = WS * PS * R * CC * 64;
+  static constexpr int LDS_FLOATS = (WS * RING > XCH) ? WS * RING : XCH;
+  static_assert(LDS_FLOATS == wave_lds_floats(R, CC, LW, WS, S, D, WAREA, NSLOT),
+                "planner and kernel disagree on LDS size");
+  static constexpr bool fits = LDS_FLOATS * 4 <= 160 * 1024 && LW * LH == 64 && WS >= 1 && WS <= 16;
+};
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// The DMA helpers below write M0, which the compiler treats as reserved; no
+// code generated for these kernels keeps a value in M0 across them.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+
+// raw buffer descriptor (gfx9 layout: 48-bit base, stride 0, num_records
+// bytes, 32-bit data format) as four SGPRs; offsets >= bytes read zero
+__device__ __forceinline__ u32x4 make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  u32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b));
+  r.y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32) & 0xFFFFu);
+  r.z = __builtin_amdgcn_readfirstlane(bytes);
+  r.w = 0x00020000u;
+  return r;
+}
+
+// global -> LDS DMA of 16 (4) bytes per lane: lane l's data lands at LDS byte
+// lds + 16 l (4 l).  Issued as inline assembly so that the compiler neither
+// waits for it (the caller counts vmcnt) nor moves LDS reads across it.
+__device__ __forceinline__ void dma_lds_b128(u32x4 rsrc, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rsrc) : "memory", "m0");
+}
+__device__ __forceinline__ void dma_lds_b32(u32x4 rsrc, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rsrc) : "memory", "m0");
+}
+
+#pragma clang diagnostic pop
+
+// the same descriptor moved on by one channel of `bytes` bytes
+__device__ __forceinline__ u32x4 next_channel(u32x4 r, uint32_t bytes) {
+  const uint64_t b = (static_cast<uint64_t>(r.y) << 32 | r.x) + bytes;
+  r.x = static_cast<uint32_t>(b);
+  r.y = static_cast<uint32_t>(b >> 32) & 0xFFFFu;
+  return r;
+}
+
+// s_waitcnt immediate that waits for vmcnt <= n (n <= 63) and nothing else
+constexpr int vmcnt_imm(int n) {
+  return (n > 63 ? 63 : n) < 0 ? 0x0F70 : (((n > 63 ? 63 : n) & 15) | (((n > 63 ? 63 : n) >> 4) << 14) | 0x0F70);
+}
+
+// one row of a lane's patch: elements [SH, SH + PC) of the staged row that
+// starts at rb (rb aligned to VWL floats), read with the widest aligned LDS
+// loads (a partly used pair at either end reads one extra element)
+template <int J, int PC>
+__device__ __forceinline__ void put_elem(float (&d)[PC], float v) {
+  if constexpr (J >= 0 && J < PC) d[J] = v;
+}
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+template <int I, int SH, int PC, int VWL>
+__device__ __forceinline__ void read_row(float (&d)[PC], const float* rb) {
+  constexpr int END = SH + PC;
+  if constexpr (I < END) {
+    if constexpr (VWL >= 4 && I % 4 == 0 && I + 4 <= END) {
+      f32x4 v = *reinterpret_cast<const f32x4*>(rb + I);
+      asm("" : "+v"(v));   // keep the load whole (one aligned 16-byte read)
+      put_elem<I - SH>(d, v.x);
+      put_elem<I + 1 - SH>(d, v.y);
+      put_elem<I + 2 - SH>(d, v.z);
+      put_elem<I + 3 - SH>(d, v.w);
+      read_row<I + 4, SH, PC, VWL>(d, rb);
+    } else if constexpr (VWL >= 2) {
+      constexpr int B = I & ~1;
+      f32x2 v = *reinterpret_cast<const f32x2*>(rb + B);
+      asm("" : "+v"(v));   // one aligned 8-byte read
+      put_elem<B - SH>(d, v.x);
+      put_elem<B + 1 - SH>(d, v.y);
+      read_row<B + 2, SH, PC, VWL>(d, rb);
+    } else {
+      put_elem<I - SH>(d, rb[I]);
+      read_row<I + 1, SH, PC, VWL>(d, rb);
+    }
+  }
+}
+
+// SH = (-pad) mod 4: the tile's first input column sits SH columns after a
+// multiple of 4 (tile origins are multiples of 4 columns)
+template <int LIB, int S, int D, int R, int CC, int LW, int WS, int SH, class TA>
+__global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) {
+  constexpr bool ABF = sizeof(TA) == 2;
+  using G = WGeo<LIB, S, D, R, CC, LW, WS, ABF>;
+  constexpr int KW = G::KW, KT = G::KT, NWL = G::NWL;
+  constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT;
+  static_assert(G::fits, "tiling does not fit");
+  __shared__ __attribute__((aligned(16))) float lds[G::LDS_FLOATS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wk = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lx = lane % LW, ly = lane / LW;
+
+  uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int grp = blk % a.n_groups;
+  blk /= a.n_groups;
+  const int tx = blk % a.tiles_x;
+  blk /= a.tiles_x;
+  const int ty = blk % a.tiles_y;
+  const int img = blk / a.tiles_y;
+
+  const int oy0 = ty * G::TH, ox0 = tx * G::TW;
+  const int iy0 = oy0 * S - a.pad, ix0 = ox0 * S - a.pad;
+  const bool v4 = (a.w % 4) == 0;                       // 16-byte (fp32) / 8-byte (bf16) row loads
+  const int ixa = ix0 - SH;                             // a multiple of 4
+
+  const TA* __restrict__ x = static_cast<const TA*>(a.x) + static_cast<size_t>(img) * a.c_in * a.h * a.w;
+  const uint32_t chan_bytes = static_cast<uint32_t>(a.h) * a.w * sizeof(TA);
+  const uint8_t* blob = a.blob;
+
+  // ---- per-lane staging offsets (bytes within one channel), fixed for the
+  // kernel.  Staged element e is tile row e / LSTR, column e % LSTR (global
+  // column ixa + e % LSTR).  Load (t, j) of a lane stages element
+  // e = 4*(64 t + lane) + j (16-byte loads, and every bf16 load), or
+  // e = 64*(4 t + j) + lane (4-byte fp32 DMA, lane-contiguous in LDS).
+  const bool lane4 = v4 || ABF;
+  uint32_t qoff[NQ][4];
+#pragma unroll
+  for (int t = 0; t < NQ; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = lane4 ? 4 * (64 * t + lane) + j : 64 * (4 * t + j) + lane;
+      const int row = e / LSTR, col = e % LSTR;
+      const int gy = iy0 + row, gx = ixa + col;
+      const bool ok = e < G::AREA && gy >= 0 && gy < a.h && gx >= 0 && gx < a.w;
+      qoff[t][j] = ok ? (static_cast<uint32_t>(gy) * a.w + gx) * static_cast<uint32_t>(sizeof(TA)) : 0x80000000u;
+    }
+
+  // ---- this wave's channel range
+  const int per = (a.c_in + WS - 1) / WS;
+  const int c0 = min(a.c_in, wk * per), c1 = min(a.c_in, c0 + per);
+  const uint32_t e_base = static_cast<uint32_t>(grp) * a.c_in;
+  const uint32_t e_last = e_base + a.c_in - 1;
+
+  float* const ring = lds + wk * G::RING;
+  // a lane's patch row r starts SH elements after cur + lane_off + r*LSTR
+  const int lane_off = (ly * R * S) * LSTR + lx * CC * S;
+  constexpr int VWL = (CC * S) % 4 == 0 ? 4 : ((CC * S) % 2 == 0 ? 2 : 1);
+
+  // metadata of channel c (clamped to the layer's last channel): woff word
+  // and the 8 pattern codes, scalar loads
+  struct Meta {
+    uint32_t wo, cx, cy;
+  };
+  auto load_meta = [&](int c) __attribute__((always_inline)) {
+    const uint32_t e = min(e_base + static_cast<uint32_t>(c), e_last);
+    Meta m;
+    m.wo = sload<uint32_t>(blob, a.off_woff + 4 * e);
+    const uint2 cw = sload<uint2>(blob, a.off_codes + 8 * e);
+    m.cx = cw.x;
+    m.cy = cw.y;
+    return m;
+  };
+
+  // staged data of one channel in registers
+  float xs[NQ][4];
+  float ws[NWL];
+  const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(blob), static_cast<short>(0), static_cast<int>(a.blob_bytes), 0x00020000);
+
+  // expanded weight e = 64 j + lane of a channel is tap e % KW of slot e / KW
+  // (zero for padding taps, pruned slots and e >= 8 KW); its compact index is
+  // woff + (stored weights per kernel) * rank(slot) + tap
+  constexpr uint32_t KS = LIB == kLibDense9 ? (ABF ? 10u : 9u) : 4u;   // stored weights per kernel
+  int wsl[NWL], wtp[NWL];
+#pragma unroll
+  for (int j = 0; j < NWL; ++j) {
+    const int e = 64 * j + lane;
+    wsl[j] = e < 8 * KW ? e / KW : 8;
+    wtp[j] = e % KW;
+  }
+  auto weight_offs = [&](const Meta& m, uint32_t (&off)[NWL]) __attribute__((always_inline)) {
+    const uint32_t kept = m.wo >> 24;
+#pragma unroll
+    for (int j = 0; j < NWL; ++j) {
+      const int s = wsl[j], t = wtp[j];
+      const uint32_t rank = __builtin_popcount(kept & ((1u << s) - 1u));
+      const bool ok = s < 8 && t < KT && ((kept >> s) & 1u);
+      const uint32_t wi = (m.wo & 0xFFFFFFu) + KS * rank + t;
+      off[j] = ok ? a.off_w + static_cast<uint32_t>(sizeof(TA)) * wi : 0x80000000u;
+    }
+  };
+  // global -> registers: the next channel's halo tile (xf walks the channels
+  // in order) and weights
+  const TA* xf = x + static_cast<size_t>(c0) * a.h * a.w;
+  const size_t hw = static_cast<size_t>(a.h) * a.w;
+  auto fetch = [&](const uint32_t (&woff)[NWL]) __attribute__((always_inline)) {
+    // the channel as the resource: soffset is not range checked, so the
+    // channel offset goes into the base address
+    const __amdgpu_buffer_rsrc_t cr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<TA*>(xf), static_cast<short>(0), static_cast<int>(chan_bytes), 0x00020000);
+    xf += hw;
+    if (v4) {
+#pragma unroll
+      for (int t = 0; t < NQ; ++t) {
+        if constexpr (ABF) {
+          const uint2 u = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(cr, qoff[t][0], 0, 0));
+          xs[t][0] = bf16_lo(u.x); xs[t][1] = bf16_hi(u.x); xs[t][2] = bf16_lo(u.y); xs[t][3] = bf16_hi(u.y);
+        } else {
+          const float4 v = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(cr, qoff[t][0], 0, 0));
+          xs[t][0] = v.x; xs[t][1] = v.y; xs[t][2] = v.z; xs[t][3] = v.w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < NQ; ++t)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if constexpr (ABF)
+            xs[t][j] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(cr, qoff[t][j], 0, 0)) << 16);
+          else
+            xs[t][j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(cr, qoff[t][j], 0, 0));
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NWL; ++j) {
+      if constexpr (ABF)
+        ws[j] = __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(br, woff[j], 0, 0)) << 16);
+      else
+        ws[j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(br, woff[j], 0, 0));
+    }
+  };
+  // registers -> LDS ring slot
+  auto store = [&](float* slot) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < NQ; ++t)
+      *reinterpret_cast<float4*>(slot + 4 * (64 * t + lane)) = make_float4(xs[t][0], xs[t][1], xs[t][2], xs[t][3]);
+#pragma unroll
+    for (int j = 0; j < NWL; ++j) slot[G::PATCH + 64 * j + lane] = ws[j];
+  };
+
+  float acc[8][R][CC];
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int q = 0; q < CC; ++q) acc[s][r][q] = 0.0f;
+
+  if (ABF && c0 < c1) {
+    Meta m0 = load_meta(c0), m1 = load_meta(c0 + 1), m2 = load_meta(c0 + 2);
+    uint32_t wof[NWL];
+    weight_offs(m0, wof);
+    fetch(wof);
+    store(ring);
+    if (c0 + 1 < c1) {
+      weight_offs(m1, wof);
+      fetch(wof);
+    }
+#pragma unroll 1
+    for (int c = c0; c < c1; ++c) {
+      const int k = c - c0;
+      float* cur = ring + (k & 1) * SLOT;
+      float* nxt = ring + ((k + 1) & 1) * SLOT;
+      weight_offs(m2, wof);                       // needs meta(c+2): before any LDS op is in flight
+      if (c + 1 < c1) store(nxt);                 // channel c+1 -> LDS
+      if (c + 2 < c1) fetch(wof);                 // channel c+2 -> registers
+      // patch and the kept slots' weights of channel c
+      const uint32_t kept = m0.wo >> 24;
+      float p[PR][PC];
+      float w[8][KW];
+      if (kept != 0) {
+        // weights first: the patch reads end with a wait that then covers both
+        const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          if ((kept >> s) & 1u) {
+#pragma unroll
+            for (int i = 0; i < KW / 4; ++i) {
+              const float4 v = wc[s * (KW / 4) + i];
+              w[s][4 * i] = v.x; w[s][4 * i + 1] = v.y; w[s][4 * i + 2] = v.z; w[s][4 * i + 3] = v.w;
+            }
+          }
+#pragma unroll
+        for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL>(p[r], cur + lane_off + r * LSTR);
+      }
+      // everything of channel c is in registers once this wait returns; the
+      // scalar loads issued next are then waited for only one channel later
+      wait_lgkm();
+      __builtin_amdgcn_sched_barrier(0);
+      const Meta m3 = load_meta(c + 3);
+      uint32_t kc = kept;
+      asm volatile("" : "+s"(kc));   // fresh slot tests (no 64-bit condition masks kept live)
+      if (kc != 0) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          if (!((kc >> s) & 1u)) continue;
+          if constexpr (LIB == kLibDense9) {
+            fma_tap<0, S, D>(acc[s], p, w[s][0]);
+            fma_tap<1, S, D>(acc[s], p, w[s][1]);
+            fma_tap<2, S, D>(acc[s], p, w[s][2]);
+            fma_tap<3, S, D>(acc[s], p, w[s][3]);
+            fma_tap<4, S, D>(acc[s], p, w[s][4]);
+            fma_tap<5, S, D>(acc[s], p, w[s][5]);
+            fma_tap<6, S, D>(acc[s], p, w[s][6]);
+            fma_tap<7, S, D>(acc[s], p, w[s][7]);
+            fma_tap<8, S, D>(acc[s], p, w[s][8]);
+          } else {
+            const uint32_t pid = ((s < 4 ? m0.cx : m0.cy) >> (8 * (s & 3))) & 0xFFu;
+            apply_canon8<S, D>(pid, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+          }
+        }
+      }
+      m0 = m1;
+      m1 = m2;
+      m2 = m3;
+    }
+  }
+
+  if (!ABF && c0 < c1) {
+    // fp32: DMA pipeline.  Channel c lives in ring slot (c - c0) % NSLOT; its
+    // halo tile and weights are DMA'd DPF channels before it is computed.
+    // Per channel every lane issues QV DMAs, so "channel c has landed" is
+    // vmcnt <= (DPF - 1) * QV while DPF - 1 later channels are in flight.
+    constexpr int NS = G::NSLOT, DPF = G::DPF;
+    const uint32_t ring_b = lds_addr(ring);
+    const u32x4 brs = make_rsrc(blob, a.blob_bytes);
+    // descriptor of the next channel to DMA (channels are DMA'd in order)
+    u32x4 cr = make_rsrc(x + static_cast<size_t>(c0) * a.h * a.w, chan_bytes);
+    auto dma = [&](int c, uint32_t wo) __attribute__((always_inline)) {
+      const int k = c - c0;
+      const uint32_t sb = ring_b + 4u * static_cast<uint32_t>((k % NS) * SLOT);
+      if (v4) {
+#pragma unroll
+        for (int t = 0; t < NQ; ++t) dma_lds_b128(cr, qoff[t][0], sb + 1024u * t);
+      } else {
+#pragma unroll
+        for (int t = 0; t < NQ; ++t)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dma_lds_b32(cr, qoff[t][j], sb + 256u * (4 * t + j));
+      }
+      Meta mw;
+      mw.wo = wo;
+      uint32_t wof[NWL];
+      weight_offs(mw, wof);
+#pragma unroll
+      for (int j = 0; j < NWL; ++j) dma_lds_b32(brs, wof[j], sb + 4u * (G::PATCH + 64 * j));
+      cr = next_channel(cr, chan_bytes);
+    };
+    auto load_wo = [&](int c) __attribute__((always_inline)) {
+      const uint32_t e = min(e_base + static_cast<uint32_t>(c), e_last);
+      return sload<uint32_t>(blob, a.off_woff + 4 * e);
+    };
+    // running byte offsets of the scalar loads (clamped at the layer's last
+    // channel, whose entries are then read again and not used)
+    const uint32_t woff_last = a.off_woff + 4u * e_last, code_last = a.off_codes + 8u * e_last;
+    // prologue: channels c0 .. c0+DPF-1 in flight
+    {
+      uint32_t wo[DPF];
+#pragma unroll
+      for (int i = 0; i < DPF; ++i) wo[i] = load_wo(c0 + i);
+#pragma unroll
+      for (int i = 0; i < DPF; ++i)
+        if (c0 + i < c1) dma(c0 + i, wo[i]);
+    }
+    Meta m0 = load_meta(c0);
+    uint32_t wo_n = load_wo(c0 + DPF);
+    uint32_t wo_off = min(a.off_woff + 4u * (e_base + c0 + DPF + 1), woff_last);
+    uint32_t me_off = min(a.off_woff + 4u * (e_base + c0 + 1), woff_last);
+    uint32_t mc_off = min(a.off_codes + 8u * (e_base + c0 + 1), code_last);
+#pragma unroll 1
+    for (int c = c0; c < c1; ++c) {
+      const int k = c - c0;
+      const float* cur = ring + (k % NS) * SLOT;
+      // channel c has landed in LDS
+      asm volatile("" ::: "memory");
+      if (c + DPF - 1 < c1) {
+        if (v4) {
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm((DPF - 1) * (NQ + NWL)));
+        } else {
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm((DPF - 1) * (4 * NQ + NWL)));
+        }
+      } else {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+      }
+      asm volatile("" ::: "memory");
+      const uint32_t kept = m0.wo >> 24;
+      float p[PR][PC];
+      float w[8][KW];
+      if (kept != 0) {
+        // weights first: the patch reads end with a wait that then covers both
+        const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+          if ((kept >> s) & 1u) {
+#pragma unroll
+            for (int i = 0; i < KW / 4; ++i) {
+              const float4 v = wc[s * (KW / 4) + i];
+              w[s][4 * i] = v.x; w[s][4 * i + 1] = v.y; w[s][4 * i + 2] = v.z; w[s][4 * i + 3] = v.w;
+            }
+          }
+#pragma unroll
+        for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL>(p[r], cur + lane_off + r * LSTR);
+      }
+      // patch, weights, and the scalar loads of the previous iteration
+      wait_lgkm();
+      __builtin_amdgcn_sched_barrier(0);
+      // channel c+DPF -> LDS (its slot was last read for channel c-1)
+      if (c + DPF < c1) dma(c + DPF, wo_n);
+      const uint32_t wo_nn = sload<uint32_t>(blob, wo_off);
+      Meta m1;
+      m1.wo = sload<uint32_t>(blob, me_off);
+      {
+        const uint2 cw = sload<uint2>(blob, mc_off);
+        m1.cx = cw.x;
+        m1.cy = cw.y;
+      }
+      wo_off = min(wo_off + 4u, woff_last);
+      me_off = min(me_off + 4u, woff_last);
+      mc_off = min(mc_off + 8u, code_last);
+      uint32_t kc = kept;
+      asm volatile("" : "+s"(kc));   // fresh slot tests (no 64-bit condition masks kept live)
+      if (kc != 0) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          if (!((kc >> s) & 1u)) continue;
+          if constexpr (LIB == kLibDense9) {
+            fma_tap<0, S, D>(acc[s], p, w[s][0]);
+            fma_tap<1, S, D>(acc[s], p, w[s][1]);
+            fma_tap<2, S, D>(acc[s], p, w[s][2]);
+            fma_tap<3, S, D>(acc[s], p, w[s][3]);
+            fma_tap<4, S, D>(acc[s], p, w[s][4]);
+            fma_tap<5, S, D>(acc[s], p, w[s][5]);
+            fma_tap<6, S, D>(acc[s], p, w[s][6]);
+            fma_tap<7, S, D>(acc[s], p, w[s][7]);
+            fma_tap<8, S, D>(acc[s], p, w[s][8]);
+          } else {
+            const uint32_t pid = ((s < 4 ? m0.cx : m0.cy) >> (8 * (s & 3))) & 0xFFu;
+            apply_canon8<S, D>(pid, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+          }
+        }
+      }
+      m0 = m1;
+      wo_n = wo_nn;
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // no DMA may land in the exchange area below
+  }
+
+  // ---- combine the WS partial sums, PS slots at a time, in wave order; wave
+  // k then finishes units u = k, k + WS, ... of the pass (unit = slot, row)
+  TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  const bool relu = (a.flags & PP_RELU) != 0;
+  const int oxl = ox0 + lx * CC;
+  const bool vec = (CC % 4 == 0) && (a.wo % 4 == 0) && (reinterpret_cast<uintptr_t>(a.y) % (4 * sizeof(TA)) == 0);
+  constexpr int NU = G::PS * R;   // units per pass
+#pragma unroll
+  for (int s0 = 0; s0 < 8; s0 += G::PS) {
+    if (WS > 1) {
+      __syncthreads();
+      float* dst = lds + (wk * G::PS * R * CC) * 64 + lane;
+#pragma unroll
+      for (int ps = 0; ps < G::PS; ++ps)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int q = 0; q < CC; ++q) dst[((ps * R + r) * CC + q) * 64] = acc[s0 + ps][r][q];
+      __syncthreads();
+    }
+#pragma unroll
+    for (int u0 = 0; u0 < NU; u0 += WS) {
+      const int u = u0 + wk;
+      if (u >= NU) break;
+      const int ps = u / R, r = u % R;
+      const int s = s0 + ps;
+      float v[CC];
+      if (WS > 1) {
+#pragma unroll
+        for (int q = 0; q < CC; ++q) {
+          float t = 0.0f;
+          for (int k = 0; k < WS; ++k) t += lds[((k * G::PS * R + ps * R + r) * CC + q) * 64 + lane];
+          v[q] = t;
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < CC; ++q) v[q] = acc[s][r][q];
+      }
+      const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
+      const uint32_t o = sload<uint32_t>(blob, a.off_perm + 4 * slot);
+      if (o >= static_cast<uint32_t>(a.c_out)) continue;   // padding slot
+      const float bias = sload<float>(blob, a.off_bias + 4 * slot);
+      const int oy = oy0 + ly * R + r;
+      if (oy >= a.ho) continue;
+#pragma unroll
+      for (int q = 0; q < CC; ++q) {
+        v[q] += bias;
+        if (relu) v[q] = fmaxf(v[q], 0.0f);
+      }
+      TA* row = y + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
+      if (vec && oxl + CC <= a.wo) {
+#pragma unroll
+        for (int q = 0; q < CC; q += 4) {
+          if constexpr (ABF) {
+            uint2 uu;
+            uu.x = to_bf16_bits(v[q]) | (to_bf16_bits(v[q + 1]) << 16);
+            uu.y = to_bf16_bits(v[q + 2]) | (to_bf16_bits(v[q + 3]) << 16);
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(row) + oxl + q) = uu;
+          } else {
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(row) + oxl + q) =
+                make_float4(v[q], v[q + 1], v[q + 2], v[q + 3]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < CC; ++q) {
+          if (oxl + q < a.wo) {
+            if constexpr (ABF)
+              reinterpret_cast<uint16_t*>(row)[oxl + q] = static_cast<uint16_t>(to_bf16_bits(v[q]));
+            else
+              reinterpret_cast<float*>(row)[oxl + q] = v[q];
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int LIB, int S, int D, int R, int CC, int LW, int WS, class TA>
+hipError_t launch_wave_tiling(ConvParams p, hipStream_t st) {
+  using G = WGeo<LIB, S, D, R, CC, LW, WS, sizeof(TA) == 2>;
+  constexpr int SH = (4 - D % 4) % 4;   // the compiled padding is pad = D
+  if constexpr (!G::fits) {
+    return hipErrorInvalidConfiguration;
+  } else {
+    if (p.pad != D || G::TW % 4 != 0) return hipErrorInvalidConfiguration;
+    p.tiles_x = (p.wo + G::TW - 1) / G::TW;
+    p.tiles_y = (p.ho + G::TH - 1) / G::TH;
+    p.n_ftiles = p.n_groups;
+    const size_t nb = static_cast<size_t>(p.n_groups) * p.tiles_x * p.tiles_y * p.n;
+    if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((pp_conv3x3_wave_kernel<LIB, S, D, R, CC, LW, WS, SH, TA>), dim3(static_cast<uint32_t>(nb)),
+                       dim3(WS * 64), 0, st, p);
+    return hipGetLastError();
+  }
+}
+
+}  // namespace kern
+}  // namespace pp

@@ -1,0 +1,6 @@
+// Pruned 3x3 conv, wave-pipeline kernel, all-ones (dense 3x3) library, stride 1, dilation 2.
+#include "conv_pp_wave_inst.hpp"
+
+namespace pp {
+PP_WAVE_INSTANTIATE(kLibDense9, 1, 2)
+}  // namespace pp

@@ -200,18 +200,26 @@ def test_vgg16_full_size_layer_sampled(idx):
 
 
 # every compiled tiling, forced through the PP_RECIPE override of the planner
-RECIPES = list(range(20))
+RECIPES = list(range(32))
 
 
 @pytest.mark.parametrize("recipe", RECIPES)
 def test_every_tiling(recipe, monkeypatch):
     monkeypatch.setenv("PP_RECIPE", str(recipe))
-    for (s, p, d), dtype, shape in (((1, 1, 1), "f32", (19, 21, 37, 45)), ((2, 1, 1), "f32", (17, 9, 41, 50)),
-                                    ((1, 2, 2), "f32", (11, 13, 29, 33)), ((1, 1, 1), "bf16", (24, 17, 33, 70))):
+    # widths 44/48 (multiples of 4) take the 16-byte staging path, 45/50/33/70 the element-wise one
+    for (s, p, d), dtype, shape in (((1, 1, 1), "f32", (19, 21, 37, 45)), ((1, 1, 1), "f32", (19, 21, 37, 44)),
+                                    ((2, 1, 1), "f32", (17, 9, 41, 50)), ((2, 1, 1), "f32", (17, 9, 41, 48)),
+                                    ((1, 2, 2), "f32", (11, 13, 29, 33)), ((1, 1, 1), "bf16", (24, 17, 33, 70)),
+                                    ((1, 1, 1), "bf16", (24, 17, 33, 68))):
         c_out, c_in, h, w = shape
         seed = 40 + recipe
         L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
         x = workloads.random_input(seed, (2, c_in, h, w))
-        _say("recipe", recipe, (s, p, d), dtype, shape)
+        used = pp.conv2d_recipe(pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], s, p, d,
+                                        pp.PP_BF16 if dtype == "bf16" else pp.PP_F32), 2, h, w,
+                                pp.PP_BF16 if dtype == "bf16" else pp.PP_F32)
+        _say("recipe", recipe, "runs as", used, (s, p, d), dtype, shape)
+        if (s, p, d) == (1, 1, 1) and dtype == "f32":
+            assert used == recipe, "the forced tiling must run for a stride-1 fp32 canonical layer"
         y, ref, bound = run_layer(L, x, s, p, d, relu=True, dtype=dtype)
         check(y, ref, bound, dtype, f"recipe {recipe} {(s, p, d)} {dtype}")
