@@ -86,7 +86,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
     if (lib == kLibDense9 || p.c_in <= 8) {
       pref[0] = 31; pref[1] = 20; pref[2] = 0; pref[3] = 13;
     } else if (pix >= 160L * 160L) {
-      pref[0] = 30; pref[1] = 31; pref[2] = 17; pref[3] = 13;
+      pref[0] = 31; pref[1] = 30; pref[2] = 17; pref[3] = 13;
     } else if (pix >= 80L * 80L) {
       pref[0] = 20; pref[1] = 19; pref[2] = 3; pref[3] = 13;
     } else if (pix >= 40L * 40L) {

@@ -393,8 +393,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
     // descriptor of the next channel to DMA (channels are DMA'd in order)
     u32x4 cr = make_rsrc(x + static_cast<size_t>(c0) * a.h * a.w, chan_bytes);
     auto dma = [&](int c, uint32_t wo) __attribute__((always_inline)) {
-      const int k = c - c0;
-      const uint32_t sb = ring_b + 4u * static_cast<uint32_t>((k % NS) * SLOT);
+      const uint32_t k = static_cast<uint32_t>(c - c0);
+      const uint32_t sb = ring_b + 4u * ((k % NS) * SLOT);
       if (v4) {
 #pragma unroll
         for (int t = 0; t < NQ; ++t) dma_lds_b128(cr, qoff[t][0], sb + 1024u * t);
@@ -435,7 +435,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
     uint32_t mc_off = min(a.off_codes + 8u * (e_base + c0 + 1), code_last);
 #pragma unroll 1
     for (int c = c0; c < c1; ++c) {
-      const int k = c - c0;
+      const uint32_t k = static_cast<uint32_t>(c - c0);
       const float* cur = ring + (k % NS) * SLOT;
       // channel c has landed in LDS
       asm volatile("" ::: "memory");
@@ -454,10 +454,12 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       float w[8][KW];
       if (kept != 0) {
         // weights first: the patch reads end with a wait that then covers both
+        // canonical library: all 8 slots (4 floats each) unconditionally --
+        // fewer branches than testing each slot; pruned slots hold zeros
         const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
 #pragma unroll
         for (int s = 0; s < 8; ++s)
-          if ((kept >> s) & 1u) {
+          if (LIB == kLibCanon8 || ((kept >> s) & 1u)) {
 #pragma unroll
             for (int i = 0; i < KW / 4; ++i) {
               const float4 v = wc[s * (KW / 4) + i];
@@ -469,6 +471,11 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       }
       // patch, weights, and the scalar loads of the previous iteration
       wait_lgkm();
+      if constexpr (LIB == kLibCanon8) {
+        // the weights are complete here; keep them out of the slot branches
+#pragma unroll
+        for (int s = 0; s < 8; ++s) asm("" : "+v"(w[s][0]), "+v"(w[s][1]), "+v"(w[s][2]), "+v"(w[s][3]));
+      }
       __builtin_amdgcn_sched_barrier(0);
       // channel c+DPF -> LDS (its slot was last read for channel c-1)
       if (c + DPF < c1) dma(c + DPF, wo_n);
