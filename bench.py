@@ -272,7 +272,7 @@ def main():
     for (i, op, ishape, o), prm in zip(shapes, params):
         if op["op"] != "conv3":
             continue
-        L = net.layers[li]
+        L = net.pruned[li]
         li += 1
         xin = torch.rand((batch,) + ishape, device=dev).to(tdt)
         yo = torch.empty((batch,) + o, device=dev, dtype=tdt)

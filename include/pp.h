@@ -132,26 +132,45 @@ pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
  *                       h_out = (h + 2 pad - 2 dilation - 1)/stride + 1;
  *                       must not overlap x
  *   flags               PP_RELU
+ *   workspace, ws_bytes optional device scratch (NULL, 0 for none), 256-byte
+ *                       aligned.  With pp_conv2d_workspace() bytes the
+ *                       kernel may split the input channels over more
+ *                       workgroups (grids that underfill the GPU); partial
+ *                       sums go there and a second kernel adds them.  Calls
+ *                       sharing one workspace must be ordered (same stream).
  * Output channels are in the original filter order.  Accumulation is fp32
- * in a fixed order, so repeated calls give bitwise-identical results.
+ * in a fixed order, so repeated calls with the same workspace size give
+ * bitwise-identical results.
  * Errors: PP_EINVAL, PP_EBLOB, PP_EUNSUPPORTED (stride or dilation outside
  * {1,2}, pad > 2*dilation, weight dtype not the activation dtype, h_out or
  * w_out < 1), PP_EHIP.
  */
 pp_status pp_conv2d_fwd(const void* h_blob, size_t blob_bytes, const void* d_blob,
                         const void* x, void* y, int32_t n, int32_t h, int32_t w,
-                        int32_t act_dtype, uint32_t flags, void* hip_stream);
+                        int32_t act_dtype, uint32_t flags, void* workspace, size_t ws_bytes,
+                        void* hip_stream);
 
 /*
- * pp_conv2d_recipe -- the GPU tiling ("recipe" id) pp_conv2d_fwd uses for
- * this layer, batch and input size (informational: lets callers and tests
- * see which compiled kernel runs).  The environment variable PP_RECIPE=<id>
- * forces a tiling when it can run the layer; otherwise the planner's choice
- * is reported.  Host-only.  Errors: as pp_conv2d_out_size, PP_EINVAL (recipe
- * NULL, act_dtype), PP_EUNSUPPORTED.
+ * pp_conv2d_workspace -- device scratch bytes pp_conv2d_fwd can use for this
+ * layer and input (0: it would not use any).  Host-only.  Errors: as
+ * pp_conv2d_out_size, PP_EINVAL (bytes NULL, act_dtype), PP_EUNSUPPORTED.
+ */
+pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h,
+                              int32_t w, int32_t act_dtype, size_t* bytes);
+
+/*
+ * pp_conv2d_recipe -- the GPU tiling ("recipe" id) and the channel split
+ * pp_conv2d_fwd uses for this layer, batch and input size, with
+ * (with_workspace != 0) or without a pp_conv2d_workspace()-sized workspace.
+ * Informational: lets callers and tests see which compiled kernel runs.  The
+ * environment variables PP_RECIPE=<id> and PP_KSPLIT=<k> force a tiling
+ * (when it can run the layer) and a split; otherwise the planner's choice is
+ * reported.  ksplit may be NULL.  Host-only.  Errors: as pp_conv2d_out_size,
+ * PP_EINVAL (recipe NULL, act_dtype), PP_EUNSUPPORTED.
  */
 pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
-                           int32_t act_dtype, int32_t* recipe);
+                           int32_t act_dtype, int32_t with_workspace, int32_t* recipe,
+                           int32_t* ksplit);
 
 /* pp_conv2d_out_size -- h_out, w_out of a packed layer for an h x w input. */
 pp_status pp_conv2d_out_size(const void* h_blob, size_t blob_bytes, int32_t h, int32_t w,
@@ -192,7 +211,9 @@ typedef struct {
 
 /*
  * pp_net_workspace -- bytes of workspace pp_net_fwd needs for this op list
- * and input shape, and the output shape (any output pointer may be NULL).
+ * and input shape (intermediate activations, plus scratch for the pruned
+ * convs' channel splits), and the output shape (any output pointer may be
+ * NULL).
  * Errors: PP_EINVAL (bad op, slot or shape chain), PP_EBLOB.
  */
 pp_status pp_net_workspace(const pp_net_op* ops, int32_t n_ops, int32_t n, int32_t c,

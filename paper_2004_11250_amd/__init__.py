@@ -24,8 +24,8 @@ PP_RELU = 1
 (OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
 
 # exported symbols declared in include/pp.h
-SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_recipe", "pp_conv2d_out_size",
-           "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error")
+SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_workspace", "pp_conv2d_recipe",
+           "pp_conv2d_out_size", "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error")
 
 
 class PPError(RuntimeError):
@@ -64,9 +64,10 @@ def load_library(path: str = LIB_PATH):
     lib.pp_pack.argtypes = [ctypes.POINTER(LayerDesc), vp, vp, vp, vp, vp, i32, vp, ctypes.POINTER(sz)]
     lib.pp_blob_info.argtypes = [vp, sz, ctypes.POINTER(LayerDesc), ctypes.POINTER(i32),
                                  ctypes.POINTER(ctypes.c_int64)]
-    lib.pp_conv2d_fwd.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp]
+    lib.pp_conv2d_fwd.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp, sz, vp]
+    lib.pp_conv2d_workspace.argtypes = [vp, sz, i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.pp_conv2d_out_size.argtypes = [vp, sz, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
-    lib.pp_conv2d_recipe.argtypes = [vp, sz, i32, i32, i32, i32, ctypes.POINTER(i32)]
+    lib.pp_conv2d_recipe.argtypes = [vp, sz, i32, i32, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.pp_net_workspace.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
                                      ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.pp_net_fwd.argtypes = [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp]
@@ -135,13 +136,29 @@ def out_size(blob, h, w):
     return ho.value, wo.value
 
 
-def conv2d_recipe(blob, n, h, w, act_dtype=PP_F32) -> int:
-    """Tiling id that pp_conv2d_fwd uses for this layer and input shape."""
+def conv2d_plan(blob, n, h, w, act_dtype=PP_F32, with_workspace=True):
+    """(tiling id, channel split) that pp_conv2d_fwd uses for this layer and input."""
     lib = load_library()
     blob = np.ascontiguousarray(blob, dtype=np.uint8)
-    r = ctypes.c_int32(-1)
-    _check(lib.pp_conv2d_recipe(_ptr(blob), blob.nbytes, n, h, w, act_dtype, ctypes.byref(r)), "pp_conv2d_recipe")
-    return r.value
+    r, k = ctypes.c_int32(-1), ctypes.c_int32(0)
+    _check(lib.pp_conv2d_recipe(_ptr(blob), blob.nbytes, n, h, w, act_dtype, 1 if with_workspace else 0,
+                                ctypes.byref(r), ctypes.byref(k)), "pp_conv2d_recipe")
+    return r.value, k.value
+
+
+def conv2d_recipe(blob, n, h, w, act_dtype=PP_F32, with_workspace=True) -> int:
+    """Tiling id that pp_conv2d_fwd uses for this layer and input shape."""
+    return conv2d_plan(blob, n, h, w, act_dtype, with_workspace)[0]
+
+
+def conv2d_workspace(blob, n, h, w, act_dtype=PP_F32) -> int:
+    """Scratch bytes pp_conv2d_fwd can use for this layer and input."""
+    lib = load_library()
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    b = ctypes.c_size_t(0)
+    _check(lib.pp_conv2d_workspace(_ptr(blob), blob.nbytes, n, h, w, act_dtype, ctypes.byref(b)),
+           "pp_conv2d_workspace")
+    return b.value
 
 
 # ---------------------------------------------------------------------------
@@ -178,6 +195,7 @@ class PackedLayer:
         self.d_blob = torch.from_numpy(self.h_blob.copy()).to(device)
         if self.d_blob.data_ptr() % 256:
             raise RuntimeError("device blob allocation is not 256-byte aligned")
+        self.scratch = {}   # conv2d_fwd workspaces by input shape
 
     @classmethod
     def from_weights(cls, w, b, pattern_id, conn, lib_masks, stride=1, pad=1, dilation=1, wdtype=PP_F32,
@@ -185,8 +203,10 @@ class PackedLayer:
         return cls(pack(w, b, pattern_id, conn, lib_masks, stride, pad, dilation, wdtype), device)
 
 
-def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None):
-    """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None)."""
+def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspace="auto"):
+    """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None).
+    workspace: "auto" (a scratch tensor of pp_conv2d_workspace bytes, kept on
+    the layer per input shape), None (no scratch) or a uint8 device tensor."""
     torch = _torch()
     lib = load_library()
     if not x.is_contiguous():
@@ -200,8 +220,19 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None):
         out = torch.empty(shape, dtype=x.dtype, device=x.device)
     elif tuple(out.shape) != shape or out.dtype != x.dtype or not out.is_contiguous():
         raise ValueError(f"out must be a contiguous {x.dtype} tensor of shape {shape}")
+    if isinstance(workspace, str) and workspace == "auto":
+        nb = conv2d_workspace(layer.h_blob, n, h, w, _dtype_code(x))
+        key = (n, h, w, _dtype_code(x), x.device.index)
+        workspace = layer.scratch.get(key)
+        if nb and (workspace is None or workspace.numel() < nb):
+            workspace = torch.empty(nb, dtype=torch.uint8, device=x.device)
+            layer.scratch[key] = workspace
+        if not nb:
+            workspace = None
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel()) if workspace is not None else (None, 0)
     st = lib.pp_conv2d_fwd(_ptr(layer.h_blob), layer.h_blob.nbytes, layer.d_blob.data_ptr(), x.data_ptr(),
-                           out.data_ptr(), n, h, w, _dtype_code(x), PP_RELU if relu else 0, _stream_ptr(stream))
+                           out.data_ptr(), n, h, w, _dtype_code(x), PP_RELU if relu else 0, ws_ptr, ws_bytes,
+                           _stream_ptr(stream))
     _check(st, "pp_conv2d_fwd")
     return out
 
@@ -234,6 +265,7 @@ class Net:
         self.wd = PP_BF16 if dtype == "bf16" else PP_F32
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.layers = []     # keeps device buffers alive
+        self.pruned = []     # the PackedLayer of every pruned conv, in op order
         arr = (NetOp * len(ops))()
         for i, (op, prm) in enumerate(zip(ops, params)):
             kind = self._KIND[op["op"]]
@@ -246,6 +278,7 @@ class Net:
                 L = PackedLayer.from_weights(prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"],
                                              op["stride"], op["pad"], op["dil"], self.wd, device)
                 self.layers.append(L)
+                self.pruned.append(L)
                 e.h_blob = L.h_blob.ctypes.data
                 e.blob_bytes = L.h_blob.nbytes
                 e.d_blob = L.d_blob.data_ptr()

@@ -59,7 +59,8 @@ pp_status conv_check(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t
 ConvParams layer_params(const BlobView& v, int32_t n, int32_t h, int32_t w, int ho, int wo);
 
 pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
-                       int32_t w, int32_t act_dtype, uint32_t flags, hipStream_t st) {
+                       int32_t w, int32_t act_dtype, uint32_t flags, void* scratch, size_t scratch_bytes,
+                       hipStream_t st) {
   int ho = 0, wo = 0;
   pp_status s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
   if (s != PP_OK) return s;
@@ -81,10 +82,24 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   p.y = y;
   p.flags = flags;
   const int lib = library_kind(v);
-  const ConvPlan plan = plan_conv(p, lib, act_dtype == PP_BF16);
-  hipError_t e = launch_conv(lib, plan, p, act_dtype == PP_BF16, st);
+  const bool bf = act_dtype == PP_BF16;
+  ConvPlan plan = plan_conv(p, lib, bf, scratch != nullptr);
+  if (plan.ksplit > 1) {
+    if (split_bytes(plan, p) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
+      plan = plan_conv(p, lib, bf, false);   // not enough scratch: no split
+    else
+      p.part = static_cast<float*>(scratch);
+  }
+  hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;
+}
+
+size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype) {
+  int ho = 0, wo = 0;
+  if (conv_check(v, n, h, w, act_dtype, &ho, &wo) != PP_OK) return 0;
+  const ConvParams p = layer_params(v, n, h, w, ho, wo);
+  return split_bytes(plan_conv(p, library_kind(v), act_dtype == PP_BF16, true), p);
 }
 
 // launch parameters of one layer for an n x c_in x h x w input (device
@@ -133,7 +148,7 @@ extern "C" pp_status pp_conv2d_out_size(const void* h_blob, size_t blob_bytes, i
 }
 
 extern "C" pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
-                                      int32_t act_dtype, int32_t* recipe) {
+                                      int32_t act_dtype, int32_t with_workspace, int32_t* recipe, int32_t* ksplit) {
   clear_error();
   BlobView v;
   pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
@@ -143,16 +158,34 @@ extern "C" pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int
   s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
   if (s != PP_OK) return s;
   const ConvParams p = layer_params(v, n, h, w, ho, wo);
-  *recipe = plan_conv(p, library_kind(v), act_dtype == PP_BF16).recipe;
+  const ConvPlan plan = plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_workspace != 0);
+  *recipe = plan.recipe;
+  if (ksplit) *ksplit = plan.ksplit;
+  return PP_OK;
+}
+
+extern "C" pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
+                                         int32_t act_dtype, size_t* bytes) {
+  clear_error();
+  BlobView v;
+  pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
+  if (s != PP_OK) return s;
+  if (!bytes) return fail(PP_EINVAL, "bytes is NULL");
+  int ho = 0, wo = 0;
+  s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
+  if (s != PP_OK) return s;
+  *bytes = conv_scratch_bytes(v, n, h, w, act_dtype);
   return PP_OK;
 }
 
 extern "C" pp_status pp_conv2d_fwd(const void* h_blob, size_t blob_bytes, const void* d_blob, const void* x,
                                    void* y, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
-                                   void* hip_stream) {
+                                   void* workspace, size_t ws_bytes, void* hip_stream) {
   clear_error();
   BlobView v;
   pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
   if (s != PP_OK) return s;
-  return conv_enqueue(v, d_blob, x, y, n, h, w, act_dtype, flags, static_cast<hipStream_t>(hip_stream));
+  if (ws_bytes && !workspace) return fail(PP_EINVAL, "NULL workspace with nonzero size");
+  return conv_enqueue(v, d_blob, x, y, n, h, w, act_dtype, flags, workspace, workspace ? ws_bytes : 0,
+                      static_cast<hipStream_t>(hip_stream));
 }

@@ -13,8 +13,14 @@ int library_kind(const BlobView& v);
 // validate shapes of a pruned conv; returns the output size
 pp_status conv_check(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, int* ho, int* wo);
 
-// validate pointers and enqueue one pruned conv on `st`
+// validate pointers and enqueue one pruned conv on `st`.  scratch (may be
+// NULL) of scratch_bytes lets the planner split the input channels over
+// workgroups (partial sums there, added by a second kernel)
 pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
-                       int32_t w, int32_t act_dtype, uint32_t flags, hipStream_t st);
+                       int32_t w, int32_t act_dtype, uint32_t flags, void* scratch, size_t scratch_bytes,
+                       hipStream_t st);
+
+// scratch bytes pp_conv2d_fwd can use for this layer and input (0: none)
+size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype);
 
 }  // namespace pp

@@ -71,18 +71,59 @@ static int env_recipe() {
   return std::atoi(e);
 }
 
-ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
+static int env_int(const char* name) {
+  const char* e = std::getenv(name);
+  if (!e || !*e) return -1;
+  return std::atoi(e);
+}
+
+// output tiles of a recipe for this layer
+static long tiles_of(int id, const ConvParams& p) {
+  const RecipeInfo r = recipe_info(id);
+  const long th = (64 / r.lw) * r.r, tw = static_cast<long>(r.lw) * r.cc;
+  return ((p.ho + th - 1) / th) * ((p.wo + tw - 1) / tw);
+}
+
+// channel split of a wave-pipeline recipe: only for grids of at most one
+// wave per SIMD (1024 waves), up to about 4 waves per SIMD, keeping at least
+// 8 channels per wave (measured on MI355X: splitting grids that already hold
+// 1.5-2 waves per SIMD costs more in partial sums than it gains)
+static int choose_split(int id, const ConvParams& p) {
+  const RecipeInfo r = recipe_info(id);
+  const long items = static_cast<long>(p.n) * tiles_of(id, p) * p.n_groups;
+  const long waves = items * r.ws;
+  int ks = 1;
+  if (waves <= 1024)
+    while (waves * ks * 2 <= 4096 && static_cast<long>(p.c_in) / (ks * 2) >= 8L * r.ws) ks *= 2;
+  const int forced = env_int("PP_KSPLIT");
+  if (forced >= 1) ks = forced < p.c_in ? forced : p.c_in;
+  return ks;
+}
+
+static ConvPlan finish_plan(int id, const ConvParams& p, bool allow_split) {
   ConvPlan plan;
+  plan.recipe = id;
+  plan.ksplit = (allow_split && is_wave_recipe(id)) ? choose_split(id, p) : 1;
+  return plan;
+}
+
+size_t split_bytes(const ConvPlan& plan, const ConvParams& p) {
+  if (plan.ksplit <= 1) return 0;
+  const RecipeInfo r = recipe_info(plan.recipe);
+  const size_t items = static_cast<size_t>(p.n) * tiles_of(plan.recipe, p) * p.n_groups;
+  return items * plan.ksplit * 8 * r.r * r.cc * 64 * sizeof(float);
+}
+
+ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
   const int forced = env_recipe();
-  if (forced >= 0 && forced < kNumRecipes && recipe_usable(forced, p, lib, bf16)) {
-    plan.recipe = forced;
-    return plan;
-  }
+  if (forced >= 0 && forced < kNumRecipes && recipe_usable(forced, p, lib, bf16))
+    return finish_plan(forced, p, allow_split);
   const long pix = static_cast<long>(p.ho) * p.wo;
   int pref[4];
-  if ((lib == kLibCanon8 || lib == kLibDense9) && !bf16 && p.stride == 1 && p.pad == p.dil) {
-    // fp32, stride 1: the wave-pipeline tilings that timed fastest on the
-    // VGG-16 layer shapes (MI355X), by output size; v4 tilings as fallback
+  const bool wave_ok = (lib == kLibCanon8 || lib == kLibDense9) && p.pad == p.dil;
+  if (wave_ok && !bf16 && p.stride == 1 && p.n == 1) {
+    // fp32, stride 1, one image: the wave-pipeline tilings that timed fastest
+    // on the VGG-16 layer shapes (MI355X), by output size; v4 tilings as fallback
     if (lib == kLibDense9 || p.c_in <= 8) {
       pref[0] = 31; pref[1] = 20; pref[2] = 0; pref[3] = 13;
     } else if (pix >= 160L * 160L) {
@@ -93,8 +134,23 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
       pref[0] = 27; pref[1] = 22; pref[2] = 8; pref[3] = 13;
     } else if (pix >= 20L * 20L) {
       pref[0] = 23; pref[1] = 22; pref[2] = 8; pref[3] = 13;
+    } else if (allow_split) {
+      pref[0] = 24; pref[1] = 25; pref[2] = 10; pref[3] = 13;   // 24 runs split 4 ways at 14 x 14
     } else {
       pref[0] = 25; pref[1] = 23; pref[2] = 10; pref[3] = 13;
+    }
+  } else if (wave_ok) {
+    // batches, strides 2, bf16 (timed on the style-transfer, super-resolution
+    // and colourization layer shapes): 2 x 4 outputs per lane; two channel
+    // splits per tile for very large grids, else four; few input channels
+    // (first layers) with 1 x 4 outputs per lane
+    const long items = static_cast<long>(p.n) * tiles_of(31, p) * p.n_groups;
+    if (p.c_in <= 8) {
+      pref[0] = 29; pref[1] = 31; pref[2] = 13; pref[3] = 13;
+    } else if (items >= 4096) {
+      pref[0] = 31; pref[1] = 20; pref[2] = 13; pref[3] = 13;
+    } else {
+      pref[0] = 20; pref[1] = 31; pref[2] = 13; pref[3] = 13;
     }
   } else if (pix >= 100L * 100L) {
     pref[0] = 0; pref[1] = 3; pref[2] = 12; pref[3] = 13;
@@ -106,12 +162,8 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16) {
     pref[0] = 8; pref[1] = 13; pref[2] = 13; pref[3] = 13;
   }
   for (int id : pref)
-    if (recipe_usable(id, p, lib, bf16)) {
-      plan.recipe = id;
-      return plan;
-    }
-  plan.recipe = 13;
-  return plan;
+    if (recipe_usable(id, p, lib, bf16)) return finish_plan(id, p, allow_split);
+  return finish_plan(13, p, allow_split);
 }
 
 template <int LIB, class TA>
@@ -132,7 +184,10 @@ static hipError_t launch_wave(int id, const ConvParams& p, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st) {
+hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p0, bool bf16_act, hipStream_t st) {
+  ConvParams p = p0;
+  p.ksplit = plan.ksplit;
+  if (plan.ksplit > 1 && !is_wave_recipe(plan.recipe)) return hipErrorInvalidConfiguration;
   if (!recipe_usable(plan.recipe, p, lib, bf16_act)) return hipErrorInvalidConfiguration;
   if (is_wave_recipe(plan.recipe)) {
     if (lib == kLibDense9)

@@ -24,6 +24,10 @@ struct ConvParams {
   int n_patterns = 0;
   uint32_t flags = 0;
   int tiles_x = 0, tiles_y = 0, n_ftiles = 0;   // filled by the launcher
+  // channel split over workgroups (wave-pipeline kernel): ksplit partial-sum
+  // blocks per output tile in `part`, added by a second kernel
+  int ksplit = 1;
+  float* part = nullptr;
 };
 
 // The compiled tilings ("recipes"):
@@ -105,9 +109,13 @@ bool recipe_compiled(int lib, int id);
 
 struct ConvPlan {
   int recipe = 0;
+  int ksplit = 1;   // channel split over workgroups (needs scratch, see split_bytes)
 };
 
-ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16);
+// allow_split: the caller can provide scratch for a channel split
+ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split);
+// scratch bytes a plan needs (its partial-sum blocks); 0 without a split
+size_t split_bytes(const ConvPlan& plan, const ConvParams& p);
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st);
 
 template <int LIB, int S, int D, class TA>

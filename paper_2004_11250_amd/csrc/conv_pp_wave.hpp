@@ -169,6 +169,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
   const int grp = blk % a.n_groups;
   blk /= a.n_groups;
+  const int ks = blk % a.ksplit;       // this workgroup's share of the input channels
+  blk /= a.ksplit;
   const int tx = blk % a.tiles_x;
   blk /= a.tiles_x;
   const int ty = blk % a.tiles_y;
@@ -202,8 +204,12 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
     }
 
   // ---- this wave's channel range
-  const int per = (a.c_in + WS - 1) / WS;
-  const int c0 = min(a.c_in, wk * per), c1 = min(a.c_in, c0 + per);
+  // channels [kc0, kc1) of this workgroup (split ks of ksplit), then the
+  // wave's contiguous part of them
+  const int kc0 = static_cast<int>(static_cast<int64_t>(ks) * a.c_in / a.ksplit);
+  const int kc1 = static_cast<int>(static_cast<int64_t>(ks + 1) * a.c_in / a.ksplit);
+  const int per = (kc1 - kc0 + WS - 1) / WS;
+  const int c0 = min(kc1, kc0 + wk * per), c1 = min(kc1, c0 + per);
   const uint32_t e_base = static_cast<uint32_t>(grp) * a.c_in;
   const uint32_t e_last = e_base + a.c_in - 1;
 
@@ -519,12 +525,56 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   }
 
   // ---- combine the WS partial sums, PS slots at a time, in wave order; wave
-  // k then finishes units u = k, k + WS, ... of the pass (unit = slot, row)
+  // k then finishes units u = k, k + WS, ... of the pass (unit = slot, row).
+  // With a channel split over workgroups (ksplit > 1) the unit's sum goes to
+  // this workgroup's block of the partial-sum buffer instead; a second kernel
+  // adds the ksplit blocks of each tile in split order and finishes.
   TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
   const bool relu = (a.flags & PP_RELU) != 0;
   const int oxl = ox0 + lx * CC;
   const bool vec = (CC % 4 == 0) && (a.wo % 4 == 0) && (reinterpret_cast<uintptr_t>(a.y) % (4 * sizeof(TA)) == 0);
   constexpr int NU = G::PS * R;   // units per pass
+  constexpr int BLK = 8 * R * CC * 64;   // floats of one workgroup's partial-sum block
+  const bool split = a.ksplit > 1;
+  const uint32_t item = ((static_cast<uint32_t>(img) * a.tiles_y + ty) * a.tiles_x + tx) * a.n_groups + grp;
+  auto finish = [&](int s, int r, float (&v)[CC]) __attribute__((always_inline)) {
+    const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
+    const uint32_t o = sload<uint32_t>(blob, a.off_perm + 4 * slot);
+    if (o >= static_cast<uint32_t>(a.c_out)) return;   // padding slot
+    const float bias = sload<float>(blob, a.off_bias + 4 * slot);
+    const int oy = oy0 + ly * R + r;
+    if (oy >= a.ho) return;
+#pragma unroll
+    for (int q = 0; q < CC; ++q) {
+      v[q] += bias;
+      if (relu) v[q] = fmaxf(v[q], 0.0f);
+    }
+    TA* row = y + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
+    if (vec && oxl + CC <= a.wo) {
+#pragma unroll
+      for (int q = 0; q < CC; q += 4) {
+        if constexpr (ABF) {
+          uint2 uu;
+          uu.x = to_bf16_bits(v[q]) | (to_bf16_bits(v[q + 1]) << 16);
+          uu.y = to_bf16_bits(v[q + 2]) | (to_bf16_bits(v[q + 3]) << 16);
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(row) + oxl + q) = uu;
+        } else {
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(row) + oxl + q) =
+              make_float4(v[q], v[q + 1], v[q + 2], v[q + 3]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < CC; ++q) {
+        if (oxl + q < a.wo) {
+          if constexpr (ABF)
+            reinterpret_cast<uint16_t*>(row)[oxl + q] = static_cast<uint16_t>(to_bf16_bits(v[q]));
+          else
+            reinterpret_cast<float*>(row)[oxl + q] = v[q];
+        }
+      }
+    }
+  };
 #pragma unroll
   for (int s0 = 0; s0 < 8; s0 += G::PS) {
     if (WS > 1) {
@@ -556,43 +606,54 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
 #pragma unroll
         for (int q = 0; q < CC; ++q) v[q] = acc[s][r][q];
       }
-      const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
-      const uint32_t o = sload<uint32_t>(blob, a.off_perm + 4 * slot);
-      if (o >= static_cast<uint32_t>(a.c_out)) continue;   // padding slot
-      const float bias = sload<float>(blob, a.off_bias + 4 * slot);
-      const int oy = oy0 + ly * R + r;
-      if (oy >= a.ho) continue;
+      if (split) {
+        float* pb = a.part + static_cast<size_t>(item * a.ksplit + ks) * BLK + lane;
 #pragma unroll
-      for (int q = 0; q < CC; ++q) {
-        v[q] += bias;
-        if (relu) v[q] = fmaxf(v[q], 0.0f);
-      }
-      TA* row = y + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
-      if (vec && oxl + CC <= a.wo) {
-#pragma unroll
-        for (int q = 0; q < CC; q += 4) {
-          if constexpr (ABF) {
-            uint2 uu;
-            uu.x = to_bf16_bits(v[q]) | (to_bf16_bits(v[q + 1]) << 16);
-            uu.y = to_bf16_bits(v[q + 2]) | (to_bf16_bits(v[q + 3]) << 16);
-            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(row) + oxl + q) = uu;
-          } else {
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(row) + oxl + q) =
-                make_float4(v[q], v[q + 1], v[q + 2], v[q + 3]);
-          }
-        }
+        for (int q = 0; q < CC; ++q) pb[((s * R + r) * CC + q) * 64] = v[q];
       } else {
-#pragma unroll
-        for (int q = 0; q < CC; ++q) {
-          if (oxl + q < a.wo) {
-            if constexpr (ABF)
-              reinterpret_cast<uint16_t*>(row)[oxl + q] = static_cast<uint16_t>(to_bf16_bits(v[q]));
-            else
-              reinterpret_cast<float*>(row)[oxl + q] = v[q];
-          }
-        }
+        finish(s, r, v);
       }
     }
+  }
+}
+
+// Second pass of a channel split: y = act(sum over the ksplit partial-sum
+// blocks of a tile, in split order, + bias), stored through perm.  One
+// workgroup per (image, tile, slot group); thread i handles element i of the
+// tile's block layout ((slot, row, col) x lane).
+template <int R, int CC, int LW, class TA>
+__global__ __launch_bounds__(256) void pp_split_reduce_kernel(ConvParams a) {
+  constexpr bool ABF = sizeof(TA) == 2;
+  constexpr int LH = 64 / LW, TH = LH * R, TW = LW * CC;
+  constexpr int BLK = 8 * R * CC * 64;
+  const uint32_t item = blockIdx.x;
+  const int grp = item % a.n_groups;
+  uint32_t t = item / a.n_groups;
+  const int tx = t % a.tiles_x;
+  t /= a.tiles_x;
+  const int ty = t % a.tiles_y;
+  const int img = t / a.tiles_y;
+  const float* pb = a.part + static_cast<size_t>(item) * a.ksplit * BLK;
+  TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  const bool relu = (a.flags & PP_RELU) != 0;
+  for (int i = threadIdx.x; i < BLK; i += 256) {
+    const int lane = i % 64, e = i / 64;       // e = (s * R + r) * CC + q
+    const int q = e % CC, r = (e / CC) % R, s = e / (CC * R);
+    const int lx = lane % LW, ly = lane / LW;
+    const int oy = ty * TH + ly * R + r, ox = tx * TW + lx * CC + q;
+    if (oy >= a.ho || ox >= a.wo) continue;
+    const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
+    const uint32_t o = reinterpret_cast<const uint32_t*>(a.blob + a.off_perm)[slot];
+    if (o >= static_cast<uint32_t>(a.c_out)) continue;   // padding slot
+    float v = 0.0f;
+    for (int k = 0; k < a.ksplit; ++k) v += pb[static_cast<size_t>(k) * BLK + i];
+    v += reinterpret_cast<const float*>(a.blob + a.off_bias)[slot];
+    if (relu) v = fmaxf(v, 0.0f);
+    const size_t at = (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
+    if constexpr (ABF)
+      reinterpret_cast<uint16_t*>(y)[at] = static_cast<uint16_t>(to_bf16_bits(v));
+    else
+      reinterpret_cast<float*>(y)[at] = v;
   }
 }
 
@@ -607,10 +668,15 @@ hipError_t launch_wave_tiling(ConvParams p, hipStream_t st) {
     p.tiles_x = (p.wo + G::TW - 1) / G::TW;
     p.tiles_y = (p.ho + G::TH - 1) / G::TH;
     p.n_ftiles = p.n_groups;
-    const size_t nb = static_cast<size_t>(p.n_groups) * p.tiles_x * p.tiles_y * p.n;
+    if (p.ksplit < 1 || p.ksplit > p.c_in || (p.ksplit > 1 && !p.part)) return hipErrorInvalidValue;
+    const size_t nb = static_cast<size_t>(p.n_groups) * p.tiles_x * p.tiles_y * p.n * p.ksplit;
     if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((pp_conv3x3_wave_kernel<LIB, S, D, R, CC, LW, WS, SH, TA>), dim3(static_cast<uint32_t>(nb)),
                        dim3(WS * 64), 0, st, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.ksplit == 1) return e;
+    hipLaunchKernelGGL((pp_split_reduce_kernel<R, CC, LW, TA>), dim3(static_cast<uint32_t>(nb / p.ksplit)), dim3(256),
+                       0, st, p);
     return hipGetLastError();
   }
 }

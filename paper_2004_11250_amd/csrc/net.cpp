@@ -26,6 +26,8 @@ struct Plan {
   size_t slot_bytes[PP_MAX_SLOTS] = {};
   size_t slot_off[PP_MAX_SLOTS] = {};
   size_t ws_bytes = 0;
+  // scratch of the pruned convs' channel splits (partial sums), after the slots
+  size_t scratch_off = 0, scratch_bytes = 0;
   Shape final_shape;
 };
 
@@ -43,6 +45,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
   pl->out.resize(n_ops);
   pl->views.resize(n_ops);
   std::vector<Shape> writes1;
+  size_t part_max = 0;
   for (int i = 0; i < n_ops; ++i) {
     const pp_net_op& op = ops[i];
     if (op.src < 0 || op.src >= PP_MAX_SLOTS || op.dst < 1 || op.dst >= PP_MAX_SLOTS) return bad(i, "slot out of range");
@@ -57,6 +60,10 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
         if (!op.d_blob) return bad(i, "d_blob is NULL");
         const BlobView& v = pl->views[i];
         if (v.c_in != s.c) return bad(i, "input channels do not match the blob");
+        {
+          const size_t pb = conv_scratch_bytes(v, n, s.h, s.w, act);
+          if (pb > part_max) part_max = pb;
+        }
         if (op.flags & ~static_cast<uint32_t>(PP_RELU)) return bad(i, "unknown flags");
         int ho = 0, wo = 0;
         st = conv_check(v, n, s.h, s.w, act, &ho, &wo);
@@ -125,7 +132,9 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
     pl->slot_off[sl] = off;
     off += (pl->slot_bytes[sl] + 255) / 256 * 256;
   }
-  pl->ws_bytes = off;
+  pl->scratch_off = off;
+  pl->scratch_bytes = (part_max + 255) / 256 * 256;
+  pl->ws_bytes = off + pl->scratch_bytes;
   return PP_OK;
 }
 
@@ -166,6 +175,7 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
     if (s == 1) return y;
     return static_cast<uint8_t*>(workspace) + pl.slot_off[s];
   };
+  void* scratch = pl.scratch_bytes ? static_cast<uint8_t*>(workspace) + pl.scratch_off : nullptr;
   for (int i = 0; i < n_ops; ++i) {
     const pp_net_op& op = ops[i];
     const Shape& si = pl.in[i];
@@ -175,7 +185,8 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
     hipError_t e = hipSuccess;
     switch (op.kind) {
       case PP_OP_CONV_PP:
-        st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags, stream);
+        st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags, scratch,
+                          pl.scratch_bytes, stream);
         if (st != PP_OK) return st;
         break;
       case PP_OP_CONV_DENSE:

@@ -105,7 +105,7 @@ def test_pack_rejects_bad_arguments(lib):
 
 def _conv(lib, blob, x=0x100000, y=0x200000, n=1, h=16, w=16, dt=0, flags=0, dblob=0x300000):
     b = np.ascontiguousarray(blob, np.uint8)
-    return lib.pp_conv2d_fwd(b.ctypes.data, b.nbytes, dblob, x, y, n, h, w, dt, flags, None)
+    return lib.pp_conv2d_fwd(b.ctypes.data, b.nbytes, dblob, x, y, n, h, w, dt, flags, None, 0, None)
 
 
 def test_conv_validation_happens_before_any_launch(lib):

@@ -223,3 +223,31 @@ def test_every_tiling(recipe, monkeypatch):
             assert used == recipe, "the forced tiling must run for a stride-1 fp32 canonical layer"
         y, ref, bound = run_layer(L, x, s, p, d, relu=True, dtype=dtype)
         check(y, ref, bound, dtype, f"recipe {recipe} {(s, p, d)} {dtype}")
+
+
+# channel split over workgroups (partial sums in the workspace, the last
+# workgroup of a tile adds them in split order): forced splits, ragged
+# channel shares, both activation dtypes
+@pytest.mark.parametrize("recipe,ksplit", [(20, 2), (21, 3), (23, 4), (25, 7), (27, 5), (22, 16)])
+def test_channel_split(recipe, ksplit, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    for dtype, shape in (("f32", (21, 77, 29, 36)), ("f32", (16, 64, 14, 14)), ("bf16", (19, 70, 23, 28))):
+        c_out, c_in, h, w = shape
+        seed = 300 + recipe
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.4)
+        x = workloads.random_input(seed, (1, c_in, h, w))
+        wd = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
+        blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, wd)
+        used = pp.conv2d_plan(blob, 1, h, w, wd)
+        _say("split", recipe, ksplit, dtype, shape, "runs as", used)
+        if dtype == "f32":
+            assert used == (recipe, ksplit)
+        y, ref, bound = run_layer(L, x, relu=True, dtype=dtype)
+        check(y, ref, bound, dtype, f"split {recipe}/{ksplit} {dtype} {shape}")
+        # repeated calls (counters left at zero, partials rewritten): bitwise equal
+        layer = pp.PackedLayer(blob)
+        xd = _to_dev(obf16.round_f32(x) if dtype == "bf16" else x, dtype)
+        y1 = _from_dev(pp.conv2d_fwd(layer, xd, relu=True))
+        y2 = _from_dev(pp.conv2d_fwd(layer, xd, relu=True))
+        assert np.array_equal(y1, y2)

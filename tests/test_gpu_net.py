@@ -111,7 +111,7 @@ def test_vgg16_net_equals_chained_layer_calls():
     li = 0
     for op, prm in zip(spec["ops"], params):
         if op["op"] == "conv3":
-            cur = pp.conv2d_fwd(net.layers[li], cur, relu=op["relu"])
+            cur = pp.conv2d_fwd(net.pruned[li], cur, relu=op["relu"])
             li += 1
         else:
             one = pp.Net([dict(op, src=0, dst=1)], [prm], "f32")
