@@ -82,7 +82,8 @@ def surviving_macs(op, prm, oshape, batch):
     return 0
 
 
-KERNEL_SOURCES = ("conv_pp_kernel.hpp", "conv_pp_inst.hpp", "conv_pp.hpp", "conv_plan.cpp", "conv_pp_c8_s1d1.hip")
+KERNEL_SOURCES = ("conv_pp_kernel.hpp", "conv_pp_inst.hpp", "conv_pp.hpp", "conv_plan.cpp", "conv_pp_c8_s1d1.hip",
+                  "conv_pp_wave.hpp", "conv_pp_wave_inst.hpp", "conv_pp_wave_s1d1.hip", "conv_pp_wave_d9_s1d1.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pp_conv3x3_vgg16_224x224_b1_traffic.json")
 
 
@@ -98,9 +99,12 @@ def kernel_source_hash():
 
 
 def _kernel_label(name):
-    """Kernel name without 'void ' and without its parameter list."""
-    name = name.replace("void ", "")
-    return name[:name.rfind("(")] if name.endswith(")") else name
+    """Kernel name(s) without 'void ' and without the parameter lists."""
+    out = []
+    for part in name.split(" + "):
+        part = part.replace("void ", "")
+        out.append(part[:part.rfind("(")] if part.endswith(")") else part)
+    return " + ".join(out)
 
 
 def summarize_profile(root, cfg=2):
@@ -134,19 +138,36 @@ def summarize_profile(root, cfg=2):
         return [d[k] for k in sorted(d)]
 
     def frames(ds):
-        first = next(i for i, e in enumerate(ds) if "pp_conv3x3_kernel" in e["name"])
+        # a frame is one dispatch per op, starting at the first pruned-conv
+        # launch; a channel-split conv is followed by its reduction dispatch,
+        # which is merged into the conv's entry
+        def is_conv(e):
+            return "pp_conv3x3" in e["name"]
+
+        first = next(i for i, e in enumerate(ds) if is_conv(e))
         out = []
-        while first + n_ops <= len(ds) and "pp_conv3x3_kernel" in ds[first]["name"]:
-            out.append(ds[first:first + n_ops])
-            first += n_ops
-            if len(out) == 3:
-                break
+        while len(out) < 3 and first < len(ds) and is_conv(ds[first]):
+            fr, j = [], first
+            for _ in range(n_ops):
+                if j >= len(ds):
+                    return out
+                e = dict(ds[j], c=dict(ds[j]["c"]))
+                j += 1
+                if j < len(ds) and "pp_split_reduce" in ds[j]["name"]:
+                    e["dur_ns"] += ds[j]["dur_ns"]
+                    for k, v in ds[j]["c"].items():
+                        e["c"][k] = e["c"].get(k, 0.0) + v
+                    e["name"] += " + " + ds[j]["name"]
+                    j += 1
+                fr.append(e)
+            out.append(fr)
+            first = j
         return out
 
     def calib(ds, counter, mib):
         # the elementwise copy: the largest grid among the non-library kernels
         # before the first frame, reads and writes exactly mib MiB
-        first = next(i for i, e in enumerate(ds) if "pp_conv3x3_kernel" in e["name"])
+        first = next(i for i, e in enumerate(ds) if "pp_conv3x3" in e["name"])
         cands = [e for e in ds[:first] if "mul" in e["name"].lower() or "elementwise" in e["name"].lower()]
         e = max(cands, key=lambda e: int(e["grid"]))
         return mib * 1024.0 / e["c"][counter], e["c"][counter]
