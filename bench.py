@@ -112,14 +112,17 @@ def summarize_profile(root, cfg=2):
     --stats; fetch/, write/: --pmc FETCH_SIZE / WRITE_SIZE of a run with
     --copy-mib; sq*/: other --pmc passes) for one frame of the network: the
     dispatches of the first frame are the len(ops) dispatches starting at the
-    first pruned-conv launch.  Writes the traffic JSON read by the benchmark
-    and prints a markdown summary."""
+    first pruned-conv launch (a max pool fused into the conv before it has no
+    dispatch of its own).  Writes the traffic JSON read by the benchmark and
+    prints a markdown summary."""
     import csv
     import glob
 
+    import paper_2004_11250_amd as pp
     import workloads
     spec = workloads.net_spec(cfg)
-    n_ops = len(spec["ops"])
+    fused = pp.fused_pools(spec["ops"])
+    n_disp = len(spec["ops"]) - len(fused)
     shapes = layer_shapes(spec)
 
     def rows(sub):
@@ -138,9 +141,9 @@ def summarize_profile(root, cfg=2):
         return [d[k] for k in sorted(d)]
 
     def frames(ds):
-        # a frame is one dispatch per op, starting at the first pruned-conv
-        # launch; a channel-split conv is followed by its reduction dispatch,
-        # which is merged into the conv's entry
+        # a frame is one dispatch per unfused op, starting at the first
+        # pruned-conv launch; a channel-split conv is followed by its
+        # reduction dispatch, which is merged into the conv's entry
         def is_conv(e):
             return "pp_conv3x3" in e["name"]
 
@@ -148,7 +151,7 @@ def summarize_profile(root, cfg=2):
         out = []
         while len(out) < 3 and first < len(ds) and is_conv(ds[first]):
             fr, j = [], first
-            for _ in range(n_ops):
+            for _ in range(n_disp):
                 if j >= len(ds):
                     return out
                 e = dict(ds[j], c=dict(ds[j]["c"]))
@@ -182,17 +185,24 @@ def summarize_profile(root, cfg=2):
     for sub in sorted(os.listdir(root)):
         if sub.startswith("sq") and os.path.isdir(os.path.join(root, sub)):
             for fr in frames(by_dispatch(rows(sub)))[:1]:
-                for i, e in enumerate(fr):
-                    sq.setdefault(i, {}).update(e["c"])
+                for di, e in enumerate(fr):
+                    sq.setdefault(di, {}).update(e["c"])
     lay = []
+    di = -1   # dispatch index within a frame
     for i, (k, op, ish, osh) in enumerate(shapes):
-        dur = sum(f[i]["dur_ns"] for f in kt_fr) / len(kt_fr) / 1e3
-        fetch = sum(f[i]["c"]["FETCH_SIZE"] for f in fe_fr) / len(fe_fr) * ff * 1024
-        write = sum(f[i]["c"]["WRITE_SIZE"] for f in wr_fr) / len(wr_fr) * wf * 1024
-        lay.append(dict(op=i, kind=op["op"], lib=op.get("lib", ""), c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
-                        kernel=_kernel_label(kt_fr[0][i]["name"]), us=round(dur, 3),
-                        fetch_mb=round(fetch / 1e6, 3), write_mb=round(write / 1e6, 3), sq=sq.get(i, {})))
-    pr = [l for l in lay if l["kind"] == "conv3" and l["lib"] == "canon8"]
+        if i in fused:
+            lay.append(dict(op=i, kind=op["op"], lib="", c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
+                            kernel=f"(fused into op {i - 1})", us=0.0, fetch_mb=0.0, write_mb=0.0, sq={}))
+            continue
+        di += 1
+        dur = sum(f[di]["dur_ns"] for f in kt_fr) / len(kt_fr) / 1e3
+        fetch = sum(f[di]["c"]["FETCH_SIZE"] for f in fe_fr) / len(fe_fr) * ff * 1024
+        write = sum(f[di]["c"]["WRITE_SIZE"] for f in wr_fr) / len(wr_fr) * wf * 1024
+        kind = op["op"] + ("+maxpool2" if i + 1 in fused else "")
+        lay.append(dict(op=i, kind=kind, lib=op.get("lib", ""), c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
+                        kernel=_kernel_label(kt_fr[0][di]["name"]), us=round(dur, 3),
+                        fetch_mb=round(fetch / 1e6, 3), write_mb=round(write / 1e6, 3), sq=sq.get(di, {})))
+    pr = [l for l in lay if l["kind"].startswith("conv3") and l["lib"] == "canon8"]
     traffic = dict(kernel_source_sha256=kernel_source_hash(), fetch_factor=round(ff, 4), write_factor=round(wf, 4),
                    launches=len(pr), bytes_per_frame=int(sum((l["fetch_mb"] + l["write_mb"]) * 1e6 for l in pr)),
                    us_per_frame=round(sum(l["us"] for l in pr), 3),
@@ -286,30 +296,36 @@ def main():
     total_macs = sum(surviving_macs(op, prm, o, batch) for (i, op, _, o), prm in zip(shapes, params))
     value = total_macs / (ms * 1e-3) / 1e9
 
-    # ---- per-layer timing of the pruned-conv kernel (same launches as in the frame)
+    # ---- per-layer timing of the pruned-conv kernel (same launches as in the
+    # frame: a conv whose max pool pp_net_fwd fuses runs with PP_MAXPOOL2)
     layers = []
     li = 0
     esz = 2 if dtype == "bf16" else 4
+    fused = pp.fused_pools(spec["ops"])
     for (i, op, ishape, o), prm in zip(shapes, params):
         if op["op"] != "conv3":
             continue
         L = net.pruned[li]
         li += 1
+        pool = i + 1 in fused
+        if pool:
+            o = (o[0], o[1] // 2, o[2] // 2)
         xin = torch.rand((batch,) + ishape, device=dev).to(tdt)
         yo = torch.empty((batch,) + o, device=dev, dtype=tdt)
         for _ in range(5):
-            pp.conv2d_fwd(L, xin, relu=op["relu"], out=yo)
+            pp.conv2d_fwd(L, xin, relu=op["relu"], out=yo, maxpool2=pool)
         torch.cuda.synchronize()
         a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a0.record(stream)
         for _ in range(args.layer_steps):
-            pp.conv2d_fwd(L, xin, relu=op["relu"], out=yo)
+            pp.conv2d_fwd(L, xin, relu=op["relu"], out=yo, maxpool2=pool)
         a1.record(stream)
         torch.cuda.synchronize()
         us = a0.elapsed_time(a1) * 1e3 / args.layer_steps
-        macs = surviving_macs(op, prm, o, batch)
+        macs = surviving_macs(op, prm, shapes[i][3], batch)
         alg_bytes = batch * (int(np.prod(ishape)) + int(np.prod(o))) * esz + L.h_blob.nbytes
         layers.append(dict(op=i, c_in=op["c_in"], c_out=op["c_out"], hw=f"{o[1]}x{o[2]}", lib=op["lib"],
+                           maxpool2=pool,
                            surviving_mmac=round(macs / 1e6, 3), us=round(us, 3),
                            eff_tmacs=round(macs / us / 1e6, 3), alg_mb=round(alg_bytes / 1e6, 3),
                            frac_fp32_peak=round(2 * macs / us / 1e6 / PEAK_FP32_VECTOR_TFLOPS, 4)))

@@ -49,8 +49,10 @@ typedef enum {
 
 typedef enum { PP_F32 = 0, PP_BF16 = 1 } pp_dtype;
 
-/* flags of pp_conv2d_fwd / pp_net_op */
-enum { PP_RELU = 1u };
+/* flags of pp_conv2d_fwd / pp_net_op.  PP_MAXPOOL2 (pp_conv2d_fwd only):
+ * store the 2 x 2, stride 2 max pool of the activated output instead of the
+ * output itself (graph-level fusion of conv, activation and pooling). */
+enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u };
 
 /* Shape and storage of one pruned 3x3 layer. */
 typedef struct {
@@ -130,8 +132,16 @@ pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
  *   x                   device [n][c_in][h][w] in act_dtype
  *   y                   device [n][c_out][h_out][w_out] in act_dtype,
  *                       h_out = (h + 2 pad - 2 dilation - 1)/stride + 1;
- *                       must not overlap x
- *   flags               PP_RELU
+ *                       with PP_MAXPOOL2 [n][c_out][h_out/2][w_out/2]
+ *                       (floor); must not overlap x
+ *   flags               PP_RELU, PP_MAXPOOL2 (y = maxpool2x2(act(conv +
+ *                       bias)): the max of the same activated values the
+ *                       unpooled call would store when both run the same
+ *                       tiling (within the fp32 accumulation tolerance
+ *                       otherwise); needs h_out, w_out >= 2 and a tiling
+ *                       that holds whole 2 x 2 windows per lane: the
+ *                       canonical or all-ones library with pad = dilation,
+ *                       else PP_EUNSUPPORTED; never splits the channels)
  *   workspace, ws_bytes optional device scratch (NULL, 0 for none), 256-byte
  *                       aligned.  With pp_conv2d_workspace() bytes the
  *                       kernel may split the input channels over more

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_PKG, "libppconv.so")
 PP_OK, PP_EINVAL, PP_ESIZE, PP_EBLOB, PP_EUNSUPPORTED, PP_EHIP = 0, -1, -2, -3, -4, -5
 PP_F32, PP_BF16 = 0, 1
 PP_RELU = 1
+PP_MAXPOOL2 = 2
 (OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
 
 # exported symbols declared in include/pp.h
@@ -203,10 +204,12 @@ class PackedLayer:
         return cls(pack(w, b, pattern_id, conn, lib_masks, stride, pad, dilation, wdtype), device)
 
 
-def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspace="auto"):
+def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspace="auto", maxpool2=False):
     """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None).
     workspace: "auto" (a scratch tensor of pp_conv2d_workspace bytes, kept on
-    the layer per input shape), None (no scratch) or a uint8 device tensor."""
+    the layer per input shape), None (no scratch) or a uint8 device tensor.
+    maxpool2: store the 2 x 2 max pool of the activated output (PP_MAXPOOL2);
+    the channel split is then never used, so no workspace is needed."""
     torch = _torch()
     lib = load_library()
     if not x.is_contiguous():
@@ -215,6 +218,9 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     if c != layer.info["c_in"]:
         raise ValueError(f"x has {c} channels, the layer expects {layer.info['c_in']}")
     ho, wo = out_size(layer.h_blob, h, w)
+    if maxpool2:
+        ho, wo = ho // 2, wo // 2
+        workspace = None
     shape = (n, layer.info["c_out"], ho, wo)
     if out is None:
         out = torch.empty(shape, dtype=x.dtype, device=x.device)
@@ -231,7 +237,8 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
             workspace = None
     ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel()) if workspace is not None else (None, 0)
     st = lib.pp_conv2d_fwd(_ptr(layer.h_blob), layer.h_blob.nbytes, layer.d_blob.data_ptr(), x.data_ptr(),
-                           out.data_ptr(), n, h, w, _dtype_code(x), PP_RELU if relu else 0, ws_ptr, ws_bytes,
+                           out.data_ptr(), n, h, w, _dtype_code(x),
+                           (PP_RELU if relu else 0) | (PP_MAXPOOL2 if maxpool2 else 0), ws_ptr, ws_bytes,
                            _stream_ptr(stream))
     _check(st, "pp_conv2d_fwd")
     return out
@@ -245,6 +252,34 @@ def _bf16_bits(a: np.ndarray) -> np.ndarray:
     """fp32 -> bf16 bit patterns, round to nearest even (offline weight prep)."""
     u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
     return (((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF).astype(np.uint16)
+
+
+def fused_pools(ops) -> set:
+    """Indices of the 2 x 2 max-pool ops that pp_net_fwd runs inside the
+    pruned conv just before them (one launch, PP_MAXPOOL2): the pool reads
+    that conv's output slot, the conv does not write slot 1, a pool that
+    writes the conv's input slot has it in the workspace (slot >= 2), no
+    later op reads the conv's output before an op rewrites that slot, and
+    the conv is a canonical / all-ones layer with padding equal to its
+    dilation.  ops: the op dicts of a network spec."""
+    out = set()
+    for i in range(1, len(ops)):
+        cv, mp = ops[i - 1], ops[i]
+        if mp["op"] != "maxpool2" or cv["op"] != "conv3" or mp["src"] != cv["dst"] or cv["dst"] == 1:
+            continue
+        if (mp["dst"] == cv["src"] and cv["src"] < 2) or cv["pad"] != cv["dil"] or \
+                cv.get("lib") not in ("canon8", "dense9"):
+            continue
+        read_later = False
+        for o in ops[i + 1:]:
+            if o["src"] == cv["dst"] or (o["op"] == "add" and o.get("src2") == cv["dst"]):
+                read_later = True
+                break
+            if o["dst"] == cv["dst"]:
+                break
+        if not read_later:
+            out.add(i)
+    return out
 
 
 class Net:

@@ -69,12 +69,14 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const size_t esz = act_dtype == PP_BF16 ? 2 : 4;
   if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % esz)
     return fail(PP_EINVAL, "activation pointers misaligned");
+  if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2)) return fail(PP_EINVAL, "unknown flags");
+  const bool pool = (flags & PP_MAXPOOL2) != 0;
+  if (pool && (ho < 2 || wo < 2)) return fail(PP_EINVAL, "pooled output needs h_out, w_out >= 2");
   const uint8_t* xb = static_cast<const uint8_t*>(x);
   const uint8_t* yb = static_cast<const uint8_t*>(y);
   const size_t xbytes = static_cast<size_t>(n) * v.c_in * h * w * esz;
-  const size_t ybytes = static_cast<size_t>(n) * v.c_out * ho * wo * esz;
+  const size_t ybytes = static_cast<size_t>(n) * v.c_out * (pool ? (ho / 2) * (wo / 2) : ho * wo) * esz;
   if (xb < yb + ybytes && yb < xb + xbytes) return fail(PP_EINVAL, "x and y overlap");
-  if (flags & ~static_cast<uint32_t>(PP_RELU)) return fail(PP_EINVAL, "unknown flags");
 
   ConvParams p = layer_params(v, n, h, w, ho, wo);
   p.blob = static_cast<const uint8_t*>(d_blob);
@@ -84,6 +86,7 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const int lib = library_kind(v);
   const bool bf = act_dtype == PP_BF16;
   ConvPlan plan = plan_conv(p, lib, bf, scratch != nullptr);
+  if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the max pool for this layer");
   if (plan.ksplit > 1) {
     if (split_bytes(plan, p) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
       plan = plan_conv(p, lib, bf, false);   // not enough scratch: no split
@@ -93,6 +96,14 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;
+}
+
+bool conv_pool_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype) {
+  int ho = 0, wo = 0;
+  if (conv_check(v, n, h, w, act_dtype, &ho, &wo) != PP_OK || ho < 2 || wo < 2) return false;
+  ConvParams p = layer_params(v, n, h, w, ho, wo);
+  p.flags = PP_MAXPOOL2;
+  return plan_conv(p, library_kind(v), act_dtype == PP_BF16, false).recipe >= 0;
 }
 
 size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype) {

@@ -10,16 +10,16 @@ RecipeInfo recipe_info(int id) {
   switch (id) {
 #define PP_X(ID, R, CC, LW, WF, WS, CPW) \
   case ID:                               \
-    return RecipeInfo{R, CC, LW, WF, WS, CPW};
+    return RecipeInfo{R, CC, LW, WF, WS, CPW, 0};
     PP_RECIPES(PP_X)
 #undef PP_X
-#define PP_W(ID, R, CC, LW, WS) \
-  case ID:                      \
-    return RecipeInfo{R, CC, LW, 1, WS, 0};
+#define PP_W(ID, R, CC, LW, WS, P) \
+  case ID:                         \
+    return RecipeInfo{R, CC, LW, 1, WS, 0, P};
     PP_WRECIPES(PP_W)
 #undef PP_W
   }
-  return RecipeInfo{0, 0, 0, 0, 0, 0};
+  return RecipeInfo{0, 0, 0, 0, 0, 0, 0};
 }
 
 static bool is_wave_recipe(int id) { return id >= kFirstWaveRecipe && id < kNumRecipes; }
@@ -27,8 +27,7 @@ static bool is_wave_recipe(int id) { return id >= kFirstWaveRecipe && id < kNumR
 // LDS accounting of the wave-pipeline kernel (shared with WGeo in conv_pp_wave.hpp)
 static bool wave_recipe_fits(const RecipeInfo& r, int s, int d, int lib, bool bf16) {
   const int warea = lib == kLibDense9 ? 128 : 64;
-  const int nslot = bf16 ? 2 : 4;
-  return wave_lds_floats(r.r, r.cc, r.lw, r.ws, s, d, warea, nslot) * 4 <= 160 * 1024 && r.ws >= 1 && r.ws <= 16;
+  return wave_lds_floats(r.r, r.cc, r.lw, r.ws, s, d, warea, bf16) * 4 <= 160 * 1024 && r.ws >= 1 && r.ws <= 16;
 }
 
 bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
@@ -59,9 +58,11 @@ bool recipe_compiled(int lib, int id) {
 }
 
 // a recipe that can run this layer: compiled for the library, fits in LDS,
-// and (wave-pipeline kernel) compiled for the layer's padding (pad = dilation)
+// (wave-pipeline kernel) compiled for the layer's padding (pad = dilation),
+// and (register-pipelined tilings) fp32 with the canonical library
 static bool recipe_usable(int id, const ConvParams& p, int lib, bool bf16) {
   if (!recipe_compiled(lib, id) || !recipe_fits(id, p.stride, p.dil, bf16, lib)) return false;
+  if (recipe_info(id).pipe && (bf16 || lib != kLibCanon8)) return false;
   return !is_wave_recipe(id) || p.pad == p.dil;
 }
 
@@ -82,6 +83,11 @@ static long tiles_of(int id, const ConvParams& p) {
   const RecipeInfo r = recipe_info(id);
   const long th = (64 / r.lw) * r.r, tw = static_cast<long>(r.lw) * r.cc;
   return ((p.ho + th - 1) / th) * ((p.wo + tw - 1) / tw);
+}
+
+// waves of a wave-pipeline recipe's grid (no split)
+static long waves_of(int id, const ConvParams& p) {
+  return static_cast<long>(p.n) * tiles_of(id, p) * p.n_groups * recipe_info(id).ws;
 }
 
 // channel split of a wave-pipeline recipe: only for grids of at most one
@@ -114,24 +120,43 @@ size_t split_bytes(const ConvPlan& plan, const ConvParams& p) {
   return items * plan.ksplit * 8 * r.r * r.cc * 64 * sizeof(float);
 }
 
+// a fused 2 x 2 max pool needs whole windows per lane: wave-pipeline tilings
+// with even R and CC (tile origins are then even too)
+static bool pool_fits(int id) {
+  const RecipeInfo r = recipe_info(id);
+  return is_wave_recipe(id) && r.r % 2 == 0 && r.cc % 2 == 0;
+}
+
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
+  const bool pool = (p.flags & PP_MAXPOOL2) != 0;
+  auto ok = [&](int id) { return recipe_usable(id, p, lib, bf16) && (!pool || pool_fits(id)); };
+  if (pool) allow_split = false;
   const int forced = env_recipe();
-  if (forced >= 0 && forced < kNumRecipes && recipe_usable(forced, p, lib, bf16))
-    return finish_plan(forced, p, allow_split);
+  if (forced >= 0 && forced < kNumRecipes && ok(forced)) return finish_plan(forced, p, allow_split);
   const long pix = static_cast<long>(p.ho) * p.wo;
   int pref[4];
   const bool wave_ok = (lib == kLibCanon8 || lib == kLibDense9) && p.pad == p.dil;
   if (wave_ok && !bf16 && p.stride == 1 && p.n == 1) {
     // fp32, stride 1, one image: the wave-pipeline tilings that timed fastest
-    // on the VGG-16 layer shapes (MI355X), by output size; v4 tilings as fallback
+    // on the VGG-16 and super-resolution layer shapes (MI355X), by output
+    // size; v4 tilings as fallback.  The register-pipelined tilings (32-34,
+    // about 200 registers: two waves per SIMD) win while the whole grid is
+    // resident at once (<= 2048 waves), and lose beyond that.
     if (lib == kLibDense9 || p.c_in <= 8) {
       pref[0] = 31; pref[1] = 20; pref[2] = 0; pref[3] = 13;
     } else if (pix >= 160L * 160L) {
-      pref[0] = 31; pref[1] = 30; pref[2] = 17; pref[3] = 13;
+      const long items31 = static_cast<long>(p.n) * tiles_of(31, p) * p.n_groups;
+      if (waves_of(32, p) <= 2048) {
+        pref[0] = 32; pref[1] = 31; pref[2] = 30; pref[3] = 17;
+      } else if (items31 <= 4096) {
+        pref[0] = 20; pref[1] = 31; pref[2] = 30; pref[3] = 17;
+      } else {
+        pref[0] = 31; pref[1] = 20; pref[2] = 30; pref[3] = 17;
+      }
     } else if (pix >= 80L * 80L) {
-      pref[0] = 20; pref[1] = 19; pref[2] = 3; pref[3] = 13;
+      pref[0] = waves_of(33, p) <= 2048 ? 33 : 20; pref[1] = 20; pref[2] = 19; pref[3] = 3;
     } else if (pix >= 40L * 40L) {
-      pref[0] = 27; pref[1] = 22; pref[2] = 8; pref[3] = 13;
+      pref[0] = waves_of(34, p) <= 2048 ? 34 : 27; pref[1] = 27; pref[2] = 22; pref[3] = 8;
     } else if (pix >= 20L * 20L) {
       pref[0] = 23; pref[1] = 22; pref[2] = 8; pref[3] = 13;
     } else if (allow_split) {
@@ -162,7 +187,15 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
     pref[0] = 8; pref[1] = 13; pref[2] = 13; pref[3] = 13;
   }
   for (int id : pref)
-    if (recipe_usable(id, p, lib, bf16)) return finish_plan(id, p, allow_split);
+    if (ok(id)) return finish_plan(id, p, allow_split);
+  if (pool) {
+    // the pooled layer's fallbacks (2 x 4, then 2 x 2 outputs per lane)
+    for (int id : {31, 20, 27, 23, 22, 21, 28})
+      if (ok(id)) return finish_plan(id, p, false);
+    ConvPlan none;
+    none.recipe = -1;   // no tiling can fuse the pool
+    return none;
+  }
   return finish_plan(13, p, allow_split);
 }
 

@@ -57,19 +57,24 @@ struct ConvParams {
 
 // Tilings of the wave-pipeline kernel (canonical library): id, R x CC
 // outputs per lane, LW lanes across, WS channel-split waves of one slot group.
-#define PP_WRECIPES(X)  \
-  X(20, 2, 4, 8, 4)     \
-  X(21, 2, 2, 8, 4)     \
-  X(22, 2, 2, 8, 8)     \
-  X(23, 2, 2, 8, 16)    \
-  X(24, 1, 2, 8, 8)     \
-  X(25, 1, 1, 8, 16)    \
-  X(26, 4, 4, 8, 4)     \
-  X(27, 2, 4, 8, 8)     \
-  X(28, 2, 2, 8, 2)     \
-  X(29, 1, 4, 8, 2)     \
-  X(30, 1, 4, 8, 4)     \
-  X(31, 2, 4, 8, 2)
+#define PP_WRECIPES(X)    \
+  X(20, 2, 4, 8, 4, 0)    \
+  X(21, 2, 2, 8, 4, 0)    \
+  X(22, 2, 2, 8, 8, 0)    \
+  X(23, 2, 2, 8, 16, 0)   \
+  X(24, 1, 2, 8, 8, 0)    \
+  X(25, 1, 1, 8, 16, 0)   \
+  X(26, 4, 4, 8, 4, 0)    \
+  X(27, 2, 4, 8, 8, 0)    \
+  X(28, 2, 2, 8, 2, 0)    \
+  X(29, 1, 4, 8, 2, 0)    \
+  X(30, 1, 4, 8, 4, 0)    \
+  X(31, 2, 4, 8, 2, 0)    \
+  X(32, 2, 4, 8, 2, 1)    \
+  X(33, 2, 4, 8, 4, 1)    \
+  X(34, 2, 4, 8, 8, 1)    \
+  X(35, 2, 2, 8, 8, 1)    \
+  X(36, 1, 2, 8, 8, 1)
 
 constexpr int kFirstWaveRecipe = 20;
 
@@ -82,23 +87,32 @@ constexpr int wave_row_stride(int n, int rstep) {
   return n;
 }
 
-// LDS floats of one wave-pipeline workgroup: per wave a ring of nslot
-// (staged tile rounded up to 256 floats + 64 weight floats), or the
-// partial-sum exchange of 2 slots per wave, whichever is larger; warea =
-// expanded weight floats per staged channel (64 canonical, 128 all-ones)
-constexpr long wave_lds_floats(int r, int cc, int lw, int ws, int s, int d, int warea, int nslot) {
+// staged floats of one channel in a wave's ring slot: the input tile rounded
+// up to 256 floats, plus warea expanded weight floats (64 canonical, 128
+// all-ones)
+constexpr long wave_slot_floats(int r, int cc, int lw, int s, int d, int warea) {
   const int th = (64 / lw) * r, tw = lw * cc;
   const int tih = (th - 1) * s + 2 * d + 1, tiw = (tw - 1) * s + 2 * d + 1;
   const int lstr = wave_row_stride((tiw + 6) / 4 * 4, r * s);
-  const long nq = (static_cast<long>(tih) * lstr + 255) / 256;
-  const long ring = nslot * (nq * 256 + warea);
+  return (static_cast<long>(tih) * lstr + 255) / 256 * 256 + warea;
+}
+// ring slots per wave: fp32 channels are DMA'd into LDS three channels ahead
+// (4 slots); bf16 stages through registers (2 slots)
+constexpr int wave_nslot(bool bf16) { return bf16 ? 2 : 4; }
+// LDS floats of one wave-pipeline workgroup: per wave a ring of nslot
+// slots, or the partial-sum exchange of 2 slots per wave, whichever is larger
+constexpr long wave_lds_floats(int r, int cc, int lw, int ws, int s, int d, int warea, bool bf16) {
+  const long ring = wave_nslot(bf16) * wave_slot_floats(r, cc, lw, s, d, warea);
   const long xch = static_cast<long>(ws) * 2 * r * cc * 64;
   return ws * ring > xch ? ws * ring : xch;
 }
-constexpr int kNumRecipes = 32;
+constexpr int kNumRecipes = 37;
 
+// pipe: the wave-pipeline kernel reads the next channel from LDS into a
+// second register set while it computes the current one (fp32, canonical
+// library only)
 struct RecipeInfo {
-  int r, cc, lw, wf, ws, cpw;
+  int r, cc, lw, wf, ws, cpw, pipe;
 };
 
 // geometry of a recipe, and whether its LDS footprint fits for (stride, dilation)
@@ -112,7 +126,9 @@ struct ConvPlan {
   int ksplit = 1;   // channel split over workgroups (needs scratch, see split_bytes)
 };
 
-// allow_split: the caller can provide scratch for a channel split
+// allow_split: the caller can provide scratch for a channel split.  With
+// PP_MAXPOOL2 in p.flags only tilings that can fuse the pool are chosen (no
+// split), and recipe -1 means none can.
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split);
 // scratch bytes a plan needs (its partial-sum blocks); 0 without a split
 size_t split_bytes(const ConvPlan& plan, const ConvParams& p);

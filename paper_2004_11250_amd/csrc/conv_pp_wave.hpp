@@ -33,12 +33,8 @@
 namespace pp {
 namespace kern {
 
-template <int LIB, int S, int D, int R, int CC, int LW, int WS, bool ABF>
+template <int LIB, int S, int D, int R, int CC, int LW, int WS, bool ABF, bool PIPE_REQ>
 struct WGeo {
-  // ring slots per wave: fp32 channels are DMA'd straight into LDS DPF
-  // channels ahead (DPF + 1 slots); bf16 goes through registers (2 slots)
-  static constexpr int DPF = 3;
-  static constexpr int NSLOT = ABF ? 2 : DPF + 1;
   // expanded weights per slot in LDS: 4 taps (canonical library) or the 9
   // taps padded to 12 (all-ones library)
   static constexpr int KW = LIB == kLibDense9 ? 12 : 4;
@@ -58,13 +54,24 @@ struct WGeo {
   static constexpr int NQ = (AREA + 255) / 256;           // 4-float staging groups per lane
   static constexpr int PATCH = NQ * 256;                  // floats per staged channel
   static constexpr int SLOT = PATCH + WAREA;
+  // ring slots per wave: fp32 channels are DMA'd straight into LDS DPF
+  // channels ahead (DPF + 1 slots); bf16 goes through registers (2 slots)
+  static constexpr int NSLOT = wave_nslot(ABF);
+  static constexpr int DPF = NSLOT - 1;
+  static_assert(SLOT == wave_slot_floats(R, CC, LW, S, D, WAREA), "planner and kernel disagree on the slot size");
   static constexpr int RING = NSLOT * SLOT;               // per wave
   static constexpr int NACC = 8 * R * CC;
+  // fp32 canonical library, on request: the next channel's patch and weights
+  // are read into a second register set while this one is computed (both
+  // sets and the accumulators must fit the registers a wave may hold: 256,
+  // or 128 with 16 waves per workgroup)
+  static constexpr int VBUDGET = WS > 8 ? 128 : 256;
+  static constexpr bool PIPE = PIPE_REQ && !ABF && LIB == kLibCanon8 && NACC + 2 * (PR * PC + 8 * KW) + 24 <= VBUDGET;
   // partial-sum exchange: PS slots at a time, every wave writes PS*R*CC floats per lane
   static constexpr int PS = 2;
   static constexpr int XCH = WS * PS * R * CC * 64;
   static constexpr int LDS_FLOATS = (WS * RING > XCH) ? WS * RING : XCH;
-  static_assert(LDS_FLOATS == wave_lds_floats(R, CC, LW, WS, S, D, WAREA, NSLOT),
+  static_assert(LDS_FLOATS == wave_lds_floats(R, CC, LW, WS, S, D, WAREA, ABF),
                 "planner and kernel disagree on LDS size");
   static constexpr bool fits = LDS_FLOATS * 4 <= 160 * 1024 && LW * LH == 64 && WS >= 1 && WS <= 16;
 };
@@ -124,38 +131,44 @@ __device__ __forceinline__ void put_elem(float (&d)[PC], float v) {
 }
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-template <int I, int SH, int PC, int VWL>
+template <int I, int SH, int PC, int VWL, bool PIN>
 __device__ __forceinline__ void read_row(float (&d)[PC], const float* rb) {
   constexpr int END = SH + PC;
   if constexpr (I < END) {
     if constexpr (VWL >= 4 && I % 4 == 0 && I + 4 <= END) {
-      f32x4 v = *reinterpret_cast<const f32x4*>(rb + I);
-      asm("" : "+v"(v));   // keep the load whole (one aligned 16-byte read)
+      f32x4 v = *reinterpret_cast<const f32x4*>(__builtin_assume_aligned(rb + I, 16));
+      if constexpr (PIN) asm("" : "+v"(v));   // keep the load whole (one aligned 16-byte read)
       put_elem<I - SH>(d, v.x);
       put_elem<I + 1 - SH>(d, v.y);
       put_elem<I + 2 - SH>(d, v.z);
       put_elem<I + 3 - SH>(d, v.w);
-      read_row<I + 4, SH, PC, VWL>(d, rb);
+      read_row<I + 4, SH, PC, VWL, PIN>(d, rb);
+    } else if constexpr (VWL >= 2 && !PIN && (I % 2 == 1 || I + 1 == END)) {
+      // a single element of a pair: read it alone (a pair read whose other
+      // half is dead lets the register allocator reuse that half for the
+      // next read, which then has to wait for this one)
+      put_elem<I - SH>(d, rb[I]);
+      read_row<I + 1, SH, PC, VWL, PIN>(d, rb);
     } else if constexpr (VWL >= 2) {
       constexpr int B = I & ~1;
-      f32x2 v = *reinterpret_cast<const f32x2*>(rb + B);
-      asm("" : "+v"(v));   // one aligned 8-byte read
+      f32x2 v = *reinterpret_cast<const f32x2*>(__builtin_assume_aligned(rb + B, 8));
+      if constexpr (PIN) asm("" : "+v"(v));   // one aligned 8-byte read
       put_elem<B - SH>(d, v.x);
       put_elem<B + 1 - SH>(d, v.y);
-      read_row<B + 2, SH, PC, VWL>(d, rb);
+      read_row<B + 2, SH, PC, VWL, PIN>(d, rb);
     } else {
       put_elem<I - SH>(d, rb[I]);
-      read_row<I + 1, SH, PC, VWL>(d, rb);
+      read_row<I + 1, SH, PC, VWL, PIN>(d, rb);
     }
   }
 }
 
 // SH = (-pad) mod 4: the tile's first input column sits SH columns after a
 // multiple of 4 (tile origins are multiples of 4 columns)
-template <int LIB, int S, int D, int R, int CC, int LW, int WS, int SH, class TA>
+template <int LIB, int S, int D, int R, int CC, int LW, int WS, int SH, bool PIPE, class TA>
 __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) {
   constexpr bool ABF = sizeof(TA) == 2;
-  using G = WGeo<LIB, S, D, R, CC, LW, WS, ABF>;
+  using G = WGeo<LIB, S, D, R, CC, LW, WS, ABF, PIPE>;
   constexpr int KW = G::KW, KT = G::KT, NWL = G::NWL;
   constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT;
   static_assert(G::fits, "tiling does not fit");
@@ -353,7 +366,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
             }
           }
 #pragma unroll
-        for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL>(p[r], cur + lane_off + r * LSTR);
+        for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL, true>(p[r], cur + lane_off + r * LSTR);
       }
       // everything of channel c is in registers once this wait returns; the
       // scalar loads issued next are then waited for only one channel later
@@ -389,11 +402,16 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   }
 
   if (!ABF && c0 < c1) {
-    // fp32: DMA pipeline.  Channel c lives in ring slot (c - c0) % NSLOT; its
-    // halo tile and weights are DMA'd DPF channels before it is computed.
-    // Per channel every lane issues QV DMAs, so "channel c has landed" is
-    // vmcnt <= (DPF - 1) * QV while DPF - 1 later channels are in flight.
+    // fp32: DMA pipeline.  Channel c lives in ring slot (c - c0) % NSLOT;
+    // its halo tile and weights are DMA'd DPF channels before it is computed.
+    // With PIPE its patch and weights are read from LDS into one of two
+    // register sets one channel before it is computed, so those reads overlap
+    // the previous channel's FMAs.  Per channel every lane issues QV (QS)
+    // DMAs, so "channel c has landed" is vmcnt <= n * QV while n later
+    // channels are in flight.
     constexpr int NS = G::NSLOT, DPF = G::DPF;
+    constexpr int QV = G::NQ + NWL;       // 16-byte patch loads + weight loads
+    constexpr int QS = 4 * G::NQ + NWL;   // 4-byte patch loads + weight loads
     const uint32_t ring_b = lds_addr(ring);
     const u32x4 brs = make_rsrc(blob, a.blob_bytes);
     // descriptor of the next channel to DMA (channels are DMA'd in order)
@@ -422,10 +440,46 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       const uint32_t e = min(e_base + static_cast<uint32_t>(c), e_last);
       return sload<uint32_t>(blob, a.off_woff + 4 * e);
     };
+    // wait until channel c has landed in LDS; the DMAs of channels up to
+    // min(c + n, c1 - 1) have been issued
+    auto wait_landed = [&](int c, auto later) __attribute__((always_inline)) {
+      constexpr int n = decltype(later)::value;
+      asm volatile("" ::: "memory");
+      if (c + n < c1) {
+        if (v4)
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QV));
+        else
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QS));
+      } else {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+      }
+      asm volatile("" ::: "memory");
+    };
+    // LDS -> registers: patch and weights of channel c (no wait).  Canonical
+    // library: all 8 slots' weights unconditionally (pruned slots hold zeros;
+    // fewer branches than testing each slot); all-ones library: kept slots.
+    auto lds_read = [&](int c, uint32_t kept, float (&p)[PR][PC], float (&w)[8][KW]) __attribute__((always_inline)) {
+      const uint32_t k = static_cast<uint32_t>(c - c0);
+      const float* cur = ring + (k % NS) * SLOT;
+      const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        if (LIB == kLibCanon8 || ((kept >> s) & 1u)) {
+#pragma unroll
+          for (int i = 0; i < KW / 4; ++i) {
+            const float4 v = wc[s * (KW / 4) + i];
+            w[s][4 * i] = v.x; w[s][4 * i + 1] = v.y; w[s][4 * i + 2] = v.z; w[s][4 * i + 3] = v.w;
+          }
+        }
+#pragma unroll
+      for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL, false>(p[r], cur + lane_off + r * LSTR);
+    };
     // running byte offsets of the scalar loads (clamped at the layer's last
     // channel, whose entries are then read again and not used)
     const uint32_t woff_last = a.off_woff + 4u * e_last, code_last = a.off_codes + 8u * e_last;
-    // prologue: channels c0 .. c0+DPF-1 in flight
+    uint32_t wo_n, wo_off, me_off, mc_off;
+    Meta m0, m1;
+    // prologue: channels c0 .. c0+DPF-1 in flight, channel c0 read into set A
     {
       uint32_t wo[DPF];
 #pragma unroll
@@ -433,93 +487,91 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
 #pragma unroll
       for (int i = 0; i < DPF; ++i)
         if (c0 + i < c1) dma(c0 + i, wo[i]);
+      m0 = load_meta(c0);
+      m1 = load_meta(c0 + 1);
+      wo_n = load_wo(c0 + DPF);
+      wo_off = min(a.off_woff + 4u * (e_base + c0 + DPF + 1), woff_last);
+      me_off = min(a.off_woff + 4u * (e_base + c0 + 2), woff_last);
+      mc_off = min(a.off_codes + 8u * (e_base + c0 + 2), code_last);
     }
-    Meta m0 = load_meta(c0);
-    uint32_t wo_n = load_wo(c0 + DPF);
-    uint32_t wo_off = min(a.off_woff + 4u * (e_base + c0 + DPF + 1), woff_last);
-    uint32_t me_off = min(a.off_woff + 4u * (e_base + c0 + 1), woff_last);
-    uint32_t mc_off = min(a.off_codes + 8u * (e_base + c0 + 1), code_last);
-#pragma unroll 1
-    for (int c = c0; c < c1; ++c) {
-      const uint32_t k = static_cast<uint32_t>(c - c0);
-      const float* cur = ring + (k % NS) * SLOT;
-      // channel c has landed in LDS
-      asm volatile("" ::: "memory");
-      if (c + DPF - 1 < c1) {
-        if (v4) {
-          __builtin_amdgcn_s_waitcnt(vmcnt_imm((DPF - 1) * (NQ + NWL)));
-        } else {
-          __builtin_amdgcn_s_waitcnt(vmcnt_imm((DPF - 1) * (4 * NQ + NWL)));
-        }
-      } else {
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-      }
-      asm volatile("" ::: "memory");
-      const uint32_t kept = m0.wo >> 24;
-      float p[PR][PC];
-      float w[8][KW];
-      if (kept != 0) {
-        // weights first: the patch reads end with a wait that then covers both
-        // canonical library: all 8 slots (4 floats each) unconditionally --
-        // fewer branches than testing each slot; pruned slots hold zeros
-        const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-          if (LIB == kLibCanon8 || ((kept >> s) & 1u)) {
-#pragma unroll
-            for (int i = 0; i < KW / 4; ++i) {
-              const float4 v = wc[s * (KW / 4) + i];
-              w[s][4 * i] = v.x; w[s][4 * i + 1] = v.y; w[s][4 * i + 2] = v.z; w[s][4 * i + 3] = v.w;
-            }
-          }
-#pragma unroll
-        for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL>(p[r], cur + lane_off + r * LSTR);
-      }
-      // patch, weights, and the scalar loads of the previous iteration
+    float pa[PR][PC], pb[PR][PC];
+    float wa[8][KW], wb[8][KW];
+    if constexpr (G::PIPE) {
       wait_lgkm();
-      if constexpr (LIB == kLibCanon8) {
-        // the weights are complete here; keep them out of the slot branches
-#pragma unroll
-        for (int s = 0; s < 8; ++s) asm("" : "+v"(w[s][0]), "+v"(w[s][1]), "+v"(w[s][2]), "+v"(w[s][3]));
+      wait_landed(c0, std::integral_constant<int, DPF - 1>{});
+      lds_read(c0, m0.wo >> 24, pa, wa);
+    }
+    // one channel.  Pipelined: X holds channel c (read one step earlier) and
+    // Y receives channel c + 1.  Otherwise channel c is read into X here.
+    auto step = [&](int c, float (&px)[PR][PC], float (&wx)[8][KW], float (&py)[PR][PC], float (&wy)[8][KW])
+        __attribute__((always_inline)) {
+      if constexpr (!G::PIPE) {
+        wait_landed(c, std::integral_constant<int, DPF - 1>{});
+        if ((m0.wo >> 24) != 0) lds_read(c, m0.wo >> 24, px, wx);
       }
+      // channel c's patch and weights, and the previous step's scalar loads
+      wait_lgkm();
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int i = 0; i < KW; ++i) asm("" : "+v"(wx[s][i]));
       __builtin_amdgcn_sched_barrier(0);
+      if constexpr (G::PIPE) {
+        if (c + 1 < c1) {
+          wait_landed(c + 1, std::integral_constant<int, DPF - 2>{});
+          lds_read(c + 1, m1.wo >> 24, py, wy);
+        }
+      }
       // channel c+DPF -> LDS (its slot was last read for channel c-1)
       if (c + DPF < c1) dma(c + DPF, wo_n);
       const uint32_t wo_nn = sload<uint32_t>(blob, wo_off);
-      Meta m1;
-      m1.wo = sload<uint32_t>(blob, me_off);
+      Meta m2;
+      m2.wo = sload<uint32_t>(blob, me_off);
       {
         const uint2 cw = sload<uint2>(blob, mc_off);
-        m1.cx = cw.x;
-        m1.cy = cw.y;
+        m2.cx = cw.x;
+        m2.cy = cw.y;
       }
       wo_off = min(wo_off + 4u, woff_last);
       me_off = min(me_off + 4u, woff_last);
       mc_off = min(mc_off + 8u, code_last);
-      uint32_t kc = kept;
+      __builtin_amdgcn_sched_barrier(0);
+      uint32_t kc = m0.wo >> 24;
       asm volatile("" : "+s"(kc));   // fresh slot tests (no 64-bit condition masks kept live)
       if (kc != 0) {
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
           if (!((kc >> s) & 1u)) continue;
           if constexpr (LIB == kLibDense9) {
-            fma_tap<0, S, D>(acc[s], p, w[s][0]);
-            fma_tap<1, S, D>(acc[s], p, w[s][1]);
-            fma_tap<2, S, D>(acc[s], p, w[s][2]);
-            fma_tap<3, S, D>(acc[s], p, w[s][3]);
-            fma_tap<4, S, D>(acc[s], p, w[s][4]);
-            fma_tap<5, S, D>(acc[s], p, w[s][5]);
-            fma_tap<6, S, D>(acc[s], p, w[s][6]);
-            fma_tap<7, S, D>(acc[s], p, w[s][7]);
-            fma_tap<8, S, D>(acc[s], p, w[s][8]);
+            fma_tap<0, S, D>(acc[s], px, wx[s][0]);
+            fma_tap<1, S, D>(acc[s], px, wx[s][1]);
+            fma_tap<2, S, D>(acc[s], px, wx[s][2]);
+            fma_tap<3, S, D>(acc[s], px, wx[s][3]);
+            fma_tap<4, S, D>(acc[s], px, wx[s][4]);
+            fma_tap<5, S, D>(acc[s], px, wx[s][5]);
+            fma_tap<6, S, D>(acc[s], px, wx[s][6]);
+            fma_tap<7, S, D>(acc[s], px, wx[s][7]);
+            fma_tap<8, S, D>(acc[s], px, wx[s][8]);
           } else {
             const uint32_t pid = ((s < 4 ? m0.cx : m0.cy) >> (8 * (s & 3))) & 0xFFu;
-            apply_canon8<S, D>(pid, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+            apply_canon8<S, D>(pid, acc[s], px, wx[s][0], wx[s][1], wx[s][2], wx[s][3]);
           }
         }
       }
       m0 = m1;
+      m1 = m2;
       wo_n = wo_nn;
+    };
+    if constexpr (G::PIPE) {
+#pragma unroll 1
+      for (int c = c0; c < c1; c += 2) {
+        step(c, pa, wa, pb, wb);
+        if (c + 1 >= c1) break;
+        step(c + 1, pb, wb, pa, wa);
+      }
+    } else {
+#pragma unroll 1
+      for (int c = c0; c < c1; ++c) step(c, pa, wa, pa, wa);
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // no DMA may land in the exchange area below
   }
@@ -529,7 +581,12 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   // With a channel split over workgroups (ksplit > 1) the unit's sum goes to
   // this workgroup's block of the partial-sum buffer instead; a second kernel
   // adds the ksplit blocks of each tile in split order and finishes.
-  TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  // with PP_MAXPOOL2 the output is the 2 x 2 max pool (floor) of the
+  // activated conv output: each lane's R x CC block holds whole windows
+  const bool pool = (a.flags & PP_MAXPOOL2) != 0;
+  const int pho = a.ho / 2, pwo = a.wo / 2;
+  TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out *
+                                                   (pool ? static_cast<size_t>(pho) * pwo : static_cast<size_t>(a.ho) * a.wo);
   const bool relu = (a.flags & PP_RELU) != 0;
   const int oxl = ox0 + lx * CC;
   const bool vec = (CC % 4 == 0) && (a.wo % 4 == 0) && (reinterpret_cast<uintptr_t>(a.y) % (4 * sizeof(TA)) == 0);
@@ -575,6 +632,52 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       }
     }
   };
+  // pooled store of rows r, r + 1 (r even) of slot s: max over each 2 x 2
+  // window of the activated values, as a separate pool of the stored conv
+  // output would take it
+  auto finish_pool = [&](int s, int r, float (&v0)[CC], float (&v1)[CC]) __attribute__((always_inline)) {
+    const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
+    const uint32_t o = sload<uint32_t>(blob, a.off_perm + 4 * slot);
+    if (o >= static_cast<uint32_t>(a.c_out)) return;   // padding slot
+    const float bias = sload<float>(blob, a.off_bias + 4 * slot);
+    const int oy = oy0 + ly * R + r;
+    if (oy + 1 >= a.ho) return;   // incomplete window (floor)
+    TA* row = y + (static_cast<size_t>(o) * pho + oy / 2) * pwo;
+#pragma unroll
+    for (int q = 0; q < CC; ++q) {
+      v0[q] += bias;
+      v1[q] += bias;
+      if (relu) {
+        v0[q] = fmaxf(v0[q], 0.0f);
+        v1[q] = fmaxf(v1[q], 0.0f);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < CC / 2; ++j) {
+      const int ox = oxl + 2 * j;
+      if (ox + 1 < a.wo) {
+        const float m = fmaxf(fmaxf(v0[2 * j], v0[2 * j + 1]), fmaxf(v1[2 * j], v1[2 * j + 1]));
+        if constexpr (ABF)
+          reinterpret_cast<uint16_t*>(row)[ox / 2] = static_cast<uint16_t>(to_bf16_bits(m));
+        else
+          reinterpret_cast<float*>(row)[ox / 2] = m;
+      }
+    }
+  };
+  // the unit's sum over the WS waves (exchange area) or this wave's accumulators
+  auto gather = [&](int s, int ps, int r, float (&v)[CC]) __attribute__((always_inline)) {
+    if (WS > 1) {
+#pragma unroll
+      for (int q = 0; q < CC; ++q) {
+        float t = 0.0f;
+        for (int k = 0; k < WS; ++k) t += lds[((k * G::PS * R + ps * R + r) * CC + q) * 64 + lane];
+        v[q] = t;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < CC; ++q) v[q] = acc[s][r][q];
+    }
+  };
 #pragma unroll
   for (int s0 = 0; s0 < 8; s0 += G::PS) {
     if (WS > 1) {
@@ -588,6 +691,24 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
           for (int q = 0; q < CC; ++q) dst[((ps * R + r) * CC + q) * 64] = acc[s0 + ps][r][q];
       __syncthreads();
     }
+    if constexpr (R % 2 == 0 && CC % 2 == 0) {
+      if (pool) {
+        // units (slot, row pair); the planner runs pooled layers unsplit
+        constexpr int NUP = G::PS * (R / 2);
+#pragma unroll
+        for (int u0 = 0; u0 < NUP; u0 += WS) {
+          const int u = u0 + wk;
+          if (u >= NUP) break;
+          const int ps = u / (R / 2), r = 2 * (u % (R / 2));
+          const int s = s0 + ps;
+          float v0[CC], v1[CC];
+          gather(s, ps, r, v0);
+          gather(s, ps, r + 1, v1);
+          finish_pool(s, r, v0, v1);
+        }
+        continue;
+      }
+    }
 #pragma unroll
     for (int u0 = 0; u0 < NU; u0 += WS) {
       const int u = u0 + wk;
@@ -595,17 +716,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       const int ps = u / R, r = u % R;
       const int s = s0 + ps;
       float v[CC];
-      if (WS > 1) {
-#pragma unroll
-        for (int q = 0; q < CC; ++q) {
-          float t = 0.0f;
-          for (int k = 0; k < WS; ++k) t += lds[((k * G::PS * R + ps * R + r) * CC + q) * 64 + lane];
-          v[q] = t;
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < CC; ++q) v[q] = acc[s][r][q];
-      }
+      gather(s, ps, r, v);
       if (split) {
         float* pb = a.part + static_cast<size_t>(item * a.ksplit + ks) * BLK + lane;
 #pragma unroll
@@ -657,9 +768,9 @@ __global__ __launch_bounds__(256) void pp_split_reduce_kernel(ConvParams a) {
   }
 }
 
-template <int LIB, int S, int D, int R, int CC, int LW, int WS, class TA>
+template <int LIB, int S, int D, int R, int CC, int LW, int WS, bool PIPE, class TA>
 hipError_t launch_wave_tiling(ConvParams p, hipStream_t st) {
-  using G = WGeo<LIB, S, D, R, CC, LW, WS, sizeof(TA) == 2>;
+  using G = WGeo<LIB, S, D, R, CC, LW, WS, sizeof(TA) == 2, PIPE>;
   constexpr int SH = (4 - D % 4) % 4;   // the compiled padding is pad = D
   if constexpr (!G::fits) {
     return hipErrorInvalidConfiguration;
@@ -671,7 +782,7 @@ hipError_t launch_wave_tiling(ConvParams p, hipStream_t st) {
     if (p.ksplit < 1 || p.ksplit > p.c_in || (p.ksplit > 1 && !p.part)) return hipErrorInvalidValue;
     const size_t nb = static_cast<size_t>(p.n_groups) * p.tiles_x * p.tiles_y * p.n * p.ksplit;
     if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((pp_conv3x3_wave_kernel<LIB, S, D, R, CC, LW, WS, SH, TA>), dim3(static_cast<uint32_t>(nb)),
+    hipLaunchKernelGGL((pp_conv3x3_wave_kernel<LIB, S, D, R, CC, LW, WS, SH, PIPE, TA>), dim3(static_cast<uint32_t>(nb)),
                        dim3(WS * 64), 0, st, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.ksplit == 1) return e;

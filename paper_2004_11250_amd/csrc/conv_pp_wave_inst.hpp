@@ -6,12 +6,17 @@
 
 namespace pp {
 
+// the register-pipelined tilings exist for fp32 and the canonical library
 template <int LIB, int S, int D, class TA>
 hipError_t launch_wave_recipe(int id, const ConvParams& p, hipStream_t st) {
+  constexpr bool kPipeOk = LIB == kLibCanon8 && sizeof(TA) == 4;
   switch (id) {
-#define PP_W(ID, R, CC, LW, WS) \
-  case ID:                      \
-    return kern::launch_wave_tiling<LIB, S, D, R, CC, LW, WS, TA>(p, st);
+#define PP_W(ID, R, CC, LW, WS, P)                                                    \
+  case ID:                                                                            \
+    if constexpr (!P || kPipeOk)                                                      \
+      return kern::launch_wave_tiling<LIB, S, D, R, CC, LW, WS, (P != 0), TA>(p, st); \
+    else                                                                              \
+      return hipErrorInvalidValue;
     PP_WRECIPES(PP_W)
 #undef PP_W
     default:

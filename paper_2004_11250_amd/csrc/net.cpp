@@ -2,7 +2,12 @@
 // per fused layer, the layer-wise representation of Sec. 3) on one stream.
 // Slot 0 is the input, slot 1 the output, slots 2.. live in the caller's
 // workspace at fixed 256-byte-aligned offsets.  Validation of the whole list
-// happens before the first launch.
+// happens before the first launch.  A pruned conv whose output only feeds
+// the 2 x 2 max pool right after it runs as one fused launch (graph-level
+// fusion, Sec. 3): the pool is taken in the conv's store.  Logical slots map
+// to workspace buffers; when such a pool writes back into the conv's input
+// slot (ping-pong slot use), the fused launch writes the conv's output
+// buffer instead and the two slots swap buffers.
 #include <hip/hip_runtime.h>
 
 #include <string>
@@ -23,8 +28,11 @@ struct Shape {
 struct Plan {
   std::vector<Shape> in, in2, out;
   std::vector<BlobView> views;
-  size_t slot_bytes[PP_MAX_SLOTS] = {};
-  size_t slot_off[PP_MAX_SLOTS] = {};
+  std::vector<char> fuse_pool;   // op i is a pruned conv fused with the max pool at i + 1
+  // per op: the buffers (0 = x, 1 = y, >= 2 workspace) of src, src2, dst
+  std::vector<int> b_src, b_src2, b_dst;
+  size_t buf_bytes[PP_MAX_SLOTS] = {};
+  size_t buf_off[PP_MAX_SLOTS] = {};
   size_t ws_bytes = 0;
   // scratch of the pruned convs' channel splits (partial sums), after the slots
   size_t scratch_off = 0, scratch_bytes = 0;
@@ -44,6 +52,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
   pl->in2.resize(n_ops);
   pl->out.resize(n_ops);
   pl->views.resize(n_ops);
+  pl->fuse_pool.assign(n_ops, 0);
   std::vector<Shape> writes1;
   size_t part_max = 0;
   for (int i = 0; i < n_ops; ++i) {
@@ -118,19 +127,70 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
     pl->in[i] = s;
     pl->out[i] = o;
     slots[op.dst] = o;
-    const size_t bytes = static_cast<size_t>(n) * o.c * o.h * o.w * esz;
-    if (bytes > pl->slot_bytes[op.dst]) pl->slot_bytes[op.dst] = bytes;
     if (op.dst == 1) writes1.push_back(o);
   }
   if (!slots[1].defined) return fail(PP_EINVAL, "no op writes the output slot 1");
+  // conv + max pool fusion: the pool reads the conv's output slot, which no
+  // later op reads before rewriting it; a pool that writes the conv's input
+  // slot needs that slot in the workspace (its buffer is swapped)
+  for (int i = 0; i + 1 < n_ops; ++i) {
+    const pp_net_op& cv = ops[i];
+    const pp_net_op& mp = ops[i + 1];
+    if (cv.kind != PP_OP_CONV_PP || mp.kind != PP_OP_MAXPOOL2 || mp.src != cv.dst || cv.dst == 1 ||
+        (mp.dst == cv.src && cv.src < 2))
+      continue;
+    bool read_later = false;
+    for (int j = i + 2; j < n_ops && !read_later; ++j) {
+      read_later = ops[j].src == cv.dst || (ops[j].kind == PP_OP_ADD && ops[j].src2 == cv.dst);
+      if (ops[j].dst == cv.dst) break;   // rewritten: later reads see the new value
+    }
+    if (!read_later && conv_pool_fusable(pl->views[i], n, pl->in[i].h, pl->in[i].w, act)) {
+      pl->fuse_pool[i] = 1;
+      ++i;   // the pool is taken; it cannot start another pair
+    }
+  }
+  // buffers: each op reads and writes the buffers its slots map to now; a
+  // fused pair whose pool writes the conv's input slot writes the conv's
+  // output buffer and then swaps the two slots' buffers (the conv's output
+  // slot is dead after the pool, the input slot is overwritten by it)
+  int buf[PP_MAX_SLOTS];
+  for (int s = 0; s < PP_MAX_SLOTS; ++s) buf[s] = s;
+  pl->b_src.assign(n_ops, 0);
+  pl->b_src2.assign(n_ops, 0);
+  pl->b_dst.assign(n_ops, 0);
+  for (int i = 0; i < n_ops; ++i) {
+    const pp_net_op& op = ops[i];
+    pl->b_src[i] = buf[op.src];
+    pl->b_src2[i] = op.kind == PP_OP_ADD ? buf[op.src2] : 0;
+    Shape o = pl->out[i];
+    bool swap = false;
+    if (pl->fuse_pool[i]) {
+      const pp_net_op& mp = ops[i + 1];
+      swap = mp.dst == op.src;
+      pl->b_dst[i] = swap ? buf[op.dst] : buf[mp.dst];
+      o = pl->out[i + 1];
+    } else {
+      pl->b_dst[i] = buf[op.dst];
+    }
+    const size_t bytes = static_cast<size_t>(n) * o.c * o.h * o.w * esz;
+    if (bytes > pl->buf_bytes[pl->b_dst[i]]) pl->buf_bytes[pl->b_dst[i]] = bytes;
+    if (pl->fuse_pool[i]) {
+      if (swap) {
+        const int t = buf[op.dst];
+        buf[op.dst] = buf[ops[i + 1].dst];
+        buf[ops[i + 1].dst] = t;
+      }
+      ++i;
+    }
+  }
   for (const Shape& s : writes1)
     if (s.c != slots[1].c || s.h != slots[1].h || s.w != slots[1].w)
       return fail(PP_EINVAL, "slot 1 is written with different shapes");
   pl->final_shape = slots[1];
   size_t off = 0;
-  for (int sl = 2; sl < PP_MAX_SLOTS; ++sl) {
-    pl->slot_off[sl] = off;
-    off += (pl->slot_bytes[sl] + 255) / 256 * 256;
+  for (int b = 2; b < PP_MAX_SLOTS; ++b) {
+    pl->buf_off[b] = off;
+    off += (pl->buf_bytes[b] + 255) / 256 * 256;
   }
   pl->scratch_off = off;
   pl->scratch_bytes = (part_max + 255) / 256 * 256;
@@ -170,21 +230,29 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
   if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(PP_EINVAL, "workspace must be 256-byte aligned");
   const bool bf = act_dtype == PP_BF16;
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  auto slot_ptr = [&](int s) -> void* {
-    if (s == 0) return const_cast<void*>(x);
-    if (s == 1) return y;
-    return static_cast<uint8_t*>(workspace) + pl.slot_off[s];
+  auto buf_ptr = [&](int b) -> void* {
+    if (b == 0) return const_cast<void*>(x);
+    if (b == 1) return y;
+    return static_cast<uint8_t*>(workspace) + pl.buf_off[b];
   };
   void* scratch = pl.scratch_bytes ? static_cast<uint8_t*>(workspace) + pl.scratch_off : nullptr;
   for (int i = 0; i < n_ops; ++i) {
     const pp_net_op& op = ops[i];
     const Shape& si = pl.in[i];
     const Shape& so = pl.out[i];
-    void* dst = slot_ptr(op.dst);
-    const void* src = slot_ptr(op.src);
+    void* dst = buf_ptr(pl.b_dst[i]);
+    const void* src = buf_ptr(pl.b_src[i]);
     hipError_t e = hipSuccess;
     switch (op.kind) {
       case PP_OP_CONV_PP:
+        if (pl.fuse_pool[i]) {
+          // conv + the max pool of op i + 1
+          st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags | PP_MAXPOOL2,
+                            nullptr, 0, stream);
+          if (st != PP_OK) return st;
+          ++i;
+          break;
+        }
         st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags, scratch,
                           pl.scratch_bytes, stream);
         if (st != PP_OK) return st;
@@ -216,7 +284,7 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
              : op.kind == PP_OP_UPSAMPLE2 ? kGlueUp2
              : op.kind == PP_OP_PIXSHUF2 ? kGluePixShuf2 : kGlueAdd;
         p.x = src;
-        p.x2 = op.kind == PP_OP_ADD ? slot_ptr(op.src2) : nullptr;
+        p.x2 = op.kind == PP_OP_ADD ? buf_ptr(pl.b_src2[i]) : nullptr;
         p.y = dst;
         p.n = n;
         p.c_in = si.c;

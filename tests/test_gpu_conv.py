@@ -200,7 +200,7 @@ def test_vgg16_full_size_layer_sampled(idx):
 
 
 # every compiled tiling, forced through the PP_RECIPE override of the planner
-RECIPES = list(range(32))
+RECIPES = list(range(37))
 
 
 @pytest.mark.parametrize("recipe", RECIPES)
@@ -225,9 +225,52 @@ def test_every_tiling(recipe, monkeypatch):
         check(y, ref, bound, dtype, f"recipe {recipe} {(s, p, d)} {dtype}")
 
 
-# channel split over workgroups (partial sums in the workspace, the last
-# workgroup of a tile adds them in split order): forced splits, ragged
-# channel shares, both activation dtypes
+# conv + ReLU + 2 x 2 max pool in one launch (PP_MAXPOOL2): against the
+# oracle conv pooled (max is 1-Lipschitz: the pooled S bounds the error), and
+# bitwise against pooling the unpooled output of the same tiling; odd output
+# sizes drop the last row / column
+POOL_RECIPES = [None, 20, 21, 22, 23, 26, 27, 28, 31, 32, 33, 34, 35]
+
+
+@pytest.mark.parametrize("recipe", POOL_RECIPES)
+def test_fused_maxpool(recipe, monkeypatch):
+    if recipe is not None:
+        monkeypatch.setenv("PP_RECIPE", str(recipe))
+    for (s, p, d), dtype, shape in (((1, 1, 1), "f32", (19, 21, 37, 45)), ((1, 1, 1), "f32", (16, 24, 30, 44)),
+                                    ((2, 1, 1), "f32", (17, 9, 41, 50)), ((1, 2, 2), "f32", (11, 13, 29, 33)),
+                                    ((1, 1, 1), "bf16", (24, 17, 33, 70)), ((1, 1, 1), "bf16", (8, 20, 14, 14))):
+        c_out, c_in, h, w = shape
+        seed = 500 + (recipe or 0)
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        if dtype == "bf16":
+            x = obf16.round_f32(x)
+            w_or = obf16.round_f32(L["w"])
+        else:
+            w_or = L["w"]
+        wd = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], s, p, d, wd)
+        _say("fused maxpool, recipe", recipe, (s, p, d), dtype, shape)
+        xd = _to_dev(x, dtype)
+        yp = pp.conv2d_fwd(layer, xd, relu=True, maxpool2=True)
+        args = (x, w_or, L["b"], L["pid"], L["conn"], L["lib"])
+        ref = oconv.maxpool2(oconv.conv3x3_pruned(*args, s, p, d, True))
+        bound = oconv.maxpool2(oconv.conv3x3_bound(*args, s, p, d))
+        got = _from_dev(yp)
+        check(got, ref, bound, dtype, f"fused maxpool recipe {recipe} {(s, p, d)} {dtype} {shape}")
+        if recipe is not None and pp.conv2d_recipe(layer.h_blob, 2, h, w, wd) == recipe:
+            # the same tiling unpooled (no split: no workspace), pooled on the CPU
+            y = pp.conv2d_fwd(layer, xd, relu=True, workspace=None)
+            pooled = torch.nn.functional.max_pool2d(y.float().cpu(), 2)
+            if dtype == "bf16":
+                pooled = pooled.to(torch.bfloat16)
+            torch.cuda.synchronize()
+            assert torch.equal(yp.cpu(), pooled), f"recipe {recipe}: fused pool differs from pooling the output"
+
+
+# channel split over workgroups (partial sums in the workspace, added by a
+# second kernel in split order): forced splits, ragged channel shares, both
+# activation dtypes
 @pytest.mark.parametrize("recipe,ksplit", [(20, 2), (21, 3), (23, 4), (25, 7), (27, 5), (22, 16)])
 def test_channel_split(recipe, ksplit, monkeypatch):
     monkeypatch.setenv("PP_RECIPE", str(recipe))

@@ -3,13 +3,15 @@
 Teacher-forced check: every op's GPU output is compared with the oracle run
 on that op's GPU input (sampled output channels for the large layers), so
 errors do not compound.  The op outputs come from pp_net_fwd itself, run on
-the op-list prefix that ends with that op.  pp_net_fwd must also equal the
-chain of single-layer calls bitwise."""
+the op-list prefix that ends with that op.  A max pool that pp_net_fwd fuses
+into the pruned conv before it is checked as that conv followed by the pool.
+pp_net_fwd must also equal the chain of single-layer calls bitwise."""
 import numpy as np
 import pytest
 
 import workloads
 from oracle import bf16 as obf16
+from oracle import conv as oconv
 from oracle import net as onet
 from tests.tolerance import check
 
@@ -61,6 +63,25 @@ def _sampled(op, prm, n_keep, seed):
     return dict(op, c_out=len(sel)), p, sel
 
 
+def _fused_pool(ops, i):
+    """pp_net_fwd runs op i (a 2 x 2 max pool) inside the pruned conv before
+    it: the pool reads that conv's output, which no later op reads before
+    rewriting it, and the conv's padding equals its dilation (the fused
+    tilings)."""
+    if i < 1 or ops[i]["op"] != "maxpool2" or ops[i - 1]["op"] != "conv3":
+        return False
+    cv, mp = ops[i - 1], ops[i]
+    if mp["src"] != cv["dst"] or cv["dst"] == 1 or (mp["dst"] == cv["src"] and cv["src"] < 2) or \
+            cv["pad"] != cv["dil"]:
+        return False
+    for o in ops[i + 1:]:
+        if o["src"] == cv["dst"] or (o["op"] == "add" and o.get("src2") == cv["dst"]):
+            return False
+        if o["dst"] == cv["dst"]:
+            return True
+    return True
+
+
 def teacher_forced(cfg, dtype, n_keep=6):
     spec = workloads.net_spec(cfg)
     params = workloads.net_params(cfg)
@@ -79,6 +100,16 @@ def teacher_forced(cfg, dtype, n_keep=6):
         arr[i].dst = 1
         sub.ops, sub.n_ops, sub._ws = arr, i + 1, None
         y = _np(sub.forward(x))
+        if _fused_pool(spec["ops"][:i + 1], i):
+            # conv + pool in one launch: the oracle conv on the conv's GPU input,
+            # pooled (max is 1-Lipschitz, so the pooled bound is the pooled S)
+            cop, cprm = spec["ops"][i - 1], params[i - 1]
+            sop, sprm, sel = _sampled(cop, cprm, n_keep, 1000 * cfg + i)
+            cref, cbound = onet.run_op(sop, sprm, slots[cop["src"]], None, dtype)
+            worst = max(worst, check(y[:, sel], oconv.maxpool2(cref), oconv.maxpool2(cbound), dtype,
+                                     f"cfg {cfg} op {i} (conv3 + maxpool2)"))
+            slots[op["dst"]] = y
+            continue
         src = slots[op["src"]]
         src2 = slots.get(op.get("src2")) if "src2" in op else None
         sop, sprm, sel = _sampled(op, prm, n_keep, 1000 * cfg + i)
@@ -105,14 +136,18 @@ def test_vgg16_net_equals_chained_layer_calls():
     params = workloads.net_params(2)
     net = pp.Net(spec["ops"], params, "f32")
     _, x = _input(2, "f32")
-    _say("vgg16 pp_net_fwd vs chained pp_conv2d_fwd + maxpool")
+    _say("vgg16 pp_net_fwd vs chained pp_conv2d_fwd (pool fused where the net fuses it) + maxpool")
     y_net = _np(net.forward(x))
+    ops = spec["ops"]
     cur = x
     li = 0
-    for op, prm in zip(spec["ops"], params):
+    for i, (op, prm) in enumerate(zip(ops, params)):
         if op["op"] == "conv3":
-            cur = pp.conv2d_fwd(net.pruned[li], cur, relu=op["relu"])
+            fuse = i + 1 < len(ops) and _fused_pool(ops, i + 1)
+            cur = pp.conv2d_fwd(net.pruned[li], cur, relu=op["relu"], maxpool2=fuse)
             li += 1
+        elif _fused_pool(ops, i):
+            continue
         else:
             one = pp.Net([dict(op, src=0, dst=1)], [prm], "f32")
             cur = one.forward(cur)
