@@ -361,3 +361,23 @@ class Net:
         _check(lib.pp_net_fwd(self.ops, self.n_ops, x.data_ptr(), out.data_ptr(), n, c, h, w, self.wd,
                               workspace.data_ptr(), workspace.numel(), _stream_ptr(stream)), "pp_net_fwd")
         return out
+
+    def capture(self, x, out, workspace):
+        """Record one pp_net_fwd on these fixed buffers (x, out, workspace:
+        device tensors that stay alive and in place) as a HIP graph, and
+        return it: graph.replay() relaunches the whole network in one call,
+        each kernel then costing a graph node's launch instead of a stream
+        launch's.  pp_net_fwd launches kernels only (no allocation, copy or
+        memset), so the graph holds kernel nodes only.  Replays read x and
+        write out as they are at replay time."""
+        torch = _torch()
+        side = torch.cuda.Stream(device=x.device)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.forward(x, out, workspace, stream=side)   # first call outside the capture
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize(x.device)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            self.forward(x, out, workspace)
+        return graph

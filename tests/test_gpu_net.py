@@ -154,6 +154,31 @@ def test_vgg16_net_equals_chained_layer_calls():
     assert np.array_equal(y_net, _np(cur))
 
 
+def test_vgg16_net_graph_replays():
+    # pp_net_fwd captured as a HIP graph: every replay, with eager work and
+    # synchronisation between replays and a new input each time, equals the
+    # eager pp_net_fwd on that input bitwise
+    spec = workloads.net_spec(2)
+    params = workloads.net_params(2)
+    net = pp.Net(spec["ops"], params, "f32")
+    _, x0 = _input(2, "f32")
+    nbytes, oshape = net.plan(*x0.shape)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+    xg = x0.clone()
+    yg = torch.empty(oshape, dtype=torch.float32, device="cuda")
+    _say("vgg16 graph capture")
+    graph = net.capture(xg, yg, ws)
+    for rep in range(4):
+        _say("vgg16 graph replay", rep)
+        xg.copy_(x0 * (1.0 + 0.25 * rep))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = _np(yg)
+        ref = _np(net.forward(xg.clone()))   # eager, its own workspace and output
+        assert np.array_equal(got, ref), f"replay {rep} differs from the eager run"
+
+
 def test_vgg16_end_to_end_vs_oracle_chain():
     # informational bound: the all-oracle chain vs the GPU chain, errors compound
     spec = workloads.net_spec(2)
