@@ -78,8 +78,11 @@ struct WGeo {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// The DMA helpers below write M0, which the compiler treats as reserved; no
-// code generated for these kernels keeps a value in M0 across them.
+// The DMA helpers below write and read M0, which the compiler treats as
+// reserved; no code generated for these kernels keeps or sets a value in M0
+// (no indirect register indexing), so M0 holds between set_m0 and the DMAs.
+// They are inline assembly so that the compiler neither waits for the DMAs
+// (the caller counts vmcnt) nor moves LDS reads across them.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 
@@ -95,19 +98,60 @@ __device__ __forceinline__ u32x4 make_rsrc(const void* base, uint32_t bytes) {
   return r;
 }
 
-// global -> LDS DMA of 16 (4) bytes per lane: lane l's data lands at LDS byte
-// lds + 16 l (4 l).  Issued as inline assembly so that the compiler neither
-// waits for it (the caller counts vmcnt) nor moves LDS reads across it.
-__device__ __forceinline__ void dma_lds_b128(u32x4 rsrc, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :: "s"(lds), "v"(voff), "s"(rsrc) : "memory", "m0");
+// M0 for the LDS DMAs that follow (with the wait state the hardware needs
+// between an M0 write and its use)
+__device__ __forceinline__ void set_m0(uint32_t v) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" :: "s"(v) : "memory", "m0");
 }
-__device__ __forceinline__ void dma_lds_b32(u32x4 rsrc, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-               :: "s"(lds), "v"(voff), "s"(rsrc) : "memory", "m0");
+// global -> LDS DMA of 16 (4) bytes per lane with immediate offset OFF: it
+// moves both the global offset and the LDS address, so lane l's data lands
+// at LDS byte M0 + OFF + 16 l (4 l) and comes from offset voff + OFF
+template <uint32_t OFF>
+__device__ __forceinline__ void dma_lds_b128_at(u32x4 rsrc, uint32_t voff) {
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds" :: "v"(voff), "s"(rsrc), "n"(OFF) : "memory");
+}
+template <uint32_t OFF>
+__device__ __forceinline__ void dma_lds_b32_at(u32x4 rsrc, uint32_t voff) {
+  asm volatile("buffer_load_dword %0, %1, 0 offen offset:%2 lds" :: "v"(voff), "s"(rsrc), "n"(OFF) : "memory");
 }
 
 #pragma clang diagnostic pop
+
+// A channel's DMAs land at LDS byte offsets L from its ring slot; each is
+// issued with immediate offset L % 4096 and M0 = slot + (L - L % 4096), set
+// once per 4 KB group.  The descriptors' bases sit kDmaShift bytes below the
+// data (ranges kDmaShift bytes longer), and every in-range per-lane offset
+// carries + kDmaShift - L % 4096, so the offsets stay non-negative.
+constexpr uint32_t kDmaShift = 4096;
+template <uint32_t L, uint32_t LPREV, bool FIRST>
+__device__ __forceinline__ void dma_b128_at(u32x4 rsrc, uint32_t voff, uint32_t slot) {
+  if constexpr (FIRST || (L & ~4095u) != (LPREV & ~4095u)) set_m0(slot + (L & ~4095u));
+  dma_lds_b128_at<(L & 4095u)>(rsrc, voff);
+}
+template <uint32_t L, uint32_t LPREV, bool FIRST>
+__device__ __forceinline__ void dma_b32_at(u32x4 rsrc, uint32_t voff, uint32_t slot) {
+  if constexpr (FIRST || (L & ~4095u) != (LPREV & ~4095u)) set_m0(slot + (L & ~4095u));
+  dma_lds_b32_at<(L & 4095u)>(rsrc, voff);
+}
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+// a descriptor whose base sits `shift` bytes below `base` and whose range
+// covers those bytes too (no access ever lands below base)
+__device__ __forceinline__ u32x4 make_rsrc_below(const void* base, uint32_t bytes, uint32_t shift) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base) - shift;
+  u32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b));
+  r.y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32) & 0xFFFFu);
+  r.z = __builtin_amdgcn_readfirstlane(bytes + shift);
+  r.w = 0x00020000u;
+  return r;
+}
 
 // the same descriptor moved on by one channel of `bytes` bytes
 __device__ __forceinline__ u32x4 next_channel(u32x4 r, uint32_t bytes) {
@@ -263,7 +307,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
     wsl[j] = e < 8 * KW ? e / KW : 8;
     wtp[j] = e % KW;
   }
-  auto weight_offs = [&](const Meta& m, uint32_t (&off)[NWL]) __attribute__((always_inline)) {
+  // adj: added to the in-range offsets (the DMA path's descriptor shift)
+  auto weight_offs = [&](const Meta& m, uint32_t (&off)[NWL], auto adj) __attribute__((always_inline)) {
     const uint32_t kept = m.wo >> 24;
 #pragma unroll
     for (int j = 0; j < NWL; ++j) {
@@ -271,9 +316,10 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       const uint32_t rank = __builtin_popcount(kept & ((1u << s) - 1u));
       const bool ok = s < 8 && t < KT && ((kept >> s) & 1u);
       const uint32_t wi = (m.wo & 0xFFFFFFu) + KS * rank + t;
-      off[j] = ok ? a.off_w + static_cast<uint32_t>(sizeof(TA)) * wi : 0x80000000u;
+      off[j] = ok ? a.off_w + static_cast<uint32_t>(sizeof(TA)) * wi + adj(j) : 0x80000000u;
     }
   };
+  auto no_adj = [](int) { return 0u; };
   // global -> registers: the next channel's halo tile (xf walks the channels
   // in order) and weights
   const TA* xf = x + static_cast<size_t>(c0) * a.h * a.w;
@@ -334,11 +380,11 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   if (ABF && c0 < c1) {
     Meta m0 = load_meta(c0), m1 = load_meta(c0 + 1), m2 = load_meta(c0 + 2);
     uint32_t wof[NWL];
-    weight_offs(m0, wof);
+    weight_offs(m0, wof, no_adj);
     fetch(wof);
     store(ring);
     if (c0 + 1 < c1) {
-      weight_offs(m1, wof);
+      weight_offs(m1, wof, no_adj);
       fetch(wof);
     }
 #pragma unroll 1
@@ -346,7 +392,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       const int k = c - c0;
       float* cur = ring + (k & 1) * SLOT;
       float* nxt = ring + ((k + 1) & 1) * SLOT;
-      weight_offs(m2, wof);                       // needs meta(c+2): before any LDS op is in flight
+      weight_offs(m2, wof, no_adj);               // needs meta(c+2): before any LDS op is in flight
       if (c + 1 < c1) store(nxt);                 // channel c+1 -> LDS
       if (c + 2 < c1) fetch(wof);                 // channel c+2 -> registers
       // patch and the kept slots' weights of channel c
@@ -413,27 +459,46 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
     constexpr int QV = G::NQ + NWL;       // 16-byte patch loads + weight loads
     constexpr int QS = 4 * G::NQ + NWL;   // 4-byte patch loads + weight loads
     const uint32_t ring_b = lds_addr(ring);
-    const u32x4 brs = make_rsrc(blob, a.blob_bytes);
+    // LDS byte offsets within a ring slot: 16-byte patch loads t at 1024 t,
+    // 4-byte ones (t, j) at 256 (4 t + j), weight loads j at 4 PATCH + 256 j
+    constexpr uint32_t LW0 = 4u * G::PATCH;
+    const u32x4 brs = make_rsrc_below(blob, a.blob_bytes, kDmaShift);
     // descriptor of the next channel to DMA (channels are DMA'd in order)
-    u32x4 cr = make_rsrc(x + static_cast<size_t>(c0) * a.h * a.w, chan_bytes);
+    u32x4 cr = make_rsrc_below(x + static_cast<size_t>(c0) * a.h * a.w, chan_bytes, kDmaShift);
+#pragma unroll
+    for (int t = 0; t < NQ; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t l = v4 ? 1024u * t : 256u * (4 * t + j);
+        if (qoff[t][j] != 0x80000000u) qoff[t][j] += kDmaShift - (l & 4095u);
+      }
+    auto wadj = [](int j) { return kDmaShift - ((LW0 + 256u * j) & 4095u); };
     auto dma = [&](int c, uint32_t wo) __attribute__((always_inline)) {
       const uint32_t k = static_cast<uint32_t>(c - c0);
       const uint32_t sb = ring_b + 4u * ((k % NS) * SLOT);
-      if (v4) {
-#pragma unroll
-        for (int t = 0; t < NQ; ++t) dma_lds_b128(cr, qoff[t][0], sb + 1024u * t);
-      } else {
-#pragma unroll
-        for (int t = 0; t < NQ; ++t)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) dma_lds_b32(cr, qoff[t][j], sb + 256u * (4 * t + j));
-      }
       Meta mw;
       mw.wo = wo;
       uint32_t wof[NWL];
-      weight_offs(mw, wof);
-#pragma unroll
-      for (int j = 0; j < NWL; ++j) dma_lds_b32(brs, wof[j], sb + 4u * (G::PATCH + 64 * j));
+      weight_offs(mw, wof, wadj);
+      if (v4) {
+        static_for<0, NQ>([&](auto ti) __attribute__((always_inline)) {
+          constexpr int T = decltype(ti)::value;
+          dma_b128_at<1024u * T, 1024u * (T - 1), T == 0>(cr, qoff[T][0], sb);
+        });
+        static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
+          constexpr int J = decltype(ji)::value;
+          dma_b32_at<LW0 + 256u * J, (J == 0 ? 1024u * (NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
+        });
+      } else {
+        static_for<0, 4 * NQ>([&](auto ii) __attribute__((always_inline)) {
+          constexpr int I = decltype(ii)::value;
+          dma_b32_at<256u * I, 256u * (I - 1), I == 0>(cr, qoff[I / 4][I % 4], sb);
+        });
+        static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
+          constexpr int J = decltype(ji)::value;
+          dma_b32_at<LW0 + 256u * J, (J == 0 ? 256u * (4 * NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
+        });
+      }
       cr = next_channel(cr, chan_bytes);
     };
     auto load_wo = [&](int c) __attribute__((always_inline)) {
