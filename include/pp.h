@@ -141,7 +141,8 @@ pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
  *                       otherwise); needs h_out, w_out >= 2 and a tiling
  *                       that holds whole 2 x 2 windows per lane: the
  *                       canonical or all-ones library with pad = dilation,
- *                       else PP_EUNSUPPORTED; never splits the channels)
+ *                       else PP_EUNSUPPORTED; with a channel split the
+ *                       second pass takes the pool)
  *   workspace, ws_bytes optional device scratch (NULL, 0 for none), 256-byte
  *                       aligned.  With pp_conv2d_workspace() bytes the
  *                       kernel may split the input channels over more

@@ -208,8 +208,7 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None).
     workspace: "auto" (a scratch tensor of pp_conv2d_workspace bytes, kept on
     the layer per input shape), None (no scratch) or a uint8 device tensor.
-    maxpool2: store the 2 x 2 max pool of the activated output (PP_MAXPOOL2);
-    the channel split is then never used, so no workspace is needed."""
+    maxpool2: store the 2 x 2 max pool of the activated output (PP_MAXPOOL2)."""
     torch = _torch()
     lib = load_library()
     if not x.is_contiguous():
@@ -220,7 +219,6 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     ho, wo = out_size(layer.h_blob, h, w)
     if maxpool2:
         ho, wo = ho // 2, wo // 2
-        workspace = None
     shape = (n, layer.info["c_out"], ho, wo)
     if out is None:
         out = torch.empty(shape, dtype=x.dtype, device=x.device)

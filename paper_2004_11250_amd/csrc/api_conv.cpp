@@ -86,24 +86,24 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const int lib = library_kind(v);
   const bool bf = act_dtype == PP_BF16;
   ConvPlan plan = plan_conv(p, lib, bf, scratch != nullptr);
-  if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the max pool for this layer");
   if (plan.ksplit > 1) {
     if (split_bytes(plan, p) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
       plan = plan_conv(p, lib, bf, false);   // not enough scratch: no split
     else
       p.part = static_cast<float*>(scratch);
   }
+  if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the max pool for this layer");
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;
 }
 
-bool conv_pool_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype) {
+bool conv_pool_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, bool with_scratch) {
   int ho = 0, wo = 0;
   if (conv_check(v, n, h, w, act_dtype, &ho, &wo) != PP_OK || ho < 2 || wo < 2) return false;
   ConvParams p = layer_params(v, n, h, w, ho, wo);
   p.flags = PP_MAXPOOL2;
-  return plan_conv(p, library_kind(v), act_dtype == PP_BF16, false).recipe >= 0;
+  return plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_scratch).recipe >= 0;
 }
 
 size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype) {

@@ -21,8 +21,8 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
                        hipStream_t st);
 
 // whether pp_conv2d_fwd can fuse a 2 x 2 max pool (PP_MAXPOOL2) for this
-// layer and input
-bool conv_pool_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype);
+// layer and input, with or without split scratch
+bool conv_pool_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, bool with_scratch);
 
 // scratch bytes pp_conv2d_fwd can use for this layer and input (0: none)
 size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype);

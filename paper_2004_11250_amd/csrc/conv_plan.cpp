@@ -120,8 +120,10 @@ size_t split_bytes(const ConvPlan& plan, const ConvParams& p) {
   return items * plan.ksplit * 8 * r.r * r.cc * 64 * sizeof(float);
 }
 
-// a fused 2 x 2 max pool needs whole windows per lane: wave-pipeline tilings
-// with even R and CC (tile origins are then even too)
+// a fused 2 x 2 max pool is taken by the conv kernel when each lane holds
+// whole windows (wave-pipeline tilings with even R and CC; tile origins are
+// then even too), or by the second pass of a channel split, which sees whole
+// tiles (every wave-pipeline tile is 8 R x 8 CC outputs: even)
 static bool pool_fits(int id) {
   const RecipeInfo r = recipe_info(id);
   return is_wave_recipe(id) && r.r % 2 == 0 && r.cc % 2 == 0;
@@ -129,10 +131,21 @@ static bool pool_fits(int id) {
 
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
   const bool pool = (p.flags & PP_MAXPOOL2) != 0;
-  auto ok = [&](int id) { return recipe_usable(id, p, lib, bf16) && (!pool || pool_fits(id)); };
-  if (pool) allow_split = false;
+  // a plan for recipe id, or recipe -1 when it cannot take the pool
+  auto try_plan = [&](int id) {
+    ConvPlan pl;
+    pl.recipe = -1;
+    if (!recipe_usable(id, p, lib, bf16)) return pl;
+    if (pool && !is_wave_recipe(id)) return pl;
+    pl = finish_plan(id, p, allow_split);
+    if (pool && pl.ksplit == 1 && !pool_fits(id)) pl.recipe = -1;
+    return pl;
+  };
   const int forced = env_recipe();
-  if (forced >= 0 && forced < kNumRecipes && ok(forced)) return finish_plan(forced, p, allow_split);
+  if (forced >= 0 && forced < kNumRecipes) {
+    const ConvPlan pl = try_plan(forced);
+    if (pl.recipe >= 0) return pl;
+  }
   const long pix = static_cast<long>(p.ho) * p.wo;
   int pref[4];
   const bool wave_ok = (lib == kLibCanon8 || lib == kLibDense9) && p.pad == p.dil;
@@ -186,12 +199,16 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
   } else {
     pref[0] = 8; pref[1] = 13; pref[2] = 13; pref[3] = 13;
   }
-  for (int id : pref)
-    if (ok(id)) return finish_plan(id, p, allow_split);
+  for (int id : pref) {
+    const ConvPlan pl = try_plan(id);
+    if (pl.recipe >= 0) return pl;
+  }
   if (pool) {
     // the pooled layer's fallbacks (2 x 4, then 2 x 2 outputs per lane)
-    for (int id : {31, 20, 27, 23, 22, 21, 28})
-      if (ok(id)) return finish_plan(id, p, false);
+    for (int id : {31, 20, 27, 23, 22, 21, 28}) {
+      const ConvPlan pl = try_plan(id);
+      if (pl.recipe >= 0) return pl;
+    }
     ConvPlan none;
     none.recipe = -1;   // no tiling can fuse the pool
     return none;

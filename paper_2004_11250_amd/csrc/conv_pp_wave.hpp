@@ -757,8 +757,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       __syncthreads();
     }
     if constexpr (R % 2 == 0 && CC % 2 == 0) {
-      if (pool) {
-        // units (slot, row pair); the planner runs pooled layers unsplit
+      if (pool && !split) {
+        // units (slot, row pair); a split pools in its second pass
         constexpr int NUP = G::PS * (R / 2);
 #pragma unroll
         for (int u0 = 0; u0 < NUP; u0 += WS) {
@@ -796,7 +796,10 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
 // Second pass of a channel split: y = act(sum over the ksplit partial-sum
 // blocks of a tile, in split order, + bias), stored through perm.  One
 // workgroup per (image, tile, slot group); thread i handles element i of the
-// tile's block layout ((slot, row, col) x lane).
+// tile's block layout ((slot, row, col) x lane).  With PP_MAXPOOL2 thread i
+// handles pooled output i of the tile instead: the max over its 2 x 2
+// window of the activated sums, in the order the conv kernel's own pooled
+// store takes them.
 template <int R, int CC, int LW, class TA>
 __global__ __launch_bounds__(256) void pp_split_reduce_kernel(ConvParams a) {
   constexpr bool ABF = sizeof(TA) == 2;
@@ -810,8 +813,43 @@ __global__ __launch_bounds__(256) void pp_split_reduce_kernel(ConvParams a) {
   const int ty = t % a.tiles_y;
   const int img = t / a.tiles_y;
   const float* pb = a.part + static_cast<size_t>(item) * a.ksplit * BLK;
-  TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
   const bool relu = (a.flags & PP_RELU) != 0;
+  if (a.flags & PP_MAXPOOL2) {
+    const int pho = a.ho / 2, pwo = a.wo / 2;
+    TA* __restrict__ yp = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * pho * pwo;
+    constexpr int PH = TH / 2, PW = TW / 2;
+    static_assert(TH % 2 == 0 && TW % 2 == 0, "pooled tiles need even sides");
+    for (int i = threadIdx.x; i < 8 * PH * PW; i += 256) {
+      const int s = i / (PH * PW), px = i % PW, py = (i / PW) % PH;
+      const int oy = ty * TH + 2 * py, ox = tx * TW + 2 * px;
+      if (oy + 1 >= a.ho || ox + 1 >= a.wo) continue;   // incomplete window (floor)
+      const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
+      const uint32_t o = reinterpret_cast<const uint32_t*>(a.blob + a.off_perm)[slot];
+      if (o >= static_cast<uint32_t>(a.c_out)) continue;   // padding slot
+      const float bias = reinterpret_cast<const float*>(a.blob + a.off_bias)[slot];
+      float v[2][2];
+#pragma unroll
+      for (int dy = 0; dy < 2; ++dy)
+#pragma unroll
+        for (int dx = 0; dx < 2; ++dx) {
+          const int yl = 2 * py + dy, xl = 2 * px + dx;   // tile-local output
+          const int lane = (yl / R) * LW + xl / CC;
+          const int e = (s * R + yl % R) * CC + xl % CC;
+          float t = 0.0f;
+          for (int k = 0; k < a.ksplit; ++k) t += pb[static_cast<size_t>(k) * BLK + e * 64 + lane];
+          t += bias;
+          v[dy][dx] = relu ? fmaxf(t, 0.0f) : t;
+        }
+      const float m = fmaxf(fmaxf(v[0][0], v[0][1]), fmaxf(v[1][0], v[1][1]));
+      const size_t at = (static_cast<size_t>(o) * pho + oy / 2) * pwo + ox / 2;
+      if constexpr (ABF)
+        reinterpret_cast<uint16_t*>(yp)[at] = static_cast<uint16_t>(to_bf16_bits(m));
+      else
+        reinterpret_cast<float*>(yp)[at] = m;
+    }
+    return;
+  }
+  TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
   for (int i = threadIdx.x; i < BLK; i += 256) {
     const int lane = i % 64, e = i / 64;       // e = (s * R + r) * CC + q
     const int q = e % CC, r = (e / CC) % R, s = e / (CC * R);

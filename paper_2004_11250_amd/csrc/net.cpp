@@ -144,7 +144,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
       read_later = ops[j].src == cv.dst || (ops[j].kind == PP_OP_ADD && ops[j].src2 == cv.dst);
       if (ops[j].dst == cv.dst) break;   // rewritten: later reads see the new value
     }
-    if (!read_later && conv_pool_fusable(pl->views[i], n, pl->in[i].h, pl->in[i].w, act)) {
+    if (!read_later && conv_pool_fusable(pl->views[i], n, pl->in[i].h, pl->in[i].w, act, true)) {
       pl->fuse_pool[i] = 1;
       ++i;   // the pool is taken; it cannot start another pair
     }
@@ -248,7 +248,7 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
         if (pl.fuse_pool[i]) {
           // conv + the max pool of op i + 1
           st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags | PP_MAXPOOL2,
-                            nullptr, 0, stream);
+                            scratch, pl.scratch_bytes, stream);
           if (st != PP_OK) return st;
           ++i;
           break;

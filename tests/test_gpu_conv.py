@@ -225,17 +225,21 @@ def test_every_tiling(recipe, monkeypatch):
         check(y, ref, bound, dtype, f"recipe {recipe} {(s, p, d)} {dtype}")
 
 
-# conv + ReLU + 2 x 2 max pool in one launch (PP_MAXPOOL2): against the
-# oracle conv pooled (max is 1-Lipschitz: the pooled S bounds the error), and
-# bitwise against pooling the unpooled output of the same tiling; odd output
-# sizes drop the last row / column
-POOL_RECIPES = [None, 20, 21, 22, 23, 26, 27, 28, 31, 32, 33, 34, 35]
+# conv + ReLU + 2 x 2 max pool (PP_MAXPOOL2): against the oracle conv pooled
+# (max is 1-Lipschitz: the pooled S bounds the error), and bitwise against
+# pooling the unpooled output of the same plan; odd output sizes drop the
+# last row / column.  Forced splits pool in the second pass, also for
+# tilings with one output row per lane (24, 25).
+POOL_RECIPES = [(None, 0), (20, 0), (21, 0), (22, 0), (23, 0), (26, 0), (27, 0), (28, 0), (31, 0), (32, 0),
+                (33, 0), (34, 0), (35, 0), (24, 3), (25, 2), (20, 4)]
 
 
-@pytest.mark.parametrize("recipe", POOL_RECIPES)
-def test_fused_maxpool(recipe, monkeypatch):
+@pytest.mark.parametrize("recipe,ksplit", POOL_RECIPES)
+def test_fused_maxpool(recipe, ksplit, monkeypatch):
     if recipe is not None:
         monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
     for (s, p, d), dtype, shape in (((1, 1, 1), "f32", (19, 21, 37, 45)), ((1, 1, 1), "f32", (16, 24, 30, 44)),
                                     ((2, 1, 1), "f32", (17, 9, 41, 50)), ((1, 2, 2), "f32", (11, 13, 29, 33)),
                                     ((1, 1, 1), "bf16", (24, 17, 33, 70)), ((1, 1, 1), "bf16", (8, 20, 14, 14))):
@@ -250,7 +254,7 @@ def test_fused_maxpool(recipe, monkeypatch):
             w_or = L["w"]
         wd = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
         layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], s, p, d, wd)
-        _say("fused maxpool, recipe", recipe, (s, p, d), dtype, shape)
+        _say("fused maxpool, recipe", recipe, "ksplit", ksplit, (s, p, d), dtype, shape)
         xd = _to_dev(x, dtype)
         yp = pp.conv2d_fwd(layer, xd, relu=True, maxpool2=True)
         args = (x, w_or, L["b"], L["pid"], L["conn"], L["lib"])
@@ -258,9 +262,11 @@ def test_fused_maxpool(recipe, monkeypatch):
         bound = oconv.maxpool2(oconv.conv3x3_bound(*args, s, p, d))
         got = _from_dev(yp)
         check(got, ref, bound, dtype, f"fused maxpool recipe {recipe} {(s, p, d)} {dtype} {shape}")
-        if recipe is not None and pp.conv2d_recipe(layer.h_blob, 2, h, w, wd) == recipe:
-            # the same tiling unpooled (no split: no workspace), pooled on the CPU
-            y = pp.conv2d_fwd(layer, xd, relu=True, workspace=None)
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, wd)
+        if recipe is not None and plan[0] == recipe and (not ksplit or plan[1] == ksplit):
+            # the same plan unpooled (the pooled plan keeps the forced tiling
+            # and the planner's split), pooled on the CPU
+            y = pp.conv2d_fwd(layer, xd, relu=True)
             pooled = torch.nn.functional.max_pool2d(y.float().cpu(), 2)
             if dtype == "bf16":
                 pooled = pooled.to(torch.bfloat16)
