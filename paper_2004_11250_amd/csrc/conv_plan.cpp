@@ -159,7 +159,11 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
       pref[0] = 31; pref[1] = 20; pref[2] = 0; pref[3] = 13;
     } else if (pix >= 160L * 160L) {
       const long items31 = static_cast<long>(p.n) * tiles_of(31, p) * p.n_groups;
-      if (waves_of(32, p) <= 2048) {
+      if (static_cast<long>(p.n) * tiles_of(26, p) * p.n_groups <= 512) {
+        // 4 x 4 outputs per lane: twice the FMAs per channel step for about
+        // 1.3x its time, while its grid stays within two workgroups per CU
+        pref[0] = 26; pref[1] = 32; pref[2] = 31; pref[3] = 30;
+      } else if (waves_of(32, p) <= 2048) {
         pref[0] = 32; pref[1] = 31; pref[2] = 30; pref[3] = 17;
       } else if (items31 <= 4096) {
         pref[0] = 20; pref[1] = 31; pref[2] = 30; pref[3] = 17;
@@ -177,9 +181,24 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
     } else {
       pref[0] = 25; pref[1] = 23; pref[2] = 10; pref[3] = 13;
     }
+  } else if (wave_ok && !bf16 && lib == kLibCanon8 && p.c_in > 8) {
+    // fp32 batches and strides 2 (timed on the style-transfer and
+    // colourization layer shapes): 2 x 4 outputs per lane, two channel splits
+    // per tile for very large grids, register-pipelined two- or four-way
+    // splits for the smaller ones
+    const long items = static_cast<long>(p.n) * tiles_of(31, p) * p.n_groups;
+    if (items >= 4096) {
+      pref[0] = 31; pref[1] = 20; pref[2] = 13; pref[3] = 13;
+    } else if (items >= 2048) {
+      pref[0] = p.stride == 2 ? 32 : 20; pref[1] = 31; pref[2] = 20; pref[3] = 13;
+    } else if (items >= 1024) {
+      pref[0] = p.stride == 2 ? 32 : 33; pref[1] = 31; pref[2] = 20; pref[3] = 13;
+    } else {
+      pref[0] = 33; pref[1] = 20; pref[2] = 31; pref[3] = 13;
+    }
   } else if (wave_ok) {
-    // batches, strides 2, bf16 (timed on the style-transfer, super-resolution
-    // and colourization layer shapes): 2 x 4 outputs per lane; two channel
+    // bf16, and the all-ones library (timed on the super-resolution and
+    // colourization layer shapes): 2 x 4 outputs per lane; two channel
     // splits per tile for very large grids, else four; few input channels
     // (first layers) with 1 x 4 outputs per lane
     const long items = static_cast<long>(p.n) * tiles_of(31, p) * p.n_groups;

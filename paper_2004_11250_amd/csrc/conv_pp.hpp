@@ -74,7 +74,8 @@ struct ConvParams {
   X(33, 2, 4, 8, 4, 1)    \
   X(34, 2, 4, 8, 8, 1)    \
   X(35, 2, 2, 8, 8, 1)    \
-  X(36, 1, 2, 8, 8, 1)
+  X(36, 1, 2, 8, 8, 1)    \
+  X(37, 4, 4, 8, 2, 0)
 
 constexpr int kFirstWaveRecipe = 20;
 
@@ -97,16 +98,23 @@ constexpr long wave_slot_floats(int r, int cc, int lw, int s, int d, int warea) 
   return (static_cast<long>(tih) * lstr + 255) / 256 * 256 + warea;
 }
 // ring slots per wave: fp32 channels are DMA'd into LDS three channels ahead
-// (4 slots); bf16 stages through registers (2 slots)
-constexpr int wave_nslot(bool bf16) { return bf16 ? 2 : 4; }
+// (4 slots), or two (3 slots) for stride-1 tilings where 4 would leave a
+// compute unit fewer than 8 waves' worth of LDS (160 KB / 8 per wave; timed
+// on the 4 x 4 outputs-per-lane tilings); bf16 stages through registers
+// (2 slots)
+constexpr int wave_nslot(int r, int cc, int lw, int ws, int s, int d, int warea, bool bf16) {
+  if (bf16) return 2;
+  const long per_wave = (ws >= 8 ? 160L * 1024 / ws : 20L * 1024);
+  return s != 1 || 4 * 4 * wave_slot_floats(r, cc, lw, s, d, warea) <= per_wave ? 4 : 3;
+}
 // LDS floats of one wave-pipeline workgroup: per wave a ring of nslot
 // slots, or the partial-sum exchange of 2 slots per wave, whichever is larger
 constexpr long wave_lds_floats(int r, int cc, int lw, int ws, int s, int d, int warea, bool bf16) {
-  const long ring = wave_nslot(bf16) * wave_slot_floats(r, cc, lw, s, d, warea);
+  const long ring = wave_nslot(r, cc, lw, ws, s, d, warea, bf16) * wave_slot_floats(r, cc, lw, s, d, warea);
   const long xch = static_cast<long>(ws) * 2 * r * cc * 64;
   return ws * ring > xch ? ws * ring : xch;
 }
-constexpr int kNumRecipes = 37;
+constexpr int kNumRecipes = 38;
 
 // pipe: the wave-pipeline kernel reads the next channel from LDS into a
 // second register set while it computes the current one (fp32, canonical

@@ -56,7 +56,7 @@ struct WGeo {
   static constexpr int SLOT = PATCH + WAREA;
   // ring slots per wave: fp32 channels are DMA'd straight into LDS DPF
   // channels ahead (DPF + 1 slots); bf16 goes through registers (2 slots)
-  static constexpr int NSLOT = wave_nslot(ABF);
+  static constexpr int NSLOT = wave_nslot(R, CC, LW, WS, S, D, WAREA, ABF);
   static constexpr int DPF = NSLOT - 1;
   static_assert(SLOT == wave_slot_floats(R, CC, LW, S, D, WAREA), "planner and kernel disagree on the slot size");
   static constexpr int RING = NSLOT * SLOT;               // per wave

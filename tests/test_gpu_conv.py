@@ -200,7 +200,7 @@ def test_vgg16_full_size_layer_sampled(idx):
 
 
 # every compiled tiling, forced through the PP_RECIPE override of the planner
-RECIPES = list(range(37))
+RECIPES = list(range(38))
 
 
 @pytest.mark.parametrize("recipe", RECIPES)
@@ -231,7 +231,7 @@ def test_every_tiling(recipe, monkeypatch):
 # last row / column.  Forced splits pool in the second pass, also for
 # tilings with one output row per lane (24, 25).
 POOL_RECIPES = [(None, 0), (20, 0), (21, 0), (22, 0), (23, 0), (26, 0), (27, 0), (28, 0), (31, 0), (32, 0),
-                (33, 0), (34, 0), (35, 0), (24, 3), (25, 2), (20, 4)]
+                (33, 0), (34, 0), (35, 0), (37, 0), (24, 3), (25, 2), (20, 4)]
 
 
 @pytest.mark.parametrize("recipe,ksplit", POOL_RECIPES)
