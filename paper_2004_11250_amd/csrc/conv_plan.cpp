@@ -177,7 +177,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
     } else if (pix >= 20L * 20L) {
       pref[0] = 23; pref[1] = 22; pref[2] = 8; pref[3] = 13;
     } else if (allow_split) {
-      pref[0] = 24; pref[1] = 25; pref[2] = 10; pref[3] = 13;   // 24 runs split 4 ways at 14 x 14
+      pref[0] = 36; pref[1] = 24; pref[2] = 25; pref[3] = 10;   // 36 / 24 run split 4 ways at 14 x 14
     } else {
       pref[0] = 25; pref[1] = 23; pref[2] = 10; pref[3] = 13;
     }

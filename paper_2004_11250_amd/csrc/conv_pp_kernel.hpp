@@ -130,6 +130,46 @@ __device__ __forceinline__ void apply_canon8(uint32_t p, float (&acc)[R][CC], co
   }
 }
 
+// the same dispatch on the 3-bit pattern code held at bit SH of a code word,
+// as a tree of bit tests on the word itself (no extraction, no compares).
+// Each level re-reads the word in place through an empty asm, so its test
+// stays a scalar bit test right before its branch (tests hoisted above the
+// tree become 64-bit condition masks and extra instructions).
+template <int BIT>
+__device__ __forceinline__ bool sbit(uint32_t& cw) {
+  asm volatile("" : "+s"(cw));
+  return (cw >> BIT) & 1u;
+}
+template <int SH, int S, int D, int R, int CC, int PR, int PC>
+__device__ __forceinline__ void apply_canon8_bits(uint32_t cw, float (&acc)[R][CC], const float (&pt)[PR][PC],
+                                                  float w0, float w1, float w2, float w3) {
+  if (sbit<SH + 2>(cw)) {
+    if (sbit<SH + 1>(cw)) {
+      if (sbit<SH>(cw))
+        apply4<kCanon8[7], S, D>(acc, pt, w0, w1, w2, w3);
+      else
+        apply4<kCanon8[6], S, D>(acc, pt, w0, w1, w2, w3);
+    } else {
+      if (sbit<SH>(cw))
+        apply4<kCanon8[5], S, D>(acc, pt, w0, w1, w2, w3);
+      else
+        apply4<kCanon8[4], S, D>(acc, pt, w0, w1, w2, w3);
+    }
+  } else {
+    if (sbit<SH + 1>(cw)) {
+      if (sbit<SH>(cw))
+        apply4<kCanon8[3], S, D>(acc, pt, w0, w1, w2, w3);
+      else
+        apply4<kCanon8[2], S, D>(acc, pt, w0, w1, w2, w3);
+    } else {
+      if (sbit<SH>(cw))
+        apply4<kCanon8[1], S, D>(acc, pt, w0, w1, w2, w3);
+      else
+        apply4<kCanon8[0], S, D>(acc, pt, w0, w1, w2, w3);
+    }
+  }
+}
+
 // generic library: taps tested one by one against the runtime mask
 template <int S, int D, int R, int CC, int PR, int PC>
 __device__ __forceinline__ void apply_generic(uint32_t mask, float (&acc)[R][CC], const float (&pt)[PR][PC],

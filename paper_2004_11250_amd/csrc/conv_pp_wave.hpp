@@ -300,23 +300,26 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   // (zero for padding taps, pruned slots and e >= 8 KW); its compact index is
   // woff + (stored weights per kernel) * rank(slot) + tap
   constexpr uint32_t KS = LIB == kLibDense9 ? (ABF ? 10u : 9u) : 4u;   // stored weights per kernel
-  int wsl[NWL], wtp[NWL];
+  // per lane and weight load j: the slots below this lane's slot (rank mask),
+  // its own slot bit (0 for padding taps and lanes past the 8 slots), its tap
+  uint32_t wlow[NWL], wbit[NWL], wtp[NWL];
 #pragma unroll
   for (int j = 0; j < NWL; ++j) {
     const int e = 64 * j + lane;
-    wsl[j] = e < 8 * KW ? e / KW : 8;
-    wtp[j] = e % KW;
+    const int s = e < 8 * KW ? e / KW : 8, t = e % KW;
+    wlow[j] = s < 8 ? (1u << s) - 1u : 0u;
+    wbit[j] = (s < 8 && t < KT) ? 1u << s : 0u;
+    wtp[j] = static_cast<uint32_t>(t);
   }
   // adj: added to the in-range offsets (the DMA path's descriptor shift)
   auto weight_offs = [&](const Meta& m, uint32_t (&off)[NWL], auto adj) __attribute__((always_inline)) {
     const uint32_t kept = m.wo >> 24;
 #pragma unroll
     for (int j = 0; j < NWL; ++j) {
-      const int s = wsl[j], t = wtp[j];
-      const uint32_t rank = __builtin_popcount(kept & ((1u << s) - 1u));
-      const bool ok = s < 8 && t < KT && ((kept >> s) & 1u);
-      const uint32_t wi = (m.wo & 0xFFFFFFu) + KS * rank + t;
-      off[j] = ok ? a.off_w + static_cast<uint32_t>(sizeof(TA)) * wi + adj(j) : 0x80000000u;
+      const uint32_t rank = __builtin_popcount(kept & wlow[j]);
+      const uint32_t wi = (m.wo & 0xFFFFFFu) + KS * rank + wtp[j];
+      const uint32_t o = a.off_w + static_cast<uint32_t>(sizeof(TA)) * wi + adj(j);
+      off[j] = (kept & wbit[j]) != 0 ? o : 0x80000000u;
     }
   };
   auto no_adj = [](int) { return 0u; };
@@ -376,6 +379,31 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
     for (int r = 0; r < R; ++r)
 #pragma unroll
       for (int q = 0; q < CC; ++q) acc[s][r][q] = 0.0f;
+  // the FMAs of channel c for its kept slots, slot by slot (compile-time
+  // slot index, so the accumulators stay in registers whatever the unroller
+  // decides); canonical library: slot s's pattern code is byte s % 4 of code
+  // word cx (slots 0-3) or cy (4-7), branched on bit by bit in place
+  auto compute = [&](const Meta& m, uint32_t kc, const float (&pt)[PR][PC], const float (&wt)[8][KW])
+      __attribute__((always_inline)) {
+    static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
+      constexpr int s = decltype(si)::value;
+      if (!((kc >> s) & 1u)) return;
+      if constexpr (LIB == kLibDense9) {
+        fma_tap<0, S, D>(acc[s], pt, wt[s][0]);
+        fma_tap<1, S, D>(acc[s], pt, wt[s][1]);
+        fma_tap<2, S, D>(acc[s], pt, wt[s][2]);
+        fma_tap<3, S, D>(acc[s], pt, wt[s][3]);
+        fma_tap<4, S, D>(acc[s], pt, wt[s][4]);
+        fma_tap<5, S, D>(acc[s], pt, wt[s][5]);
+        fma_tap<6, S, D>(acc[s], pt, wt[s][6]);
+        fma_tap<7, S, D>(acc[s], pt, wt[s][7]);
+        fma_tap<8, S, D>(acc[s], pt, wt[s][8]);
+      } else {
+        apply_canon8_bits<8 * (s & 3), S, D>(s < 4 ? m.cx : m.cy, acc[s], pt, wt[s][0], wt[s][1], wt[s][2],
+                                             wt[s][3]);
+      }
+    });
+  };
 
   if (ABF && c0 < c1) {
     Meta m0 = load_meta(c0), m1 = load_meta(c0 + 1), m2 = load_meta(c0 + 2);
@@ -422,24 +450,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       uint32_t kc = kept;
       asm volatile("" : "+s"(kc));   // fresh slot tests (no 64-bit condition masks kept live)
       if (kc != 0) {
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          if (!((kc >> s) & 1u)) continue;
-          if constexpr (LIB == kLibDense9) {
-            fma_tap<0, S, D>(acc[s], p, w[s][0]);
-            fma_tap<1, S, D>(acc[s], p, w[s][1]);
-            fma_tap<2, S, D>(acc[s], p, w[s][2]);
-            fma_tap<3, S, D>(acc[s], p, w[s][3]);
-            fma_tap<4, S, D>(acc[s], p, w[s][4]);
-            fma_tap<5, S, D>(acc[s], p, w[s][5]);
-            fma_tap<6, S, D>(acc[s], p, w[s][6]);
-            fma_tap<7, S, D>(acc[s], p, w[s][7]);
-            fma_tap<8, S, D>(acc[s], p, w[s][8]);
-          } else {
-            const uint32_t pid = ((s < 4 ? m0.cx : m0.cy) >> (8 * (s & 3))) & 0xFFu;
-            apply_canon8<S, D>(pid, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
-          }
-        }
+        compute(m0, kc, p, w);
       }
       m0 = m1;
       m1 = m2;
@@ -604,24 +615,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       uint32_t kc = m0.wo >> 24;
       asm volatile("" : "+s"(kc));   // fresh slot tests (no 64-bit condition masks kept live)
       if (kc != 0) {
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          if (!((kc >> s) & 1u)) continue;
-          if constexpr (LIB == kLibDense9) {
-            fma_tap<0, S, D>(acc[s], px, wx[s][0]);
-            fma_tap<1, S, D>(acc[s], px, wx[s][1]);
-            fma_tap<2, S, D>(acc[s], px, wx[s][2]);
-            fma_tap<3, S, D>(acc[s], px, wx[s][3]);
-            fma_tap<4, S, D>(acc[s], px, wx[s][4]);
-            fma_tap<5, S, D>(acc[s], px, wx[s][5]);
-            fma_tap<6, S, D>(acc[s], px, wx[s][6]);
-            fma_tap<7, S, D>(acc[s], px, wx[s][7]);
-            fma_tap<8, S, D>(acc[s], px, wx[s][8]);
-          } else {
-            const uint32_t pid = ((s < 4 ? m0.cx : m0.cy) >> (8 * (s & 3))) & 0xFFu;
-            apply_canon8<S, D>(pid, acc[s], px, wx[s][0], wx[s][1], wx[s][2], wx[s][3]);
-          }
-        }
+        compute(m0, kc, px, wx);
       }
       m0 = m1;
       m1 = m2;
