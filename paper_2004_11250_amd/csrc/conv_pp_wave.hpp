@@ -459,180 +459,189 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   }
 
   if (!ABF && c0 < c1) {
-    // fp32: DMA pipeline.  Channel c lives in ring slot (c - c0) % NSLOT;
-    // its halo tile and weights are DMA'd DPF channels before it is computed.
-    // With PIPE its patch and weights are read from LDS into one of two
-    // register sets one channel before it is computed, so those reads overlap
-    // the previous channel's FMAs.  Per channel every lane issues QV (QS)
-    // DMAs, so "channel c has landed" is vmcnt <= n * QV while n later
-    // channels are in flight.
-    constexpr int NS = G::NSLOT, DPF = G::DPF;
-    constexpr int QV = G::NQ + NWL;       // 16-byte patch loads + weight loads
-    constexpr int QS = 4 * G::NQ + NWL;   // 4-byte patch loads + weight loads
-    const uint32_t ring_b = lds_addr(ring);
-    // LDS byte offsets within a ring slot: 16-byte patch loads t at 1024 t,
-    // 4-byte ones (t, j) at 256 (4 t + j), weight loads j at 4 PATCH + 256 j
-    constexpr uint32_t LW0 = 4u * G::PATCH;
-    const u32x4 brs = make_rsrc_below(blob, a.blob_bytes, kDmaShift);
-    // descriptor of the next channel to DMA (channels are DMA'd in order)
-    u32x4 cr = make_rsrc_below(x + static_cast<size_t>(c0) * a.h * a.w, chan_bytes, kDmaShift);
-#pragma unroll
-    for (int t = 0; t < NQ; ++t)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t l = v4 ? 1024u * t : 256u * (4 * t + j);
-        if (qoff[t][j] != 0x80000000u) qoff[t][j] += kDmaShift - (l & 4095u);
+    // the row-load width (16-byte or 4-byte DMAs) as a compile-time choice:
+    // the channel loop is instantiated for both, so it carries no branch on it
+    auto fp32_path = [&](auto v4c) __attribute__((always_inline)) {
+      constexpr bool V4 = decltype(v4c)::value;
+      // fp32: DMA pipeline.  Channel c lives in ring slot (c - c0) % NSLOT;
+      // its halo tile and weights are DMA'd DPF channels before it is computed.
+      // With PIPE its patch and weights are read from LDS into one of two
+      // register sets one channel before it is computed, so those reads overlap
+      // the previous channel's FMAs.  Per channel every lane issues QV (QS)
+      // DMAs, so "channel c has landed" is vmcnt <= n * QV while n later
+      // channels are in flight.
+      constexpr int NS = G::NSLOT, DPF = G::DPF;
+      constexpr int QV = G::NQ + NWL;       // 16-byte patch loads + weight loads
+      constexpr int QS = 4 * G::NQ + NWL;   // 4-byte patch loads + weight loads
+      const uint32_t ring_b = lds_addr(ring);
+      // LDS byte offsets within a ring slot: 16-byte patch loads t at 1024 t,
+      // 4-byte ones (t, j) at 256 (4 t + j), weight loads j at 4 PATCH + 256 j
+      constexpr uint32_t LW0 = 4u * G::PATCH;
+      const u32x4 brs = make_rsrc_below(blob, a.blob_bytes, kDmaShift);
+      // descriptor of the next channel to DMA (channels are DMA'd in order)
+      u32x4 cr = make_rsrc_below(x + static_cast<size_t>(c0) * a.h * a.w, chan_bytes, kDmaShift);
+  #pragma unroll
+      for (int t = 0; t < NQ; ++t)
+  #pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t l = V4 ? 1024u * t : 256u * (4 * t + j);
+          if (qoff[t][j] != 0x80000000u) qoff[t][j] += kDmaShift - (l & 4095u);
+        }
+      auto wadj = [](int j) { return kDmaShift - ((LW0 + 256u * j) & 4095u); };
+      auto dma = [&](int c, uint32_t wo) __attribute__((always_inline)) {
+        const uint32_t k = static_cast<uint32_t>(c - c0);
+        const uint32_t sb = ring_b + 4u * ((k % NS) * SLOT);
+        Meta mw;
+        mw.wo = wo;
+        uint32_t wof[NWL];
+        weight_offs(mw, wof, wadj);
+        if constexpr (V4) {
+          static_for<0, NQ>([&](auto ti) __attribute__((always_inline)) {
+            constexpr int T = decltype(ti)::value;
+            dma_b128_at<1024u * T, 1024u * (T - 1), T == 0>(cr, qoff[T][0], sb);
+          });
+          static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
+            constexpr int J = decltype(ji)::value;
+            dma_b32_at<LW0 + 256u * J, (J == 0 ? 1024u * (NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
+          });
+        } else {
+          static_for<0, 4 * NQ>([&](auto ii) __attribute__((always_inline)) {
+            constexpr int I = decltype(ii)::value;
+            dma_b32_at<256u * I, 256u * (I - 1), I == 0>(cr, qoff[I / 4][I % 4], sb);
+          });
+          static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
+            constexpr int J = decltype(ji)::value;
+            dma_b32_at<LW0 + 256u * J, (J == 0 ? 256u * (4 * NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
+          });
+        }
+        cr = next_channel(cr, chan_bytes);
+      };
+      auto load_wo = [&](int c) __attribute__((always_inline)) {
+        const uint32_t e = min(e_base + static_cast<uint32_t>(c), e_last);
+        return sload<uint32_t>(blob, a.off_woff + 4 * e);
+      };
+      // wait until channel c has landed in LDS; the DMAs of channels up to
+      // min(c + n, c1 - 1) have been issued
+      auto wait_landed = [&](int c, auto later) __attribute__((always_inline)) {
+        constexpr int n = decltype(later)::value;
+        asm volatile("" ::: "memory");
+        if (c + n < c1) {
+          if constexpr (V4)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QV));
+          else
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QS));
+        } else {
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        }
+        asm volatile("" ::: "memory");
+      };
+      // LDS -> registers: patch and weights of channel c (no wait).  Canonical
+      // library: all 8 slots' weights unconditionally (pruned slots hold zeros;
+      // fewer branches than testing each slot); all-ones library: kept slots.
+      auto lds_read = [&](int c, uint32_t kept, float (&p)[PR][PC], float (&w)[8][KW]) __attribute__((always_inline)) {
+        const uint32_t k = static_cast<uint32_t>(c - c0);
+        const float* cur = ring + (k % NS) * SLOT;
+        const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
+  #pragma unroll
+        for (int s = 0; s < 8; ++s)
+          if (LIB == kLibCanon8 || ((kept >> s) & 1u)) {
+  #pragma unroll
+            for (int i = 0; i < KW / 4; ++i) {
+              const float4 v = wc[s * (KW / 4) + i];
+              w[s][4 * i] = v.x; w[s][4 * i + 1] = v.y; w[s][4 * i + 2] = v.z; w[s][4 * i + 3] = v.w;
+            }
+          }
+  #pragma unroll
+        for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL, false>(p[r], cur + lane_off + r * LSTR);
+      };
+      // running byte offsets of the scalar loads (clamped at the layer's last
+      // channel, whose entries are then read again and not used)
+      const uint32_t woff_last = a.off_woff + 4u * e_last, code_last = a.off_codes + 8u * e_last;
+      uint32_t wo_n, wo_off, me_off, mc_off;
+      Meta m0, m1;
+      // prologue: channels c0 .. c0+DPF-1 in flight, channel c0 read into set A
+      {
+        uint32_t wo[DPF];
+  #pragma unroll
+        for (int i = 0; i < DPF; ++i) wo[i] = load_wo(c0 + i);
+  #pragma unroll
+        for (int i = 0; i < DPF; ++i)
+          if (c0 + i < c1) dma(c0 + i, wo[i]);
+        m0 = load_meta(c0);
+        m1 = load_meta(c0 + 1);
+        wo_n = load_wo(c0 + DPF);
+        wo_off = min(a.off_woff + 4u * (e_base + c0 + DPF + 1), woff_last);
+        me_off = min(a.off_woff + 4u * (e_base + c0 + 2), woff_last);
+        mc_off = min(a.off_codes + 8u * (e_base + c0 + 2), code_last);
       }
-    auto wadj = [](int j) { return kDmaShift - ((LW0 + 256u * j) & 4095u); };
-    auto dma = [&](int c, uint32_t wo) __attribute__((always_inline)) {
-      const uint32_t k = static_cast<uint32_t>(c - c0);
-      const uint32_t sb = ring_b + 4u * ((k % NS) * SLOT);
-      Meta mw;
-      mw.wo = wo;
-      uint32_t wof[NWL];
-      weight_offs(mw, wof, wadj);
-      if (v4) {
-        static_for<0, NQ>([&](auto ti) __attribute__((always_inline)) {
-          constexpr int T = decltype(ti)::value;
-          dma_b128_at<1024u * T, 1024u * (T - 1), T == 0>(cr, qoff[T][0], sb);
-        });
-        static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
-          constexpr int J = decltype(ji)::value;
-          dma_b32_at<LW0 + 256u * J, (J == 0 ? 1024u * (NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
-        });
-      } else {
-        static_for<0, 4 * NQ>([&](auto ii) __attribute__((always_inline)) {
-          constexpr int I = decltype(ii)::value;
-          dma_b32_at<256u * I, 256u * (I - 1), I == 0>(cr, qoff[I / 4][I % 4], sb);
-        });
-        static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
-          constexpr int J = decltype(ji)::value;
-          dma_b32_at<LW0 + 256u * J, (J == 0 ? 256u * (4 * NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
-        });
+      float pa[PR][PC], pb[PR][PC];
+      float wa[8][KW], wb[8][KW];
+      if constexpr (G::PIPE) {
+        wait_lgkm();
+        wait_landed(c0, std::integral_constant<int, DPF - 1>{});
+        lds_read(c0, m0.wo >> 24, pa, wa);
       }
-      cr = next_channel(cr, chan_bytes);
-    };
-    auto load_wo = [&](int c) __attribute__((always_inline)) {
-      const uint32_t e = min(e_base + static_cast<uint32_t>(c), e_last);
-      return sload<uint32_t>(blob, a.off_woff + 4 * e);
-    };
-    // wait until channel c has landed in LDS; the DMAs of channels up to
-    // min(c + n, c1 - 1) have been issued
-    auto wait_landed = [&](int c, auto later) __attribute__((always_inline)) {
-      constexpr int n = decltype(later)::value;
-      asm volatile("" ::: "memory");
-      if (c + n < c1) {
-        if (v4)
-          __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QV));
-        else
-          __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QS));
-      } else {
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-      }
-      asm volatile("" ::: "memory");
-    };
-    // LDS -> registers: patch and weights of channel c (no wait).  Canonical
-    // library: all 8 slots' weights unconditionally (pruned slots hold zeros;
-    // fewer branches than testing each slot); all-ones library: kept slots.
-    auto lds_read = [&](int c, uint32_t kept, float (&p)[PR][PC], float (&w)[8][KW]) __attribute__((always_inline)) {
-      const uint32_t k = static_cast<uint32_t>(c - c0);
-      const float* cur = ring + (k % NS) * SLOT;
-      const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        if (LIB == kLibCanon8 || ((kept >> s) & 1u)) {
-#pragma unroll
-          for (int i = 0; i < KW / 4; ++i) {
-            const float4 v = wc[s * (KW / 4) + i];
-            w[s][4 * i] = v.x; w[s][4 * i + 1] = v.y; w[s][4 * i + 2] = v.z; w[s][4 * i + 3] = v.w;
+      // one channel.  Pipelined: X holds channel c (read one step earlier) and
+      // Y receives channel c + 1.  Otherwise channel c is read into X here.
+      auto step = [&](int c, float (&px)[PR][PC], float (&wx)[8][KW], float (&py)[PR][PC], float (&wy)[8][KW])
+          __attribute__((always_inline)) {
+        if constexpr (!G::PIPE) {
+          wait_landed(c, std::integral_constant<int, DPF - 1>{});
+          if ((m0.wo >> 24) != 0) lds_read(c, m0.wo >> 24, px, wx);
+        }
+        // channel c's patch and weights, and the previous step's scalar loads
+        wait_lgkm();
+  #pragma unroll
+        for (int s = 0; s < 8; ++s)
+  #pragma unroll
+          for (int i = 0; i < KW; ++i) asm("" : "+v"(wx[s][i]));
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (G::PIPE) {
+          if (c + 1 < c1) {
+            wait_landed(c + 1, std::integral_constant<int, DPF - 2>{});
+            lds_read(c + 1, m1.wo >> 24, py, wy);
           }
         }
-#pragma unroll
-      for (int r = 0; r < PR; ++r) read_row<SH, SH, PC, VWL, false>(p[r], cur + lane_off + r * LSTR);
-    };
-    // running byte offsets of the scalar loads (clamped at the layer's last
-    // channel, whose entries are then read again and not used)
-    const uint32_t woff_last = a.off_woff + 4u * e_last, code_last = a.off_codes + 8u * e_last;
-    uint32_t wo_n, wo_off, me_off, mc_off;
-    Meta m0, m1;
-    // prologue: channels c0 .. c0+DPF-1 in flight, channel c0 read into set A
-    {
-      uint32_t wo[DPF];
-#pragma unroll
-      for (int i = 0; i < DPF; ++i) wo[i] = load_wo(c0 + i);
-#pragma unroll
-      for (int i = 0; i < DPF; ++i)
-        if (c0 + i < c1) dma(c0 + i, wo[i]);
-      m0 = load_meta(c0);
-      m1 = load_meta(c0 + 1);
-      wo_n = load_wo(c0 + DPF);
-      wo_off = min(a.off_woff + 4u * (e_base + c0 + DPF + 1), woff_last);
-      me_off = min(a.off_woff + 4u * (e_base + c0 + 2), woff_last);
-      mc_off = min(a.off_codes + 8u * (e_base + c0 + 2), code_last);
-    }
-    float pa[PR][PC], pb[PR][PC];
-    float wa[8][KW], wb[8][KW];
-    if constexpr (G::PIPE) {
-      wait_lgkm();
-      wait_landed(c0, std::integral_constant<int, DPF - 1>{});
-      lds_read(c0, m0.wo >> 24, pa, wa);
-    }
-    // one channel.  Pipelined: X holds channel c (read one step earlier) and
-    // Y receives channel c + 1.  Otherwise channel c is read into X here.
-    auto step = [&](int c, float (&px)[PR][PC], float (&wx)[8][KW], float (&py)[PR][PC], float (&wy)[8][KW])
-        __attribute__((always_inline)) {
-      if constexpr (!G::PIPE) {
-        wait_landed(c, std::integral_constant<int, DPF - 1>{});
-        if ((m0.wo >> 24) != 0) lds_read(c, m0.wo >> 24, px, wx);
-      }
-      // channel c's patch and weights, and the previous step's scalar loads
-      wait_lgkm();
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-#pragma unroll
-        for (int i = 0; i < KW; ++i) asm("" : "+v"(wx[s][i]));
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (G::PIPE) {
-        if (c + 1 < c1) {
-          wait_landed(c + 1, std::integral_constant<int, DPF - 2>{});
-          lds_read(c + 1, m1.wo >> 24, py, wy);
+        // channel c+DPF -> LDS (its slot was last read for channel c-1)
+        if (c + DPF < c1) dma(c + DPF, wo_n);
+        const uint32_t wo_nn = sload<uint32_t>(blob, wo_off);
+        Meta m2;
+        m2.wo = sload<uint32_t>(blob, me_off);
+        {
+          const uint2 cw = sload<uint2>(blob, mc_off);
+          m2.cx = cw.x;
+          m2.cy = cw.y;
         }
+        wo_off = min(wo_off + 4u, woff_last);
+        me_off = min(me_off + 4u, woff_last);
+        mc_off = min(mc_off + 8u, code_last);
+        __builtin_amdgcn_sched_barrier(0);
+        uint32_t kc = m0.wo >> 24;
+        asm volatile("" : "+s"(kc));   // fresh slot tests (no 64-bit condition masks kept live)
+        if (kc != 0) {
+          compute(m0, kc, px, wx);
+        }
+        m0 = m1;
+        m1 = m2;
+        wo_n = wo_nn;
+      };
+      if constexpr (G::PIPE) {
+  #pragma unroll 1
+        for (int c = c0; c < c1; c += 2) {
+          step(c, pa, wa, pb, wb);
+          if (c + 1 >= c1) break;
+          step(c + 1, pb, wb, pa, wa);
+        }
+      } else {
+  #pragma unroll 1
+        for (int c = c0; c < c1; ++c) step(c, pa, wa, pa, wa);
       }
-      // channel c+DPF -> LDS (its slot was last read for channel c-1)
-      if (c + DPF < c1) dma(c + DPF, wo_n);
-      const uint32_t wo_nn = sload<uint32_t>(blob, wo_off);
-      Meta m2;
-      m2.wo = sload<uint32_t>(blob, me_off);
-      {
-        const uint2 cw = sload<uint2>(blob, mc_off);
-        m2.cx = cw.x;
-        m2.cy = cw.y;
-      }
-      wo_off = min(wo_off + 4u, woff_last);
-      me_off = min(me_off + 4u, woff_last);
-      mc_off = min(mc_off + 8u, code_last);
-      __builtin_amdgcn_sched_barrier(0);
-      uint32_t kc = m0.wo >> 24;
-      asm volatile("" : "+s"(kc));   // fresh slot tests (no 64-bit condition masks kept live)
-      if (kc != 0) {
-        compute(m0, kc, px, wx);
-      }
-      m0 = m1;
-      m1 = m2;
-      wo_n = wo_nn;
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // no DMA may land in the exchange area below
     };
-    if constexpr (G::PIPE) {
-#pragma unroll 1
-      for (int c = c0; c < c1; c += 2) {
-        step(c, pa, wa, pb, wb);
-        if (c + 1 >= c1) break;
-        step(c + 1, pb, wb, pa, wa);
-      }
-    } else {
-#pragma unroll 1
-      for (int c = c0; c < c1; ++c) step(c, pa, wa, pa, wa);
-    }
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // no DMA may land in the exchange area below
+    if (v4)
+      fp32_path(std::true_type{});
+    else
+      fp32_path(std::false_type{});
   }
 
   // ---- combine the WS partial sums, PS slots at a time, in wave order; wave
