@@ -491,15 +491,17 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       auto dma = [&](int c, uint32_t wo) __attribute__((always_inline)) {
         const uint32_t k = static_cast<uint32_t>(c - c0);
         const uint32_t sb = ring_b + 4u * ((k % NS) * SLOT);
+        // the patch first: it does not depend on the channel's metadata, whose
+        // scalar load may still be in flight (the first channels)
         Meta mw;
         mw.wo = wo;
         uint32_t wof[NWL];
-        weight_offs(mw, wof, wadj);
         if constexpr (V4) {
           static_for<0, NQ>([&](auto ti) __attribute__((always_inline)) {
             constexpr int T = decltype(ti)::value;
             dma_b128_at<1024u * T, 1024u * (T - 1), T == 0>(cr, qoff[T][0], sb);
           });
+          weight_offs(mw, wof, wadj);
           static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
             constexpr int J = decltype(ji)::value;
             dma_b32_at<LW0 + 256u * J, (J == 0 ? 1024u * (NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
@@ -509,6 +511,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
             constexpr int I = decltype(ii)::value;
             dma_b32_at<256u * I, 256u * (I - 1), I == 0>(cr, qoff[I / 4][I % 4], sb);
           });
+          weight_offs(mw, wof, wadj);
           static_for<0, NWL>([&](auto ji) __attribute__((always_inline)) {
             constexpr int J = decltype(ji)::value;
             dma_b32_at<LW0 + 256u * J, (J == 0 ? 256u * (4 * NQ - 1) : LW0 + 256u * (J - 1)), false>(brs, wof[J], sb);
@@ -662,11 +665,19 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   constexpr int BLK = 8 * R * CC * 64;   // floats of one workgroup's partial-sum block
   const bool split = a.ksplit > 1;
   const uint32_t item = ((static_cast<uint32_t>(img) * a.tiles_y + ty) * a.tiles_x + tx) * a.n_groups + grp;
-  auto finish = [&](int s, int r, float (&v)[CC]) __attribute__((always_inline)) {
-    const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
-    const uint32_t o = sload<uint32_t>(blob, a.off_perm + 4 * slot);
+  // the group's 8 output channels (through perm) and biases, loaded together
+  // once instead of one dependent pair per stored unit
+  uint32_t permv[8];
+  float biasv[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    permv[s] = sload<uint32_t>(blob, a.off_perm + 4 * (static_cast<uint32_t>(grp) * 8 + s));
+    biasv[s] = sload<float>(blob, a.off_bias + 4 * (static_cast<uint32_t>(grp) * 8 + s));
+  }
+  static_assert(G::PS == 2, "the exchange passes cover two slots");
+  // store of row r of the unit's slot: output channel o (>= c_out for a padding slot)
+  auto finish = [&](uint32_t o, float bias, int r, float (&v)[CC]) __attribute__((always_inline)) {
     if (o >= static_cast<uint32_t>(a.c_out)) return;   // padding slot
-    const float bias = sload<float>(blob, a.off_bias + 4 * slot);
     const int oy = oy0 + ly * R + r;
     if (oy >= a.ho) return;
 #pragma unroll
@@ -703,11 +714,9 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   // pooled store of rows r, r + 1 (r even) of slot s: max over each 2 x 2
   // window of the activated values, as a separate pool of the stored conv
   // output would take it
-  auto finish_pool = [&](int s, int r, float (&v0)[CC], float (&v1)[CC]) __attribute__((always_inline)) {
-    const uint32_t slot = static_cast<uint32_t>(grp) * 8 + s;
-    const uint32_t o = sload<uint32_t>(blob, a.off_perm + 4 * slot);
+  auto finish_pool = [&](uint32_t o, float bias, int r, float (&v0)[CC], float (&v1)[CC])
+      __attribute__((always_inline)) {
     if (o >= static_cast<uint32_t>(a.c_out)) return;   // padding slot
-    const float bias = sload<float>(blob, a.off_bias + 4 * slot);
     const int oy = oy0 + ly * R + r;
     if (oy + 1 >= a.ho) return;   // incomplete window (floor)
     TA* row = y + (static_cast<size_t>(o) * pho + oy / 2) * pwo;
@@ -772,7 +781,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
           float v0[CC], v1[CC];
           gather(s, ps, r, v0);
           gather(s, ps, r + 1, v1);
-          finish_pool(s, r, v0, v1);
+          finish_pool(ps == 0 ? permv[s0] : permv[s0 + 1], ps == 0 ? biasv[s0] : biasv[s0 + 1], r, v0, v1);
         }
         continue;
       }
@@ -790,7 +799,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
 #pragma unroll
         for (int q = 0; q < CC; ++q) pb[((s * R + r) * CC + q) * 64] = v[q];
       } else {
-        finish(s, r, v);
+        finish(ps == 0 ? permv[s0] : permv[s0 + 1], ps == 0 ? biasv[s0] : biasv[s0 + 1], r, v);
       }
     }
   }
