@@ -112,7 +112,7 @@ def summarize_profile(root, cfg=2):
     --stats; fetch/, write/: --pmc FETCH_SIZE / WRITE_SIZE of a run with
     --copy-mib; sq*/: other --pmc passes) for one frame of the network: the
     dispatches of the first frame are the len(ops) dispatches starting at the
-    first pruned-conv launch (a max pool fused into the conv before it has no
+    first pruned-conv launch (an op fused into the conv before it has no
     dispatch of its own).  Writes the traffic JSON read by the benchmark and
     prints a markdown summary."""
     import csv
@@ -121,7 +121,7 @@ def summarize_profile(root, cfg=2):
     import paper_2004_11250_amd as pp
     import workloads
     spec = workloads.net_spec(cfg)
-    fused = pp.fused_pools(spec["ops"])
+    fused = pp.fused_ops(spec["ops"])
     n_disp = len(spec["ops"]) - len(fused)
     shapes = layer_shapes(spec)
 
@@ -198,7 +198,7 @@ def summarize_profile(root, cfg=2):
         dur = sum(f[di]["dur_ns"] for f in kt_fr) / len(kt_fr) / 1e3
         fetch = sum(f[di]["c"]["FETCH_SIZE"] for f in fe_fr) / len(fe_fr) * ff * 1024
         write = sum(f[di]["c"]["WRITE_SIZE"] for f in wr_fr) / len(wr_fr) * wf * 1024
-        kind = op["op"] + ("+maxpool2" if i + 1 in fused else "")
+        kind = op["op"] + ("+" + fused[i + 1] if i + 1 in fused else "")
         lay.append(dict(op=i, kind=kind, lib=op.get("lib", ""), c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
                         kernel=_kernel_label(kt_fr[0][di]["name"]), us=round(dur, 3),
                         fetch_mb=round(fetch / 1e6, 3), write_mb=round(write / 1e6, 3), sq=sq.get(di, {})))
@@ -310,35 +310,41 @@ def main():
     value = total_macs / (ms * 1e-3) / 1e9
 
     # ---- per-layer timing of the pruned-conv kernel (same launches as in the
-    # frame: a conv whose max pool pp_net_fwd fuses runs with PP_MAXPOOL2)
+    # frame: a conv whose next op pp_net_fwd fuses runs with that op's flag;
+    # an accumulating conv adds into the same tensor every call)
     layers = []
     li = 0
     esz = 2 if dtype == "bf16" else 4
-    fused = pp.fused_pools(spec["ops"])
+    fused = pp.fused_ops(spec["ops"])
     for (i, op, ishape, o), prm in zip(shapes, params):
         if op["op"] != "conv3":
             continue
         L = net.pruned[li]
         li += 1
-        pool = i + 1 in fused
-        if pool:
+        f = fused.get(i + 1)
+        if f == "maxpool2":
             o = (o[0], o[1] // 2, o[2] // 2)
+        elif f == "pshuf2":
+            o = (o[0] // 4, 2 * o[1], 2 * o[2])
+        kw = dict(relu=op["relu"], maxpool2=f == "maxpool2", accumulate=f == "add", pixshuf2=f == "pshuf2")
         xin = torch.rand((batch,) + ishape, device=dev).to(tdt)
-        yo = torch.empty((batch,) + o, device=dev, dtype=tdt)
+        yo = torch.zeros((batch,) + o, device=dev, dtype=tdt)
         for _ in range(5):
-            pp.conv2d_fwd(L, xin, relu=op["relu"], out=yo, maxpool2=pool)
+            pp.conv2d_fwd(L, xin, out=yo, **kw)
         torch.cuda.synchronize()
         a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a0.record(stream)
         for _ in range(args.layer_steps):
-            pp.conv2d_fwd(L, xin, relu=op["relu"], out=yo, maxpool2=pool)
+            pp.conv2d_fwd(L, xin, out=yo, **kw)
         a1.record(stream)
         torch.cuda.synchronize()
         us = a0.elapsed_time(a1) * 1e3 / args.layer_steps
         macs = surviving_macs(op, prm, shapes[i][3], batch)
-        alg_bytes = batch * (int(np.prod(ishape)) + int(np.prod(o))) * esz + L.h_blob.nbytes
+        # the residual of an accumulating conv is read as well as written
+        alg_bytes = batch * (int(np.prod(ishape)) + (2 if f == "add" else 1) * int(np.prod(o))) * esz + \
+            L.h_blob.nbytes
         layers.append(dict(op=i, c_in=op["c_in"], c_out=op["c_out"], hw=f"{o[1]}x{o[2]}", lib=op["lib"],
-                           maxpool2=pool,
+                           fused=f,
                            surviving_mmac=round(macs / 1e6, 3), us=round(us, 3),
                            eff_tmacs=round(macs / us / 1e6, 3), alg_mb=round(alg_bytes / 1e6, 3),
                            frac_fp32_peak=round(2 * macs / us / 1e6 / PEAK_FP32_VECTOR_TFLOPS, 4)))

@@ -49,10 +49,13 @@ typedef enum {
 
 typedef enum { PP_F32 = 0, PP_BF16 = 1 } pp_dtype;
 
-/* flags of pp_conv2d_fwd / pp_net_op.  PP_MAXPOOL2 (pp_conv2d_fwd only):
- * store the 2 x 2, stride 2 max pool of the activated output instead of the
- * output itself (graph-level fusion of conv, activation and pooling). */
-enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u };
+/* flags of pp_conv2d_fwd / pp_net_op.  The others than PP_RELU are for
+ * pp_conv2d_fwd only and fuse the op after the conv into its store
+ * (graph-level fusion, Sec. 3): PP_MAXPOOL2 stores the 2 x 2, stride 2 max
+ * pool of the activated output instead of the output itself; PP_ACCUMULATE
+ * adds the activated output to what y holds (a residual connection);
+ * PP_PIXSHUF2 stores the activated output through PixelShuffle(2). */
+enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u, PP_ACCUMULATE = 4u, PP_PIXSHUF2 = 8u };
 
 /* Shape and storage of one pruned 3x3 layer. */
 typedef struct {
@@ -142,7 +145,18 @@ pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
  *                       that holds whole 2 x 2 windows per lane: the
  *                       canonical or all-ones library with pad = dilation,
  *                       else PP_EUNSUPPORTED; with a channel split the
- *                       second pass takes the pool)
+ *                       second pass takes the pool),
+ *                       PP_ACCUMULATE (y holds a residual r on entry and
+ *                       becomes r + act(conv + bias), element by element, the
+ *                       activated value rounded to act_dtype before the add:
+ *                       bitwise what a separate add of the stored output
+ *                       gives; canonical or all-ones library with pad =
+ *                       dilation, else PP_EUNSUPPORTED), PP_PIXSHUF2 (y is
+ *                       [n][c_out/4][2 h_out][2 w_out], y[c][2i+a][2j+b] =
+ *                       act(conv + bias)[4c+2a+b][i][j]; c_out a multiple of
+ *                       4, else PP_EINVAL; same libraries as PP_ACCUMULATE);
+ *                       at most one of PP_MAXPOOL2, PP_ACCUMULATE and
+ *                       PP_PIXSHUF2, else PP_EINVAL
  *   workspace, ws_bytes optional device scratch (NULL, 0 for none), 256-byte
  *                       aligned.  With pp_conv2d_workspace() bytes the
  *                       kernel may split the input channels over more
@@ -234,8 +248,14 @@ pp_status pp_net_workspace(const pp_net_op* ops, int32_t n_ops, int32_t n, int32
 /*
  * pp_net_fwd -- run the op list on the stream, one launch per op, no host
  * synchronisation.  x is device [n][c][h][w]; y receives slot 1 (shape from
- * pp_net_workspace).  Errors: as pp_net_workspace, PP_ESIZE (ws_bytes too
- * small), PP_EUNSUPPORTED, PP_EHIP.
+ * pp_net_workspace).  A pruned conv (canonical or all-ones library, pad =
+ * dilation) whose output slot only feeds the next op -- a max pool, a pixel
+ * shuffle, or an add whose other operand is dead afterwards too -- runs
+ * fused with that op in one launch (pp_conv2d_fwd's PP_MAXPOOL2,
+ * PP_PIXSHUF2, PP_ACCUMULATE); the result is the same.  The workspace is
+ * only valid for the op list and shape it was sized for.
+ * Errors: as pp_net_workspace, PP_ESIZE (ws_bytes too small),
+ * PP_EUNSUPPORTED, PP_EHIP.
  */
 pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void* x, void* y,
                      int32_t n, int32_t c, int32_t h, int32_t w, int32_t act_dtype,

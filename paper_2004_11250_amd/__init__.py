@@ -22,6 +22,8 @@ PP_OK, PP_EINVAL, PP_ESIZE, PP_EBLOB, PP_EUNSUPPORTED, PP_EHIP = 0, -1, -2, -3, 
 PP_F32, PP_BF16 = 0, 1
 PP_RELU = 1
 PP_MAXPOOL2 = 2
+PP_ACCUMULATE = 4
+PP_PIXSHUF2 = 8
 (OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
 
 # exported symbols declared in include/pp.h
@@ -204,11 +206,15 @@ class PackedLayer:
         return cls(pack(w, b, pattern_id, conn, lib_masks, stride, pad, dilation, wdtype), device)
 
 
-def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspace="auto", maxpool2=False):
+def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspace="auto", maxpool2=False,
+               accumulate=False, pixshuf2=False):
     """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None).
     workspace: "auto" (a scratch tensor of pp_conv2d_workspace bytes, kept on
     the layer per input shape), None (no scratch) or a uint8 device tensor.
-    maxpool2: store the 2 x 2 max pool of the activated output (PP_MAXPOOL2)."""
+    maxpool2: store the 2 x 2 max pool of the activated output (PP_MAXPOOL2).
+    accumulate: add the activated output to ``out`` in place (PP_ACCUMULATE;
+    out is required).  pixshuf2: store through PixelShuffle(2)
+    (PP_PIXSHUF2)."""
     torch = _torch()
     lib = load_library()
     if not x.is_contiguous():
@@ -217,9 +223,14 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     if c != layer.info["c_in"]:
         raise ValueError(f"x has {c} channels, the layer expects {layer.info['c_in']}")
     ho, wo = out_size(layer.h_blob, h, w)
+    c_out = layer.info["c_out"]
     if maxpool2:
         ho, wo = ho // 2, wo // 2
-    shape = (n, layer.info["c_out"], ho, wo)
+    if pixshuf2:
+        c_out, ho, wo = c_out // 4, 2 * ho, 2 * wo
+    shape = (n, c_out, ho, wo)
+    if accumulate and out is None:
+        raise ValueError("accumulate needs out (the residual, updated in place)")
     if out is None:
         out = torch.empty(shape, dtype=x.dtype, device=x.device)
     elif tuple(out.shape) != shape or out.dtype != x.dtype or not out.is_contiguous():
@@ -236,7 +247,8 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel()) if workspace is not None else (None, 0)
     st = lib.pp_conv2d_fwd(_ptr(layer.h_blob), layer.h_blob.nbytes, layer.d_blob.data_ptr(), x.data_ptr(),
                            out.data_ptr(), n, h, w, _dtype_code(x),
-                           (PP_RELU if relu else 0) | (PP_MAXPOOL2 if maxpool2 else 0), ws_ptr, ws_bytes,
+                           (PP_RELU if relu else 0) | (PP_MAXPOOL2 if maxpool2 else 0) |
+                           (PP_ACCUMULATE if accumulate else 0) | (PP_PIXSHUF2 if pixshuf2 else 0), ws_ptr, ws_bytes,
                            _stream_ptr(stream))
     _check(st, "pp_conv2d_fwd")
     return out
@@ -252,32 +264,51 @@ def _bf16_bits(a: np.ndarray) -> np.ndarray:
     return (((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF).astype(np.uint16)
 
 
-def fused_pools(ops) -> set:
-    """Indices of the 2 x 2 max-pool ops that pp_net_fwd runs inside the
-    pruned conv just before them (one launch, PP_MAXPOOL2): the pool reads
-    that conv's output slot, the conv does not write slot 1, a pool that
-    writes the conv's input slot has it in the workspace (slot >= 2), no
-    later op reads the conv's output before an op rewrites that slot, and
-    the conv is a canonical / all-ones layer with padding equal to its
-    dilation.  ops: the op dicts of a network spec."""
-    out = set()
-    for i in range(1, len(ops)):
-        cv, mp = ops[i - 1], ops[i]
-        if mp["op"] != "maxpool2" or cv["op"] != "conv3" or mp["src"] != cv["dst"] or cv["dst"] == 1:
-            continue
-        if (mp["dst"] == cv["src"] and cv["src"] < 2) or cv["pad"] != cv["dil"] or \
-                cv.get("lib") not in ("canon8", "dense9"):
-            continue
-        read_later = False
-        for o in ops[i + 1:]:
-            if o["src"] == cv["dst"] or (o["op"] == "add" and o.get("src2") == cv["dst"]):
-                read_later = True
-                break
-            if o["dst"] == cv["dst"]:
-                break
-        if not read_later:
-            out.add(i)
+def _dead_after(ops, slot, j0) -> bool:
+    for o in ops[j0:]:
+        if o["src"] == slot or (o["op"] == "add" and o.get("src2") == slot):
+            return False
+        if o["dst"] == slot:
+            return True
+    return True
+
+
+def fused_ops(ops) -> dict:
+    """The ops that pp_net_fwd runs inside the pruned conv just before them
+    (one launch), as {index: "maxpool2" | "pshuf2" | "add"}.  The op reads
+    that conv's output slot, the conv does not write slot 1, the conv's
+    output is dead after the op (no later op reads it before one rewrites
+    it), and the conv is a canonical / all-ones layer with padding equal to
+    its dilation; a pool or shuffle that writes the conv's input slot has it
+    in the workspace (slot >= 2); an add's other operand and its dst are
+    workspace slots, that operand is not the conv's input and is dead after
+    the add too.  ops: the op dicts of a network spec."""
+    out = {}
+    i = 1
+    while i < len(ops):
+        cv, nx = ops[i - 1], ops[i]
+        f = None
+        if cv["op"] == "conv3" and cv["dst"] != 1 and cv["pad"] == cv["dil"] and \
+                cv.get("lib") in ("canon8", "dense9"):
+            if nx["op"] in ("maxpool2", "pshuf2") and nx["src"] == cv["dst"] and \
+                    not (nx["dst"] == cv["src"] and cv["src"] < 2):
+                if nx["op"] == "maxpool2" or cv["c_out"] % 4 == 0:
+                    f = nx["op"]
+            elif nx["op"] == "add" and (nx["src"] == cv["dst"]) != (nx["src2"] == cv["dst"]):
+                r = nx["src2"] if nx["src"] == cv["dst"] else nx["src"]
+                if r >= 2 and nx["dst"] >= 2 and r != cv["src"] and _dead_after(ops, r, i + 1):
+                    f = "add"
+        if f is not None and _dead_after(ops, cv["dst"], i + 1):
+            out[i] = f
+            i += 2
+        else:
+            i += 1
     return out
+
+
+def fused_pools(ops) -> set:
+    """Indices of the max-pool ops fused into the conv before them."""
+    return {i for i, k in fused_ops(ops).items() if k == "maxpool2"}
 
 
 class Net:

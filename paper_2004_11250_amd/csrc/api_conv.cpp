@@ -69,7 +69,13 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const size_t esz = act_dtype == PP_BF16 ? 2 : 4;
   if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % esz)
     return fail(PP_EINVAL, "activation pointers misaligned");
-  if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2)) return fail(PP_EINVAL, "unknown flags");
+  if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2))
+    return fail(PP_EINVAL, "unknown flags");
+  {
+    const uint32_t f = flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2);
+    if (f & (f - 1)) return fail(PP_EINVAL, "more than one of PP_MAXPOOL2, PP_ACCUMULATE, PP_PIXSHUF2");
+  }
+  if ((flags & PP_PIXSHUF2) && v.c_out % 4) return fail(PP_EINVAL, "PP_PIXSHUF2 needs c_out a multiple of 4");
   const bool pool = (flags & PP_MAXPOOL2) != 0;
   if (pool && (ho < 2 || wo < 2)) return fail(PP_EINVAL, "pooled output needs h_out, w_out >= 2");
   const uint8_t* xb = static_cast<const uint8_t*>(x);
@@ -92,17 +98,20 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
     else
       p.part = static_cast<float*>(scratch);
   }
-  if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the max pool for this layer");
+  if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the max pool / accumulation / pixel shuffle for this layer");
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;
 }
 
-bool conv_pool_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, bool with_scratch) {
+bool conv_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flag,
+                  bool with_scratch) {
   int ho = 0, wo = 0;
-  if (conv_check(v, n, h, w, act_dtype, &ho, &wo) != PP_OK || ho < 2 || wo < 2) return false;
+  if (conv_check(v, n, h, w, act_dtype, &ho, &wo) != PP_OK) return false;
+  if (flag == PP_MAXPOOL2 && (ho < 2 || wo < 2)) return false;
+  if (flag == PP_PIXSHUF2 && v.c_out % 4) return false;
   ConvParams p = layer_params(v, n, h, w, ho, wo);
-  p.flags = PP_MAXPOOL2;
+  p.flags = flag;
   return plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_scratch).recipe >= 0;
 }
 

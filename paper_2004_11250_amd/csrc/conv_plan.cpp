@@ -131,12 +131,14 @@ static bool pool_fits(int id) {
 
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
   const bool pool = (p.flags & PP_MAXPOOL2) != 0;
-  // a plan for recipe id, or recipe -1 when it cannot take the pool
+  // epilogues of the wave-pipeline kernel only
+  const bool fused = (p.flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2)) != 0;
+  // a plan for recipe id, or recipe -1 when it cannot take the fused epilogue
   auto try_plan = [&](int id) {
     ConvPlan pl;
     pl.recipe = -1;
     if (!recipe_usable(id, p, lib, bf16)) return pl;
-    if (pool && !is_wave_recipe(id)) return pl;
+    if (fused && !is_wave_recipe(id)) return pl;
     pl = finish_plan(id, p, allow_split);
     if (pool && pl.ksplit == 1 && !pool_fits(id)) pl.recipe = -1;
     return pl;
@@ -222,14 +224,14 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
     const ConvPlan pl = try_plan(id);
     if (pl.recipe >= 0) return pl;
   }
-  if (pool) {
-    // the pooled layer's fallbacks (2 x 4, then 2 x 2 outputs per lane)
+  if (fused) {
+    // the fused layer's fallbacks (2 x 4, then 2 x 2 outputs per lane)
     for (int id : {31, 20, 27, 23, 22, 21, 28}) {
       const ConvPlan pl = try_plan(id);
       if (pl.recipe >= 0) return pl;
     }
     ConvPlan none;
-    none.recipe = -1;   // no tiling can fuse the pool
+    none.recipe = -1;   // no tiling can fuse the epilogue
     return none;
   }
   return finish_plan(13, p, allow_split);

@@ -659,6 +659,11 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   TA* __restrict__ y = static_cast<TA*>(a.y) + static_cast<size_t>(img) * a.c_out *
                                                    (pool ? static_cast<size_t>(pho) * pwo : static_cast<size_t>(a.ho) * a.wo);
   const bool relu = (a.flags & PP_RELU) != 0;
+  // with PP_ACCUMULATE y holds a residual on entry: y = y + act(...), as a
+  // separate add of the stored output would give (the activated value is
+  // rounded to the storage type first)
+  const bool accum = (a.flags & PP_ACCUMULATE) != 0;
+  const bool shuf = (a.flags & PP_PIXSHUF2) != 0;
   const int oxl = ox0 + lx * CC;
   const bool vec = (CC % 4 == 0) && (a.wo % 4 == 0) && (reinterpret_cast<uintptr_t>(a.y) % (4 * sizeof(TA)) == 0);
   constexpr int NU = G::PS * R;   // units per pass
@@ -684,11 +689,44 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
     for (int q = 0; q < CC; ++q) {
       v[q] += bias;
       if (relu) v[q] = fmaxf(v[q], 0.0f);
+      if constexpr (ABF) {
+        if (accum) v[q] = bf16_lo(to_bf16_bits(v[q]));
+      }
+    }
+    if (shuf) {
+      // PixelShuffle(2): channel o lands in channel o / 4 of the 2ho x 2wo
+      // output, row 2 oy + bit 1 of o, columns 2 ox + bit 0 of o
+      TA* row2 = y + (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + (o & 1);
+#pragma unroll
+      for (int q = 0; q < CC; ++q) {
+        if (oxl + q < a.wo) {
+          if constexpr (ABF)
+            reinterpret_cast<uint16_t*>(row2)[2 * (oxl + q)] = static_cast<uint16_t>(to_bf16_bits(v[q]));
+          else
+            reinterpret_cast<float*>(row2)[2 * (oxl + q)] = v[q];
+        }
+      }
+      return;
     }
     TA* row = y + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
     if (vec && oxl + CC <= a.wo) {
 #pragma unroll
       for (int q = 0; q < CC; q += 4) {
+        if (accum) {
+          if constexpr (ABF) {
+            const uint2 old = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(row) + oxl + q);
+            v[q] = bf16_lo(old.x) + v[q];
+            v[q + 1] = bf16_hi(old.x) + v[q + 1];
+            v[q + 2] = bf16_lo(old.y) + v[q + 2];
+            v[q + 3] = bf16_hi(old.y) + v[q + 3];
+          } else {
+            const float4 old = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(row) + oxl + q);
+            v[q] = old.x + v[q];
+            v[q + 1] = old.y + v[q + 1];
+            v[q + 2] = old.z + v[q + 2];
+            v[q + 3] = old.w + v[q + 3];
+          }
+        }
         if constexpr (ABF) {
           uint2 uu;
           uu.x = to_bf16_bits(v[q]) | (to_bf16_bits(v[q + 1]) << 16);
@@ -703,10 +741,14 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
 #pragma unroll
       for (int q = 0; q < CC; ++q) {
         if (oxl + q < a.wo) {
-          if constexpr (ABF)
-            reinterpret_cast<uint16_t*>(row)[oxl + q] = static_cast<uint16_t>(to_bf16_bits(v[q]));
-          else
-            reinterpret_cast<float*>(row)[oxl + q] = v[q];
+          if constexpr (ABF) {
+            uint16_t* e = reinterpret_cast<uint16_t*>(row) + oxl + q;
+            const float t = accum ? bf16_lo(*e) + v[q] : v[q];
+            *e = static_cast<uint16_t>(to_bf16_bits(t));
+          } else {
+            float* e = reinterpret_cast<float*>(row) + oxl + q;
+            *e = accum ? *e + v[q] : v[q];
+          }
         }
       }
     }
@@ -875,11 +917,18 @@ __global__ __launch_bounds__(256) void pp_split_reduce_kernel(ConvParams a) {
     for (int k = 0; k < a.ksplit; ++k) v += pb[static_cast<size_t>(k) * BLK + i];
     v += reinterpret_cast<const float*>(a.blob + a.off_bias)[slot];
     if (relu) v = fmaxf(v, 0.0f);
-    const size_t at = (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
-    if constexpr (ABF)
-      reinterpret_cast<uint16_t*>(y)[at] = static_cast<uint16_t>(to_bf16_bits(v));
-    else
-      reinterpret_cast<float*>(y)[at] = v;
+    const size_t at = (a.flags & PP_PIXSHUF2)
+                        ? (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + 2 * ox + (o & 1)
+                        : (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
+    if constexpr (ABF) {
+      uint16_t* e = reinterpret_cast<uint16_t*>(y) + at;
+      // PP_ACCUMULATE: y = y + act(...), the activated value rounded to bf16 first
+      const float t = (a.flags & PP_ACCUMULATE) ? bf16_lo(*e) + bf16_lo(to_bf16_bits(v)) : v;
+      *e = static_cast<uint16_t>(to_bf16_bits(t));
+    } else {
+      float* e = reinterpret_cast<float*>(y) + at;
+      *e = (a.flags & PP_ACCUMULATE) ? *e + v : v;
+    }
   }
 }
 

@@ -3,11 +3,14 @@
 // Slot 0 is the input, slot 1 the output, slots 2.. live in the caller's
 // workspace at fixed 256-byte-aligned offsets.  Validation of the whole list
 // happens before the first launch.  A pruned conv whose output only feeds
-// the 2 x 2 max pool right after it runs as one fused launch (graph-level
-// fusion, Sec. 3): the pool is taken in the conv's store.  Logical slots map
-// to workspace buffers; when such a pool writes back into the conv's input
-// slot (ping-pong slot use), the fused launch writes the conv's output
-// buffer instead and the two slots swap buffers.
+// the op right after it -- a 2 x 2 max pool, a residual add or a pixel
+// shuffle -- runs as one fused launch (graph-level fusion, Sec. 3): that op
+// is taken in the conv's store.  Logical slots map to workspace buffers, and
+// a fused pair may leave two slots with swapped buffers:
+//   - a pool or shuffle that writes the conv's input slot (ping-pong slot
+//     use) is written to the conv's output buffer instead;
+//   - an add dst = src + conv(x) whose skip operand src is dead afterwards
+//     accumulates into src's buffer in place, which becomes dst's.
 #include <hip/hip_runtime.h>
 
 #include <string>
@@ -28,7 +31,9 @@ struct Shape {
 struct Plan {
   std::vector<Shape> in, in2, out;
   std::vector<BlobView> views;
-  std::vector<char> fuse_pool;   // op i is a pruned conv fused with the max pool at i + 1
+  // op i is a pruned conv fused with op i + 1: the conv's extra flag
+  // (PP_MAXPOOL2, PP_ACCUMULATE or PP_PIXSHUF2), else 0
+  std::vector<uint32_t> fuse;
   // per op: the buffers (0 = x, 1 = y, >= 2 workspace) of src, src2, dst
   std::vector<int> b_src, b_src2, b_dst;
   size_t buf_bytes[PP_MAX_SLOTS] = {};
@@ -52,7 +57,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
   pl->in2.resize(n_ops);
   pl->out.resize(n_ops);
   pl->views.resize(n_ops);
-  pl->fuse_pool.assign(n_ops, 0);
+  pl->fuse.assign(n_ops, 0);
   std::vector<Shape> writes1;
   size_t part_max = 0;
   for (int i = 0; i < n_ops; ++i) {
@@ -130,29 +135,42 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
     if (op.dst == 1) writes1.push_back(o);
   }
   if (!slots[1].defined) return fail(PP_EINVAL, "no op writes the output slot 1");
-  // conv + max pool fusion: the pool reads the conv's output slot, which no
-  // later op reads before rewriting it; a pool that writes the conv's input
-  // slot needs that slot in the workspace (its buffer is swapped)
+  // conv fusion.  The op after the conv reads the conv's output slot, which
+  // is not slot 1 and which no later op reads before rewriting it:
+  //   - max pool / pixel shuffle: one that writes the conv's input slot
+  //     needs that slot in the workspace (its buffer is swapped);
+  //   - add of a skip slot r (both in the workspace, as is the add's dst)
+  //     that is not the conv's input and is dead after the add as well.
+  auto dead_after = [&](int slot, int j0) {
+    for (int j = j0; j < n_ops; ++j) {
+      if (ops[j].src == slot || (ops[j].kind == PP_OP_ADD && ops[j].src2 == slot)) return false;
+      if (ops[j].dst == slot) return true;   // rewritten: later reads see the new value
+    }
+    return true;
+  };
   for (int i = 0; i + 1 < n_ops; ++i) {
     const pp_net_op& cv = ops[i];
-    const pp_net_op& mp = ops[i + 1];
-    if (cv.kind != PP_OP_CONV_PP || mp.kind != PP_OP_MAXPOOL2 || mp.src != cv.dst || cv.dst == 1 ||
-        (mp.dst == cv.src && cv.src < 2))
-      continue;
-    bool read_later = false;
-    for (int j = i + 2; j < n_ops && !read_later; ++j) {
-      read_later = ops[j].src == cv.dst || (ops[j].kind == PP_OP_ADD && ops[j].src2 == cv.dst);
-      if (ops[j].dst == cv.dst) break;   // rewritten: later reads see the new value
+    const pp_net_op& nx = ops[i + 1];
+    if (cv.kind != PP_OP_CONV_PP || cv.dst == 1) continue;
+    uint32_t f = 0;
+    if ((nx.kind == PP_OP_MAXPOOL2 || nx.kind == PP_OP_PIXSHUF2) && nx.src == cv.dst &&
+        !(nx.dst == cv.src && cv.src < 2)) {
+      f = nx.kind == PP_OP_MAXPOOL2 ? PP_MAXPOOL2 : PP_PIXSHUF2;
+    } else if (nx.kind == PP_OP_ADD && (nx.src == cv.dst) != (nx.src2 == cv.dst)) {
+      const int r = nx.src == cv.dst ? nx.src2 : nx.src;
+      if (r >= 2 && nx.dst >= 2 && r != cv.src && dead_after(r, i + 2)) f = PP_ACCUMULATE;
     }
-    if (!read_later && conv_pool_fusable(pl->views[i], n, pl->in[i].h, pl->in[i].w, act, true)) {
-      pl->fuse_pool[i] = 1;
-      ++i;   // the pool is taken; it cannot start another pair
+    if (f && dead_after(cv.dst, i + 2) && conv_fusable(pl->views[i], n, pl->in[i].h, pl->in[i].w, act, f, true)) {
+      pl->fuse[i] = f;
+      ++i;   // the second op is taken; it cannot start another pair
     }
   }
-  // buffers: each op reads and writes the buffers its slots map to now; a
-  // fused pair whose pool writes the conv's input slot writes the conv's
-  // output buffer and then swaps the two slots' buffers (the conv's output
-  // slot is dead after the pool, the input slot is overwritten by it)
+  // buffers: each op reads and writes the buffers its slots map to now.  A
+  // fused pair whose pool / shuffle writes the conv's input slot writes the
+  // conv's output buffer and then swaps the two slots' buffers (the conv's
+  // output slot is dead after the pair, the input slot is overwritten by
+  // it); a fused add writes the skip slot's buffer and then swaps it with
+  // the add's dst (the skip slot is dead after the add)
   int buf[PP_MAX_SLOTS];
   for (int s = 0; s < PP_MAX_SLOTS; ++s) buf[s] = s;
   pl->b_src.assign(n_ops, 0);
@@ -163,22 +181,32 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
     pl->b_src[i] = buf[op.src];
     pl->b_src2[i] = op.kind == PP_OP_ADD ? buf[op.src2] : 0;
     Shape o = pl->out[i];
-    bool swap = false;
-    if (pl->fuse_pool[i]) {
-      const pp_net_op& mp = ops[i + 1];
-      swap = mp.dst == op.src;
-      pl->b_dst[i] = swap ? buf[op.dst] : buf[mp.dst];
+    int swap_a = -1, swap_b = -1;   // slots whose buffers swap after the op
+    if (pl->fuse[i]) {
+      const pp_net_op& nx = ops[i + 1];
+      if (pl->fuse[i] == PP_ACCUMULATE) {
+        const int r = nx.src == op.dst ? nx.src2 : nx.src;
+        pl->b_dst[i] = buf[r];
+        swap_a = r;
+        swap_b = nx.dst;
+      } else if (nx.dst == op.src) {
+        pl->b_dst[i] = buf[op.dst];
+        swap_a = op.dst;
+        swap_b = nx.dst;
+      } else {
+        pl->b_dst[i] = buf[nx.dst];
+      }
       o = pl->out[i + 1];
     } else {
       pl->b_dst[i] = buf[op.dst];
     }
     const size_t bytes = static_cast<size_t>(n) * o.c * o.h * o.w * esz;
     if (bytes > pl->buf_bytes[pl->b_dst[i]]) pl->buf_bytes[pl->b_dst[i]] = bytes;
-    if (pl->fuse_pool[i]) {
-      if (swap) {
-        const int t = buf[op.dst];
-        buf[op.dst] = buf[ops[i + 1].dst];
-        buf[ops[i + 1].dst] = t;
+    if (pl->fuse[i]) {
+      if (swap_a >= 0) {
+        const int t = buf[swap_a];
+        buf[swap_a] = buf[swap_b];
+        buf[swap_b] = t;
       }
       ++i;
     }
@@ -245,9 +273,9 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
     hipError_t e = hipSuccess;
     switch (op.kind) {
       case PP_OP_CONV_PP:
-        if (pl.fuse_pool[i]) {
-          // conv + the max pool of op i + 1
-          st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags | PP_MAXPOOL2,
+        if (pl.fuse[i]) {
+          // conv + the pool / add / shuffle of op i + 1
+          st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags | pl.fuse[i],
                             scratch, pl.scratch_bytes, stream);
           if (st != PP_OK) return st;
           ++i;

@@ -274,6 +274,76 @@ def test_fused_maxpool(recipe, ksplit, monkeypatch):
             assert torch.equal(yp.cpu(), pooled), f"recipe {recipe}: fused pool differs from pooling the output"
 
 
+# conv + activation fused with a residual add (PP_ACCUMULATE: y += act(conv))
+# or a pixel shuffle (PP_PIXSHUF2): against the oracle conv followed by the
+# op (x -> x + r is 1-Lipschitz and the shuffle moves data, so S + |r| and
+# the shuffled S bound the error), and bitwise against the same plan's plain
+# store followed by the op in torch.  Ragged and vector-store widths, stride
+# 2, dilation 2, bf16, and forced channel splits (the second pass takes the
+# epilogue).
+EPI_RECIPES = [(None, 0), (20, 0), (21, 0), (23, 0), (24, 0), (25, 0), (26, 0), (29, 0), (31, 0), (32, 0),
+               (34, 0), (36, 0), (37, 0), (24, 3), (25, 2), (20, 4)]
+
+
+@pytest.mark.parametrize("recipe,ksplit", EPI_RECIPES)
+@pytest.mark.parametrize("mode", ["add", "pshuf2"])
+def test_fused_add_pixshuf(mode, recipe, ksplit, monkeypatch):
+    if recipe is not None:
+        monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    cases = (((1, 1, 1), "f32", (20, 21, 37, 45), True), ((1, 1, 1), "f32", (16, 24, 30, 44), False),
+             ((2, 1, 1), "f32", (12, 9, 41, 50), True), ((1, 2, 2), "f32", (8, 13, 29, 36), False),
+             ((1, 1, 1), "bf16", (24, 17, 33, 70), False), ((1, 1, 1), "bf16", (8, 20, 14, 16), True))
+    for (s, p, d), dtype, shape, relu in cases:
+        c_out, c_in, h, w = shape
+        seed = 700 + (recipe or 0) + (50 if mode == "add" else 0)
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        if dtype == "bf16":
+            x = obf16.round_f32(x)
+            w_or = obf16.round_f32(L["w"])
+        else:
+            w_or = L["w"]
+        wd = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], s, p, d, wd)
+        ho, wo = pp.out_size(layer.h_blob, h, w)
+        _say("fused", mode, "recipe", recipe, "ksplit", ksplit, (s, p, d), dtype, shape, "relu", relu)
+        xd = _to_dev(x, dtype)
+        args = (x, w_or, L["b"], L["pid"], L["conn"], L["lib"])
+        cref = oconv.conv3x3_pruned(*args, s, p, d, relu)
+        cbound = oconv.conv3x3_bound(*args, s, p, d)
+        if mode == "add":
+            r = workloads.random_input(seed + 1, (2, c_out, ho, wo))
+            if dtype == "bf16":
+                r = obf16.round_f32(r)
+            rd = _to_dev(r, dtype)
+            yd = rd.clone()
+            pp.conv2d_fwd(layer, xd, relu=relu, out=yd, accumulate=True)
+            ref, bound = cref + r.astype(np.float64), cbound + np.abs(r.astype(np.float64))
+        else:
+            yd = pp.conv2d_fwd(layer, xd, relu=relu, pixshuf2=True)
+            ref, bound = oconv.pixel_shuffle2(cref), oconv.pixel_shuffle2(cbound)
+        check(_from_dev(yd), ref, bound, dtype, f"fused {mode} recipe {recipe} {(s, p, d)} {dtype} {shape}")
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, wd)
+        if recipe is not None and plan[0] == recipe and (not ksplit or plan[1] == ksplit):
+            y = pp.conv2d_fwd(layer, xd, relu=relu)
+            want = rd + y if mode == "add" else torch.nn.functional.pixel_shuffle(y, 2)
+            torch.cuda.synchronize()
+            assert torch.equal(yd.cpu(), want.cpu()), f"recipe {recipe}: fused {mode} differs from the op after the conv"
+
+
+def test_fused_flags_rejected():
+    # at most one fused op; the shuffle needs c_out % 4 == 0
+    L = workloads.random_layer(9, 6, 8, keep=0.5)
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+    xd = _to_dev(workloads.random_input(9, (1, 8, 12, 12)), "f32")
+    with pytest.raises(pp.PPError):
+        pp.conv2d_fwd(layer, xd, maxpool2=True, accumulate=True, out=torch.zeros((1, 6, 6, 6), device="cuda"))
+    with pytest.raises(pp.PPError):
+        pp.conv2d_fwd(layer, xd, pixshuf2=True, out=torch.zeros((1, 1, 24, 24), device="cuda"))
+
+
 # channel split over workgroups (partial sums in the workspace, added by a
 # second kernel in split order): forced splits, ragged channel shares, both
 # activation dtypes

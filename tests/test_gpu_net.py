@@ -3,9 +3,13 @@
 Teacher-forced check: every op's GPU output is compared with the oracle run
 on that op's GPU input (sampled output channels for the large layers), so
 errors do not compound.  The op outputs come from pp_net_fwd itself, run on
-the op-list prefix that ends with that op.  A max pool that pp_net_fwd fuses
-into the pruned conv before it is checked as that conv followed by the pool.
-pp_net_fwd must also equal the chain of single-layer calls bitwise."""
+the op-list prefix that ends with that op.  An op that pp_net_fwd fuses into
+the pruned conv before it (max pool, residual add, pixel shuffle) is checked
+as that conv followed by the op; its prefix keeps the real slots (so the
+fusion, with its buffer renaming, happens as in the whole network) and ends
+with a nearest x2 upsample of the op's output into slot 1, which is exact
+data movement.  pp_net_fwd must also equal the chain of single-layer calls
+bitwise."""
 import numpy as np
 import pytest
 
@@ -46,11 +50,13 @@ def _np(t):
     return t.float().cpu().numpy()
 
 
-def _sampled(op, prm, n_keep, seed):
-    """Restrict an op to a subset of its output channels (oracle cost)."""
-    if op["op"] not in ("conv3", "conv", "deconv") or op["c_out"] <= n_keep:
+def _sampled(op, prm, n_keep, seed, group=1):
+    """Restrict an op to a subset of its output channels (oracle cost); with
+    group g whole aligned groups of g channels (n_keep groups)."""
+    if op["op"] not in ("conv3", "conv", "deconv") or op["c_out"] <= n_keep * group:
         return op, prm, slice(None)
-    sel = np.sort(np.random.default_rng(seed).choice(op["c_out"], size=n_keep, replace=False))
+    g = np.sort(np.random.default_rng(seed).choice(op["c_out"] // group, size=n_keep, replace=False))
+    sel = (group * g[:, None] + np.arange(group)[None, :]).reshape(-1)
     p = dict(prm)
     if op["op"] == "deconv":
         p["w"] = prm["w"][:, sel]
@@ -63,53 +69,56 @@ def _sampled(op, prm, n_keep, seed):
     return dict(op, c_out=len(sel)), p, sel
 
 
-def _fused_pool(ops, i):
-    """pp_net_fwd runs op i (a 2 x 2 max pool) inside the pruned conv before
-    it: the pool reads that conv's output, which no later op reads before
-    rewriting it, and the conv's padding equals its dilation (the fused
-    tilings)."""
-    if i < 1 or ops[i]["op"] != "maxpool2" or ops[i - 1]["op"] != "conv3":
-        return False
-    cv, mp = ops[i - 1], ops[i]
-    if mp["src"] != cv["dst"] or cv["dst"] == 1 or (mp["dst"] == cv["src"] and cv["src"] < 2) or \
-            cv["pad"] != cv["dil"]:
-        return False
-    for o in ops[i + 1:]:
-        if o["src"] == cv["dst"] or (o["op"] == "add" and o.get("src2") == cv["dst"]):
-            return False
-        if o["dst"] == cv["dst"]:
-            return True
-    return True
+def _prefix_net(net, i, readout):
+    """pp_net_fwd on ops 0..i: op i writes slot 1, or (readout) keeps its slot
+    and an x2 upsample copies that slot into slot 1."""
+    sub = pp.Net.__new__(pp.Net)
+    sub.__dict__.update(net.__dict__)
+    arr = (pp.NetOp * (i + 1 + readout))()
+    for j in range(i + 1):
+        arr[j] = net.ops[j]
+    if readout:
+        arr[i + 1].kind = pp.OP_UPSAMPLE2
+        arr[i + 1].src, arr[i + 1].dst = net.ops[i].dst, 1
+    else:
+        arr[i].dst = 1
+    sub.ops, sub.n_ops, sub._ws = arr, i + 1 + readout, None
+    return sub
 
 
 def teacher_forced(cfg, dtype, n_keep=6):
     spec = workloads.net_spec(cfg)
     params = workloads.net_params(cfg)
     net = pp.Net(spec["ops"], params, dtype)
+    fused = pp.fused_ops(spec["ops"])
     x_np, x = _input(cfg, dtype)
     slots = {0: x_np}
     worst = 0.0
     for i, (op, prm) in enumerate(zip(spec["ops"], params)):
-        _say(f"cfg {cfg} {dtype} op {i} {op['op']} c_in={op.get('c_in')} c_out={op.get('c_out')}")
-        # pp_net_fwd on the prefix ending at op i, with op i writing slot 1
-        sub = pp.Net.__new__(pp.Net)
-        sub.__dict__.update(net.__dict__)
-        arr = (pp.NetOp * (i + 1))()
-        for j in range(i + 1):
-            arr[j] = net.ops[j]
-        arr[i].dst = 1
-        sub.ops, sub.n_ops, sub._ws = arr, i + 1, None
-        y = _np(sub.forward(x))
-        if _fused_pool(spec["ops"][:i + 1], i):
-            # conv + pool in one launch: the oracle conv on the conv's GPU input,
-            # pooled (max is 1-Lipschitz, so the pooled bound is the pooled S)
+        _say(f"cfg {cfg} {dtype} op {i} {op['op']} c_in={op.get('c_in')} c_out={op.get('c_out')}"
+             f"{' (fused into op %d)' % (i - 1) if i in fused else ''}")
+        if i in fused:
+            # the fused pair in one launch: the oracle conv on the conv's GPU
+            # input, then the op (max and x -> x + r are 1-Lipschitz, the
+            # shuffle moves data: the pair's bound is the op applied to S,
+            # plus |r| for the add)
+            y = _np(_prefix_net(net, i, True).forward(x))[:, :, ::2, ::2]
             cop, cprm = spec["ops"][i - 1], params[i - 1]
-            sop, sprm, sel = _sampled(cop, cprm, n_keep, 1000 * cfg + i)
+            group = 4 if op["op"] == "pshuf2" else 1
+            sop, sprm, sel = _sampled(cop, cprm, n_keep, 1000 * cfg + i, group)
             cref, cbound = onet.run_op(sop, sprm, slots[cop["src"]], None, dtype)
-            worst = max(worst, check(y[:, sel], oconv.maxpool2(cref), oconv.maxpool2(cbound), dtype,
-                                     f"cfg {cfg} op {i} (conv3 + maxpool2)"))
+            if op["op"] == "maxpool2":
+                ref, bound, got = oconv.maxpool2(cref), oconv.maxpool2(cbound), y[:, sel]
+            elif op["op"] == "pshuf2":
+                ref, bound = oconv.pixel_shuffle2(cref), oconv.pixel_shuffle2(cbound)
+                got = y if isinstance(sel, slice) else y[:, sel[::4] // 4]
+            else:
+                r = slots[op["src2"] if op["src"] == cop["dst"] else op["src"]][:, sel].astype(np.float64)
+                ref, bound, got = cref + r, cbound + np.abs(r), y[:, sel]
+            worst = max(worst, check(got, ref, bound, dtype, f"cfg {cfg} op {i} (conv3 + {op['op']})"))
             slots[op["dst"]] = y
             continue
+        y = _np(_prefix_net(net, i, False).forward(x))
         src = slots[op["src"]]
         src2 = slots.get(op.get("src2")) if "src2" in op else None
         sop, sprm, sel = _sampled(op, prm, n_keep, 1000 * cfg + i)
@@ -139,19 +148,49 @@ def test_vgg16_net_equals_chained_layer_calls():
     _say("vgg16 pp_net_fwd vs chained pp_conv2d_fwd (pool fused where the net fuses it) + maxpool")
     y_net = _np(net.forward(x))
     ops = spec["ops"]
+    fused = pp.fused_ops(ops)
     cur = x
     li = 0
     for i, (op, prm) in enumerate(zip(ops, params)):
         if op["op"] == "conv3":
-            fuse = i + 1 < len(ops) and _fused_pool(ops, i + 1)
-            cur = pp.conv2d_fwd(net.pruned[li], cur, relu=op["relu"], maxpool2=fuse)
+            cur = pp.conv2d_fwd(net.pruned[li], cur, relu=op["relu"], maxpool2=fused.get(i + 1) == "maxpool2")
             li += 1
-        elif _fused_pool(ops, i):
+        elif i in fused:
             continue
         else:
             one = pp.Net([dict(op, src=0, dst=1)], [prm], "f32")
             cur = one.forward(cur)
     assert np.array_equal(y_net, _np(cur))
+
+
+@pytest.mark.parametrize("cfg,dtype", [(3, "f32"), (4, "f32"), (4, "bf16")])
+def test_net_fused_equals_unfused(cfg, dtype):
+    # the fused residual adds and pixel shuffles give bitwise the output of
+    # the same network run op by op (each op its own pp_net_fwd), whose
+    # convs are the same plans with the plain store
+    spec = workloads.net_spec(cfg)
+    params = workloads.net_params(cfg)
+    ops = spec["ops"]
+    fused = pp.fused_ops(ops)
+    assert any(k == "add" for k in fused.values()), "the network has fusable residual adds"
+    if cfg == 4:
+        assert sum(k == "pshuf2" for k in fused.values()) == 2
+    net = pp.Net(ops, params, dtype)
+    _, x = _input(cfg, dtype)
+    _say(f"cfg {cfg} {dtype}: pp_net_fwd ({len(fused)} fused ops) vs op-by-op")
+    y_net = _np(net.forward(x))
+    slots = {0: x}
+    li = 0
+    for i, (op, prm) in enumerate(zip(ops, params)):
+        if op["op"] == "conv3":
+            slots[op["dst"]] = pp.conv2d_fwd(net.pruned[li], slots[op["src"]], relu=op["relu"])
+            li += 1
+        elif op["op"] == "add":
+            slots[op["dst"]] = slots[op["src"]] + slots[op["src2"]]
+        else:
+            one = pp.Net([dict(op, src=0, dst=1)], [prm], dtype)
+            slots[op["dst"]] = one.forward(slots[op["src"]].contiguous())
+    assert np.array_equal(y_net, _np(slots[1]))
 
 
 def test_vgg16_net_graph_replays():
