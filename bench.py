@@ -191,14 +191,16 @@ def summarize_profile(root, cfg=2):
     di = -1   # dispatch index within a frame
     for i, (k, op, ish, osh) in enumerate(shapes):
         if i in fused:
+            into = i + 1 if fused[i] == "up2" else i - 1
             lay.append(dict(op=i, kind=op["op"], lib="", c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
-                            kernel=f"(fused into op {i - 1})", us=0.0, fetch_mb=0.0, write_mb=0.0, sq={}))
+                            kernel=f"(fused into op {into})", us=0.0, fetch_mb=0.0, write_mb=0.0, sq={}))
             continue
         di += 1
         dur = sum(f[di]["dur_ns"] for f in kt_fr) / len(kt_fr) / 1e3
         fetch = sum(f[di]["c"]["FETCH_SIZE"] for f in fe_fr) / len(fe_fr) * ff * 1024
         write = sum(f[di]["c"]["WRITE_SIZE"] for f in wr_fr) / len(wr_fr) * wf * 1024
-        kind = op["op"] + ("+" + fused[i + 1] if i + 1 in fused else "")
+        kind = ("up2+" if fused.get(i - 1) == "up2" else "") + op["op"] + \
+            ("+" + fused[i + 1] if i + 1 in fused and fused[i + 1] != "up2" else "")
         lay.append(dict(op=i, kind=kind, lib=op.get("lib", ""), c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
                         kernel=_kernel_label(kt_fr[0][di]["name"]), us=round(dur, 3),
                         fetch_mb=round(fetch / 1e6, 3), write_mb=round(write / 1e6, 3), sq=sq.get(di, {})))
@@ -322,11 +324,16 @@ def main():
         L = net.pruned[li]
         li += 1
         f = fused.get(i + 1)
+        f = None if f == "up2" else f
+        up = fused.get(i - 1) == "up2"
         if f == "maxpool2":
             o = (o[0], o[1] // 2, o[2] // 2)
         elif f == "pshuf2":
             o = (o[0] // 4, 2 * o[1], 2 * o[2])
-        kw = dict(relu=op["relu"], maxpool2=f == "maxpool2", accumulate=f == "add", pixshuf2=f == "pshuf2")
+        if up:
+            ishape = (ishape[0], ishape[1] // 2, ishape[2] // 2)   # read as stored, upsampled on load
+        kw = dict(relu=op["relu"], maxpool2=f == "maxpool2", accumulate=f == "add", pixshuf2=f == "pshuf2",
+                  upsample2=up)
         xin = torch.rand((batch,) + ishape, device=dev).to(tdt)
         yo = torch.zeros((batch,) + o, device=dev, dtype=tdt)
         for _ in range(5):
@@ -344,7 +351,7 @@ def main():
         alg_bytes = batch * (int(np.prod(ishape)) + (2 if f == "add" else 1) * int(np.prod(o))) * esz + \
             L.h_blob.nbytes
         layers.append(dict(op=i, c_in=op["c_in"], c_out=op["c_out"], hw=f"{o[1]}x{o[2]}", lib=op["lib"],
-                           fused=f,
+                           fused=f, upsample2_in=up,
                            surviving_mmac=round(macs / 1e6, 3), us=round(us, 3),
                            eff_tmacs=round(macs / us / 1e6, 3), alg_mb=round(alg_bytes / 1e6, 3),
                            frac_fp32_peak=round(2 * macs / us / 1e6 / PEAK_FP32_VECTOR_TFLOPS, 4)))

@@ -50,12 +50,13 @@ typedef enum {
 typedef enum { PP_F32 = 0, PP_BF16 = 1 } pp_dtype;
 
 /* flags of pp_conv2d_fwd / pp_net_op.  The others than PP_RELU are for
- * pp_conv2d_fwd only and fuse the op after the conv into its store
- * (graph-level fusion, Sec. 3): PP_MAXPOOL2 stores the 2 x 2, stride 2 max
+ * pp_conv2d_fwd only and fuse the op before or after the conv into its
+ * loads or its store (graph-level fusion, Sec. 3): PP_UPSAMPLE2 convolves
+ * the nearest x2 upsampling of x; PP_MAXPOOL2 stores the 2 x 2, stride 2 max
  * pool of the activated output instead of the output itself; PP_ACCUMULATE
  * adds the activated output to what y holds (a residual connection);
  * PP_PIXSHUF2 stores the activated output through PixelShuffle(2). */
-enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u, PP_ACCUMULATE = 4u, PP_PIXSHUF2 = 8u };
+enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u, PP_ACCUMULATE = 4u, PP_PIXSHUF2 = 8u, PP_UPSAMPLE2 = 16u };
 
 /* Shape and storage of one pruned 3x3 layer. */
 typedef struct {
@@ -156,7 +157,11 @@ pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
  *                       act(conv + bias)[4c+2a+b][i][j]; c_out a multiple of
  *                       4, else PP_EINVAL; same libraries as PP_ACCUMULATE);
  *                       at most one of PP_MAXPOOL2, PP_ACCUMULATE and
- *                       PP_PIXSHUF2, else PP_EINVAL
+ *                       PP_PIXSHUF2, else PP_EINVAL; PP_UPSAMPLE2 (the conv
+ *                       reads x [n][c_in][h][w] as its nearest x2 upsampling
+ *                       [n][c_in][2h][2w]: h_out, w_out are those of a 2h x 2w
+ *                       input; same libraries as PP_ACCUMULATE; combines with
+ *                       the others)
  *   workspace, ws_bytes optional device scratch (NULL, 0 for none), 256-byte
  *                       aligned.  With pp_conv2d_workspace() bytes the
  *                       kernel may split the input channels over more
@@ -177,7 +182,9 @@ pp_status pp_conv2d_fwd(const void* h_blob, size_t blob_bytes, const void* d_blo
 
 /*
  * pp_conv2d_workspace -- device scratch bytes pp_conv2d_fwd can use for this
- * layer and input (0: it would not use any).  Host-only.  Errors: as
+ * layer and input (0: it would not use any); h, w are the conv's input size
+ * (for a PP_UPSAMPLE2 call the upsampled size 2h x 2w; a call with fused
+ * flags needs no more than the plain call).  Host-only.  Errors: as
  * pp_conv2d_out_size, PP_EINVAL (bytes NULL, act_dtype), PP_EUNSUPPORTED.
  */
 pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h,

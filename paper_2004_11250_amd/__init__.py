@@ -24,6 +24,7 @@ PP_RELU = 1
 PP_MAXPOOL2 = 2
 PP_ACCUMULATE = 4
 PP_PIXSHUF2 = 8
+PP_UPSAMPLE2 = 16
 (OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
 
 # exported symbols declared in include/pp.h
@@ -207,14 +208,15 @@ class PackedLayer:
 
 
 def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspace="auto", maxpool2=False,
-               accumulate=False, pixshuf2=False):
+               accumulate=False, pixshuf2=False, upsample2=False):
     """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None).
     workspace: "auto" (a scratch tensor of pp_conv2d_workspace bytes, kept on
     the layer per input shape), None (no scratch) or a uint8 device tensor.
     maxpool2: store the 2 x 2 max pool of the activated output (PP_MAXPOOL2).
     accumulate: add the activated output to ``out`` in place (PP_ACCUMULATE;
     out is required).  pixshuf2: store through PixelShuffle(2)
-    (PP_PIXSHUF2)."""
+    (PP_PIXSHUF2).  upsample2: convolve the nearest x2 upsampling of x
+    (PP_UPSAMPLE2)."""
     torch = _torch()
     lib = load_library()
     if not x.is_contiguous():
@@ -222,7 +224,8 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     n, c, h, w = x.shape
     if c != layer.info["c_in"]:
         raise ValueError(f"x has {c} channels, the layer expects {layer.info['c_in']}")
-    ho, wo = out_size(layer.h_blob, h, w)
+    hc, wc = (2 * h, 2 * w) if upsample2 else (h, w)   # the conv's input size
+    ho, wo = out_size(layer.h_blob, hc, wc)
     c_out = layer.info["c_out"]
     if maxpool2:
         ho, wo = ho // 2, wo // 2
@@ -236,8 +239,8 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     elif tuple(out.shape) != shape or out.dtype != x.dtype or not out.is_contiguous():
         raise ValueError(f"out must be a contiguous {x.dtype} tensor of shape {shape}")
     if isinstance(workspace, str) and workspace == "auto":
-        nb = conv2d_workspace(layer.h_blob, n, h, w, _dtype_code(x))
-        key = (n, h, w, _dtype_code(x), x.device.index)
+        nb = conv2d_workspace(layer.h_blob, n, hc, wc, _dtype_code(x))
+        key = (n, hc, wc, _dtype_code(x), x.device.index)
         workspace = layer.scratch.get(key)
         if nb and (workspace is None or workspace.numel() < nb):
             workspace = torch.empty(nb, dtype=torch.uint8, device=x.device)
@@ -248,7 +251,8 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     st = lib.pp_conv2d_fwd(_ptr(layer.h_blob), layer.h_blob.nbytes, layer.d_blob.data_ptr(), x.data_ptr(),
                            out.data_ptr(), n, h, w, _dtype_code(x),
                            (PP_RELU if relu else 0) | (PP_MAXPOOL2 if maxpool2 else 0) |
-                           (PP_ACCUMULATE if accumulate else 0) | (PP_PIXSHUF2 if pixshuf2 else 0), ws_ptr, ws_bytes,
+                           (PP_ACCUMULATE if accumulate else 0) | (PP_PIXSHUF2 if pixshuf2 else 0) |
+                           (PP_UPSAMPLE2 if upsample2 else 0), ws_ptr, ws_bytes,
                            _stream_ptr(stream))
     _check(st, "pp_conv2d_fwd")
     return out
@@ -274,29 +278,46 @@ def _dead_after(ops, slot, j0) -> bool:
 
 
 def fused_ops(ops) -> dict:
-    """The ops that pp_net_fwd runs inside the pruned conv just before them
-    (one launch), as {index: "maxpool2" | "pshuf2" | "add"}.  The op reads
-    that conv's output slot, the conv does not write slot 1, the conv's
-    output is dead after the op (no later op reads it before one rewrites
-    it), and the conv is a canonical / all-ones layer with padding equal to
-    its dilation; a pool or shuffle that writes the conv's input slot has it
-    in the workspace (slot >= 2); an add's other operand and its dst are
-    workspace slots, that operand is not the conv's input and is dead after
-    the add too.  ops: the op dicts of a network spec."""
-    out = {}
+    """The ops that pp_net_fwd does not launch on their own, as {index:
+    "up2" | "maxpool2" | "pshuf2" | "add"}: an x2 upsample taken by the pruned
+    conv right after it ("up2"), or a max pool, pixel shuffle or add taken by
+    the pruned conv right before it.  The conv is a canonical / all-ones layer
+    with padding equal to its dilation.  Upsample: the conv reads its output
+    slot, which is not slot 1 and is dead after the conv (no later op reads
+    it before one rewrites it); a conv that writes the upsample's input slot
+    needs it in the workspace (slot >= 2).  Pool / shuffle / add: the op
+    reads the conv's output slot, the conv does not write slot 1, the conv's
+    output is dead after the op; a pool or shuffle that writes the slot the
+    conv reads has it in the workspace; an add's other operand and its dst
+    are workspace slots, that operand is not the slot the conv reads and is
+    dead after the add too; a conv that reads an upsample's input and writes
+    that slot takes no op after it.  ops: the op dicts of a network spec."""
+    def conv_ok(cv):
+        return cv["op"] == "conv3" and cv["pad"] == cv["dil"] and cv.get("lib") in ("canon8", "dense9")
+
+    out, up_in = {}, set()
+    i = 0
+    while i + 1 < len(ops):
+        us, cv = ops[i], ops[i + 1]
+        if us["op"] == "up2" and conv_ok(cv) and cv["src"] == us["dst"] and us["dst"] != 1 and \
+                not (cv["dst"] == us["src"] and cv["dst"] < 2) and _dead_after(ops, us["dst"], i + 2):
+            out[i] = "up2"
+            up_in.add(i + 1)
+            i += 2
+        else:
+            i += 1
     i = 1
     while i < len(ops):
         cv, nx = ops[i - 1], ops[i]
         f = None
-        if cv["op"] == "conv3" and cv["dst"] != 1 and cv["pad"] == cv["dil"] and \
-                cv.get("lib") in ("canon8", "dense9"):
-            if nx["op"] in ("maxpool2", "pshuf2") and nx["src"] == cv["dst"] and \
-                    not (nx["dst"] == cv["src"] and cv["src"] < 2):
+        cs = ops[i - 2]["src"] if (i - 1) in up_in else cv.get("src")
+        if conv_ok(cv) and cv["dst"] != 1 and cs != cv["dst"]:
+            if nx["op"] in ("maxpool2", "pshuf2") and nx["src"] == cv["dst"] and not (nx["dst"] == cs and cs < 2):
                 if nx["op"] == "maxpool2" or cv["c_out"] % 4 == 0:
                     f = nx["op"]
             elif nx["op"] == "add" and (nx["src"] == cv["dst"]) != (nx["src2"] == cv["dst"]):
                 r = nx["src2"] if nx["src"] == cv["dst"] else nx["src"]
-                if r >= 2 and nx["dst"] >= 2 and r != cv["src"] and _dead_after(ops, r, i + 1):
+                if r >= 2 and nx["dst"] >= 2 and r != cs and _dead_after(ops, r, i + 1):
                     f = "add"
         if f is not None and _dead_after(ops, cv["dst"], i + 1):
             out[i] = f

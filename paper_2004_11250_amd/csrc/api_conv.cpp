@@ -61,15 +61,19 @@ ConvParams layer_params(const BlobView& v, int32_t n, int32_t h, int32_t w, int 
 pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
                        int32_t w, int32_t act_dtype, uint32_t flags, void* scratch, size_t scratch_bytes,
                        hipStream_t st) {
+  // with PP_UPSAMPLE2 the conv's input is x upsampled to 2h x 2w
+  const bool up = (flags & PP_UPSAMPLE2) != 0;
+  if (up && (h < 1 || w < 1 || h > (1 << 29) || w > (1 << 29))) return fail(PP_EINVAL, "bad h, w");
+  const int hv = up ? 2 * h : h, wv = up ? 2 * w : w;
   int ho = 0, wo = 0;
-  pp_status s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
+  pp_status s = conv_check(v, n, hv, wv, act_dtype, &ho, &wo);
   if (s != PP_OK) return s;
   if (!d_blob || !x || !y) return fail(PP_EINVAL, "NULL device pointer");
   if (reinterpret_cast<uintptr_t>(d_blob) % 256) return fail(PP_EINVAL, "device blob must be 256-byte aligned");
   const size_t esz = act_dtype == PP_BF16 ? 2 : 4;
   if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % esz)
     return fail(PP_EINVAL, "activation pointers misaligned");
-  if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2))
+  if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2))
     return fail(PP_EINVAL, "unknown flags");
   {
     const uint32_t f = flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2);
@@ -84,7 +88,7 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const size_t ybytes = static_cast<size_t>(n) * v.c_out * (pool ? (ho / 2) * (wo / 2) : ho * wo) * esz;
   if (xb < yb + ybytes && yb < xb + xbytes) return fail(PP_EINVAL, "x and y overlap");
 
-  ConvParams p = layer_params(v, n, h, w, ho, wo);
+  ConvParams p = layer_params(v, n, hv, wv, ho, wo);
   p.blob = static_cast<const uint8_t*>(d_blob);
   p.x = x;
   p.y = y;
@@ -98,20 +102,21 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
     else
       p.part = static_cast<float*>(scratch);
   }
-  if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the max pool / accumulation / pixel shuffle for this layer");
+  if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the upsampling / max pool / accumulation / pixel shuffle for this layer");
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;
 }
 
-bool conv_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flag,
+bool conv_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
                   bool with_scratch) {
   int ho = 0, wo = 0;
   if (conv_check(v, n, h, w, act_dtype, &ho, &wo) != PP_OK) return false;
-  if (flag == PP_MAXPOOL2 && (ho < 2 || wo < 2)) return false;
-  if (flag == PP_PIXSHUF2 && v.c_out % 4) return false;
+  if ((flags & PP_MAXPOOL2) && (ho < 2 || wo < 2)) return false;
+  if ((flags & PP_PIXSHUF2) && v.c_out % 4) return false;
+  if ((flags & PP_UPSAMPLE2) && (h % 2 || w % 2)) return false;
   ConvParams p = layer_params(v, n, h, w, ho, wo);
-  p.flags = flag;
+  p.flags = flags;
   return plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_scratch).recipe >= 0;
 }
 

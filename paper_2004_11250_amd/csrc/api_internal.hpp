@@ -20,9 +20,11 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
                        int32_t w, int32_t act_dtype, uint32_t flags, void* scratch, size_t scratch_bytes,
                        hipStream_t st);
 
-// whether pp_conv2d_fwd can fuse the op after the conv (flag PP_MAXPOOL2 or
-// PP_ACCUMULATE) for this layer and input, with or without split scratch
-bool conv_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flag,
+// whether pp_conv2d_fwd can fuse the ops before / after the conv (flags:
+// PP_UPSAMPLE2 and one of PP_MAXPOOL2, PP_ACCUMULATE, PP_PIXSHUF2) for this
+// layer, with or without split scratch; h, w: the conv's input size (with
+// PP_UPSAMPLE2 the upsampled size)
+bool conv_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
                   bool with_scratch);
 
 // scratch bytes pp_conv2d_fwd can use for this layer and input (0: none)

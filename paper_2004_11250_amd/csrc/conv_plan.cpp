@@ -132,7 +132,7 @@ static bool pool_fits(int id) {
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
   const bool pool = (p.flags & PP_MAXPOOL2) != 0;
   // epilogues of the wave-pipeline kernel only
-  const bool fused = (p.flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2)) != 0;
+  const bool fused = (p.flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2)) != 0;
   // a plan for recipe id, or recipe -1 when it cannot take the fused epilogue
   auto try_plan = [&](int id) {
     ConvPlan pl;

@@ -137,8 +137,9 @@ struct ConvPlan {
 // allow_split: the caller can provide scratch for a channel split.  With
 // PP_MAXPOOL2 in p.flags only plans that can fuse the pool are chosen (a
 // split, whose second pass pools, or a tiling with whole windows per lane),
-// with PP_ACCUMULATE or PP_PIXSHUF2 only wave-pipeline tilings, and recipe
-// -1 means none can.
+// with PP_ACCUMULATE, PP_PIXSHUF2 or PP_UPSAMPLE2 only wave-pipeline
+// tilings, and recipe -1 means none can.  (p.h, p.w are the conv's input
+// size: the upsampled size with PP_UPSAMPLE2.)
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split);
 // scratch bytes a plan needs (its partial-sum blocks); 0 without a split
 size_t split_bytes(const ConvPlan& plan, const ConvParams& p);

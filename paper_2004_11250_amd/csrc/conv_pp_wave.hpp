@@ -235,11 +235,16 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
 
   const int oy0 = ty * G::TH, ox0 = tx * G::TW;
   const int iy0 = oy0 * S - a.pad, ix0 = ox0 * S - a.pad;
-  const bool v4 = (a.w % 4) == 0;                       // 16-byte (fp32) / 8-byte (bf16) row loads
+  // with PP_UPSAMPLE2 the conv's input is the nearest x2 upsampling of x:
+  // a.h x a.w is the upsampled size and element (gy, gx) is read from
+  // x[gy / 2][gx / 2] (element loads: a row of the tile is not contiguous)
+  const bool up = (a.flags & PP_UPSAMPLE2) != 0;
+  const int sh = up ? a.h >> 1 : a.h, sw = up ? a.w >> 1 : a.w;   // stored input size
+  const bool v4 = !up && (a.w % 4) == 0;                // 16-byte (fp32) / 8-byte (bf16) row loads
   const int ixa = ix0 - SH;                             // a multiple of 4
 
-  const TA* __restrict__ x = static_cast<const TA*>(a.x) + static_cast<size_t>(img) * a.c_in * a.h * a.w;
-  const uint32_t chan_bytes = static_cast<uint32_t>(a.h) * a.w * sizeof(TA);
+  const TA* __restrict__ x = static_cast<const TA*>(a.x) + static_cast<size_t>(img) * a.c_in * sh * sw;
+  const uint32_t chan_bytes = static_cast<uint32_t>(sh) * sw * sizeof(TA);
   const uint8_t* blob = a.blob;
 
   // ---- per-lane staging offsets (bytes within one channel), fixed for the
@@ -257,7 +262,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       const int row = e / LSTR, col = e % LSTR;
       const int gy = iy0 + row, gx = ixa + col;
       const bool ok = e < G::AREA && gy >= 0 && gy < a.h && gx >= 0 && gx < a.w;
-      qoff[t][j] = ok ? (static_cast<uint32_t>(gy) * a.w + gx) * static_cast<uint32_t>(sizeof(TA)) : 0x80000000u;
+      const uint32_t el = up ? static_cast<uint32_t>(gy >> 1) * sw + (gx >> 1) : static_cast<uint32_t>(gy) * a.w + gx;
+      qoff[t][j] = ok ? el * static_cast<uint32_t>(sizeof(TA)) : 0x80000000u;
     }
 
   // ---- this wave's channel range
@@ -325,8 +331,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
   auto no_adj = [](int) { return 0u; };
   // global -> registers: the next channel's halo tile (xf walks the channels
   // in order) and weights
-  const TA* xf = x + static_cast<size_t>(c0) * a.h * a.w;
-  const size_t hw = static_cast<size_t>(a.h) * a.w;
+  const TA* xf = x + static_cast<size_t>(c0) * sh * sw;
+  const size_t hw = static_cast<size_t>(sh) * sw;
   auto fetch = [&](const uint32_t (&woff)[NWL]) __attribute__((always_inline)) {
     // the channel as the resource: soffset is not range checked, so the
     // channel offset goes into the base address
@@ -479,7 +485,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_wave_kernel(ConvParams a) 
       constexpr uint32_t LW0 = 4u * G::PATCH;
       const u32x4 brs = make_rsrc_below(blob, a.blob_bytes, kDmaShift);
       // descriptor of the next channel to DMA (channels are DMA'd in order)
-      u32x4 cr = make_rsrc_below(x + static_cast<size_t>(c0) * a.h * a.w, chan_bytes, kDmaShift);
+      u32x4 cr = make_rsrc_below(x + static_cast<size_t>(c0) * sh * sw, chan_bytes, kDmaShift);
   #pragma unroll
       for (int t = 0; t < NQ; ++t)
   #pragma unroll

@@ -5,12 +5,16 @@
 // happens before the first launch.  A pruned conv whose output only feeds
 // the op right after it -- a 2 x 2 max pool, a residual add or a pixel
 // shuffle -- runs as one fused launch (graph-level fusion, Sec. 3): that op
-// is taken in the conv's store.  Logical slots map to workspace buffers, and
-// a fused pair may leave two slots with swapped buffers:
+// is taken in the conv's store; an x2 upsample whose output only feeds the
+// pruned conv right after it is taken in the conv's loads.  Logical slots
+// map to workspace buffers, and a fused pair may leave two slots with
+// swapped buffers:
 //   - a pool or shuffle that writes the conv's input slot (ping-pong slot
 //     use) is written to the conv's output buffer instead;
 //   - an add dst = src + conv(x) whose skip operand src is dead afterwards
-//     accumulates into src's buffer in place, which becomes dst's.
+//     accumulates into src's buffer in place, which becomes dst's;
+//   - a conv that reads an upsample's input slot and writes that slot
+//     writes the upsample's unused output buffer instead.
 #include <hip/hip_runtime.h>
 
 #include <string>
@@ -34,6 +38,9 @@ struct Plan {
   // op i is a pruned conv fused with op i + 1: the conv's extra flag
   // (PP_MAXPOOL2, PP_ACCUMULATE or PP_PIXSHUF2), else 0
   std::vector<uint32_t> fuse;
+  // op i is a pruned conv that reads the input of the upsample at i - 1
+  // (PP_UPSAMPLE2); that upsample does not run
+  std::vector<char> up_in;
   // per op: the buffers (0 = x, 1 = y, >= 2 workspace) of src, src2, dst
   std::vector<int> b_src, b_src2, b_dst;
   size_t buf_bytes[PP_MAX_SLOTS] = {};
@@ -58,6 +65,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
   pl->out.resize(n_ops);
   pl->views.resize(n_ops);
   pl->fuse.assign(n_ops, 0);
+  pl->up_in.assign(n_ops, 0);
   std::vector<Shape> writes1;
   size_t part_max = 0;
   for (int i = 0; i < n_ops; ++i) {
@@ -135,12 +143,6 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
     if (op.dst == 1) writes1.push_back(o);
   }
   if (!slots[1].defined) return fail(PP_EINVAL, "no op writes the output slot 1");
-  // conv fusion.  The op after the conv reads the conv's output slot, which
-  // is not slot 1 and which no later op reads before rewriting it:
-  //   - max pool / pixel shuffle: one that writes the conv's input slot
-  //     needs that slot in the workspace (its buffer is swapped);
-  //   - add of a skip slot r (both in the workspace, as is the add's dst)
-  //     that is not the conv's input and is dead after the add as well.
   auto dead_after = [&](int slot, int j0) {
     for (int j = j0; j < n_ops; ++j) {
       if (ops[j].src == slot || (ops[j].kind == PP_OP_ADD && ops[j].src2 == slot)) return false;
@@ -148,19 +150,45 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
     }
     return true;
   };
+  // upsample + conv: the conv reads the upsample's output slot v (not slot
+  // 1), which no later op reads before rewriting it.  A conv that writes the
+  // upsample's input slot u (which it now reads) writes v's buffer instead,
+  // which then becomes u's (u in the workspace; no op after the conv fused)
+  for (int i = 0; i + 1 < n_ops; ++i) {
+    const pp_net_op& us = ops[i];
+    const pp_net_op& cv = ops[i + 1];
+    if (us.kind != PP_OP_UPSAMPLE2 || cv.kind != PP_OP_CONV_PP || cv.src != us.dst || us.dst == 1 ||
+        (cv.dst == us.src && cv.dst < 2) || !dead_after(us.dst, i + 2))
+      continue;
+    if (conv_fusable(pl->views[i + 1], n, pl->in[i + 1].h, pl->in[i + 1].w, act, PP_UPSAMPLE2, true)) {
+      pl->up_in[i + 1] = 1;
+      ++i;
+    }
+  }
+  // the slot a pruned conv reads
+  auto read_slot = [&](int i) { return pl->up_in[i] ? ops[i - 1].src : ops[i].src; };
+  // conv fusion.  The op after the conv reads the conv's output slot, which
+  // is not slot 1 and which no later op reads before rewriting it:
+  //   - max pool / pixel shuffle: one that writes the slot the conv reads
+  //     needs that slot in the workspace (its buffer is swapped);
+  //   - add of a skip slot r (both in the workspace, as is the add's dst)
+  //     that the conv does not read and that is dead after the add as well.
   for (int i = 0; i + 1 < n_ops; ++i) {
     const pp_net_op& cv = ops[i];
     const pp_net_op& nx = ops[i + 1];
     if (cv.kind != PP_OP_CONV_PP || cv.dst == 1) continue;
+    const int cs = read_slot(i);
+    if (cs == cv.dst) continue;   // upsample + conv writing its own input slot: no third op
     uint32_t f = 0;
-    if ((nx.kind == PP_OP_MAXPOOL2 || nx.kind == PP_OP_PIXSHUF2) && nx.src == cv.dst &&
-        !(nx.dst == cv.src && cv.src < 2)) {
+    if ((nx.kind == PP_OP_MAXPOOL2 || nx.kind == PP_OP_PIXSHUF2) && nx.src == cv.dst && !(nx.dst == cs && cs < 2)) {
       f = nx.kind == PP_OP_MAXPOOL2 ? PP_MAXPOOL2 : PP_PIXSHUF2;
     } else if (nx.kind == PP_OP_ADD && (nx.src == cv.dst) != (nx.src2 == cv.dst)) {
       const int r = nx.src == cv.dst ? nx.src2 : nx.src;
-      if (r >= 2 && nx.dst >= 2 && r != cv.src && dead_after(r, i + 2)) f = PP_ACCUMULATE;
+      if (r >= 2 && nx.dst >= 2 && r != cs && dead_after(r, i + 2)) f = PP_ACCUMULATE;
     }
-    if (f && dead_after(cv.dst, i + 2) && conv_fusable(pl->views[i], n, pl->in[i].h, pl->in[i].w, act, f, true)) {
+    const uint32_t fin = pl->up_in[i] ? PP_UPSAMPLE2 : 0u;
+    if (f && dead_after(cv.dst, i + 2) &&
+        conv_fusable(pl->views[i], n, pl->in[i].h, pl->in[i].w, act, f | fin, true)) {
       pl->fuse[i] = f;
       ++i;   // the second op is taken; it cannot start another pair
     }
@@ -170,7 +198,10 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
   // conv's output buffer and then swaps the two slots' buffers (the conv's
   // output slot is dead after the pair, the input slot is overwritten by
   // it); a fused add writes the skip slot's buffer and then swaps it with
-  // the add's dst (the skip slot is dead after the add)
+  // the add's dst (the skip slot is dead after the add).  A conv that takes
+  // the upsample before it reads that upsample's input buffer; the upsample
+  // writes nothing, and a conv that writes the upsample's input slot writes
+  // the upsample's output buffer and then swaps the two slots' buffers.
   int buf[PP_MAX_SLOTS];
   for (int s = 0; s < PP_MAX_SLOTS; ++s) buf[s] = s;
   pl->b_src.assign(n_ops, 0);
@@ -178,7 +209,8 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
   pl->b_dst.assign(n_ops, 0);
   for (int i = 0; i < n_ops; ++i) {
     const pp_net_op& op = ops[i];
-    pl->b_src[i] = buf[op.src];
+    if (i + 1 < n_ops && pl->up_in[i + 1]) continue;   // taken by the conv after it
+    pl->b_src[i] = buf[pl->up_in[i] ? ops[i - 1].src : op.src];
     pl->b_src2[i] = op.kind == PP_OP_ADD ? buf[op.src2] : 0;
     Shape o = pl->out[i];
     int swap_a = -1, swap_b = -1;   // slots whose buffers swap after the op
@@ -189,7 +221,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
         pl->b_dst[i] = buf[r];
         swap_a = r;
         swap_b = nx.dst;
-      } else if (nx.dst == op.src) {
+      } else if (nx.dst == read_slot(i)) {
         pl->b_dst[i] = buf[op.dst];
         swap_a = op.dst;
         swap_b = nx.dst;
@@ -197,19 +229,21 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
         pl->b_dst[i] = buf[nx.dst];
       }
       o = pl->out[i + 1];
+    } else if (pl->up_in[i] && op.dst == ops[i - 1].src) {
+      pl->b_dst[i] = buf[ops[i - 1].dst];   // the upsample's (unwritten) output buffer
+      swap_a = op.dst;
+      swap_b = ops[i - 1].dst;
     } else {
       pl->b_dst[i] = buf[op.dst];
     }
     const size_t bytes = static_cast<size_t>(n) * o.c * o.h * o.w * esz;
     if (bytes > pl->buf_bytes[pl->b_dst[i]]) pl->buf_bytes[pl->b_dst[i]] = bytes;
-    if (pl->fuse[i]) {
-      if (swap_a >= 0) {
-        const int t = buf[swap_a];
-        buf[swap_a] = buf[swap_b];
-        buf[swap_b] = t;
-      }
-      ++i;
+    if (swap_a >= 0) {
+      const int t = buf[swap_a];
+      buf[swap_a] = buf[swap_b];
+      buf[swap_b] = t;
     }
+    if (pl->fuse[i]) ++i;
   }
   for (const Shape& s : writes1)
     if (s.c != slots[1].c || s.h != slots[1].h || s.w != slots[1].w)
@@ -266,25 +300,23 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
   void* scratch = pl.scratch_bytes ? static_cast<uint8_t*>(workspace) + pl.scratch_off : nullptr;
   for (int i = 0; i < n_ops; ++i) {
     const pp_net_op& op = ops[i];
-    const Shape& si = pl.in[i];
+    if (i + 1 < n_ops && pl.up_in[i + 1]) continue;   // the upsample runs in the conv after it
+    const Shape& si = pl.up_in[i] ? pl.in[i - 1] : pl.in[i];   // the input as stored
     const Shape& so = pl.out[i];
     void* dst = buf_ptr(pl.b_dst[i]);
     const void* src = buf_ptr(pl.b_src[i]);
     hipError_t e = hipSuccess;
     switch (op.kind) {
-      case PP_OP_CONV_PP:
-        if (pl.fuse[i]) {
-          // conv + the pool / add / shuffle of op i + 1
-          st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags | pl.fuse[i],
-                            scratch, pl.scratch_bytes, stream);
-          if (st != PP_OK) return st;
-          ++i;
-          break;
-        }
-        st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, op.flags, scratch,
-                          pl.scratch_bytes, stream);
+      case PP_OP_CONV_PP: {
+        // with the upsample before it (PP_UPSAMPLE2) and / or the pool, add or
+        // shuffle after it (then op i + 1 is taken too)
+        const uint32_t fl = op.flags | pl.fuse[i] | (pl.up_in[i] ? PP_UPSAMPLE2 : 0u);
+        st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl, scratch, pl.scratch_bytes,
+                          stream);
         if (st != PP_OK) return st;
+        if (pl.fuse[i]) ++i;
         break;
+      }
       case PP_OP_CONV_DENSE:
       case PP_OP_DECONV: {
         DenseParams p;

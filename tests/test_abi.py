@@ -117,7 +117,7 @@ def test_conv_validation_happens_before_any_launch(lib):
     assert _conv(lib, blob, n=0) == pp.PP_EINVAL
     assert _conv(lib, blob, dt=1) == pp.PP_EUNSUPPORTED               # weight dtype != activation dtype
     assert _conv(lib, blob, dt=5) == pp.PP_EINVAL
-    assert _conv(lib, blob, flags=16) == pp.PP_EINVAL                  # unknown flag
+    assert _conv(lib, blob, flags=32) == pp.PP_EINVAL                  # unknown flag
     for f in (pp.PP_MAXPOOL2 | pp.PP_ACCUMULATE, pp.PP_ACCUMULATE | pp.PP_PIXSHUF2, 14):
         assert _conv(lib, blob, flags=f) == pp.PP_EINVAL               # more than one fused op
     assert _conv(lib, _blob(c_out=10), flags=pp.PP_PIXSHUF2) == pp.PP_EINVAL   # c_out % 4 != 0

@@ -333,6 +333,70 @@ def test_fused_add_pixshuf(mode, recipe, ksplit, monkeypatch):
             assert torch.equal(yd.cpu(), want.cpu()), f"recipe {recipe}: fused {mode} differs from the op after the conv"
 
 
+# convolving the nearest x2 upsampling of x, read on the fly (PP_UPSAMPLE2),
+# alone and with a fused epilogue: against the oracle conv of the upsampled
+# input, and bitwise against the same plan run on the upsampled tensor
+UP_RECIPES = [(None, 0), (20, 0), (23, 0), (25, 0), (26, 0), (31, 0), (32, 0), (36, 0), (24, 3), (20, 4)]
+
+
+@pytest.mark.parametrize("recipe,ksplit", UP_RECIPES)
+@pytest.mark.parametrize("mode", ["plain", "add", "maxpool2"])
+def test_fused_upsample(mode, recipe, ksplit, monkeypatch):
+    if recipe is not None:
+        monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    cases = (((1, 1, 1), "f32", (16, 21, 13, 22)), ((1, 1, 1), "f32", (12, 9, 15, 16)),
+             ((2, 1, 1), "f32", (8, 11, 17, 12)), ((1, 2, 2), "f32", (20, 7, 9, 14)),
+             ((1, 1, 1), "bf16", (24, 17, 11, 35)))
+    for (s, p, d), dtype, shape in cases:
+        c_out, c_in, h, w = shape
+        seed = 900 + (recipe or 0)
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        if dtype == "bf16":
+            x = obf16.round_f32(x)
+            w_or = obf16.round_f32(L["w"])
+        else:
+            w_or = L["w"]
+        xu = np.ascontiguousarray(np.repeat(np.repeat(x, 2, axis=2), 2, axis=3))
+        wd = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], s, p, d, wd)
+        ho, wo = pp.out_size(layer.h_blob, 2 * h, 2 * w)
+        _say("fused upsample", mode, "recipe", recipe, "ksplit", ksplit, (s, p, d), dtype, shape)
+        args = (xu, w_or, L["b"], L["pid"], L["conn"], L["lib"])
+        ref = oconv.conv3x3_pruned(*args, s, p, d, True)
+        bound = oconv.conv3x3_bound(*args, s, p, d)
+        xd = _to_dev(x, dtype)
+        kw = dict(relu=True, upsample2=True)
+        if mode == "add":
+            r = workloads.random_input(seed + 1, (2, c_out, ho, wo))
+            r = obf16.round_f32(r) if dtype == "bf16" else r
+            rd = _to_dev(r, dtype)
+            yd = rd.clone()
+            pp.conv2d_fwd(layer, xd, out=yd, accumulate=True, **kw)
+            ref, bound = ref + r.astype(np.float64), bound + np.abs(r.astype(np.float64))
+        elif mode == "maxpool2":
+            yd = pp.conv2d_fwd(layer, xd, maxpool2=True, **kw)
+            ref, bound = oconv.maxpool2(ref), oconv.maxpool2(bound)
+        else:
+            yd = pp.conv2d_fwd(layer, xd, **kw)
+        check(_from_dev(yd), ref, bound, dtype, f"upsample {mode} recipe {recipe} {(s, p, d)} {dtype} {shape}")
+        plan = pp.conv2d_plan(layer.h_blob, 2, 2 * h, 2 * w, wd)
+        # (a pooled call cannot keep a tiling with odd R or CC unless it splits)
+        same = mode != "maxpool2" or ksplit or recipe not in (25, 36)
+        if recipe is not None and same and plan[0] == recipe and (not ksplit or plan[1] == ksplit):
+            y = pp.conv2d_fwd(layer, _to_dev(xu, dtype), relu=True)
+            if mode == "add":
+                want = rd + y
+            elif mode == "maxpool2":
+                want = torch.nn.functional.max_pool2d(y.float(), 2).to(y.dtype)
+            else:
+                want = y
+            torch.cuda.synchronize()
+            assert torch.equal(yd.cpu(), want.cpu()), f"recipe {recipe}: fused upsample ({mode}) differs"
+
+
 def test_fused_flags_rejected():
     # at most one fused op; the shuffle needs c_out % 4 == 0
     L = workloads.random_layer(9, 6, 8, keep=0.5)
