@@ -120,6 +120,48 @@ pp_status pp_pack(const pp_layer_desc* d, const float* w, const float* bias,
                   void* out, size_t* inout_bytes);
 
 /*
+ * Pruning-structure helpers (host-only, pure, deterministic).  ADMM-based
+ * structured pruning (Sec. 2) alternates training with a Euclidean
+ * projection of each layer's weights onto its structure set; these are those
+ * projections, for the structures the paper names, plus the conv + batch
+ * norm fusion of its graph rewrite (Sec. 3).  Sums of squares are taken in
+ * double, in ascending tap (filter) order.  w is fp32 [c_out][c_in][3][3];
+ * channel counts 1..65535.  Errors: PP_EINVAL (NULL pointer, sizes, bad mask,
+ * n_keep out of range, negative or NaN energy).
+ *
+ * pp_project_patterns -- pattern pruning: pattern_id[o][c] (u8) = the library
+ *   pattern with the largest sum of w[o][c][t]^2 over its taps t (ties: the
+ *   lowest index), i.e. the nearest kernel that keeps one pattern's taps;
+ *   kept_energy (double [c_out][c_in], may be NULL) receives that sum.
+ * pp_project_connectivity -- connectivity pruning: conn[o][c] = 1 for the
+ *   n_keep kernels of largest energy[o][c] (e.g. kept_energy above; ties:
+ *   the lower o * c_in + c), else 0.
+ * pp_project_columns -- column pruning (one (input channel, tap) position of
+ *   every filter): keep the n_keep columns with the largest sum over filters
+ *   of w^2 (ties: the lower 9 c + t); col_mask[c] (u16) = 9-bit mask of
+ *   channel c's kept taps.
+ * pp_column_library -- a column-pruned layer in pp_pack's terms: lib_masks
+ *   (capacity 255) = the distinct nonzero channel masks ascending, its count
+ *   in *n_patterns, pattern_id / conn (u8 [c_out][c_in]) = channel c's mask
+ *   and (mask != 0) for every filter.  PP_EUNSUPPORTED: more than 255
+ *   distinct masks.
+ * pp_fold_bn -- fold an inference-mode batch norm that follows a conv into
+ *   it, in place: s = gamma / sqrt(var + eps) per output channel, w[o][*] *=
+ *   s, bias[o] = s (bias[o] - mean[o]) + beta (double, one rounding to fp32);
+ *   w is [c_out][k_elems], bias [c_out] (zeros for a conv without one).
+ *   PP_EINVAL also when var + eps <= 0.
+ */
+pp_status pp_project_patterns(const float* w, int32_t c_out, int32_t c_in, const uint16_t* lib_masks,
+                              int32_t n_patterns, uint8_t* pattern_id, double* kept_energy);
+pp_status pp_project_connectivity(const double* energy, int32_t c_out, int32_t c_in, int64_t n_keep,
+                                  uint8_t* conn);
+pp_status pp_project_columns(const float* w, int32_t c_out, int32_t c_in, int64_t n_keep, uint16_t* col_mask);
+pp_status pp_column_library(const uint16_t* col_mask, int32_t c_out, int32_t c_in, uint16_t* lib_masks,
+                            int32_t* n_patterns, uint8_t* pattern_id, uint8_t* conn);
+pp_status pp_fold_bn(float* w, float* bias, int32_t c_out, int32_t k_elems, const float* gamma,
+                     const float* beta, const float* mean, const float* var, float eps);
+
+/*
  * pp_blob_info -- validate a host copy of a blob and return its description.
  * Any output pointer may be NULL.  Errors: PP_EINVAL (blob NULL), PP_EBLOB
  * (bad magic/version, sizes or offsets inconsistent with `bytes`, woff not

@@ -29,7 +29,9 @@ PP_UPSAMPLE2 = 16
 
 # exported symbols declared in include/pp.h
 SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_workspace", "pp_conv2d_recipe",
-           "pp_conv2d_out_size", "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error")
+           "pp_conv2d_out_size", "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error",
+           "pp_project_patterns", "pp_project_connectivity", "pp_project_columns", "pp_column_library",
+           "pp_fold_bn")
 
 
 class PPError(RuntimeError):
@@ -75,13 +77,18 @@ def load_library(path: str = LIB_PATH):
     lib.pp_net_workspace.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
                                      ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.pp_net_fwd.argtypes = [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp]
+    lib.pp_project_patterns.argtypes = [vp, i32, i32, vp, i32, vp, vp]
+    lib.pp_project_connectivity.argtypes = [vp, i32, i32, ctypes.c_int64, vp]
+    lib.pp_project_columns.argtypes = [vp, i32, i32, ctypes.c_int64, vp]
+    lib.pp_column_library.argtypes = [vp, i32, i32, vp, ctypes.POINTER(i32), vp, vp]
+    lib.pp_fold_bn.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, ctypes.c_float]
     lib.pp_status_str.argtypes = [i32]
     lib.pp_status_str.restype = ctypes.c_char_p
     lib.pp_last_error.argtypes = []
     lib.pp_last_error.restype = ctypes.c_char_p
-    for name in ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_out_size", "pp_net_workspace",
-                 "pp_net_fwd"):
-        getattr(lib, name).restype = i32
+    for name in SYMBOLS:
+        if name not in ("pp_status_str", "pp_last_error"):
+            getattr(lib, name).restype = i32
     _lib = lib
     return lib
 
@@ -117,6 +124,69 @@ def pack(w, b, pattern_id, conn, lib_masks, stride=1, pad=1, dilation=1, wdtype=
     out = np.zeros(n.value, dtype=np.uint8)
     _check(lib.pp_pack(*args, _ptr(out), ctypes.byref(n)), "pp_pack")
     return out
+
+
+# ---------------------------------------------------------------------------
+# pruning-structure helpers (host only)
+# ---------------------------------------------------------------------------
+
+def project_patterns(w, lib_masks):
+    """pp_project_patterns: (pattern_id u8 [c_out][c_in], kept energy float64
+    [c_out][c_in]) of dense 3x3 weights w [c_out][c_in][3][3]."""
+    lib = load_library()
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    masks = np.ascontiguousarray(lib_masks, dtype=np.uint16)
+    c_out, c_in = w.shape[:2]
+    pid = np.zeros((c_out, c_in), np.uint8)
+    e = np.zeros((c_out, c_in), np.float64)
+    _check(lib.pp_project_patterns(_ptr(w), c_out, c_in, _ptr(masks), len(masks), _ptr(pid), _ptr(e)),
+           "pp_project_patterns")
+    return pid, e
+
+
+def project_connectivity(energy, n_keep):
+    """pp_project_connectivity: conn u8 keeping the n_keep largest energies."""
+    lib = load_library()
+    e = np.ascontiguousarray(energy, dtype=np.float64)
+    conn = np.zeros(e.shape, np.uint8)
+    _check(lib.pp_project_connectivity(_ptr(e), e.shape[0], e.shape[1], int(n_keep), _ptr(conn)),
+           "pp_project_connectivity")
+    return conn
+
+
+def project_columns(w, n_keep):
+    """pp_project_columns: u16 [c_in] kept-tap masks of column pruning."""
+    lib = load_library()
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    m = np.zeros(w.shape[1], np.uint16)
+    _check(lib.pp_project_columns(_ptr(w), w.shape[0], w.shape[1], int(n_keep), _ptr(m)), "pp_project_columns")
+    return m
+
+
+def column_library(col_mask, c_out):
+    """pp_column_library: (lib_masks u16[n_p], pattern_id, conn) of a
+    column-pruned layer, ready for pack()."""
+    lib = load_library()
+    m = np.ascontiguousarray(col_mask, dtype=np.uint16)
+    masks = np.zeros(255, np.uint16)
+    n = ctypes.c_int32(0)
+    pid = np.zeros((c_out, len(m)), np.uint8)
+    conn = np.zeros((c_out, len(m)), np.uint8)
+    _check(lib.pp_column_library(_ptr(m), c_out, len(m), _ptr(masks), ctypes.byref(n), _ptr(pid), _ptr(conn)),
+           "pp_column_library")
+    return masks[:n.value].copy(), pid, conn
+
+
+def fold_bn(w, b, gamma, beta, mean, var, eps=1e-5):
+    """pp_fold_bn on copies: (w', b') of a conv followed by an inference-mode
+    batch norm (b None: no conv bias)."""
+    lib = load_library()
+    w = np.array(w, dtype=np.float32, order="C", copy=True)
+    b = np.zeros(w.shape[0], np.float32) if b is None else np.array(b, dtype=np.float32, copy=True)
+    g, bt, mu, v = (np.ascontiguousarray(a, dtype=np.float32) for a in (gamma, beta, mean, var))
+    _check(lib.pp_fold_bn(_ptr(w), _ptr(b), w.shape[0], w[0].size, _ptr(g), _ptr(bt), _ptr(mu), _ptr(v),
+                          float(eps)), "pp_fold_bn")
+    return w, b
 
 
 def blob_info(blob) -> dict:

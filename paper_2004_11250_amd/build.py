@@ -65,10 +65,11 @@ def build(verbose: bool = False) -> str:
 
 
 def build_host() -> str:
-    """The packer and blob validation alone, built with g++ (no HIP)."""
+    """The packer, the pruning projections and blob validation alone, built
+    with g++ (no HIP)."""
     tmp = HOST_LIB + ".tmp"
     _run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", f"-I{INCLUDE}", f"-I{CSRC}",
-          os.path.join(CSRC, "pack.cpp"), "-o", tmp])
+          os.path.join(CSRC, "pack.cpp"), os.path.join(CSRC, "project.cpp"), "-o", tmp])
     os.replace(tmp, HOST_LIB)
     return HOST_LIB
 

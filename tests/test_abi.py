@@ -36,7 +36,8 @@ def test_host_only_library_exports_packer():
     from paper_2004_11250_amd import build
     path = build.build_host()
     h = ctypes.CDLL(path)
-    for name in ("pp_pack", "pp_blob_info", "pp_status_str", "pp_last_error"):
+    for name in ("pp_pack", "pp_blob_info", "pp_status_str", "pp_last_error", "pp_project_patterns",
+                 "pp_project_connectivity", "pp_project_columns", "pp_column_library", "pp_fold_bn"):
         assert hasattr(h, name)
 
 
