@@ -492,10 +492,15 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
       }
       const uint32_t kept = wo >> 24;   // bit s: slot s has a kept kernel
       if (kept == 0) continue;
-      // first weight of the entry, clamped so that every slot's read stays
-      // inside the weight array (plus the >= 32 bytes that follow it)
+      // first weight of the entry.  Canonical library: clamped so that the
+      // unconditional 4-weight read of every slot stays inside the weight
+      // array (plus the >= 32 bytes that follow it); other libraries read
+      // kernel by kernel with clamped reads, and their kernels may hold fewer
+      // than 4 weights, so the entry's own offset is used (a clamp assuming
+      // 4 per kernel would move it)
       const uint32_t nk4 = static_cast<uint32_t>(__builtin_popcount(kept)) * 4u;
-      const uint32_t w0 = min(wo & 0xFFFFFFu, a.n_wt - min(a.n_wt, nk4));
+      const uint32_t w0 = LIB == kLibCanon8 ? min(wo & 0xFFFFFFu, a.n_wt - min(a.n_wt, nk4))
+                                            : min(wo & 0xFFFFFFu, a.n_wt);
       // patch: the lane's input neighbourhood for this channel
       float p[PR][PC];
       load_patch(p, base + (cl0 + k) * CHSTR + lane_off);

@@ -112,6 +112,18 @@ def test_pattern_libraries(libname, dtype):
         check(y, ref, bound, dtype, f"{libname} {dtype} {(s, p, d)}")
 
 
+def test_generic_library_short_patterns():
+    # patterns of 1-3 taps: the last entries of the weight array hold fewer
+    # than 4 weights per kernel (a clamp assuming 4 would read the wrong ones)
+    lib = np.array([0x002, 0x010, 0x030, 0x111, 0x0C0, 0x100], np.uint16)
+    L = workloads.random_layer(91, 24, 9, lib=lib, keep=0.7)
+    x = workloads.random_input(91, (2, 9, 15, 13))
+    for dtype in ("f32", "bf16"):
+        _say("short-pattern library", dtype)
+        y, ref, bound = run_layer(L, x, 1, 1, 1, relu=False, dtype=dtype)
+        check(y, ref, bound, dtype, f"short patterns {dtype}")
+
+
 def test_all_kernels_pruned_gives_relu_bias_exactly():
     L = workloads.random_layer(8, 13, 6)
     L["conn"][:] = 0

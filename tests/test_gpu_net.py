@@ -102,7 +102,10 @@ def teacher_forced(cfg, dtype, n_keep=6):
             # input, then the op (max and x -> x + r are 1-Lipschitz, the
             # shuffle moves data: the pair's bound is the op applied to S,
             # plus |r| for the add)
-            y = _np(_prefix_net(net, i, True).forward(x))[:, :, ::2, ::2]
+            if op["dst"] == 1:
+                y = _np(_prefix_net(net, i, False).forward(x))   # already the output slot
+            else:
+                y = _np(_prefix_net(net, i, True).forward(x))[:, :, ::2, ::2]
             cop, cprm = spec["ops"][i - 1], params[i - 1]
             group = 4 if op["op"] == "pshuf2" else 1
             sop, sprm, sel = _sampled(cop, cprm, n_keep, 1000 * cfg + i, group)
