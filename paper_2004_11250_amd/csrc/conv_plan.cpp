@@ -93,13 +93,15 @@ static long waves_of(int id, const ConvParams& p) {
 // channel split of a wave-pipeline recipe: only for grids of at most one
 // wave per SIMD (1024 waves), up to about 4 waves per SIMD, keeping at least
 // 8 channels per wave (measured on MI355X: splitting grids that already hold
-// 1.5-2 waves per SIMD costs more in partial sums than it gains)
+// 1.5-2 waves per SIMD costs more in partial sums than it gains, except for
+// the 16-wave 1 x 2 tilings on the 14 x 14 layers, where 2 splits of 2048
+// waves beat both no split and the 8-wave tilings split 4 ways)
 static int choose_split(int id, const ConvParams& p) {
   const RecipeInfo r = recipe_info(id);
   const long items = static_cast<long>(p.n) * tiles_of(id, p) * p.n_groups;
   const long waves = items * r.ws;
   int ks = 1;
-  if (waves <= 1024)
+  if (waves <= (r.ws == 16 && r.r == 1 ? 2048 : 1024))
     while (waves * ks * 2 <= 4096 && static_cast<long>(p.c_in) / (ks * 2) >= 8L * r.ws) ks *= 2;
   const int forced = env_int("PP_KSPLIT");
   if (forced >= 1) ks = forced < p.c_in ? forced : p.c_in;
@@ -179,7 +181,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
     } else if (pix >= 20L * 20L) {
       pref[0] = 23; pref[1] = 22; pref[2] = 8; pref[3] = 13;
     } else if (allow_split) {
-      pref[0] = 36; pref[1] = 24; pref[2] = 25; pref[3] = 10;   // 36 / 24 run split 4 ways at 14 x 14
+      pref[0] = 38; pref[1] = 36; pref[2] = 24; pref[3] = 25;   // split 2 / 4 / 4 ways at 14 x 14
     } else {
       pref[0] = 25; pref[1] = 23; pref[2] = 10; pref[3] = 13;
     }

@@ -75,7 +75,9 @@ struct ConvParams {
   X(34, 2, 4, 8, 8, 1)    \
   X(35, 2, 2, 8, 8, 1)    \
   X(36, 1, 2, 8, 8, 1)    \
-  X(37, 4, 4, 8, 2, 0)
+  X(37, 4, 4, 8, 2, 0)    \
+  X(38, 1, 2, 8, 16, 1)   \
+  X(39, 1, 2, 8, 16, 0)
 
 constexpr int kFirstWaveRecipe = 20;
 
@@ -114,7 +116,7 @@ constexpr long wave_lds_floats(int r, int cc, int lw, int ws, int s, int d, int 
   const long xch = static_cast<long>(ws) * 2 * r * cc * 64;
   return ws * ring > xch ? ws * ring : xch;
 }
-constexpr int kNumRecipes = 38;
+constexpr int kNumRecipes = 40;
 
 // pipe: the wave-pipeline kernel reads the next channel from LDS into a
 // second register set while it computes the current one (fp32, canonical

@@ -212,7 +212,7 @@ def test_vgg16_full_size_layer_sampled(idx):
 
 
 # every compiled tiling, forced through the PP_RECIPE override of the planner
-RECIPES = list(range(38))
+RECIPES = list(range(40))
 
 
 @pytest.mark.parametrize("recipe", RECIPES)
