@@ -136,8 +136,9 @@ __global__ __launch_bounds__(256) void dense_conv_vec_kernel(DenseParams p) {
 // way into LDS (exact products, fp32 accumulation, one rounding at the
 // store).
 //
-// Workgroup: 4 waves as WM x (4 / WM), each wave one 32 x 32 block of C, so a
-// tile is BM = 32 WM filters by BN = 32 (4 / WM) pixels.  K advances in steps
+// Workgroup: 4 waves as WM x (4 / WM), each wave TM x TN blocks of 32 x 32
+// of C, so a tile is BM = 32 TM WM filters by BN = 32 TN (4 / WM) pixels
+// (larger tiles load each operand element for more MACs).  K advances in steps
 // of kMK through two LDS buffers: the next step's global loads are in
 // registers while the matrix cores run this one.  LDS is k-major ([k][m],
 // [k][n]): the MFMA operand reads of a wave are lane-consecutive.  Weights
@@ -147,9 +148,9 @@ __global__ __launch_bounds__(256) void dense_conv_vec_kernel(DenseParams p) {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kMK = 32;
 
-template <int MODE, int KD, int WM, class TA>
+template <int MODE, int KD, int WM, int TM, int TN, class TA>
 __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_tiles, int m_tiles) {
-  constexpr int WN = 4 / WM, BM = 32 * WM, BN = 32 * WN;
+  constexpr int WN = 4 / WM, BM = 32 * TM * WM, BN = 32 * TN * WN;
   constexpr int JA = kMK * BM / 256, JB = kMK * BN / 256;   // A / B elements per thread per step
   constexpr int AR = 256 / kMK;                             // A rows per load pass
   constexpr int KK = MODE == 0 ? KD * KD : 4;               // k per input channel
@@ -183,29 +184,53 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
     by = static_cast<int>(q % gh);
     bimg = q / gh;
   }
-  const TA* __restrict__ xi = static_cast<const TA*>(p.x) + static_cast<size_t>(bimg) * p.c_in * p.h * p.w;
+  const TA* __restrict__ x = static_cast<const TA*>(p.x);
+  // this thread's pixel's image, as an element offset into x
+  const uint32_t ximg = static_cast<uint32_t>(bimg) * p.c_in * p.h * p.w;
 
+  // loads through buffer resources (x and the weights, whole: the
+  // descriptors stay wave-uniform): an element outside the layer or the
+  // image gets an offset past the range and reads zero, so the loads need no
+  // branches
+  constexpr uint32_t kOut = 0x80000000u;
+  const size_t x_elems = static_cast<size_t>(p.n) * p.c_in * p.h * p.w;
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<TA*>(x), static_cast<short>(0), static_cast<int>(x_elems * sizeof(TA)), 0x00020000);
+  const size_t n_w = static_cast<size_t>(p.c_out) * p.c_in * (MODE == 0 ? KK : 16);   // the whole weight tensor
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<TA*>(wt), static_cast<short>(0), static_cast<int>(n_w * sizeof(TA)), 0x00020000);
+  // load at byte offset off (bload_b) or element el (bload)
+  auto bload_b = [&](__amdgpu_buffer_rsrc_t r, uint32_t off) __attribute__((always_inline)) {
+    if constexpr (sizeof(TA) == 2)
+      return __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0)) << 16);
+    else
+      return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+  };
+  auto bload = [&](__amdgpu_buffer_rsrc_t r, uint32_t el) __attribute__((always_inline)) {
+    return bload_b(r, el == kOut ? kOut : el * static_cast<uint32_t>(sizeof(TA)));
+  };
   float ra[JA], rb[JB];
-  auto fetch = [&](int k0) __attribute__((always_inline)) {
+  // the general gather: every element's offset from (k, filter / pixel)
+  auto fetch_any = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < JA; ++j) {
       const int kk = k0 + ak, ao = mt * BM + am0 + AR * j;
-      float v = 0.0f;
+      uint32_t el = kOut;
       if (ao < p.c_out && kk < K) {
         if constexpr (MODE == 0) {
-          v = ld(wt, static_cast<size_t>(ao) * K + kk);   // [c_out][c_in][k][k]
+          el = static_cast<uint32_t>(ao) * K + kk;   // [c_out][c_in][k][k]
         } else {
           const int c = kk >> 2, a = (kk >> 1) & 1, b = kk & 1;
           const int ky = 1 - py + 2 * a, kx = 1 - px + 2 * b;
-          v = ld(wt, ((static_cast<size_t>(c) * p.c_out + ao) * 4 + ky) * 4 + kx);   // [c_in][c_out][4][4]
+          el = ((static_cast<uint32_t>(c) * p.c_out + ao) * 4 + ky) * 4 + kx;   // [c_in][c_out][4][4]
         }
       }
-      ra[j] = v;
+      ra[j] = bload(wr, el);
     }
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
       const int kk = k0 + bk0 + j;
-      float v = 0.0f;
+      uint32_t el = kOut;
       if (bvalid && kk < K) {
         int c, iy, ix;
         if constexpr (MODE == 0) {
@@ -218,10 +243,68 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
           iy = by + py - ((kk >> 1) & 1);
           ix = bx + px - (kk & 1);
         }
-        if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) v = ld(xi, (static_cast<size_t>(c) * p.h + iy) * p.w + ix);
+        if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) el = ximg + (static_cast<uint32_t>(c) * p.h + iy) * p.w + ix;
       }
-      rb[j] = v;
+      rb[j] = bload(xr, el);
     }
+  };
+  // The transposed conv and the 1 x 1 conv: from one K step to the next a
+  // thread's elements move by one fixed stride, the same for every lane (the
+  // next kMK / 4 input channels, or the next kMK), so their offsets are taken
+  // once and each full K step moves the descriptors' bases instead; a
+  // partial last K step takes the general gather (past the last input
+  // channel lies the next image, or the next filter's weights).
+  constexpr bool STEPPED = MODE == 1 || KD == 1;
+  constexpr uint32_t kES = static_cast<uint32_t>(sizeof(TA));
+  uint32_t aoff[STEPPED ? JA : 1], boff[STEPPED ? JB : 1];
+  if constexpr (STEPPED) {
+#pragma unroll
+    for (int j = 0; j < JA; ++j) {
+      const int ao = mt * BM + am0 + AR * j;
+      uint32_t el = kOut;
+      if (ao < p.c_out) {
+        if constexpr (MODE == 0) {
+          el = static_cast<uint32_t>(ao) * K + ak;
+        } else {
+          const int c = ak >> 2, ky = 1 - py + 2 * ((ak >> 1) & 1), kx = 1 - px + 2 * (ak & 1);
+          el = ((static_cast<uint32_t>(c) * p.c_out + ao) * 4 + ky) * 4 + kx;
+        }
+      }
+      aoff[j] = el == kOut ? kOut : el * kES;
+    }
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int kk = bk0 + j;
+      uint32_t el = kOut;
+      if (bvalid) {
+        const int c = MODE == 0 ? kk : kk >> 2;
+        const int iy = MODE == 0 ? by : by + py - ((kk >> 1) & 1);
+        const int ix = MODE == 0 ? bx : bx + px - (kk & 1);
+        if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) el = ximg + (static_cast<uint32_t>(c) * p.h + iy) * p.w + ix;
+      }
+      boff[j] = el == kOut ? kOut : el * kES;
+    }
+  }
+  const size_t a_step = MODE == 0 ? kMK : static_cast<size_t>(kMK / 4) * p.c_out * 16;      // elements per K step
+  const size_t b_step = static_cast<size_t>(MODE == 0 ? kMK : kMK / 4) * p.h * p.w;
+  auto fetch = [&](int s) __attribute__((always_inline)) {
+    const int k0 = s * kMK;
+    if constexpr (STEPPED) {
+      if (k0 + kMK <= K) {
+        const size_t ao0 = s * a_step, bo0 = s * b_step;
+        const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<TA*>(wt + ao0), static_cast<short>(0), static_cast<int>((n_w - min(n_w, ao0)) * kES), 0x00020000);
+        const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<TA*>(x + bo0), static_cast<short>(0), static_cast<int>((x_elems - min(x_elems, bo0)) * kES),
+            0x00020000);
+#pragma unroll
+        for (int j = 0; j < JA; ++j) ra[j] = bload_b(wrs, aoff[j]);
+#pragma unroll
+        for (int j = 0; j < JB; ++j) rb[j] = bload_b(xrs, boff[j]);
+        return;
+      }
+    }
+    fetch_any(k0);
   };
   auto put = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -230,42 +313,66 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
     for (int j = 0; j < JB; ++j) Bs[buf][bk0 + j][bn] = rb[j];
   };
 
-  f32x16 acc = {};
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
   const int steps = (K + kMK - 1) / kMK;
   fetch(0);
   put(0);
   __syncthreads();
   for (int s = 0; s < steps; ++s) {
     const int buf = s & 1;
-    if (s + 1 < steps) fetch((s + 1) * kMK);
+    if (s + 1 < steps) fetch(s + 1);
+    // a 32 x 32 x 2 step takes A[l % 32][l / 32] and B[l / 32][l % 32] in
+    // lane l; the operands of half a K step are read before its MFMAs (they
+    // arrive in order, so each MFMA waits only for its own)
 #pragma unroll
-    for (int k2 = 0; k2 < kMK; k2 += 2) {
-      // operands of a 32 x 32 x 2 step: lane l holds A[l % 32][l / 32] and B[l / 32][l % 32]
-      const float a = As[buf][k2 + (lane >> 5)][wm * 32 + (lane & 31)];
-      const float b = Bs[buf][k2 + (lane >> 5)][wn * 32 + (lane & 31)];
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+    for (int h = 0; h < kMK; h += kMK / 2) {
+      float av[kMK / 4][TM], bv[kMK / 4][TN];
+#pragma unroll
+      for (int k2 = 0; k2 < kMK / 2; k2 += 2) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) av[k2 / 2][i] = As[buf][h + k2 + (lane >> 5)][(wm * TM + i) * 32 + (lane & 31)];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bv[k2 / 2][j] = Bs[buf][h + k2 + (lane >> 5)][(wn * TN + j) * 32 + (lane & 31)];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int k2 = 0; k2 < kMK / 4; ++k2)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[k2][i], bv[k2][j], acc[i][j], 0, 0, 0);
     }
     if (s + 1 < steps) put(buf ^ 1);   // that buffer's last readers passed the barrier below one step ago
     __syncthreads();
   }
 
-  // accumulator i of lane l is C[8 (i / 4) + 4 (l / 32) + i % 4][l % 32]
-  const long gp = static_cast<long>(nt) * BN + wn * 32 + (lane & 31);
-  if (gp >= np) return;
-  const int ex = static_cast<int>(gp % gw);
-  const long q = gp / gw;
-  const int ey = static_cast<int>(q % gh);
-  const long eimg = q / gh;
-  const int oy = MODE == 0 ? ey : 2 * ey + py, ox = MODE == 0 ? ex : 2 * ex + px;
-  TA* __restrict__ y = static_cast<TA*>(p.y) + static_cast<size_t>(eimg) * p.c_out * p.ho * p.wo;
+  // accumulator r of block (i, j), lane l, is C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] of the block
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int o = mt * BM + wm * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-    if (o < p.c_out) {
-      float v = acc[i] + (p.bias ? p.bias[o] : 0.0f);
-      if (p.relu) v = fmaxf(v, 0.0f);
-      st(y, (static_cast<size_t>(o) * p.ho + oy) * p.wo + ox, v);
-    }
+  for (int j = 0; j < TN; ++j) {
+    const long gp = static_cast<long>(nt) * BN + (wn * TN + j) * 32 + (lane & 31);
+    if (gp >= np) continue;
+    const int ex = static_cast<int>(gp % gw);
+    const long q = gp / gw;
+    const int ey = static_cast<int>(q % gh);
+    const long eimg = q / gh;
+    const int oy = MODE == 0 ? ey : 2 * ey + py, ox = MODE == 0 ? ex : 2 * ex + px;
+    TA* __restrict__ y = static_cast<TA*>(p.y) + static_cast<size_t>(eimg) * p.c_out * p.ho * p.wo;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int o = mt * BM + (wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (o < p.c_out) {
+          float v = acc[i][j][r] + (p.bias ? p.bias[o] : 0.0f);
+          if (p.relu) v = fmaxf(v, 0.0f);
+          st(y, (static_cast<size_t>(o) * p.ho + oy) * p.wo + ox, v);
+        }
+      }
   }
 }
 
@@ -274,19 +381,31 @@ hipError_t launch_mfma(const DenseParams& p, hipStream_t st) {
   const int gh = MODE == 0 ? p.ho : p.h, gw = MODE == 0 ? p.wo : p.w;
   const long np = static_cast<long>(p.n) * gh * gw;
   const int classes = MODE == 0 ? 1 : 4;
-  // few filters: 32 filters x 128 pixels per workgroup, else 64 x 64
-  const bool narrow = p.c_out <= 32;
-  const int bm = narrow ? 32 : 64, bn = narrow ? 128 : 64;
+  // x and the weights are addressed with 32-bit byte offsets below 2^31 (the
+  // offset 2^31 marks an element outside the layer)
+  const size_t n_w = static_cast<size_t>(p.c_out) * p.c_in * (MODE == 0 ? KD * KD : 16);
+  if (static_cast<size_t>(p.n) * p.c_in * p.h * p.w * sizeof(TA) >= (size_t{1} << 31) ||
+      n_w * sizeof(TA) >= (size_t{1} << 31))
+    return hipErrorInvalidValue;
+  // tiles: 32 filters x 128 pixels (at most 32 filters), 128 x 128 (128+
+  // filters, a reduction of 512+ and at least two such tiles per compute
+  // unit), else 64 x 64 (timed on the colourization 4 x 4 transposed conv
+  // 512 -> 256 and 1 x 1 conv 256 -> 313)
+  const long big = (np + 127) / 128 * ((p.c_out + 127) / 128) * classes;
+  const long k_len = static_cast<long>(p.c_in) * (MODE == 0 ? KD * KD : 4);
+  const int shape = p.c_out <= 32 ? 0 : (p.c_out >= 128 && k_len >= 512 && big >= 512 ? 2 : 1);
+  const int bm = shape == 0 ? 32 : (shape == 2 ? 128 : 64), bn = shape == 0 ? 128 : (shape == 2 ? 128 : 64);
   const long n_tiles = (np + bn - 1) / bn, m_tiles = (p.c_out + bm - 1) / bm;
   const long blocks = n_tiles * m_tiles * classes;
   if (blocks < 1 || blocks > 0x7FFFFFFFL) return hipErrorInvalidConfiguration;
   const dim3 grid(static_cast<uint32_t>(blocks));
-  if (narrow)
-    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 1, TA>), grid, dim3(256), 0, st, p, static_cast<int>(n_tiles),
-                       static_cast<int>(m_tiles));
+  const int nt = static_cast<int>(n_tiles), mt = static_cast<int>(m_tiles);
+  if (shape == 0)
+    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 1, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
+  else if (shape == 2)
+    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 2, 2, TA>), grid, dim3(256), 0, st, p, nt, mt);
   else
-    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, TA>), grid, dim3(256), 0, st, p, static_cast<int>(n_tiles),
-                       static_cast<int>(m_tiles));
+    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
   return hipGetLastError();
 }
 

@@ -88,3 +88,36 @@ def test_transposed_conv(case, dtype):
     y, ref, bound = _run(op, prm, x, dtype)
     assert y.shape == (n, c_out, 2 * h, 2 * w)
     check(y, ref, bound, dtype, f"deconv {case} {dtype}")
+
+
+# large layers take the 128 x 128 tiles (128+ filters and 128K+ output
+# pixels): checked on a sample of output channels (the oracle on the
+# matching slices of the weights)
+BIG_CASES = [  # (op, c_in, c_out, n, h, w)
+    ("conv", 64, 313, 2, 128, 128),
+    ("deconv", 24, 160, 2, 128, 128),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", BIG_CASES)
+def test_large_dense_layers_sampled(case, dtype):
+    kind, c_in, c_out, n, h, w = case
+    rng = np.random.default_rng(c_out + c_in)
+    k = 1 if kind == "conv" else 4
+    shape = (c_out, c_in, k, k) if kind == "conv" else (c_in, c_out, 4, 4)
+    prm = dict(w=rng.normal(0, np.sqrt(2.0 / (c_in * k * k)), shape).astype(np.float32),
+               b=rng.normal(0, 0.1, c_out).astype(np.float32))
+    op = dict(op=kind, c_in=c_in, c_out=c_out, k=k, stride=1 if kind == "conv" else 2, pad=0 if k == 1 else 1,
+              dil=1, relu=True)
+    x = rng.uniform(-1, 1, (n, c_in, h, w)).astype(np.float32)
+    xs = obf16.round_f32(x) if dtype == "bf16" else x
+    print("large", case, dtype, flush=True)
+    net = pp.Net([dict(op, src=0, dst=1)], [prm], dtype)
+    xd = torch.from_numpy(xs).cuda()
+    y = net.forward((xd.to(torch.bfloat16) if dtype == "bf16" else xd).contiguous())
+    torch.cuda.synchronize()
+    sel = np.sort(rng.choice(c_out, size=5, replace=False))
+    sub = dict(prm, b=prm["b"][sel], w=prm["w"][sel] if kind == "conv" else prm["w"][:, sel])
+    ref, bound = onet.run_op(dict(op, c_out=len(sel)), sub, xs, None, dtype)
+    check(y[:, sel].float().cpu().numpy(), ref, bound, dtype, f"large {case} {dtype}")
