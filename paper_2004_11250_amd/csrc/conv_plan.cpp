@@ -200,6 +200,18 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
     } else {
       pref[0] = 33; pref[1] = 20; pref[2] = 31; pref[3] = 13;
     }
+  } else if (wave_ok && bf16 && lib == kLibCanon8 && p.stride == 1 && p.n == 1 && pix < 80L * 80L) {
+    // bf16, one image, small maps (timed on the VGG-16 layer shapes): the
+    // stride-1 fp32 choices without register pipelining
+    if (pix >= 40L * 40L) {
+      pref[0] = 27; pref[1] = 22; pref[2] = 23; pref[3] = 13;
+    } else if (pix >= 20L * 20L) {
+      pref[0] = 23; pref[1] = 22; pref[2] = 21; pref[3] = 13;
+    } else if (allow_split) {
+      pref[0] = 39; pref[1] = 24; pref[2] = 23; pref[3] = 13;   // split 2 / 4 / 4 ways at 14 x 14
+    } else {
+      pref[0] = 25; pref[1] = 23; pref[2] = 22; pref[3] = 13;
+    }
   } else if (wave_ok) {
     // bf16, and the all-ones library (timed on the super-resolution and
     // colourization layer shapes): 2 x 4 outputs per lane; two channel
