@@ -136,8 +136,8 @@ def teacher_forced(cfg, dtype, n_keep=6):
     return worst
 
 
-@pytest.mark.parametrize("cfg,dtype", [(1, "f32"), (2, "f32"), (3, "f32"), (4, "f32"), (4, "bf16"), (5, "f32"),
-                                       (5, "bf16")])
+@pytest.mark.parametrize("cfg,dtype", [(1, "f32"), (2, "f32"), (2, "bf16"), (3, "f32"), (4, "f32"), (4, "bf16"),
+                                       (5, "f32"), (5, "bf16")])
 def test_network_teacher_forced(cfg, dtype):
     worst = teacher_forced(cfg, dtype)
     _say(f"cfg {cfg} {dtype}: worst |err|/S = {worst:.3e}")
