@@ -31,8 +31,10 @@
 #ifndef PP_H_
 #define PP_H_
 
+#ifndef __HIPCC_RTC__   /* the run-time compiler provides these itself */
 #include <stddef.h>
 #include <stdint.h>
+#endif
 
 #ifdef __cplusplus
 extern "C" {
@@ -245,6 +247,25 @@ pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, int32_t n, 
 pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
                            int32_t act_dtype, int32_t with_workspace, int32_t* recipe,
                            int32_t* ksplit);
+
+/*
+ * pp_jit_library -- compile (on the host, with the device compiler at run
+ * time: seconds) the wave-pipeline kernels specialised for this layer's own
+ * pattern library, for the plans pp_conv2d_fwd makes for this input (n, h,
+ * w, act_dtype; with a pp_conv2d_workspace()-sized workspace when
+ * with_workspace != 0, and without), and load them on the current device.
+ * From then on pp_conv2d_fwd and pp_net_fwd (unfused convs) run such a
+ * layer with them, as fast as the canonical library, instead of the generic
+ * kernel that tests taps against run-time masks (the per-layer code
+ * generation of the paper's compiler, Sec. 3); pp_conv2d_recipe reports
+ * their tiling.  For libraries of up to 8 patterns of exactly 4 taps other
+ * than the canonical one, with pad = dilation.  Idempotent and thread-safe;
+ * the kernels stay loaded until the process ends.  Errors: as
+ * pp_conv2d_out_size, PP_EUNSUPPORTED (library or layer not of that form),
+ * PP_EHIP (compilation or loading failed; pp_last_error starts the log).
+ */
+pp_status pp_jit_library(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
+                         int32_t act_dtype, int32_t with_workspace);
 
 /* pp_conv2d_out_size -- h_out, w_out of a packed layer for an h x w input. */
 pp_status pp_conv2d_out_size(const void* h_blob, size_t blob_bytes, int32_t h, int32_t w,

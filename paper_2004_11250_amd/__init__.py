@@ -31,7 +31,7 @@ PP_UPSAMPLE2 = 16
 SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_workspace", "pp_conv2d_recipe",
            "pp_conv2d_out_size", "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error",
            "pp_project_patterns", "pp_project_connectivity", "pp_project_columns", "pp_column_library",
-           "pp_fold_bn")
+           "pp_fold_bn", "pp_jit_library")
 
 
 class PPError(RuntimeError):
@@ -77,6 +77,7 @@ def load_library(path: str = LIB_PATH):
     lib.pp_net_workspace.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
                                      ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.pp_net_fwd.argtypes = [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp]
+    lib.pp_jit_library.argtypes = [vp, sz, i32, i32, i32, i32, i32]
     lib.pp_project_patterns.argtypes = [vp, i32, i32, vp, i32, vp, vp]
     lib.pp_project_connectivity.argtypes = [vp, i32, i32, ctypes.c_int64, vp]
     lib.pp_project_columns.argtypes = [vp, i32, i32, ctypes.c_int64, vp]
@@ -223,6 +224,15 @@ def conv2d_plan(blob, n, h, w, act_dtype=PP_F32, with_workspace=True):
 def conv2d_recipe(blob, n, h, w, act_dtype=PP_F32, with_workspace=True) -> int:
     """Tiling id that pp_conv2d_fwd uses for this layer and input shape."""
     return conv2d_plan(blob, n, h, w, act_dtype, with_workspace)[0]
+
+
+def jit_library(blob, n, h, w, act_dtype=PP_F32, with_workspace=True) -> None:
+    """pp_jit_library: compile and load the kernels specialised for this
+    layer's own 4-tap pattern library (seconds; once per process)."""
+    lib = load_library()
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    _check(lib.pp_jit_library(_ptr(blob), blob.nbytes, n, h, w, act_dtype, 1 if with_workspace else 0),
+           "pp_jit_library")
 
 
 def conv2d_workspace(blob, n, h, w, act_dtype=PP_F32) -> int:

@@ -95,13 +95,29 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   p.flags = flags;
   const int lib = library_kind(v);
   const bool bf = act_dtype == PP_BF16;
-  ConvPlan plan = plan_conv(p, lib, bf, scratch != nullptr);
-  if (plan.ksplit > 1) {
-    if (split_bytes(plan, p) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
-      plan = plan_conv(p, lib, bf, false);   // not enough scratch: no split
-    else
-      p.part = static_cast<float*>(scratch);
+  // the plan for library kind `kind`; a split only with enough scratch
+  auto make_plan = [&](int kind, ConvParams* pp_) {
+    ConvPlan pl = plan_conv(*pp_, kind, bf, scratch != nullptr);
+    if (pl.ksplit > 1) {
+      if (split_bytes(pl, *pp_) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
+        pl = plan_conv(*pp_, kind, bf, false);   // not enough scratch: no split
+      else
+        pp_->part = static_cast<float*>(scratch);
+    }
+    return pl;
+  };
+  if (lib == kLibGeneric && jit_library4(v)) {
+    // a 4-tap library with run-time compiled kernels (pp_jit_library): as
+    // the canonical library's plan
+    ConvParams jp = p;
+    const ConvPlan pl = make_plan(kLibCanon8, &jp);
+    hipError_t e = hipSuccess;
+    if (pl.recipe >= 0 && jit_launch(v, pl, jp, bf, st, &e)) {
+      if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
+      return PP_OK;
+    }
   }
+  ConvPlan plan = make_plan(lib, &p);
   if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the upsampling / max pool / accumulation / pixel shuffle for this layer");
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
@@ -183,9 +199,39 @@ extern "C" pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int
   s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
   if (s != PP_OK) return s;
   const ConvParams p = layer_params(v, n, h, w, ho, wo);
-  const ConvPlan plan = plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_workspace != 0);
+  ConvPlan plan = plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_workspace != 0);
+  if (library_kind(v) == kLibGeneric && jit_library4(v)) {
+    // with run-time compiled kernels the call runs the canonical library's plan
+    const ConvPlan cp = plan_conv(p, kLibCanon8, act_dtype == PP_BF16, with_workspace != 0);
+    if (cp.recipe >= 0 && jit_ready(v, cp, act_dtype == PP_BF16)) plan = cp;
+  }
   *recipe = plan.recipe;
   if (ksplit) *ksplit = plan.ksplit;
+  return PP_OK;
+}
+
+extern "C" pp_status pp_jit_library(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,
+                                    int32_t act_dtype, int32_t with_workspace) {
+  clear_error();
+  BlobView v;
+  pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
+  if (s != PP_OK) return s;
+  int ho = 0, wo = 0;
+  s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
+  if (s != PP_OK) return s;
+  if (!jit_library4(v))
+    return fail(PP_EUNSUPPORTED, "run-time kernels are for libraries of up to 8 four-tap patterns other than the "
+                                 "canonical one");
+  if (v.pad != v.dil) return fail(PP_EUNSUPPORTED, "run-time kernels need pad = dilation");
+  const ConvParams p = layer_params(v, n, h, w, ho, wo);
+  const bool bf = act_dtype == PP_BF16;
+  // the plans pp_conv2d_fwd can make: with the workspace's split, and without
+  for (bool split : {with_workspace != 0, false}) {
+    const ConvPlan plan = plan_conv(p, kLibCanon8, bf, split);
+    if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling runs this layer");
+    s = jit_prepare(v, plan, bf);
+    if (s != PP_OK) return s;
+  }
   return PP_OK;
 }
 
@@ -200,6 +246,12 @@ extern "C" pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, 
   s = conv_check(v, n, h, w, act_dtype, &ho, &wo);
   if (s != PP_OK) return s;
   *bytes = conv_scratch_bytes(v, n, h, w, act_dtype);
+  if (library_kind(v) == kLibGeneric && jit_library4(v)) {
+    // enough for the canonical plan that run-time compiled kernels run
+    const ConvParams p = layer_params(v, n, h, w, ho, wo);
+    const size_t b = split_bytes(plan_conv(p, kLibCanon8, act_dtype == PP_BF16, true), p);
+    if (b > *bytes) *bytes = b;
+  }
   return PP_OK;
 }
 

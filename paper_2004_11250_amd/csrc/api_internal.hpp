@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include "conv_pp.hpp"
 #include "ppk1.hpp"
 
 namespace pp {
@@ -26,6 +27,15 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
 // PP_UPSAMPLE2 the upsampled size)
 bool conv_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
                   bool with_scratch);
+
+// run-time specialised kernels (jit.cpp): whether the layer's library is
+// one of up to 8 four-tap patterns other than the canonical one; compile the
+// kernel(s) of a plan (made as for the canonical library) for the current
+// device; launch them if compiled (false: not compiled, nothing launched)
+bool jit_library4(const BlobView& v);
+pp_status jit_prepare(const BlobView& v, const ConvPlan& plan, bool bf16);
+bool jit_ready(const BlobView& v, const ConvPlan& plan, bool bf16);
+bool jit_launch(const BlobView& v, const ConvPlan& plan, ConvParams p, bool bf16, hipStream_t st, hipError_t* err);
 
 // scratch bytes pp_conv2d_fwd can use for this layer and input (0: none)
 size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype);

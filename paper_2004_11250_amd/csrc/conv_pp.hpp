@@ -1,9 +1,11 @@
 // conv_pp.hpp -- launch interface of the pruned 3x3 convolution kernels.
 #pragma once
 
+#ifndef __HIPCC_RTC__   // (the run-time compiler, which provides these itself)
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#endif
 
 #include "pp.h"
 
@@ -125,6 +127,7 @@ struct RecipeInfo {
   int r, cc, lw, wf, ws, cpw, pipe;
 };
 
+#ifndef __HIPCC_RTC__   // host side
 // geometry of a recipe, and whether its LDS footprint fits for (stride, dilation)
 RecipeInfo recipe_info(int id);
 bool recipe_fits(int id, int stride, int dil, bool bf16, int lib);
@@ -153,5 +156,7 @@ hipError_t launch_recipe(int id, const ConvParams& p, hipStream_t st);
 // wave-pipeline kernel, canonical (kLibCanon8) and all-ones (kLibDense9) libraries
 template <int LIB, int S, int D, class TA>
 hipError_t launch_wave_recipe(int id, const ConvParams& p, hipStream_t st);
+
+#endif
 
 }  // namespace pp

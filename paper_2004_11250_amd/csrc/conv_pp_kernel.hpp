@@ -28,9 +28,11 @@
 //     deterministic.
 #pragma once
 
+#ifndef __HIPCC_RTC__   // (the run-time compiler, which provides these itself)
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#endif
 
 #include "conv_pp.hpp"
 
@@ -84,7 +86,15 @@ __device__ __forceinline__ uint32_t lds_addr(T* p) {
 }
 __device__ __forceinline__ lds_void_ptr lds_ptr(uint32_t a) { return (lds_void_ptr)(uintptr_t)a; }
 
+// The compile-time 8-entry library of 4-tap patterns behind the "canonical"
+// kernels: the canonical library (0x03A, ...), or, in a module compiled at
+// run time for a layer's own 4-tap library (PP_JIT_LIBRARY, up to 8 masks,
+// padded with the last one), that library.
+#ifdef PP_JIT_LIBRARY
+constexpr uint32_t kCanon8[8] = {PP_JIT_LIBRARY};
+#else
 constexpr uint32_t kCanon8[8] = {0x03A, 0x0B2, 0x0B8, 0x09A, 0x01B, 0x036, 0x0D8, 0x1B0};
+#endif
 
 constexpr int nth_tap(uint32_t mask, int n) {
   for (int t = 0; t < 9; ++t)
@@ -703,6 +713,7 @@ __global__ __launch_bounds__(WF* WS * 64) void pp_conv3x3_kernel(ConvParams a) {
   }
 }
 
+#ifndef __HIPCC_RTC__   // host side
 // ---------------------------------------------------------------------------
 // host side: one tiling = one Recipe; launch helpers
 // ---------------------------------------------------------------------------
@@ -722,6 +733,8 @@ hipError_t launch_tiling(ConvParams p, hipStream_t st) {
     return hipGetLastError();
   }
 }
+
+#endif
 
 }  // namespace kern
 }  // namespace pp

@@ -103,16 +103,41 @@ __device__ __forceinline__ u32x4 make_rsrc(const void* base, uint32_t bytes) {
 __device__ __forceinline__ void set_m0(uint32_t v) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" :: "s"(v) : "memory", "m0");
 }
+// The descriptor is wave-uniform.  The run-time compiler can be an older
+// one (a host process may have loaded its own copy first) that does not
+// always prove it and then hands the asm VGPRs; a descriptor rebuilt from
+// read-first-lanes keeps it in SGPRs.  A VMEM instruction needs 5 wait states
+// after a VALU write of its SGPRs, and the compiler does not see that the
+// asm is one, so the asm waits itself (PP_DMA_WAIT).
+#ifdef __HIPCC_RTC__
+#define PP_DMA_WAIT "s_nop 4\n\t"
+#else
+#define PP_DMA_WAIT ""
+#endif
+__device__ __forceinline__ u32x4 uniform_rsrc(u32x4 r) {
+#ifdef __HIPCC_RTC__
+  u32x4 u;
+  u.x = __builtin_amdgcn_readfirstlane(r.x);
+  u.y = __builtin_amdgcn_readfirstlane(r.y);
+  u.z = __builtin_amdgcn_readfirstlane(r.z);
+  u.w = __builtin_amdgcn_readfirstlane(r.w);
+  return u;
+#else
+  return r;
+#endif
+}
 // global -> LDS DMA of 16 (4) bytes per lane with immediate offset OFF: it
 // moves both the global offset and the LDS address, so lane l's data lands
 // at LDS byte M0 + OFF + 16 l (4 l) and comes from offset voff + OFF
 template <uint32_t OFF>
 __device__ __forceinline__ void dma_lds_b128_at(u32x4 rsrc, uint32_t voff) {
-  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds" :: "v"(voff), "s"(rsrc), "n"(OFF) : "memory");
+  asm volatile(PP_DMA_WAIT "buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds" :: "v"(voff), "s"(uniform_rsrc(rsrc)),
+               "n"(OFF) : "memory");
 }
 template <uint32_t OFF>
 __device__ __forceinline__ void dma_lds_b32_at(u32x4 rsrc, uint32_t voff) {
-  asm volatile("buffer_load_dword %0, %1, 0 offen offset:%2 lds" :: "v"(voff), "s"(rsrc), "n"(OFF) : "memory");
+  asm volatile(PP_DMA_WAIT "buffer_load_dword %0, %1, 0 offen offset:%2 lds" :: "v"(voff), "s"(uniform_rsrc(rsrc)),
+               "n"(OFF) : "memory");
 }
 
 #pragma clang diagnostic pop
@@ -938,6 +963,7 @@ __global__ __launch_bounds__(256) void pp_split_reduce_kernel(ConvParams a) {
   }
 }
 
+#ifndef __HIPCC_RTC__   // host side
 template <int LIB, int S, int D, int R, int CC, int LW, int WS, bool PIPE, class TA>
 hipError_t launch_wave_tiling(ConvParams p, hipStream_t st) {
   using G = WGeo<LIB, S, D, R, CC, LW, WS, sizeof(TA) == 2, PIPE>;
@@ -961,6 +987,8 @@ hipError_t launch_wave_tiling(ConvParams p, hipStream_t st) {
     return hipGetLastError();
   }
 }
+
+#endif
 
 }  // namespace kern
 }  // namespace pp
