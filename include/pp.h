@@ -210,8 +210,11 @@ pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
  *                       aligned.  With pp_conv2d_workspace() bytes the
  *                       kernel may split the input channels over more
  *                       workgroups (grids that underfill the GPU); partial
- *                       sums go there and a second kernel adds them.  Calls
- *                       sharing one workspace must be ordered (same stream).
+ *                       sums go there and a second kernel adds them.  A
+ *                       bf16 layer may instead run on the matrix cores
+ *                       (pp_conv2d_recipe id 64): its weights are expanded
+ *                       to a dense matrix there first.  Calls sharing one
+ *                       workspace must be ordered (same stream).
  * Output channels are in the original filter order.  Accumulation is fp32
  * in a fixed order, so repeated calls with the same workspace size give
  * bitwise-identical results.
@@ -238,10 +241,12 @@ pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, int32_t n, 
  * pp_conv2d_recipe -- the GPU tiling ("recipe" id) and the channel split
  * pp_conv2d_fwd uses for this layer, batch and input size, with
  * (with_workspace != 0) or without a pp_conv2d_workspace()-sized workspace.
- * Informational: lets callers and tests see which compiled kernel runs.  The
- * environment variables PP_RECIPE=<id> and PP_KSPLIT=<k> force a tiling
- * (when it can run the layer) and a split; otherwise the planner's choice is
- * reported.  ksplit may be NULL.  Host-only.  Errors: as pp_conv2d_out_size,
+ * Informational: lets callers and tests see which compiled kernel runs: ids
+ * below 40 are vector-ALU tilings, 64 the bf16 matrix-core form (the layer as
+ * a zero-filled dense contraction on the matrix cores; needs the workspace,
+ * c_in a multiple of 32 and no fused max pool).  The environment variables
+ * PP_RECIPE=<id> and PP_KSPLIT=<k> force a tiling (when it can run the layer)
+ * and a split; otherwise the planner's choice is reported.  ksplit may be NULL.  Host-only.  Errors: as pp_conv2d_out_size,
  * PP_EINVAL (recipe NULL, act_dtype), PP_EUNSUPPORTED.
  */
 pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int32_t n, int32_t h, int32_t w,

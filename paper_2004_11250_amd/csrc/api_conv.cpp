@@ -98,7 +98,7 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   // the plan for library kind `kind`; a split only with enough scratch
   auto make_plan = [&](int kind, ConvParams* pp_) {
     ConvPlan pl = plan_conv(*pp_, kind, bf, scratch != nullptr);
-    if (pl.ksplit > 1) {
+    if (split_bytes(pl, *pp_) > 0) {
       if (split_bytes(pl, *pp_) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
         pl = plan_conv(*pp_, kind, bf, false);   // not enough scratch: no split
       else
@@ -112,7 +112,7 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
     ConvParams jp = p;
     const ConvPlan pl = make_plan(kLibCanon8, &jp);
     hipError_t e = hipSuccess;
-    if (pl.recipe >= 0 && jit_launch(v, pl, jp, bf, st, &e)) {
+    if (pl.recipe >= kFirstWaveRecipe && pl.recipe < kNumRecipes && jit_launch(v, pl, jp, bf, st, &e)) {
       if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
       return PP_OK;
     }
@@ -229,6 +229,7 @@ extern "C" pp_status pp_jit_library(const void* h_blob, size_t blob_bytes, int32
   for (bool split : {with_workspace != 0, false}) {
     const ConvPlan plan = plan_conv(p, kLibCanon8, bf, split);
     if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling runs this layer");
+    if (plan.recipe == kRecipeMfma) continue;   // the matrix-core form reads any library from the blob
     s = jit_prepare(v, plan, bf);
     if (s != PP_OK) return s;
   }

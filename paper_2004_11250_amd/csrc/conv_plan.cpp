@@ -1,5 +1,7 @@
 // conv_plan.cpp -- choice of tiling ("recipe") for a pruned 3x3 layer and
 // dispatch to the compiled kernels.
+#include <algorithm>
+#include <cmath>
 #include <cstdlib>
 
 #include "conv_pp.hpp"
@@ -116,6 +118,7 @@ static ConvPlan finish_plan(int id, const ConvParams& p, bool allow_split) {
 }
 
 size_t split_bytes(const ConvPlan& plan, const ConvParams& p) {
+  if (plan.recipe == kRecipeMfma) return mfma_bytes(p);
   if (plan.ksplit <= 1) return 0;
   const RecipeInfo r = recipe_info(plan.recipe);
   const size_t items = static_cast<size_t>(p.n) * tiles_of(plan.recipe, p) * p.n_groups;
@@ -129,6 +132,27 @@ size_t split_bytes(const ConvPlan& plan, const ConvParams& p) {
 static bool pool_fits(int id) {
   const RecipeInfo r = recipe_info(id);
   return is_wave_recipe(id) && r.r % 2 == 0 && r.cc % 2 == 0;
+}
+
+// whether the matrix-core form of a bf16 layer beats the vector kernels: a
+// time model of each, its constants fitted to the bf16 layers of the five
+// workloads on MI355X.  The vector kernels do n_wt MACs per output pixel
+// (n_wt: stored weights, about the surviving taps) at about 12 T MAC/s (half
+// that at stride 2).  The matrix-core form is latency-bound while the chip
+// holds all its workgroups (about 1.4-1.5 us per k step, each waiting for
+// its own loads), else bound by workgroup steps (about 880 / 390 per us for
+// 64 / 128-filter tiles); plus about 8 us for the weight expansion and its
+// launch.
+static bool mfma_pays(const ConvParams& p) {
+  const double pix = static_cast<double>(p.n) * p.ho * p.wo;
+  const double t_vec = pix * p.n_wt * (p.stride == 2 ? 2.2 : 1.0) / 12e12 + 8e-6;
+  const bool long_k = mfma_long_k(p);
+  const int km = long_k ? 64 : 32;
+  const double steps = (9.0 * p.c_in + km - 1) / km;
+  const long bm = p.c_out > 64 ? 128 : 64;
+  const double wgs = std::ceil(pix / 128) * ((p.c_out + bm - 1) / bm);
+  const double t_mfma = std::max(steps * (long_k ? 1.5e-6 : 1.4e-6), wgs * steps / (bm == 128 ? 390e6 : 880e6)) + 8e-6;
+  return t_mfma < t_vec;
 }
 
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
@@ -146,10 +170,15 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
     return pl;
   };
   const int forced = env_recipe();
+  ConvPlan mfma;
+  mfma.recipe = kRecipeMfma;
+  const bool mfma_ok = bf16 && allow_split && mfma_eligible(p);
+  if (forced == kRecipeMfma && mfma_ok) return mfma;
   if (forced >= 0 && forced < kNumRecipes) {
     const ConvPlan pl = try_plan(forced);
     if (pl.recipe >= 0) return pl;
   }
+  if (mfma_ok && forced < 0 && mfma_pays(p)) return mfma;
   const long pix = static_cast<long>(p.ho) * p.wo;
   int pref[4];
   const bool wave_ok = (lib == kLibCanon8 || lib == kLibDense9) && p.pad == p.dil;
@@ -271,6 +300,7 @@ static hipError_t launch_wave(int id, const ConvParams& p, hipStream_t st) {
 
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p0, bool bf16_act, hipStream_t st) {
   ConvParams p = p0;
+  if (plan.recipe == kRecipeMfma) return bf16_act ? launch_mfma_conv(p, st) : hipErrorInvalidConfiguration;
   p.ksplit = plan.ksplit;
   if (plan.ksplit > 1 && !is_wave_recipe(plan.recipe)) return hipErrorInvalidConfiguration;
   if (!recipe_usable(plan.recipe, p, lib, bf16_act)) return hipErrorInvalidConfiguration;

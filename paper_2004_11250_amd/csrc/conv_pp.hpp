@@ -139,14 +139,26 @@ struct ConvPlan {
   int ksplit = 1;   // channel split over workgroups (needs scratch, see split_bytes)
 };
 
-// allow_split: the caller can provide scratch for a channel split.  With
+// bf16 layers as a zero-filled dense contraction on the matrix cores
+// (mfma_conv.hip): the plan's recipe id, whether a layer can run so (c_in a
+// multiple of 32, no fused max pool, offsets within 32 bits), the scratch it
+// needs (the expanded weights and bias) and its launch (p.part = scratch).
+constexpr int kRecipeMfma = 64;
+bool mfma_eligible(const ConvParams& p);
+size_t mfma_bytes(const ConvParams& p);
+bool mfma_long_k(const ConvParams& p);   // k steps of 64 (else 32)
+hipError_t launch_mfma_conv(const ConvParams& p, hipStream_t st);
+
+// allow_split: the caller can provide scratch (a channel split's partial
+// sums, or the matrix-core form's expanded weights: kRecipeMfma).  With
 // PP_MAXPOOL2 in p.flags only plans that can fuse the pool are chosen (a
 // split, whose second pass pools, or a tiling with whole windows per lane),
 // with PP_ACCUMULATE, PP_PIXSHUF2 or PP_UPSAMPLE2 only wave-pipeline
 // tilings, and recipe -1 means none can.  (p.h, p.w are the conv's input
 // size: the upsampled size with PP_UPSAMPLE2.)
 ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split);
-// scratch bytes a plan needs (its partial-sum blocks); 0 without a split
+// scratch bytes a plan needs (its partial-sum blocks, or the matrix-core
+// form's expanded weights); 0 for none
 size_t split_bytes(const ConvPlan& plan, const ConvParams& p);
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p, bool bf16_act, hipStream_t st);
 
