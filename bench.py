@@ -10,6 +10,8 @@ Prints ONE JSON line:
   ms_per_step  ms per frame
   roofline     the pruned-conv kernel's rate against the MI355X fp32 vector
                peak (157.3 TFLOP/s), timed live with HIP events per layer
+               (bf16 frames whose time goes mostly to the matrix-core form:
+               that form's contraction against the bf16 matrix peak)
   cpu_baseline the fp64 CPU oracle on the same frame (reported baseline)
   dense        the same masked model run as dense convs (torch conv2d on the
                same GPU) for the speedup
@@ -34,6 +36,8 @@ PEAK_FP32_VECTOR_TFLOPS = 157.3     # MI355X: 256 CU x 2.4 GHz x 256 FLOP/clk; p
                                     # v_fmac_f32 issues every 2 cycles per SIMD on gfx950, so this is the
                                     # FMA peak of the kernels here (built without packed FP32)
 PEAK_HBM_GBS = 8000.0
+PEAK_BF16_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak
+MFMA_RECIPE = 64                    # pp_conv2d_recipe id of the bf16 matrix-core form
 
 WORKLOADS = {2: "vgg16_conv_stack_224x224_b1", 3: "style_transfer_512x512_b1", 4: "super_resolution_270x480_x4_b1",
              5: "colorization_256x256_b8", 1: "pruned_layer_16x16_32x32_b1"}
@@ -317,6 +321,7 @@ def main():
     layers = []
     li = 0
     esz = 2 if dtype == "bf16" else 4
+    pdt = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
     fused = pp.fused_ops(spec["ops"])
     for (i, op, ishape, o), prm in zip(shapes, params):
         if op["op"] != "conv3":
@@ -347,19 +352,28 @@ def main():
         torch.cuda.synchronize()
         us = a0.elapsed_time(a1) * 1e3 / args.layer_steps
         macs = surviving_macs(op, prm, shapes[i][3], batch)
+        # the form the planner runs: the vector-ALU kernels, or (bf16) the
+        # matrix-core form, which does the layer's whole masked dense contraction
+        hin, win = (2 * ishape[1], 2 * ishape[2]) if up else (ishape[1], ishape[2])
+        mfma = f != "maxpool2" and pp.conv2d_recipe(L.h_blob, batch, hin, win, pdt) == MFMA_RECIPE
+        co = shapes[i][3]
+        dense_macs = batch * co[1] * co[2] * co[0] * 9 * op["c_in"]
         # the residual of an accumulating conv is read as well as written
         alg_bytes = batch * (int(np.prod(ishape)) + (2 if f == "add" else 1) * int(np.prod(o))) * esz + \
             L.h_blob.nbytes
         layers.append(dict(op=i, c_in=op["c_in"], c_out=op["c_out"], hw=f"{o[1]}x{o[2]}", lib=op["lib"],
                            fused=f, upsample2_in=up,
+                           form="mfma" if mfma else "vector", dense_mmac=round(dense_macs / 1e6, 3),
                            surviving_mmac=round(macs / 1e6, 3), us=round(us, 3),
                            eff_tmacs=round(macs / us / 1e6, 3), alg_mb=round(alg_bytes / 1e6, 3),
                            frac_fp32_peak=round(2 * macs / us / 1e6 / PEAK_FP32_VECTOR_TFLOPS, 4)))
         del xin, yo
-    pr = [l for l in layers if l["lib"] == "canon8"]
+    pr = [l for l in layers if l["lib"] == "canon8" and l["form"] == "vector"]
     pr_macs = sum(l["surviving_mmac"] for l in pr) * 1e6
     pr_us = sum(l["us"] for l in pr)
     achieved = 2 * pr_macs / (pr_us * 1e-6) / 1e12 if pr_us else 0.0
+    mf = [l for l in layers if l["form"] == "mfma"]
+    mf_us = sum(l["us"] for l in mf)
     traffic = None
     if cfg == 2 and dtype == "f32" and os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as fh:
@@ -368,7 +382,16 @@ def main():
             traffic = t["bytes_per_frame"]
     roofline = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS, unit="TFLOP/s",
                     frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), traffic=traffic,
-                    kernel="pattern-pruned 3x3 conv kernels (the 12 pruned layers, summed over the frame)")
+                    kernel=f"pattern-pruned 3x3 conv kernels (the {len(pr)} pruned layers on the vector ALUs, "
+                           "summed over the frame)")
+    if mf_us > pr_us:
+        # the bf16 matrix-core form dominates: its contraction (the masked
+        # dense conv) against the bf16 dense matrix peak
+        mf_achieved = 2 * sum(l["dense_mmac"] for l in mf) * 1e6 / (mf_us * 1e-6) / 1e12
+        roofline = dict(bound="mfma", achieved=round(mf_achieved, 3), peak=PEAK_BF16_MFMA_TFLOPS, unit="TFLOP/s",
+                        frac=round(mf_achieved / PEAK_BF16_MFMA_TFLOPS, 4), traffic=None,
+                        kernel=f"bf16 matrix-core form of the pruned 3x3 convs (the {len(mf)} layers the planner "
+                               "puts there: weight expansion + implicit GEMM, summed over the frame)")
 
     # ---- dense comparator: the same masked model as dense convs (torch / MIOpen)
     dense = None
