@@ -166,7 +166,7 @@ def test_vgg16_net_equals_chained_layer_calls():
     assert np.array_equal(y_net, _np(cur))
 
 
-@pytest.mark.parametrize("cfg,dtype", [(3, "f32"), (4, "f32"), (4, "bf16")])
+@pytest.mark.parametrize("cfg,dtype", [(3, "f32"), (3, "bf16"), (4, "f32"), (4, "bf16")])
 def test_net_fused_equals_unfused(cfg, dtype):
     # the fused residual adds and pixel shuffles give bitwise the output of
     # the same network run op by op (each op its own pp_net_fwd), whose
