@@ -151,7 +151,10 @@ static bool mfma_pays(const ConvParams& p) {
   const double steps = (9.0 * p.c_in + km - 1) / km;
   const long bm = p.c_out > 64 ? 128 : 64;
   const double wgs = std::ceil(pix / 128) * ((p.c_out + bm - 1) / bm);
-  const double t_mfma = std::max(steps * (long_k ? 1.5e-6 : 1.4e-6), wgs * steps / (bm == 128 ? 390e6 : 880e6)) + 8e-6;
+  // (two wave groups per tile when the grid is at most one tile per compute
+  // unit: about 0.8 of the latency-bound time)
+  const double lat = steps * (long_k ? 1.5e-6 : 1.4e-6) * (wgs <= 256 ? 0.8 : 1.0);
+  const double t_mfma = std::max(lat, wgs * steps / (bm == 128 ? 390e6 : 880e6)) + 8e-6;
   return t_mfma < t_vec;
 }
 

@@ -94,9 +94,9 @@ __global__ __launch_bounds__(256) void pp_mfma_expand_kernel(ConvParams a, uint1
 // 16-byte pieces of rows; B: each thread gathers KPT consecutive channels of
 // one pixel (lanes take consecutive pixels, so each load is coalesced).  UP: the
 // conv's input is the nearest x2 upsampling of x (PP_UPSAMPLE2).
-template <int TM, int TN, int KM, bool UP>
-__global__ __launch_bounds__(256) void pp_mfma_conv_kernel(ConvParams a, const uint16_t* __restrict__ am,
-                                                           const float* __restrict__ bias, int n_tiles) {
+template <int TM, int TN, int KM, bool UP, int G>
+__global__ __launch_bounds__(256 * G) void pp_mfma_conv_kernel(ConvParams a, const uint16_t* __restrict__ am,
+                                                               const float* __restrict__ bias, int n_tiles) {
   constexpr int BM = 64 * TM, BN = 64 * TN;
   constexpr int kMK = KM;               // k per step: KM / 16 MFMAs per block
   constexpr int kPitch = kMK + 8;       // LDS row pitch in bf16 (80 or 144 bytes: a lane's 16-byte reads spread over the banks)
@@ -104,10 +104,20 @@ __global__ __launch_bounds__(256) void pp_mfma_conv_kernel(ConvParams a, const u
   constexpr int APR = kMK / 8;          // 16-byte A pieces per row and step
   constexpr int JA = BM * APR / 256;    // A pieces per thread
   static_assert(KPT % 8 == 0 && 32 % KPT == 0, "a thread's channels of a step are one tap (c_in a multiple of 32)");
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][kPitch];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][kPitch];
-  const int tid = threadIdx.x, lane = tid & 63;
+  // per wave group: two buffers of A (BM rows) and B (BN rows); after the
+  // loop the space holds the second group's accumulators
+  constexpr int kRows = BM + BN;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[G * 2 * kRows * kPitch];
+  static_assert(G == 1 || sizeof(smem) >= TM * TN * 16 * 256 * sizeof(float), "room for the group reduction");
+  const int tid = threadIdx.x & 255, lane = tid & 63;
+  const int grp = G == 1 ? 0 : __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 8));
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  auto As = [&](int buf, int row, int col) __attribute__((always_inline)) {
+    return &smem[((grp * 2 + buf) * kRows + row) * kPitch + col];
+  };
+  auto Bs = [&](int buf, int row, int col) __attribute__((always_inline)) {
+    return &smem[((grp * 2 + buf) * kRows + BM + row) * kPitch + col];
+  };
   const int wm = wv & 1, wn = wv >> 1;
   const int nt = static_cast<int>(blockIdx.x % static_cast<uint32_t>(n_tiles));
   const int mt = static_cast<int>(blockIdx.x / static_cast<uint32_t>(n_tiles));
@@ -177,12 +187,12 @@ __global__ __launch_bounds__(256) void pp_mfma_conv_kernel(ConvParams a, const u
   auto put = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < JA; ++j) {
-      uint32_t* d = reinterpret_cast<uint32_t*>(&As[buf][ar + (256 / APR) * j][8 * aq]);
+      uint32_t* d = reinterpret_cast<uint32_t*>(As(buf, ar + (256 / APR) * j, 8 * aq));
       *reinterpret_cast<uint4*>(d) = make_uint4(ra[j][0], ra[j][1], ra[j][2], ra[j][3]);
     }
 #pragma unroll
     for (int q = 0; q < KPT / 8; ++q) {
-      uint32_t* d = reinterpret_cast<uint32_t*>(&Bs[buf][bn][kb + 8 * q]);
+      uint32_t* d = reinterpret_cast<uint32_t*>(Bs(buf, bn, kb + 8 * q));
       *reinterpret_cast<uint4*>(d) =
           make_uint4((rb[8 * q] & 0xFFFFu) | (rb[8 * q + 1] << 16), (rb[8 * q + 2] & 0xFFFFu) | (rb[8 * q + 3] << 16),
                      (rb[8 * q + 4] & 0xFFFFu) | (rb[8 * q + 5] << 16), (rb[8 * q + 6] & 0xFFFFu) | (rb[8 * q + 7] << 16));
@@ -194,30 +204,61 @@ __global__ __launch_bounds__(256) void pp_mfma_conv_kernel(ConvParams a, const u
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
-  fetch(0);
-  put(0);
+  // wave group g takes k steps g, g + G, g + 2 G, ...: G tiles' worth of
+  // loads in flight per workgroup; every thread runs every iteration (and
+  // barrier), a group without a step that iteration only waits
+  const int iters = (steps + G - 1) / G;
+  if (grp < steps) {
+    fetch(grp);
+    put(0);
+  }
   __syncthreads();
-  for (int s = 0; s < steps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < steps) fetch(s + 1);
-    // a 32 x 32 x 16 MFMA takes row l % 32 of A and column l % 32 of B, k
-    // 8 (l / 32) .. 8 (l / 32) + 7 of its 16, in lane l
+  for (int it = 0; it < iters; ++it) {
+    const int buf = it & 1;
+    const int s = it * G + grp;
+    if (s + G < steps) fetch(s + G);
+    if (s < steps) {
+      // a 32 x 32 x 16 MFMA takes row l % 32 of A and column l % 32 of B, k
+      // 8 (l / 32) .. 8 (l / 32) + 7 of its 16, in lane l
 #pragma unroll
-    for (int h = 0; h < kMK; h += 16) {
-      bf16x8 av[TM], bv[TN];
+      for (int h = 0; h < kMK; h += 16) {
+        bf16x8 av[TM], bv[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          av[i] = *reinterpret_cast<const bf16x8*>(As(buf, (wm * TM + i) * 32 + (lane & 31), h + 8 * (lane >> 5)));
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bv[j] = *reinterpret_cast<const bf16x8*>(Bs(buf, (wn * TN + j) * 32 + (lane & 31), h + 8 * (lane >> 5)));
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+      }
+    }
+    if (s + G < steps) put(buf ^ 1);   // that buffer's last readers passed the barrier below one iteration ago
+    __syncthreads();
+  }
+  if constexpr (G == 2) {
+    // group 1's sums into group 0's (one fixed order), through LDS (the
+    // operand buffers are dead: every wave passed the last barrier)
+    float* red = reinterpret_cast<float*>(smem);
+    if (grp == 1) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        av[i] = *reinterpret_cast<const bf16x8*>(&As[buf][(wm * TM + i) * 32 + (lane & 31)][h + 8 * (lane >> 5)]);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) red[((i * TN + j) * 16 + r) * 256 + tid] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (grp == 1) return;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        bv[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][(wn * TN + j) * 32 + (lane & 31)][h + 8 * (lane >> 5)]);
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
-    if (s + 1 < steps) put(buf ^ 1);   // that buffer's last readers passed the barrier below one step ago
-    __syncthreads();
+        for (int r = 0; r < 16; ++r) acc[i][j][r] += red[((i * TN + j) * 16 + r) * 256 + tid];
   }
 
   // accumulator r of block (i, j), lane l, is C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] of the block
@@ -262,8 +303,16 @@ hipError_t launch_tiles(const ConvParams& p, const uint16_t* am, const float* bo
   const long n_tiles = (np + BN - 1) / BN, m_tiles = (p.c_out + BM - 1) / BM;
   const long blocks = n_tiles * m_tiles;
   if (blocks < 1 || blocks > 0x7FFFFFFFL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((pp_mfma_conv_kernel<TM, TN, KM, UP>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, st, p, am,
-                     bo, static_cast<int>(n_tiles));
+  const dim3 grid(static_cast<uint32_t>(blocks));
+  // grids of at most one tile per compute unit: two wave groups per tile
+  // splitting its k steps (twice the loads in flight; with 512 tiles, whose
+  // 8-wave workgroups no longer all fit at once, it timed slower)
+  if (mfma_groups(p) == 2)
+    hipLaunchKernelGGL((pp_mfma_conv_kernel<TM, TN, KM, UP, 2>), grid, dim3(512), 0, st, p, am, bo,
+                       static_cast<int>(n_tiles));
+  else
+    hipLaunchKernelGGL((pp_mfma_conv_kernel<TM, TN, KM, UP, 1>), grid, dim3(256), 0, st, p, am, bo,
+                       static_cast<int>(n_tiles));
   return hipGetLastError();
 }
 
@@ -283,6 +332,12 @@ bool mfma_eligible(const ConvParams& p) {
 }
 
 bool mfma_long_k(const ConvParams& p) { return 9 * p.c_in >= 1152; }
+
+int mfma_groups(const ConvParams& p) {
+  const long bm = p.c_out > 64 ? 128 : 64;
+  const long tiles = (static_cast<long>(p.n) * p.ho * p.wo + 127) / 128 * ((p.c_out + bm - 1) / bm);
+  return tiles <= 256 ? 2 : 1;
+}
 
 size_t mfma_bytes(const ConvParams& p) { return a_bytes(p) + static_cast<size_t>(p.c_out) * sizeof(float); }
 
