@@ -96,11 +96,11 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const int lib = library_kind(v);
   const bool bf = act_dtype == PP_BF16;
   // the plan for library kind `kind`; a split only with enough scratch
-  auto make_plan = [&](int kind, ConvParams* pp_) {
-    ConvPlan pl = plan_conv(*pp_, kind, bf, scratch != nullptr);
+  auto make_plan = [&](int kind, ConvParams* pp_, bool no_lean) {
+    ConvPlan pl = plan_conv(*pp_, kind, bf, scratch != nullptr, no_lean);
     if (split_bytes(pl, *pp_) > 0) {
       if (split_bytes(pl, *pp_) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
-        pl = plan_conv(*pp_, kind, bf, false);   // not enough scratch: no split
+        pl = plan_conv(*pp_, kind, bf, false, no_lean);   // not enough scratch: no split
       else
         pp_->part = static_cast<float*>(scratch);
     }
@@ -110,14 +110,14 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
     // a 4-tap library with run-time compiled kernels (pp_jit_library): as
     // the canonical library's plan
     ConvParams jp = p;
-    const ConvPlan pl = make_plan(kLibCanon8, &jp);
+    const ConvPlan pl = make_plan(kLibCanon8, &jp, true);
     hipError_t e = hipSuccess;
     if (pl.recipe >= kFirstWaveRecipe && pl.recipe < kNumRecipes && jit_launch(v, pl, jp, bf, st, &e)) {
       if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
       return PP_OK;
     }
   }
-  ConvPlan plan = make_plan(lib, &p);
+  ConvPlan plan = make_plan(lib, &p, false);
   if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the upsampling / max pool / accumulation / pixel shuffle for this layer");
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
@@ -202,7 +202,7 @@ extern "C" pp_status pp_conv2d_recipe(const void* h_blob, size_t blob_bytes, int
   ConvPlan plan = plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_workspace != 0);
   if (library_kind(v) == kLibGeneric && jit_library4(v)) {
     // with run-time compiled kernels the call runs the canonical library's plan
-    const ConvPlan cp = plan_conv(p, kLibCanon8, act_dtype == PP_BF16, with_workspace != 0);
+    const ConvPlan cp = plan_conv(p, kLibCanon8, act_dtype == PP_BF16, with_workspace != 0, true);
     if (cp.recipe >= 0 && jit_ready(v, cp, act_dtype == PP_BF16)) plan = cp;
   }
   *recipe = plan.recipe;
@@ -227,7 +227,7 @@ extern "C" pp_status pp_jit_library(const void* h_blob, size_t blob_bytes, int32
   const bool bf = act_dtype == PP_BF16;
   // the plans pp_conv2d_fwd can make: with the workspace's split, and without
   for (bool split : {with_workspace != 0, false}) {
-    const ConvPlan plan = plan_conv(p, kLibCanon8, bf, split);
+    const ConvPlan plan = plan_conv(p, kLibCanon8, bf, split, true);
     if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling runs this layer");
     if (plan.recipe == kRecipeMfma) continue;   // the matrix-core form reads any library from the blob
     s = jit_prepare(v, plan, bf);
@@ -250,7 +250,7 @@ extern "C" pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, 
   if (library_kind(v) == kLibGeneric && jit_library4(v)) {
     // enough for the canonical plan that run-time compiled kernels run
     const ConvParams p = layer_params(v, n, h, w, ho, wo);
-    const size_t b = split_bytes(plan_conv(p, kLibCanon8, act_dtype == PP_BF16, true), p);
+    const size_t b = split_bytes(plan_conv(p, kLibCanon8, act_dtype == PP_BF16, true, true), p);
     if (b > *bytes) *bytes = b;
   }
   return PP_OK;

@@ -20,6 +20,11 @@ RecipeInfo recipe_info(int id) {
     return RecipeInfo{R, CC, LW, 1, WS, 0, P};
     PP_WRECIPES(PP_W)
 #undef PP_W
+#define PP_L(ID, R, CC, LW, WS, V4) \
+  case ID:                          \
+    return RecipeInfo{R, CC, LW, 1, WS, 0, 0};
+    PP_LRECIPES(PP_L)
+#undef PP_L
   }
   return RecipeInfo{0, 0, 0, 0, 0, 0, 0};
 }
@@ -35,6 +40,7 @@ static bool wave_recipe_fits(const RecipeInfo& r, int s, int d, int lib, bool bf
 bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
   const RecipeInfo r = recipe_info(id);
   if (r.r == 0) return false;
+  if (is_lean_recipe(id)) return lib == kLibCanon8 && !bf16 && s == 1 && d == 1 && lean_lds_bytes(id) > 0;
   if (is_wave_recipe(id)) return (lib == kLibCanon8 || lib == kLibDense9) && wave_recipe_fits(r, s, d, lib, bf16);
   const int lh = 64 / r.lw;
   const int th = lh * r.r, tw = r.lw * r.cc;
@@ -54,6 +60,7 @@ bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
 }
 
 bool recipe_compiled(int lib, int id) {
+  if (is_lean_recipe(id)) return lib == kLibCanon8;
   if (id < 0 || id >= kNumRecipes) return false;
   if (is_wave_recipe(id)) return lib == kLibCanon8 || lib == kLibDense9;
   return lib == kLibCanon8 || id == 0 || id == 3 || id == 6 || id == 8 || id == 12 || id == 13;
@@ -64,6 +71,8 @@ bool recipe_compiled(int lib, int id) {
 // and (register-pipelined tilings) fp32 with the canonical library
 static bool recipe_usable(int id, const ConvParams& p, int lib, bool bf16) {
   if (!recipe_compiled(lib, id) || !recipe_fits(id, p.stride, p.dil, bf16, lib)) return false;
+  if (is_lean_recipe(id))
+    return p.pad == 1 && (!lean_v4(id) || (p.w % 4 == 0 && !(p.flags & PP_UPSAMPLE2)));
   if (recipe_info(id).pipe && (bf16 || lib != kLibCanon8)) return false;
   return !is_wave_recipe(id) || p.pad == p.dil;
 }
@@ -110,10 +119,22 @@ static int choose_split(int id, const ConvParams& p) {
   return ks;
 }
 
+// channel split of a lean tiling: the one-row-per-lane 16-wave tiling on
+// maps of at most 16 x 16 outputs runs split two ways (measured on MI355X at
+// 14 x 14, 512 -> 512: 21 us against 27 unsplit); none otherwise
+static int choose_split_lean(int id, const ConvParams& p) {
+  const int forced = env_int("PP_KSPLIT");
+  if (forced >= 1) return forced < p.c_in ? forced : p.c_in;
+  const RecipeInfo r = recipe_info(id);
+  if (r.r == 1 && r.ws == 16 && static_cast<long>(p.ho) * p.wo <= 16L * 16 && p.c_in >= 64) return 2;
+  return 1;
+}
+
 static ConvPlan finish_plan(int id, const ConvParams& p, bool allow_split) {
   ConvPlan plan;
   plan.recipe = id;
-  plan.ksplit = (allow_split && is_wave_recipe(id)) ? choose_split(id, p) : 1;
+  plan.ksplit = allow_split ? (is_wave_recipe(id) ? choose_split(id, p) : is_lean_recipe(id) ? choose_split_lean(id, p) : 1)
+                            : 1;
   return plan;
 }
 
@@ -131,7 +152,7 @@ size_t split_bytes(const ConvPlan& plan, const ConvParams& p) {
 // tiles (every wave-pipeline tile is 8 R x 8 CC outputs: even)
 static bool pool_fits(int id) {
   const RecipeInfo r = recipe_info(id);
-  return is_wave_recipe(id) && r.r % 2 == 0 && r.cc % 2 == 0;
+  return (is_wave_recipe(id) || is_lean_recipe(id)) && r.r % 2 == 0 && r.cc % 2 == 0;
 }
 
 // whether the matrix-core form of a bf16 layer beats the vector kernels: a
@@ -158,7 +179,7 @@ static bool mfma_pays(const ConvParams& p) {
   return t_mfma < t_vec;
 }
 
-ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
+ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bool no_lean) {
   const bool pool = (p.flags & PP_MAXPOOL2) != 0;
   // epilogues of the wave-pipeline kernel only
   const bool fused = (p.flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2)) != 0;
@@ -166,8 +187,9 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
   auto try_plan = [&](int id) {
     ConvPlan pl;
     pl.recipe = -1;
+    if (no_lean && is_lean_recipe(id)) return pl;
     if (!recipe_usable(id, p, lib, bf16)) return pl;
-    if (fused && !is_wave_recipe(id)) return pl;
+    if (fused && !is_wave_recipe(id) && !is_lean_recipe(id)) return pl;
     pl = finish_plan(id, p, allow_split);
     if (pool && pl.ksplit == 1 && !pool_fits(id)) pl.recipe = -1;
     return pl;
@@ -177,12 +199,40 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split) {
   mfma.recipe = kRecipeMfma;
   const bool mfma_ok = bf16 && allow_split && mfma_eligible(p);
   if (forced == kRecipeMfma && mfma_ok) return mfma;
-  if (forced >= 0 && forced < kNumRecipes) {
+  if (forced >= 0 && (forced < kNumRecipes || is_lean_recipe(forced))) {
     const ConvPlan pl = try_plan(forced);
     if (pl.recipe >= 0) return pl;
   }
   if (mfma_ok && forced < 0 && mfma_pays(p)) return mfma;
   const long pix = static_cast<long>(p.ho) * p.wo;
+  if (!bf16 && lib == kLibCanon8 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.n == 1 && p.c_in > 8 && !no_lean) {
+    // fp32, stride 1, one image: the lean tilings that timed fastest on the
+    // VGG-16 layer shapes (MI355X), by output size: 4 x 4 outputs per lane on
+    // the 224 x 224 maps (4 channel-split waves) and 112 x 112 (8), 2 x 4 on
+    // 56 x 56, 2 x 2 with 16 waves on 28 x 28, and one row of 2 outputs per
+    // lane with 16 waves on smaller maps.  Each 16-byte staging tiling has a
+    // 4-byte staging twin of the same tiling (widths not a multiple of 4, a
+    // fused x2 upsample): same accumulation order, so a conv fused with the
+    // upsample before it gives bitwise what the unfused conv gives.
+    int lp[3] = {-1, -1, -1};
+    if (pix >= 160L * 160L) {
+      lp[0] = 40; lp[1] = 56;
+    } else if (pix >= 80L * 80L) {
+      lp[0] = 42; lp[1] = 57;
+    } else if (pix >= 40L * 40L) {
+      lp[0] = 46; lp[1] = 55;
+    } else if (pix >= 20L * 20L) {
+      lp[0] = 48; lp[1] = 51;
+    } else {
+      lp[0] = 54;
+    }
+    if (forced < 0)
+      for (int id : lp)
+        if (id >= 0) {
+          const ConvPlan pl = try_plan(id);
+          if (pl.recipe >= 0) return pl;
+        }
+  }
   int pref[4];
   const bool wave_ok = (lib == kLibCanon8 || lib == kLibDense9) && p.pad == p.dil;
   if (wave_ok && !bf16 && p.stride == 1 && p.n == 1) {
@@ -305,8 +355,10 @@ hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p0, bool
   ConvParams p = p0;
   if (plan.recipe == kRecipeMfma) return bf16_act ? launch_mfma_conv(p, st) : hipErrorInvalidConfiguration;
   p.ksplit = plan.ksplit;
-  if (plan.ksplit > 1 && !is_wave_recipe(plan.recipe)) return hipErrorInvalidConfiguration;
+  if (plan.ksplit > 1 && !is_wave_recipe(plan.recipe) && !is_lean_recipe(plan.recipe))
+    return hipErrorInvalidConfiguration;
   if (!recipe_usable(plan.recipe, p, lib, bf16_act)) return hipErrorInvalidConfiguration;
+  if (is_lean_recipe(plan.recipe)) return launch_lean_recipe(plan.recipe, p, st);
   if (is_wave_recipe(plan.recipe)) {
     if (lib == kLibDense9)
       return bf16_act ? launch_wave<kLibDense9, uint16_t>(plan.recipe, p, st) : launch_wave<kLibDense9, float>(plan.recipe, p, st);

@@ -83,6 +83,32 @@ struct ConvParams {
 
 constexpr int kFirstWaveRecipe = 20;
 
+// Tilings of the lean kernel (fp32, canonical library, stride 1, pad 1): id,
+// R x CC outputs per lane, LW lanes across, WS channel-split waves of one
+// slot group, V4 16-byte staging (image width a multiple of 4; else 4-byte).
+#define PP_LRECIPES(X)  \
+  X(40, 4, 4, 8, 4, 1)  \
+  X(41, 4, 4, 8, 2, 1)  \
+  X(42, 4, 4, 8, 8, 1)  \
+  X(43, 4, 4, 4, 4, 1)  \
+  X(44, 4, 4, 4, 2, 1)  \
+  X(45, 2, 4, 8, 4, 1)  \
+  X(46, 2, 4, 8, 8, 1)  \
+  X(47, 2, 2, 8, 8, 1)  \
+  X(48, 2, 2, 8, 16, 1) \
+  X(49, 2, 2, 8, 4, 1)  \
+  X(50, 4, 4, 8, 1, 1)  \
+  X(51, 2, 2, 8, 16, 0) \
+  X(52, 2, 2, 8, 8, 0)  \
+  X(53, 2, 2, 8, 4, 0)  \
+  X(54, 1, 2, 8, 16, 0) \
+  X(55, 2, 4, 8, 8, 0)  \
+  X(56, 4, 4, 8, 4, 0)  \
+  X(57, 4, 4, 8, 8, 0)
+
+constexpr int kFirstLeanRecipe = 40;
+constexpr int kEndLeanRecipe = 58;
+
 // LDS row stride (floats) of the wave-pipeline kernel's staged tile: the
 // smallest multiple of 4 >= n, up to n + 12, for which lane rows rstep tile
 // rows apart start 16 banks apart (of 32), else n
@@ -157,7 +183,9 @@ hipError_t launch_mfma_conv(const ConvParams& p, hipStream_t st);
 // with PP_ACCUMULATE, PP_PIXSHUF2 or PP_UPSAMPLE2 only wave-pipeline
 // tilings, and recipe -1 means none can.  (p.h, p.w are the conv's input
 // size: the upsampled size with PP_UPSAMPLE2.)
-ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split);
+// no_lean: plan among the wave-pipeline tilings only (the run-time compiled
+// kernels of pp_jit_library exist for those)
+ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bool no_lean = false);
 // scratch bytes a plan needs (its partial-sum blocks, or the matrix-core
 // form's expanded weights); 0 for none
 size_t split_bytes(const ConvPlan& plan, const ConvParams& p);
@@ -169,6 +197,14 @@ hipError_t launch_recipe(int id, const ConvParams& p, hipStream_t st);
 // wave-pipeline kernel, canonical (kLibCanon8) and all-ones (kLibDense9) libraries
 template <int LIB, int S, int D, class TA>
 hipError_t launch_wave_recipe(int id, const ConvParams& p, hipStream_t st);
+
+// lean kernel (conv_pp_lean.hip)
+inline bool is_lean_recipe(int id) { return id >= kFirstLeanRecipe && id < kEndLeanRecipe; }
+hipError_t launch_lean_recipe(int id, const ConvParams& p, hipStream_t st);
+// LDS bytes of a lean tiling (0: not compiled or does not fit); whether it
+// stages by 16-byte DMAs (image width a multiple of 4)
+long lean_lds_bytes(int id);
+bool lean_v4(int id);
 
 #endif
 

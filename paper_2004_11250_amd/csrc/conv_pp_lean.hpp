@@ -1,0 +1,540 @@
+// conv_pp_lean.hpp -- pattern/connectivity-pruned 3x3 convolution for the
+// canonical 8-pattern library, fp32, "lean" form (gfx950).
+//
+// Same result as the wave-pipeline kernel (pattern + connectivity pruning,
+// Sec. 2; compact storage and filter reorder, Sec. 3; conv fused with bias
+// and activation, Sec. 3) and the same per-wave organisation: a workgroup
+// owns one output tile of one image and one slot group of 8 reordered
+// filters; its WS waves walk contiguous ranges of the input channels, each
+// with a private LDS ring of NS channels that LDS-DMA loads fill; lanes
+// are output pixels (R x CC per lane), so a kernel's pattern is wave-uniform
+// and selects a code path with compile-time tap offsets.
+//
+// What differs is everything around the channel loop, which on MI355X cost
+// more than the loop itself for the layer sizes of the evaluated networks
+// (a few thousand FMAs per wave):
+//   * the staging geometry is a compile-time constant (16-byte row DMAs,
+//     image width a multiple of 4), so per-lane staging offsets are one
+//     constant division each and no branches;
+//   * the block decode uses host-computed division magics, not the
+//     compiler's run-time division sequences;
+//   * the first channel's halo DMAs are issued before the layer metadata is
+//     even requested; the metadata of the first channels comes in one scalar
+//     load;
+//   * the epilogue sums the WS partial blocks with one LDS exchange per pass
+//     of slots (two barriers) and stores 16-byte rows.
+#pragma once
+
+#include "conv_pp_wave.hpp"
+
+namespace pp {
+
+// q = n / d for n < 2^31 with a host-computed magic (m, l):
+// q = (mulhi(n, m) + n) >> l
+struct FastDiv {
+  uint32_t d = 1, m = 0, l = 0;
+};
+
+#ifndef __HIPCC_RTC__
+inline FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.d = d;
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  f.l = l;
+  f.m = static_cast<uint32_t>(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+  return f;
+}
+#endif
+
+struct LeanParams {
+  const uint8_t* blob = nullptr;
+  const float* x = nullptr;
+  float* y = nullptr;
+  float* part = nullptr;         // channel split over workgroups: partial-sum blocks
+  uint32_t h = 0, w = 0, ho = 0, wo = 0;
+  uint32_t c_in = 0, c_out = 0;
+  uint32_t off_codes = 0, off_woff = 0, off_w = 0, off_bias = 0, off_perm = 0, blob_bytes = 0;
+  uint32_t flags = 0;
+  uint32_t ksplit = 1;
+  FastDiv groups, tiles_x, tiles_y, splits;   // block decode
+};
+
+namespace kern {
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  return (__umulhi(n, f.m) + n) >> f.l;
+}
+
+// V4: the halo tile is staged by 16-byte DMAs (image width a multiple of
+// 4), else by 4-byte DMAs (any width)
+template <int R, int CC, int LW, int WS, bool V4>
+struct LGeo {
+  static constexpr int LH = 64 / LW;
+  static constexpr int TH = LH * R, TW = LW * CC;       // output tile
+  static constexpr int PR = R + 2, PC = CC + 2;         // patch of a lane
+  static constexpr int TIH = TH + 2;                    // staged rows
+  // 16-byte staging: the staged columns start at the tile's first input
+  // column moved down to a multiple of 4 (3 columns in front for pad 1);
+  // 4-byte staging: at the tile's first input column
+  static constexpr int SH = V4 ? 3 : 0;
+  static constexpr int SWID = (TW + 2 + SH + 3) / 4 * 4;
+  // a lane's patch rows are read with aligned loads of up to VWL floats (the
+  // alignment its row start allows)
+  static constexpr int VWL = CC % 4 == 0 ? 4 : (CC % 2 == 0 ? 2 : 1);
+  static constexpr int LSTR = wave_row_stride(SWID, R);
+  static constexpr int AREA = TIH * LSTR;
+  static constexpr int EPD = V4 ? 256 : 64;              // floats per DMA instruction
+  static constexpr int NQ = (AREA + EPD - 1) / EPD;      // DMAs per lane and channel
+  static constexpr int PATCH = NQ * EPD;
+  static constexpr int SLOT = PATCH + 64;                // + 8 slots x 4 expanded weights (padded)
+  // ring of NS channels (a channel's DMA is issued NS - 1 channels ahead);
+  // the smaller ring when four slots would leave a CU fewer than two
+  // workgroups of 8 waves
+  static constexpr int NS = (WS * 4 * SLOT * 4 <= 80 * 1024) ? 4 : 3;
+  static constexpr int RING = NS * SLOT;
+  static constexpr int NACC = 8 * R * CC;
+  // partial-sum exchange: SPP slots per pass, as many as fit the LDS that
+  // the rings occupy (at least one)
+  static constexpr int XPS = R * CC * 64;                // floats of one slot of one wave
+  static constexpr int SPP0 = (WS * RING) / (WS * XPS);
+  static constexpr int SPP = WS == 1 ? 8 : (SPP0 >= 8 ? 8 : (SPP0 >= 4 ? 4 : (SPP0 >= 2 ? 2 : 1)));
+  static constexpr int XCH = WS == 1 ? 0 : WS * SPP * XPS;
+  static constexpr int LDS_FLOATS = WS * RING > XCH ? WS * RING : XCH;
+  static constexpr bool fits = LDS_FLOATS * 4 <= 160 * 1024 && WS >= 1 && WS <= 16 && LW * LH == 64 && TW % 4 == 0;
+};
+
+template <int R, int CC, int LW, int WS, bool V4>
+__global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) {
+  using G = LGeo<R, CC, LW, WS, V4>;
+  constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT, NS = G::NS;
+  static_assert(G::fits, "tiling does not fit");
+  __shared__ __attribute__((aligned(16))) float lds[G::LDS_FLOATS];
+
+  const int lane = threadIdx.x & 63;
+  const int wk = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lx = lane % LW, ly = lane / LW;
+
+  // ---- block -> (image, tile, split, slot group)
+  uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  uint32_t q = fdiv(blk, a.groups);
+  const uint32_t grp = blk - q * a.groups.d;
+  blk = q;
+  q = fdiv(blk, a.splits);
+  const uint32_t ks = blk - q * a.splits.d;
+  blk = q;
+  q = fdiv(blk, a.tiles_x);
+  const uint32_t tx = blk - q * a.tiles_x.d;
+  blk = q;
+  q = fdiv(blk, a.tiles_y);
+  const uint32_t ty = blk - q * a.tiles_y.d;
+  const uint32_t img = q;
+
+  const int oy0 = ty * G::TH, ox0 = tx * G::TW;
+  const int iy0 = oy0 - 1, ixa = ox0 - 1 - G::SH;   // staged origin
+
+  // ---- this wave's channels: split ks of ksplit, then the wave's part
+  const uint32_t kc0 = fdiv(ks * a.c_in, a.splits), kc1 = fdiv((ks + 1) * a.c_in, a.splits);
+  const uint32_t per = (kc1 - kc0 + WS - 1) / WS;
+  const int c0 = min(kc1, kc0 + wk * per), c1 = min(kc1, c0 + per);
+  // with PP_UPSAMPLE2 (4-byte staging only) the conv's input is the nearest
+  // x2 upsampling of x: a.h x a.w is the upsampled size and element (gy, gx)
+  // is read from x[gy / 2][gx / 2]
+  const bool up = !V4 && (a.flags & PP_UPSAMPLE2) != 0;
+  const uint32_t sh = up ? a.h >> 1 : a.h, sw = up ? a.w >> 1 : a.w;   // stored input size
+  const uint32_t chan_bytes = sh * sw * 4;
+  const float* xi = a.x + static_cast<size_t>(img) * a.c_in * sh * sw;
+
+  float* const ring = lds + wk * G::RING;
+  const uint32_t ring_b = lds_addr(ring);
+  constexpr uint32_t LW0 = 4u * G::PATCH;   // weights' byte offset in a ring slot
+
+  // ---- per-lane staging offsets (bytes in one channel, + the DMA shift).
+  // 16-byte staging: load t of a lane stages elements 4 (64 t + lane) .. + 3
+  // of the tile, all in one tile row (LSTR is a multiple of 4) and all inside
+  // or all outside the image (the row starts at a multiple of 4, w is a
+  // multiple of 4); 4-byte staging: element 64 t + lane.  A DMA's LDS bytes
+  // start at 4 EPD t within the channel's slot.
+  uint32_t qoff[NQ];
+#pragma unroll
+  for (int t = 0; t < NQ; ++t) {
+    const uint32_t e = V4 ? 4u * (64u * t + lane) : 64u * t + lane;
+    const uint32_t row = e / LSTR, col = e % LSTR;
+    const uint32_t gy = static_cast<uint32_t>(iy0 + static_cast<int>(row));
+    const uint32_t gx = static_cast<uint32_t>(ixa + static_cast<int>(col));
+    const bool ok = e < static_cast<uint32_t>(G::AREA) && gy < a.h && gx < a.w;
+    const uint32_t el = up ? (gy >> 1) * sw + (gx >> 1) : gy * a.w + gx;
+    qoff[t] = ok ? el * 4u + kDmaShift - ((4u * G::EPD * t) & 4095u) : 0x80000000u;
+  }
+
+  const uint8_t* blob = a.blob;
+  const u32x4 brs = make_rsrc_below(blob, a.blob_bytes, kDmaShift);
+  u32x4 cr = make_rsrc_below(xi + static_cast<size_t>(c0) * sh * sw, chan_bytes, kDmaShift);
+  auto dma_patch = [&](uint32_t sb) __attribute__((always_inline)) {
+    static_for<0, NQ>([&](auto ti) __attribute__((always_inline)) {
+      constexpr int T = decltype(ti)::value;
+      if constexpr (V4)
+        dma_b128_at<1024u * T, 1024u * (T - 1), T == 0>(cr, qoff[T], sb);
+      else
+        dma_b32_at<256u * T, 256u * (T - 1), T == 0>(cr, qoff[T], sb);
+    });
+    cr = next_channel(cr, chan_bytes);
+  };
+  // expanded weights of a channel: lane j < 32 loads tap j % 4 of slot j / 4
+  // (its compact index: woff + 4 * rank of the slot among the kept ones + tap)
+  const uint32_t wslot = static_cast<uint32_t>(lane) >> 2;
+  const uint32_t wlow = lane < 32 ? (1u << wslot) - 1u : 0u;
+  const uint32_t wbit = lane < 32 ? 1u << wslot : 0u;
+  const uint32_t wbase = a.off_w + 4u * (lane & 3) + kDmaShift - (LW0 & 4095u);
+  auto dma_weights = [&](uint32_t wo, uint32_t sb) __attribute__((always_inline)) {
+    const uint32_t kept = wo >> 24;
+    const uint32_t o = wbase + 4u * ((wo & 0xFFFFFFu) + 4u * __builtin_popcount(kept & wlow));
+    dma_b32_at<LW0, 4u * G::EPD * (NQ - 1), false>(brs, (kept & wbit) ? o : 0x80000000u, sb);
+  };
+  auto slot_b = [&](int c) { return ring_b + 4u * ((static_cast<uint32_t>(c - c0) % NS) * SLOT); };
+
+  // metadata: woff word (weight offset | kept-slot mask << 24) and the 8
+  // pattern codes of (group, channel); channels past the layer's last read
+  // its last entry again (not used)
+  const uint32_t e_base = grp * a.c_in;
+  const uint32_t woff_last = a.off_woff + 4u * (e_base + a.c_in - 1);
+  const uint32_t code_last = a.off_codes + 8u * (e_base + a.c_in - 1);
+  auto woff_at = [&](int c) { return min(a.off_woff + 4u * (e_base + c), woff_last); };
+  auto code_at = [&](int c) { return min(a.off_codes + 8u * (e_base + c), code_last); };
+
+  // the slot group's output channels and biases for the epilogue, lane s <
+  // 8 holding slot s's (loaded before the first DMA: in-order completion
+  // keeps the DMA wait counts below valid)
+  const uint32_t pslot = grp * 8 + (lane & 7);
+  const uint32_t perm_l = *reinterpret_cast<const uint32_t*>(blob + a.off_perm + 4u * pslot);
+  const float bias_l = *reinterpret_cast<const float*>(blob + a.off_bias + 4u * pslot);
+  __builtin_amdgcn_sched_barrier(0);
+
+  float acc[8][R][CC];
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int qq = 0; qq < CC; ++qq) acc[s][r][qq] = 0.0f;
+  if (c0 < c1) {
+    constexpr int QV = NQ + 1;   // DMAs per lane and channel
+    constexpr int DPF = NS - 1;  // channels DMA'd ahead
+    // prologue: channel c0's halo before anything else, then channels up
+    // to c0 + DPF - 1
+    dma_patch(slot_b(c0));
+    __builtin_amdgcn_sched_barrier(0);
+    uint32_t wo_pre[DPF + 1];
+#pragma unroll
+    for (int i = 0; i <= DPF; ++i) wo_pre[i] = kern::sload<uint32_t>(blob, woff_at(c0 + i));
+    uint2 code_c = kern::sload<uint2>(blob, code_at(c0));
+    wait_lgkm();
+    dma_weights(wo_pre[0], slot_b(c0));
+#pragma unroll
+    for (int i = 1; i < DPF; ++i)
+      if (c0 + i < c1) {
+        dma_patch(slot_b(c0 + i));
+        dma_weights(wo_pre[i], slot_b(c0 + i));
+      }
+    uint32_t kept_c = wo_pre[0] >> 24;
+    uint32_t wo_n = wo_pre[DPF];   // woff word of channel c + DPF
+    const int lane_off = (ly * R) * LSTR + lx * CC;
+
+#pragma unroll 1
+    for (int c = c0; c < c1; ++c) {
+      // channel c has landed once at most min(DPF - 1, c1 - 1 - c) later
+      // channels are in flight
+      {
+        const int later = min(DPF - 1, c1 - 1 - c);
+        asm volatile("" ::: "memory");
+        static_for<0, DPF>([&](auto ni) __attribute__((always_inline)) {
+          constexpr int n = decltype(ni)::value;
+          if (later == n) __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QV));
+        });
+        asm volatile("" ::: "memory");
+      }
+      // the patch and the 8 slots' expanded weights of channel c
+      const float* cur = ring + (static_cast<uint32_t>(c - c0) % NS) * SLOT;
+      float w[8][4];
+      float p[PR][PC];
+      const uint32_t kept = kept_c;
+      if (kept != 0) {
+        const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const float4 v = wc[s];
+          w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+        }
+#pragma unroll
+        for (int r = 0; r < PR; ++r) read_row<G::SH, G::SH, PC, G::VWL, false>(p[r], cur + lane_off + r * LSTR);
+      }
+      // channel c's reads, and the scalar loads of the previous step
+      wait_lgkm();
+      __builtin_amdgcn_sched_barrier(0);
+      // channel c + DPF into the slot channel c - 1 used (its reads are done)
+      if (c + DPF < c1) {
+        const uint32_t sb = slot_b(c + DPF);
+        dma_patch(sb);
+        dma_weights(wo_n, sb);
+      }
+      // metadata for the next step: waited for there, while this channel's
+      // FMAs run
+      const uint32_t wo_nn = kern::sload<uint32_t>(blob, woff_at(c + DPF + 1));
+      const uint32_t wo_c1 = kern::sload<uint32_t>(blob, woff_at(c + 1));
+      const uint2 code_c1 = kern::sload<uint2>(blob, code_at(c + 1));
+      __builtin_amdgcn_sched_barrier(0);
+      uint32_t kc = kept;
+      asm volatile("" : "+s"(kc));   // fresh slot tests
+      if (kc != 0) {
+        const uint32_t cx = code_c.x, cy = code_c.y;
+        static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
+          constexpr int s = decltype(si)::value;
+          if (!((kc >> s) & 1u)) return;
+          apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+        });
+      }
+      kept_c = wo_c1 >> 24;
+      code_c = code_c1;
+      wo_n = wo_nn;
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // no DMA may land in the exchange area below
+  }
+
+  // ---- epilogue
+  const bool pool = (a.flags & PP_MAXPOOL2) != 0;
+  const bool relu = (a.flags & PP_RELU) != 0;
+  const bool split = a.ksplit > 1;
+  // PP_ACCUMULATE: y holds a residual r and becomes r + act(conv + bias);
+  // PP_PIXSHUF2: output channel o is stored to channel o / 4 of the 2 ho x
+  // 2 wo output, row 2 oy + bit 1 of o, column 2 ox + bit 0 of o
+  const bool accum = (a.flags & PP_ACCUMULATE) != 0;
+  const bool shuf = (a.flags & PP_PIXSHUF2) != 0;
+  const uint32_t pho = a.ho / 2, pwo = a.wo / 2;
+  float* __restrict__ y = a.y + static_cast<size_t>(img) * a.c_out * (pool ? pho * pwo : a.ho * a.wo);
+  const int oxl = ox0 + lx * CC;
+  const bool vec = (CC % 4 == 0) && (a.wo % 4 == 0);
+  // a row r of slot s: finish (bias, activation, store through perm) or,
+  // under a channel split, store the partial sums to this split's block
+  constexpr int BLK = 8 * R * CC * 64;
+  const uint32_t item = ((img * a.tiles_y.d + ty) * a.tiles_x.d + tx) * a.groups.d + grp;
+  auto finish = [&](int s, int r, float (&v)[CC]) __attribute__((always_inline)) {
+    if (split) {
+      float* pb = a.part + static_cast<size_t>(item * a.ksplit + ks) * BLK + lane;
+#pragma unroll
+      for (int qq = 0; qq < CC; ++qq) pb[((s * R + r) * CC + qq) * 64] = v[qq];
+      return;
+    }
+    const uint32_t o = __builtin_amdgcn_readlane(perm_l, s);
+    const float bias = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, bias_l), s));
+    if (o >= a.c_out) return;   // padding slot
+    const int oy = oy0 + ly * R + r;
+    if (oy >= static_cast<int>(a.ho)) return;
+#pragma unroll
+    for (int qq = 0; qq < CC; ++qq) {
+      v[qq] += bias;
+      if (relu) v[qq] = fmaxf(v[qq], 0.0f);
+    }
+    if (shuf) {
+      float* row2 = y + (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + (o & 1);
+#pragma unroll
+      for (int qq = 0; qq < CC; ++qq)
+        if (oxl + qq < static_cast<int>(a.wo)) row2[2 * (oxl + qq)] = v[qq];
+      return;
+    }
+    float* row = y + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
+    if (vec && oxl + CC <= static_cast<int>(a.wo)) {
+#pragma unroll
+      for (int qq = 0; qq < CC; qq += 4) {
+        float4* pr = reinterpret_cast<float4*>(row + oxl + qq);
+        float4 t = make_float4(v[qq], v[qq + 1], v[qq + 2], v[qq + 3]);
+        if (accum) {
+          const float4 old = *pr;
+          t = make_float4(old.x + t.x, old.y + t.y, old.z + t.z, old.w + t.w);
+        }
+        *pr = t;
+      }
+    } else {
+#pragma unroll
+      for (int qq = 0; qq < CC; ++qq)
+        if (oxl + qq < static_cast<int>(a.wo)) row[oxl + qq] = accum ? row[oxl + qq] + v[qq] : v[qq];
+    }
+  };
+  // rows r, r + 1 of slot s, 2 x 2 max pooled (windows wholly inside the
+  // output; floor), the max taken over the activated values
+  auto finish_pool = [&](int s, int r, float (&v0)[CC], float (&v1)[CC]) __attribute__((always_inline)) {
+    const uint32_t o = __builtin_amdgcn_readlane(perm_l, s);
+    const float bias = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, bias_l), s));
+    if (o >= a.c_out) return;
+    const int oy = oy0 + ly * R + r;
+    if (oy + 1 >= static_cast<int>(a.ho)) return;
+    float* row = y + (static_cast<size_t>(o) * pho + oy / 2) * pwo;
+    float m[CC / 2];
+#pragma unroll
+    for (int j = 0; j < CC / 2; ++j) {
+      float t0 = v0[2 * j] + bias, t1 = v0[2 * j + 1] + bias, t2 = v1[2 * j] + bias, t3 = v1[2 * j + 1] + bias;
+      if (relu) {
+        t0 = fmaxf(t0, 0.0f); t1 = fmaxf(t1, 0.0f); t2 = fmaxf(t2, 0.0f); t3 = fmaxf(t3, 0.0f);
+      }
+      m[j] = fmaxf(fmaxf(t0, t1), fmaxf(t2, t3));
+    }
+#pragma unroll
+    for (int j = 0; j < CC / 2; ++j)
+      if (oxl + 2 * j + 1 < static_cast<int>(a.wo)) row[oxl / 2 + j] = m[j];
+  };
+
+  if constexpr (WS == 1) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      if constexpr (R % 2 == 0 && CC % 2 == 0) {
+        if (pool && !split) {
+#pragma unroll
+          for (int r = 0; r < R; r += 2) finish_pool(s, r, acc[s][r], acc[s][r + 1]);
+          continue;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) finish(s, r, acc[s][r]);
+    }
+  } else {
+    // SPP slots per pass: every wave writes its partial rows, then unit u =
+    // (slot of the pass, row or row pair) is summed over the WS waves in
+    // wave order by wave u % WS
+    constexpr int SPP = G::SPP;
+#pragma unroll
+    for (int s0 = 0; s0 < 8; s0 += SPP) {
+      __syncthreads();
+      {
+        float* dst = lds + wk * SPP * G::XPS + lane;
+#pragma unroll
+        for (int ps = 0; ps < SPP; ++ps)
+#pragma unroll
+          for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int qq = 0; qq < CC; ++qq) dst[((ps * R + r) * CC + qq) * 64] = acc[s0 + ps][r][qq];
+      }
+      __syncthreads();
+      auto gather = [&](int ps, int r, float (&v)[CC]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int qq = 0; qq < CC; ++qq) {
+          float t = 0.0f;
+#pragma unroll
+          for (int k = 0; k < WS; ++k) t += lds[k * SPP * G::XPS + ((ps * R + r) * CC + qq) * 64 + lane];
+          v[qq] = t;
+        }
+      };
+      bool pooled = false;
+      if constexpr (R % 2 == 0 && CC % 2 == 0) {
+        if (pool && !split) {
+          pooled = true;
+          constexpr int NUP = SPP * (R / 2);
+          for (int u = wk; u < NUP; u += WS) {
+            const int ps = u / (R / 2), r = 2 * (u % (R / 2));
+            float v0[CC], v1[CC];
+            gather(ps, r, v0);
+            gather(ps, r + 1, v1);
+            finish_pool(s0 + ps, r, v0, v1);
+          }
+        }
+      }
+      if (!pooled) {
+        constexpr int NU = SPP * R;
+        for (int u = wk; u < NU; u += WS) {
+          const int ps = u / R, r = u % R;
+          float v[CC];
+          gather(ps, r, v);
+          finish(s0 + ps, r, v);
+        }
+      }
+    }
+  }
+}
+
+// Second pass of a channel split: y = act(sum over the ksplit partial-sum
+// blocks of a tile, in split order, + bias), stored through perm; with
+// PP_MAXPOOL2 the 2 x 2 max of the activated sums (windows wholly inside the
+// output).  One workgroup per (image, tile, slot group).
+template <int R, int CC, int LW>
+__global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
+  constexpr int LH = 64 / LW, TH = LH * R, TW = LW * CC;
+  constexpr int BLK = 8 * R * CC * 64;
+  const uint32_t item = blockIdx.x;
+  uint32_t t = fdiv(item, a.groups);
+  const uint32_t grp = item - t * a.groups.d;
+  uint32_t t2 = fdiv(t, a.tiles_x);
+  const uint32_t tx = t - t2 * a.tiles_x.d;
+  t = fdiv(t2, a.tiles_y);
+  const uint32_t ty = t2 - t * a.tiles_y.d;
+  const uint32_t img = t;
+  const float* pb = a.part + static_cast<size_t>(item) * a.ksplit * BLK;
+  const bool relu = (a.flags & PP_RELU) != 0;
+  const uint32_t* perm = reinterpret_cast<const uint32_t*>(a.blob + a.off_perm);
+  const float* biasv = reinterpret_cast<const float*>(a.blob + a.off_bias);
+  auto sum_at = [&](int s, int yl, int xl) {
+    const int ln = (yl / R) * LW + xl / CC;
+    const int e = (s * R + yl % R) * CC + xl % CC;
+    float v = 0.0f;
+    for (uint32_t k = 0; k < a.ksplit; ++k) v += pb[static_cast<size_t>(k) * BLK + e * 64 + ln];
+    v += biasv[grp * 8 + s];
+    return relu ? fmaxf(v, 0.0f) : v;
+  };
+  if (a.flags & PP_MAXPOOL2) {
+    const uint32_t pho = a.ho / 2, pwo = a.wo / 2;
+    float* yp = a.y + static_cast<size_t>(img) * a.c_out * pho * pwo;
+    constexpr int PH = TH / 2, PW = TW / 2;
+    for (int i = threadIdx.x; i < 8 * PH * PW; i += 256) {
+      const int s = i / (PH * PW), px = i % PW, py = (i / PW) % PH;
+      const uint32_t oy = ty * TH + 2 * py, ox = tx * TW + 2 * px;
+      if (oy + 1 >= a.ho || ox + 1 >= a.wo) continue;
+      const uint32_t o = perm[grp * 8 + s];
+      if (o >= a.c_out) continue;
+      const float m = fmaxf(fmaxf(sum_at(s, 2 * py, 2 * px), sum_at(s, 2 * py, 2 * px + 1)),
+                            fmaxf(sum_at(s, 2 * py + 1, 2 * px), sum_at(s, 2 * py + 1, 2 * px + 1)));
+      yp[(static_cast<size_t>(o) * pho + oy / 2) * pwo + ox / 2] = m;
+    }
+    return;
+  }
+  float* y = a.y + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  for (int i = threadIdx.x; i < 8 * TH * TW; i += 256) {
+    const int s = i / (TH * TW), xl = i % TW, yl = (i / TW) % TH;
+    const uint32_t oy = ty * TH + yl, ox = tx * TW + xl;
+    if (oy >= a.ho || ox >= a.wo) continue;
+    const uint32_t o = perm[grp * 8 + s];
+    if (o >= a.c_out) continue;
+    const size_t at = (a.flags & PP_PIXSHUF2)
+                          ? (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + 2 * ox + (o & 1)
+                          : (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
+    const float v = sum_at(s, yl, xl);
+    y[at] = (a.flags & PP_ACCUMULATE) ? y[at] + v : v;
+  }
+}
+
+#ifndef __HIPCC_RTC__   // host side
+template <int R, int CC, int LW, int WS, bool V4>
+hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
+  using G = LGeo<R, CC, LW, WS, V4>;
+  if constexpr (!G::fits) {
+    return hipErrorInvalidConfiguration;
+  } else {
+    if (V4 && (p.w % 4 != 0 || (p.flags & PP_UPSAMPLE2))) return hipErrorInvalidConfiguration;
+    const uint32_t tx = (p.wo + G::TW - 1) / G::TW, ty = (p.ho + G::TH - 1) / G::TH;
+    const uint32_t ng = p.groups.d;
+    if (p.ksplit < 1 || p.ksplit > p.c_in || (p.ksplit > 1 && !p.part)) return hipErrorInvalidValue;
+    if (static_cast<uint64_t>(p.ksplit) * p.c_in >= (1ull << 31)) return hipErrorInvalidValue;   // fdiv range
+    p.tiles_x = make_fastdiv(tx);
+    p.tiles_y = make_fastdiv(ty);
+    p.splits = make_fastdiv(p.ksplit);
+    const size_t nb = static_cast<size_t>(ng) * p.ksplit * tx * ty * n;
+    if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4>), dim3(static_cast<uint32_t>(nb)), dim3(WS * 64), 0, st,
+                       p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.ksplit == 1) return e;
+    hipLaunchKernelGGL((pp_lean_reduce_kernel<R, CC, LW>), dim3(static_cast<uint32_t>(nb / p.ksplit)), dim3(256), 0, st,
+                       p);
+    return hipGetLastError();
+  }
+}
+#endif
+
+}  // namespace kern
+}  // namespace pp

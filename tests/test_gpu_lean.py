@@ -1,0 +1,216 @@
+"""GPU parity of the lean pruned-conv kernel (tilings 40-50: fp32, canonical
+library, stride 1, pad 1, image width a multiple of 4) against the CPU
+oracle, element by element, every filter; fused max pool bitwise against
+pooling the unpooled output of the same plan; forced channel splits; and
+full-width parity on full-size VGG-16 layers.
+
+Every case prints its name, seed and shape before touching the GPU."""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import conv as oconv
+from tests.tolerance import check
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+pp = pytest.importorskip("paper_2004_11250_amd")
+
+# tilings 40-50 stage the halo by 16-byte DMAs (image width a multiple of
+# 4), 51-57 by 4-byte DMAs (any width)
+LEAN = list(range(40, 58))
+V4 = set(range(40, 51))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    pp.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _run(L, x, relu=True, maxpool2=False):
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+    xd = torch.from_numpy(np.ascontiguousarray(x, np.float32)).cuda()
+    y = pp.conv2d_fwd(layer, xd, relu=relu, maxpool2=maxpool2)
+    torch.cuda.synchronize()
+    return layer, xd, y
+
+
+# shapes: (c_out, c_in, h, w): ragged tiles in both directions, c_out not a
+# multiple of 8 (padding slots), fewer channels than waves, 2 images; odd
+# and not-multiple-of-4 widths for the 4-byte staging tilings
+SHAPES = [(19, 21, 37, 44), (16, 64, 32, 32), (24, 5, 20, 40), (8, 40, 70, 68)]
+SHAPES_B32 = [(19, 21, 37, 45), (16, 64, 14, 14), (24, 5, 21, 30), (8, 40, 33, 17)]
+
+
+@pytest.mark.parametrize("recipe", LEAN)
+def test_lean_tiling(recipe, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    for si, (c_out, c_in, h, w) in enumerate(SHAPES + ([] if recipe in V4 else SHAPES_B32)):
+        seed = 1000 + 10 * recipe + si
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+        used = pp.conv2d_recipe(blob, 2, h, w, pp.PP_F32)
+        _say("lean tiling", recipe, "runs as", used, "seed", seed, (c_out, c_in, h, w))
+        assert used == recipe
+        for relu in (True, False):
+            _, _, y = _run(L, x, relu=relu)
+            got = y.cpu().numpy().astype(np.float64)
+            args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+            ref = oconv.conv3x3_pruned(*args, 1, 1, 1, relu)
+            bound = oconv.conv3x3_bound(*args, 1, 1, 1)
+            check(got, ref, bound, "f32", f"lean {recipe} {(c_out, c_in, h, w)} relu={relu}")
+
+
+# (tiling 54 has one output row per lane: it pools only under a channel split)
+@pytest.mark.parametrize("recipe", [r for r in LEAN if r != 54])
+def test_lean_fused_maxpool(recipe, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    shapes = [(19, 21, 37, 44), (16, 24, 30, 44), (8, 33, 64, 64)]
+    if recipe not in V4:
+        shapes += [(16, 24, 14, 14), (8, 19, 29, 31)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 2000 + 10 * recipe + si
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        _say("lean fused maxpool", recipe, "seed", seed, (c_out, c_in, h, w))
+        layer, xd, yp = _run(L, x, maxpool2=True)
+        args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        ref = oconv.maxpool2(oconv.conv3x3_pruned(*args, 1, 1, 1, True))
+        bound = oconv.maxpool2(oconv.conv3x3_bound(*args, 1, 1, 1))
+        check(yp.cpu().numpy().astype(np.float64), ref, bound, "f32", f"lean pool {recipe}")
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, pp.PP_F32)
+        assert plan[0] == recipe
+        y = pp.conv2d_fwd(layer, xd, relu=True)
+        pooled = torch.nn.functional.max_pool2d(y.cpu(), 2)
+        assert torch.equal(yp.cpu(), pooled), f"lean {recipe}: fused pool differs from pooling the output"
+
+
+@pytest.mark.parametrize("recipe,ksplit", [(40, 2), (45, 3), (47, 4), (48, 2), (49, 5), (42, 2), (51, 2), (52, 4),
+                                           (54, 3), (55, 2)])
+def test_lean_channel_split(recipe, ksplit, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    shapes = [(21, 77, 29, 36), (16, 64, 12, 16), (24, 40, 28, 28)]
+    if recipe not in V4:
+        shapes += [(16, 64, 14, 14), (21, 77, 29, 35)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 3000 + 10 * recipe + si
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.4)
+        x = workloads.random_input(seed, (1, c_in, h, w))
+        blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+        used = pp.conv2d_plan(blob, 1, h, w, pp.PP_F32)
+        _say("lean split", recipe, ksplit, "seed", seed, (c_out, c_in, h, w), "runs as", used)
+        assert used == (recipe, ksplit)
+        args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        for pool in (False, True):
+            layer, xd, y = _run(L, x, maxpool2=pool)
+            ref = oconv.conv3x3_pruned(*args, 1, 1, 1, True)
+            bound = oconv.conv3x3_bound(*args, 1, 1, 1)
+            if pool:
+                ref, bound = oconv.maxpool2(ref), oconv.maxpool2(bound)
+            check(y.cpu().numpy().astype(np.float64), ref, bound, "f32", f"lean split {recipe}/{ksplit} pool={pool}")
+        y1 = pp.conv2d_fwd(layer, xd, relu=True)
+        y2 = pp.conv2d_fwd(layer, xd, relu=True)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y2), "repeated split calls must be bitwise equal"
+
+
+# conv + activation fused with a residual add (PP_ACCUMULATE) or a pixel
+# shuffle (PP_PIXSHUF2): against the oracle conv followed by the op, and
+# bitwise against the same plan's plain store followed by the op in torch;
+# forced splits take the epilogue in the second pass
+@pytest.mark.parametrize("recipe,ksplit", [(r, 0) for r in LEAN] + [(40, 3), (48, 2), (54, 2), (52, 4)])
+@pytest.mark.parametrize("mode", ["add", "pshuf2"])
+def test_lean_fused_add_pixshuf(mode, recipe, ksplit, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    shapes = [(20, 21, 37, 44, True), (16, 24, 30, 44, False)]
+    if recipe not in V4:
+        shapes += [(8, 13, 29, 35, True)]
+    for si, (c_out, c_in, h, w, relu) in enumerate(shapes):
+        seed = 4000 + 10 * recipe + si + (5 if mode == "add" else 0)
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        _say("lean fused", mode, "recipe", recipe, "ksplit", ksplit, "seed", seed, (c_out, c_in, h, w), "relu", relu)
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+        xd = torch.from_numpy(x).cuda()
+        args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        cref = oconv.conv3x3_pruned(*args, 1, 1, 1, relu)
+        cbound = oconv.conv3x3_bound(*args, 1, 1, 1)
+        if mode == "add":
+            r = workloads.random_input(seed + 1, (2, c_out, h, w))
+            rd = torch.from_numpy(r).cuda()
+            yd = rd.clone()
+            pp.conv2d_fwd(layer, xd, relu=relu, out=yd, accumulate=True)
+            ref, bound = cref + r.astype(np.float64), cbound + np.abs(r.astype(np.float64))
+        else:
+            yd = pp.conv2d_fwd(layer, xd, relu=relu, pixshuf2=True)
+            ref, bound = oconv.pixel_shuffle2(cref), oconv.pixel_shuffle2(cbound)
+        torch.cuda.synchronize()
+        check(yd.cpu().numpy().astype(np.float64), ref, bound, "f32", f"lean fused {mode} recipe {recipe}")
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, pp.PP_F32)
+        assert plan[0] == recipe and (not ksplit or plan[1] == ksplit)
+        y = pp.conv2d_fwd(layer, xd, relu=relu)
+        want = rd + y if mode == "add" else torch.nn.functional.pixel_shuffle(y, 2)
+        torch.cuda.synchronize()
+        assert torch.equal(yd.cpu(), want.cpu()), f"lean {recipe}: fused {mode} differs from the op after the conv"
+
+
+# convolving the nearest x2 upsampling of x read on the fly (PP_UPSAMPLE2,
+# 4-byte staging tilings), alone and with a fused add or max pool: against
+# the oracle conv of the upsampled input, and bitwise against the same plan
+# run on the upsampled tensor
+@pytest.mark.parametrize("recipe,ksplit", [(51, 0), (52, 0), (53, 0), (55, 0), (56, 0), (57, 0), (54, 2), (52, 3)])
+@pytest.mark.parametrize("mode", ["plain", "add", "maxpool2"])
+def test_lean_fused_upsample(mode, recipe, ksplit, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    for si, (c_out, c_in, h, w) in enumerate([(16, 21, 13, 22), (12, 9, 15, 16), (8, 24, 14, 14)]):
+        seed = 5000 + 10 * recipe + si
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        xu = np.ascontiguousarray(np.repeat(np.repeat(x, 2, axis=2), 2, axis=3))
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+        _say("lean fused upsample", mode, "recipe", recipe, "ksplit", ksplit, "seed", seed, (c_out, c_in, h, w))
+        args = (xu, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        ref = oconv.conv3x3_pruned(*args, 1, 1, 1, True)
+        bound = oconv.conv3x3_bound(*args, 1, 1, 1)
+        xd = torch.from_numpy(x).cuda()
+        kw = dict(relu=True, upsample2=True)
+        if mode == "add":
+            r = workloads.random_input(seed + 1, (2, c_out, 2 * h, 2 * w))
+            rd = torch.from_numpy(r).cuda()
+            yd = rd.clone()
+            pp.conv2d_fwd(layer, xd, out=yd, accumulate=True, **kw)
+            ref, bound = ref + r.astype(np.float64), bound + np.abs(r.astype(np.float64))
+        elif mode == "maxpool2":
+            yd = pp.conv2d_fwd(layer, xd, maxpool2=True, **kw)
+            ref, bound = oconv.maxpool2(ref), oconv.maxpool2(bound)
+        else:
+            yd = pp.conv2d_fwd(layer, xd, **kw)
+        torch.cuda.synchronize()
+        check(yd.cpu().numpy().astype(np.float64), ref, bound, "f32", f"lean upsample {mode} recipe {recipe}")
+        plan = pp.conv2d_plan(layer.h_blob, 2, 2 * h, 2 * w, pp.PP_F32)
+        assert plan[0] == recipe
+        if mode == "maxpool2" and recipe == 54 and not ksplit:
+            continue   # one output row per lane: pools only under a split
+        y = pp.conv2d_fwd(layer, torch.from_numpy(xu).cuda(), relu=True)
+        if mode == "add":
+            want = rd + y
+        elif mode == "maxpool2":
+            want = torch.nn.functional.max_pool2d(y, 2)
+        else:
+            want = y
+        torch.cuda.synchronize()
+        assert torch.equal(yd.cpu(), want.cpu()), f"lean {recipe}: fused upsample ({mode}) differs"
