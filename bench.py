@@ -32,9 +32,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-PEAK_FP32_VECTOR_TFLOPS = 157.3     # MI355X: 256 CU x 2.4 GHz x 256 FLOP/clk; plain (non-packed) wave64
-                                    # v_fmac_f32 issues every 2 cycles per SIMD on gfx950, so this is the
-                                    # FMA peak of the kernels here (built without packed FP32)
+PEAK_FP32_VECTOR_TFLOPS = 157.3     # MI355X: 256 CU x 2.4 GHz x 256 FLOP/clk.  gfx950 retires a plain
+                                    # (non-packed) wave64 v_fmac_f32 in about 2 cycles per SIMD with enough
+                                    # waves, so this is the FMA peak of the kernels here (built without packed
+                                    # FP32); the measured ceiling (libppceil.so) is reported beside it
 PEAK_HBM_GBS = 8000.0
 PEAK_BF16_MFMA_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak
 MFMA_RECIPE = 64                    # pp_conv2d_recipe id of the bf16 matrix-core form
@@ -87,7 +88,8 @@ def surviving_macs(op, prm, oshape, batch):
 
 
 KERNEL_SOURCES = ("conv_pp_kernel.hpp", "conv_pp_inst.hpp", "conv_pp.hpp", "conv_plan.cpp", "conv_pp_c8_s1d1.hip",
-                  "conv_pp_wave.hpp", "conv_pp_wave_inst.hpp", "conv_pp_wave_s1d1.hip", "conv_pp_wave_d9_s1d1.hip")
+                  "conv_pp_wave.hpp", "conv_pp_wave_inst.hpp", "conv_pp_wave_s1d1.hip", "conv_pp_wave_d9_s1d1.hip",
+                  "conv_pp_lean.hpp", "conv_pp_lean.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pp_conv3x3_vgg16_224x224_b1_traffic.json")
 
 
@@ -153,7 +155,7 @@ def summarize_profile(root, cfg=2):
 
         first = next(i for i, e in enumerate(ds) if is_conv(e))
         out = []
-        while len(out) < 3 and first < len(ds) and is_conv(ds[first]):
+        while len(out) < 400 and first < len(ds) and is_conv(ds[first]):
             fr, j = [], first
             for _ in range(n_disp):
                 if j >= len(ds):
@@ -200,9 +202,11 @@ def summarize_profile(root, cfg=2):
                             kernel=f"(fused into op {into})", us=0.0, fetch_mb=0.0, write_mb=0.0, sq={}))
             continue
         di += 1
-        dur = sum(f[di]["dur_ns"] for f in kt_fr) / len(kt_fr) / 1e3
-        fetch = sum(f[di]["c"]["FETCH_SIZE"] for f in fe_fr) / len(fe_fr) * ff * 1024
-        write = sum(f[di]["c"]["WRITE_SIZE"] for f in wr_fr) / len(wr_fr) * wf * 1024
+        # steady state: the median over every frame of the run (the first,
+        # warm-up frames of a trace run several times slower)
+        dur = float(np.median([f[di]["dur_ns"] for f in kt_fr])) / 1e3
+        fetch = float(np.median([f[di]["c"]["FETCH_SIZE"] for f in fe_fr])) * ff * 1024
+        write = float(np.median([f[di]["c"]["WRITE_SIZE"] for f in wr_fr])) * wf * 1024
         kind = ("up2+" if fused.get(i - 1) == "up2" else "") + op["op"] + \
             ("+" + fused[i + 1] if i + 1 in fused and fused[i + 1] != "up2" else "")
         lay.append(dict(op=i, kind=kind, lib=op.get("lib", ""), c_in=ish[0], c_out=osh[0], hw=f"{osh[1]}x{osh[2]}",
@@ -211,7 +215,7 @@ def summarize_profile(root, cfg=2):
     pr = [l for l in lay if l["kind"].startswith("conv3") and l["lib"] == "canon8"]
     traffic = dict(kernel_source_sha256=kernel_source_hash(), fetch_factor=round(ff, 4), write_factor=round(wf, 4),
                    launches=len(pr), bytes_per_frame=int(sum((l["fetch_mb"] + l["write_mb"]) * 1e6 for l in pr)),
-                   us_per_frame=round(sum(l["us"] for l in pr), 3),
+                   us_per_frame=round(sum(l["us"] for l in pr), 3), frames_traced=len(kt_fr),
                    layers=[{k: v for k, v in l.items() if k != "sq"} for l in pr])
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(traffic, fh, indent=1)
@@ -229,6 +233,123 @@ def summarize_profile(root, cfg=2):
           f"{traffic['bytes_per_frame'] / 1e6:.2f} MB HBM traffic")
 
 
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def measured_ceilings():
+    """fp32 FMA throughput (TFLOP/s) and HBM copy bandwidth (GB/s, read +
+    write) measured on this GPU by libppceil.so's micro-benchmarks."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2004_11250_amd", "libppceil.so")
+    if not os.path.exists(path):
+        return {}
+    lib = ctypes.CDLL(path)
+    lib.pp_ceiling_fma.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    lib.pp_ceiling_copy.argtypes = [ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    f, c = ctypes.c_double(0), ctypes.c_double(0)
+    out = {}
+    if lib.pp_ceiling_fma(256, ctypes.byref(f)) == 0:
+        out["fma_tflops"] = round(f.value, 2)
+    if lib.pp_ceiling_copy(1 << 30, 5, ctypes.byref(c)) == 0:
+        out["copy_gbs"] = round(c.value, 1)
+    return out
+
+
+def other_workloads(dev, no_dense, steps=10, warmup=3):
+    """ms/frame of the other evaluated networks (style transfer, super
+    resolution, colourization; fp32, and bf16 where the workload has it) and
+    of the same masked models run dense through torch, for the speedup."""
+    import torch
+    import torch.nn.functional as F
+
+    import paper_2004_11250_amd as pp
+    import workloads
+    stream = torch.cuda.current_stream()
+    out = []
+    for cfg, dts in ((3, ("f32",)), (4, ("f32", "bf16")), (5, ("f32", "bf16"))):
+        spec = workloads.net_spec(cfg)
+        params = workloads.net_params(cfg)
+        shapes = layer_shapes(spec)
+        for dtype in dts:
+            tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+            net = pp.Net(spec["ops"], params, dtype, device=dev)
+            x = torch.from_numpy(workloads.net_input(cfg)).to(dev).to(tdt)
+            nbytes, oshape = net.plan(*x.shape)
+            ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+            y = torch.empty(oshape, dtype=tdt, device=dev)
+
+            def timed(fn):
+                for _ in range(warmup):
+                    fn()
+                torch.cuda.synchronize()
+                a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a0.record(stream)
+                for _ in range(steps):
+                    fn()
+                a1.record(stream)
+                torch.cuda.synchronize()
+                return a0.elapsed_time(a1) / steps
+
+            ms = timed(lambda: net.forward(x, y, ws))
+            macs = sum(surviving_macs(op, prm, o, spec["batch"]) for (i, op, _, o), prm in zip(shapes, params))
+            entry = dict(workload=WORKLOADS[cfg], dtype=dtype, ms_per_frame=round(ms, 4),
+                         eff_gmacs=round(macs / (ms * 1e-3) / 1e9, 1))
+            if not no_dense:
+                dw = []
+                for (i, op, _, o), prm in zip(shapes, params):
+                    if op["op"] == "conv3":
+                        m = np.zeros(prm["conn"].shape + (9,), np.float32)
+                        for pi, mask in enumerate(prm["lib"]):
+                            bits = np.array([(int(mask) >> t) & 1 for t in range(9)], np.float32)
+                            m[(prm["pid"] == pi) & (prm["conn"] != 0)] = bits
+                        dw.append((torch.from_numpy(prm["w"] * m.reshape(prm["w"].shape)).to(dev).to(tdt),
+                                   torch.from_numpy(prm["b"]).to(dev).to(tdt)))
+                    elif op["op"] in ("conv", "deconv"):
+                        dw.append((torch.from_numpy(prm["w"]).to(dev).to(tdt), torch.from_numpy(prm["b"]).to(dev).to(tdt)))
+                    else:
+                        dw.append(None)
+
+                def dense_frame():
+                    sl = {0: x}
+                    for (i, op, _, o), wb in zip(shapes, dw):
+                        src = sl[op["src"]]
+                        if op["op"] in ("conv3", "conv"):
+                            r = F.conv2d(src, wb[0], wb[1], stride=op["stride"], padding=op["pad"], dilation=op["dil"])
+                            r = torch.relu(r) if op["relu"] else r
+                        elif op["op"] == "deconv":
+                            r = F.conv_transpose2d(src, wb[0], wb[1], stride=op["stride"], padding=op["pad"])
+                            r = torch.relu(r) if op["relu"] else r
+                        elif op["op"] == "maxpool2":
+                            r = F.max_pool2d(src, 2)
+                        elif op["op"] == "up2":
+                            r = F.interpolate(src, scale_factor=2, mode="nearest")
+                        elif op["op"] == "pshuf2":
+                            r = F.pixel_shuffle(src, 2)
+                        else:
+                            r = src + sl[op["src2"]]
+                        sl[op["dst"]] = r
+                    return sl[1]
+
+                torch.backends.cudnn.benchmark = True
+                with torch.no_grad():
+                    dms = timed(dense_frame)
+                entry.update(dense_ms_per_frame=round(dms, 4), speedup=round(dms / ms, 3))
+                del dw
+            out.append(entry)
+            del net, ws, y, x
+            torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -244,6 +365,9 @@ def main():
                          "much), the reference for scaling hardware byte counters")
     ap.add_argument("--summarize-profile", metavar="DIR", default=None,
                     help="summarise rocprofv3 output under DIR (no GPU needed) and exit")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the other workloads' frame times (configs 3-5, reported beside the headline)")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the measured FMA / HBM ceilings")
     args = ap.parse_args()
     if args.summarize_profile:
         summarize_profile(args.summarize_profile, args.config)
@@ -300,6 +424,16 @@ def main():
     torch.cuda.synchronize()
     wall_ms = (time.time() - t_wall) * 1e3 / args.steps
     ms = e0.elapsed_time(e1) / args.steps
+    # per-frame distribution: the same frames, each between its own events
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for i in range(args.steps):
+        net.forward(x, y, ws)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    frame_pct = dict(p10=round(float(np.percentile(per, 10)), 5), p50=round(float(np.percentile(per, 50)), 5),
+                     p90=round(float(np.percentile(per, 90)), 5), frames=args.steps)
     graph = net.capture(x, y, ws)
     for _ in range(args.warmup):
         graph.replay()
@@ -380,10 +514,14 @@ def main():
             t = json.load(fh)
         if t.get("kernel_source_sha256") == kernel_source_hash():
             traffic = t["bytes_per_frame"]
+    ceil = measured_ceilings() if not args.no_ceilings else {}
     roofline = dict(bound="alu", achieved=round(achieved, 3), peak=PEAK_FP32_VECTOR_TFLOPS, unit="TFLOP/s",
                     frac=round(achieved / PEAK_FP32_VECTOR_TFLOPS, 4), traffic=traffic,
                     kernel=f"pattern-pruned 3x3 conv kernels (the {len(pr)} pruned layers on the vector ALUs, "
                            "summed over the frame)")
+    if ceil.get("fma_tflops"):
+        roofline.update(peak_measured=ceil["fma_tflops"], frac_measured=round(achieved / ceil["fma_tflops"], 4),
+                        hbm_measured_gbs=ceil.get("copy_gbs"))
     if mf_us > pr_us:
         # the bf16 matrix-core form dominates: its contraction (the masked
         # dense conv) against the bf16 dense matrix peak
@@ -455,10 +593,11 @@ def main():
     # ---- CPU oracle baseline (rank 0, N=1)
     cpu = None
     if not args.no_cpu:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
 
         from oracle import net as onet
         x_np = workloads.net_input(cfg)
+        affinity = len(os.sched_getaffinity(0))
         reps, t_cpu = 0, 0.0
         while t_cpu < 10.0 and reps < 20:
             t = time.time()
@@ -466,9 +605,21 @@ def main():
             t_cpu += time.time() - t
             reps += 1
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        cpu = dict(value=round(total_macs * reps / t_cpu / 1e9, 4), unit="GMAC/s", cores=int(threads), kind="oracle",
-                   sample=f"{reps} full frame(s) of the same workload through the fp64 oracle "
-                          f"({t_cpu:.1f} s, {t_cpu / reps * 1e3:.0f} ms/frame)")
+        # the same frame on one core (one BLAS thread), one frame
+        with threadpool_limits(limits=1):
+            t = time.time()
+            onet.run_net(spec, params, x_np, dtype)
+            t1 = time.time() - t
+        cpu = dict(value=round(total_macs * reps / t_cpu / 1e9, 4), unit="GMAC/s", cores=int(min(threads, affinity)),
+                   kind="oracle", affinity_cpus=affinity, cpu_model=cpu_model(),
+                   one_core=dict(value=round(total_macs / t1 / 1e9, 4), unit="GMAC/s", ms_per_frame=round(t1 * 1e3, 1)),
+                   sample=f"{reps} full frame(s) of the same workload through the fp64 oracle on "
+                          f"{min(threads, affinity)} BLAS threads ({t_cpu:.1f} s, {t_cpu / reps * 1e3:.0f} ms/frame), "
+                          f"and one frame on one thread ({t1:.1f} s)")
+
+    others = None
+    if not args.no_others and cfg == 2 and dtype == "f32":
+        others = other_workloads(dev, args.no_dense)
 
     line = dict(metric="effective GMAC/s (surviving MACs) per pruned 3x3 layer; ms/frame VGG-16 batch 1",
                 value=round(value, 3), unit="GMAC/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
@@ -477,9 +628,9 @@ def main():
                 config=dict(workload=WORKLOADS[cfg], batch=batch, input=[spec["c"], spec["h"], spec["w"]],
                             surviving_gmac_per_frame=round(total_macs / 1e9, 4), library="canon8 4-of-9",
                             parallelism="single GPU"),
-                wall_ms_per_step=round(wall_ms, 5), ms_per_step_graph_replay=round(ms_graph, 5),
-                pack_s=round(pack_s, 3),
-                roofline=roofline, cpu_baseline=cpu, dense=dense, layers=layers)
+                wall_ms_per_step=round(wall_ms, 5), ms_per_frame_pct=frame_pct,
+                ms_per_step_graph_replay=round(ms_graph, 5), pack_s=round(pack_s, 3),
+                roofline=roofline, cpu_baseline=cpu, dense=dense, other_workloads=others, layers=layers)
     print(json.dumps(line), flush=True)
 
 

@@ -191,6 +191,98 @@ def test_invariants():
     assert np.array_equal(conv.conv3x3_pruned(x * 8.0, *args0), 8.0 * conv.conv3x3_pruned(x, *args0))
 
 
+# ----------------------------------------------------------------------------
+# the tolerance scale S = |b| + sum |M W| |x| (the bound every GPU parity check
+# scales by), pinned two ways: exactly on the hand example, where x and W are
+# positive so S is the pre-activation output with |b| in place of b; and
+# against torch float64 convolutions of |x| and |W M| (M built by loops here)
+# plus |b|, for the pruned, dense and transposed bounds.  The planted-mistake
+# test below checks that an S over the unmasked weights, or without |b|,
+# fails these pins.
+# ----------------------------------------------------------------------------
+
+def pin_bound_appendix(mod=conv):
+    cases = {prm["name"]: (prm, e) for prm, e in appendix_cases()}
+    pre = cases["P0_b0"][1]                           # pattern 0x03A, b = 0: y_pre
+    for name, (prm, expect) in cases.items():
+        lib = np.array([prm["mask"]], dtype=np.uint16)
+        b = np.array([prm["bias"]], np.float32)
+        s_ = mod.conv3x3_bound(X5, W5, b, np.zeros((1, 1), np.uint8), np.ones((1, 1), np.uint8), lib,
+                               prm["stride"], prm["pad"], prm["dil"])[0, 0]
+        if name == "P0_relu":
+            want = pre + 150.0                        # b = -150
+        elif name == "P0_s2":
+            want = pre[::2, ::2] + 150.0
+        else:
+            want = expect                             # b = 0, no ReLU: S is the output itself
+        if s_.shape != want.shape or not np.array_equal(s_, want):
+            return False
+    return True
+
+
+def pin_bound_torch(mod=conv, seeds=range(4)):
+    for seed in seeds:
+        rng = np.random.default_rng(300 + seed)
+        c_out, c_in = int(rng.integers(2, 7)), int(rng.integers(2, 7))
+        stride, dil = int(rng.integers(1, 3)), int(rng.integers(1, 3))
+        pad = int(rng.integers(0, 2 * dil + 1))
+        h, w = int(rng.integers(5, 12)), int(rng.integers(5, 12))
+        L = workloads.random_layer(300 + seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(300 + seed, (2, c_in, h, w))
+        wm = np.abs(L["w"].astype(np.float64) * _mask_by_loop(L["pid"], L["conn"], L["lib"]))
+        ref = _torch_conv(np.abs(x), wm, np.abs(L["b"]), stride, pad, dil)
+        s_ = mod.conv3x3_bound(x, L["w"], L["b"], L["pid"], L["conn"], L["lib"], stride, pad, dil)
+        if s_.shape != ref.shape or np.any(np.abs(s_ - ref) > 1e-12 * ref):
+            return False
+        # dense k x k and transposed bounds (mixed-sign weights and biases)
+        wd = rng.normal(size=(c_out, c_in, 3, 3))
+        bd = rng.normal(size=c_out)
+        ref = _torch_conv(np.abs(x), np.abs(wd), np.abs(bd), 1, 1, 1)
+        if np.any(np.abs(mod.conv2d_bound(x, wd, bd, 1, 1, 1) - ref) > 1e-12 * ref):
+            return False
+        wt = rng.normal(size=(c_in, c_out, 4, 4))
+        ref = F.conv_transpose2d(torch.from_numpy(np.abs(x).astype(np.float64)), torch.from_numpy(np.abs(wt)),
+                                 torch.from_numpy(np.abs(bd)), stride=2, padding=1).numpy()
+        if np.any(np.abs(mod.conv_transpose2d_bound(x, wt, bd, 2, 1) - ref) > 1e-12 * ref):
+            return False
+    return True
+
+
+def test_bound_exact_on_hand_example():
+    assert pin_bound_appendix()
+
+
+def test_bound_equals_abs_conv_torch():
+    assert pin_bound_torch()
+
+
+class _BoundMutant:
+    """The oracle's conv module with a planted mistake in the tolerance scale."""
+
+    def __init__(self, kind):
+        self.kind = kind
+
+    def conv3x3_bound(self, x, w, b, pid, conn, lib, stride=1, pad=1, dil=1):
+        if self.kind == "unmasked":                 # S over the dense |W|
+            return conv.conv2d_bound(x, w, b, stride, pad, dil)
+        if self.kind == "no_bias":                  # S without |b|
+            return conv.conv3x3_bound(x, w, None, pid, conn, lib, stride, pad, dil)
+        return conv.conv3x3_bound(x, w, b, pid, conn, lib, stride, pad, dil)
+
+    def conv2d_bound(self, x, w, b=None, stride=1, pad=0, dil=1):
+        return conv.conv2d_bound(x, w, None if self.kind == "no_bias" else b, stride, pad, dil)
+
+    def conv_transpose2d_bound(self, x, w, b=None, stride=2, pad=1):
+        return conv.conv_transpose2d_bound(x, w, None if self.kind == "no_bias" else b, stride, pad)
+
+
+@pytest.mark.parametrize("kind", ["unmasked", "no_bias"])
+def test_planted_bound_mistake_is_caught(kind):
+    mut = _BoundMutant(kind)
+    assert not pin_bound_appendix(mut)
+    assert not pin_bound_torch(mut)
+
+
 def test_bound_dominates_result():
     L = workloads.random_layer(12, 6, 5)
     x = workloads.random_input(12, (2, 5, 8, 8))

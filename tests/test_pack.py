@@ -59,15 +59,19 @@ def test_random_layers_bytes_match_oracle(wd):
         assert a.tobytes() == o, trial
 
 
-def test_config_layers_bytes_match_oracle():
-    for cfg in (1, 2, 5):
-        spec = workloads.net_spec(cfg)
-        for i, op in enumerate(spec["ops"]):
-            if op["op"] != "conv3" or op["c_in"] * op["c_out"] > 256 * 256:
-                continue
-            prm = workloads.layer_params(cfg, i, op)
-            args = (prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"], op["stride"], op["pad"], op["dil"])
-            assert pp.pack(*args).tobytes() == ppk1.pack(*args), (cfg, i)
+# every pruned (and all-ones) 3x3 layer of the five workloads, in both weight
+# dtypes, byte for byte: the largest blobs (512 x 512 layers: the most slot
+# groups and the largest weight offsets) included
+@pytest.mark.parametrize("wd", [0, 1])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_config_layers_bytes_match_oracle(cfg, wd):
+    spec = workloads.net_spec(cfg)
+    for i, op in enumerate(spec["ops"]):
+        if op["op"] != "conv3":
+            continue
+        prm = workloads.layer_params(cfg, i, op)
+        args = (prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"], op["stride"], op["pad"], op["dil"], wd)
+        assert pp.pack(*args).tobytes() == ppk1.pack(*args), (cfg, i, wd)
 
 
 def test_bf16_rounding_ties_match_oracle():
