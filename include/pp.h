@@ -228,6 +228,23 @@ pp_status pp_conv2d_fwd(const void* h_blob, size_t blob_bytes, const void* d_blo
                         void* hip_stream);
 
 /*
+ * pp_conv2d_fwd_noalloc -- pp_conv2d_fwd for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation): the same plan and result as pp_conv2d_fwd with a
+ * pp_conv2d_workspace()-sized workspace, the scratch taken from a 16 MiB
+ * array in device memory that the library holds on each device it runs on
+ * until the process ends.  The call allocates nothing.  Every call on one
+ * GPU shares that GPU's array: calls that overlap on one GPU (different
+ * streams, host threads) race, so order them on one stream.  Arguments as
+ * pp_conv2d_fwd without the workspace.  Errors: as pp_conv2d_fwd, PP_ESIZE
+ * (the layer needs more than 16 MiB of scratch), PP_EHIP (the array's device
+ * address could not be found).
+ */
+pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes, const void* d_blob,
+                                const void* x, void* y, int32_t n, int32_t h, int32_t w,
+                                int32_t act_dtype, uint32_t flags, void* hip_stream);
+
+/*
  * pp_conv2d_workspace -- device scratch bytes pp_conv2d_fwd can use for this
  * layer and input (0: it would not use any); h, w are the conv's input size
  * (for a PP_UPSAMPLE2 call the upsampled size 2h x 2w; a call with fused

@@ -31,7 +31,7 @@ PP_UPSAMPLE2 = 16
 SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_workspace", "pp_conv2d_recipe",
            "pp_conv2d_out_size", "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error",
            "pp_project_patterns", "pp_project_connectivity", "pp_project_columns", "pp_column_library",
-           "pp_fold_bn", "pp_jit_library")
+           "pp_fold_bn", "pp_jit_library", "pp_conv2d_fwd_noalloc")
 
 
 class PPError(RuntimeError):
@@ -71,6 +71,7 @@ def load_library(path: str = LIB_PATH):
     lib.pp_blob_info.argtypes = [vp, sz, ctypes.POINTER(LayerDesc), ctypes.POINTER(i32),
                                  ctypes.POINTER(ctypes.c_int64)]
     lib.pp_conv2d_fwd.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp, sz, vp]
+    lib.pp_conv2d_fwd_noalloc.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp]
     lib.pp_conv2d_workspace.argtypes = [vp, sz, i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.pp_conv2d_out_size.argtypes = [vp, sz, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.pp_conv2d_recipe.argtypes = [vp, sz, i32, i32, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
