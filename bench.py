@@ -127,7 +127,8 @@ def summarize_profile(root, cfg=2):
     import paper_2004_11250_amd as pp
     import workloads
     spec = workloads.net_spec(cfg)
-    fused = pp.fused_ops(spec["ops"])
+    fused = pp.net_plan(spec["ops"], workloads.net_params(cfg), spec["batch"], spec["c"], spec["h"],
+                        spec["w"])["fused"]
     n_disp = len(spec["ops"]) - len(fused)
     shapes = layer_shapes(spec)
 
@@ -456,7 +457,7 @@ def main():
     li = 0
     esz = 2 if dtype == "bf16" else 4
     pdt = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
-    fused = pp.fused_ops(spec["ops"])
+    fused = net.launch_plan(spec["batch"], spec["c"], spec["h"], spec["w"])["fused"]
     for (i, op, ishape, o), prm in zip(shapes, params):
         if op["op"] != "conv3":
             continue

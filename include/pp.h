@@ -164,7 +164,14 @@ pp_status pp_fold_bn(float* w, float* bias, int32_t c_out, int32_t k_elems, cons
                      const float* beta, const float* mean, const float* var, float eps);
 
 /*
- * pp_blob_info -- validate a host copy of a blob and return its description.
+ * pp_blob_info -- validate a host copy of a blob (the compact stored model
+ * of Sec. 3, "Sparse model storage": kept weights only, filters in their
+ * reordered sequence of "Matrix reorder", per-kernel pattern codes in place
+ * of per-weight indices) and return its description.
+ *   h_blob, bytes  host blob as written by pp_pack; read only
+ *   d              out: shape and storage of the layer
+ *   n_kept         out: kernels kept by connectivity pruning (Sec. 2)
+ *   n_wt           out: stored weights (the kept kernels' pattern taps summed)
  * Any output pointer may be NULL.  Errors: PP_EINVAL (blob NULL), PP_EBLOB
  * (bad magic/version, sizes or offsets inconsistent with `bytes`, woff not
  * monotone, a code >= n_patterns, a perm entry out of range).
@@ -173,7 +180,12 @@ pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_desc* d,
                        int32_t* n_kept, int64_t* n_wt);
 
 /*
- * pp_conv2d_fwd -- y = act(conv3x3_pruned(x) + bias) for one packed layer.
+ * pp_conv2d_fwd -- y = act(conv3x3_pruned(x) + bias) for one packed layer:
+ * the 3x3 convolution whose kernels keep only the taps of their pattern
+ * and whose connectivity-pruned kernels are absent (Sec. 2, "Structured
+ * Model Pruning"), run from the compact reordered storage (Sec. 3, "Sparse
+ * model storage", "Matrix reorder") with the bias and activation fused
+ * into the same launch (Sec. 3, "DSL related optimization").
  *   h_blob, blob_bytes  host copy of the blob (its header is read here, so no
  *                       device-to-host copy is needed)
  *   d_blob              the same bytes in device memory, 256-byte aligned
@@ -352,6 +364,36 @@ pp_status pp_net_workspace(const pp_net_op* ops, int32_t n_ops, int32_t n, int32
 pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void* x, void* y,
                      int32_t n, int32_t c, int32_t h, int32_t w, int32_t act_dtype,
                      void* workspace, size_t ws_bytes, void* hip_stream);
+
+/*
+ * pp_net_plan -- how pp_net_fwd runs this op list for this input shape: the
+ * graph-level fusion it applies (Sec. 3, "DSL related optimization": a conv
+ * and the cheap op next to it become one launch) and the tiling of each
+ * pruned conv.  Host-only; reads the host blobs and the op fields, never a
+ * device pointer (those may be NULL here).
+ *   op_flags  host u32 [n_ops], written: for a pruned conv, the fusion flags
+ *             its launch carries (PP_UPSAMPLE2: it takes the upsample before
+ *             it; PP_MAXPOOL2, PP_PIXSHUF2 or PP_ACCUMULATE: it takes the
+ *             max pool, pixel shuffle or add after it); PP_NET_TAKEN for an
+ *             op so taken (it has no launch of its own); 0 otherwise
+ *   recipe    host i32 [n_ops], or NULL: the pp_conv2d_recipe id of each
+ *             pruned conv's launch (with the workspace pp_net_workspace
+ *             sizes), -1 for the other ops
+ * Errors: as pp_net_workspace (without the device-pointer checks),
+ * PP_EINVAL (op_flags NULL).
+ */
+#define PP_NET_TAKEN 0x80000000u
+pp_status pp_net_plan(const pp_net_op* ops, int32_t n_ops, int32_t n, int32_t c, int32_t h,
+                      int32_t w, int32_t act_dtype, uint32_t* op_flags, int32_t* recipe);
+
+/*
+ * pp_round_bf16 -- fp32 -> bf16 bit patterns, round to nearest, ties to
+ * even (the rounding pp_pack applies to bf16 pruned weights), for the dense
+ * layers' weights of a bf16 network (pp_net_op.d_w).  NaN stays NaN.
+ * Host-only: src host fp32 [count], dst host u16 [count]; they must not
+ * overlap.  Errors: PP_EINVAL (NULL pointer with count > 0).
+ */
+pp_status pp_round_bf16(const float* src, uint16_t* dst, size_t count);
 
 const char* pp_status_str(pp_status s);
 const char* pp_last_error(void);

@@ -25,13 +25,14 @@ PP_MAXPOOL2 = 2
 PP_ACCUMULATE = 4
 PP_PIXSHUF2 = 8
 PP_UPSAMPLE2 = 16
+PP_NET_TAKEN = 0x80000000
 (OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
 
 # exported symbols declared in include/pp.h
 SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_workspace", "pp_conv2d_recipe",
            "pp_conv2d_out_size", "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error",
            "pp_project_patterns", "pp_project_connectivity", "pp_project_columns", "pp_column_library",
-           "pp_fold_bn", "pp_jit_library", "pp_conv2d_fwd_noalloc")
+           "pp_fold_bn", "pp_jit_library", "pp_conv2d_fwd_noalloc", "pp_net_plan", "pp_round_bf16")
 
 
 class PPError(RuntimeError):
@@ -78,6 +79,8 @@ def load_library(path: str = LIB_PATH):
     lib.pp_net_workspace.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
                                      ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.pp_net_fwd.argtypes = [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp]
+    lib.pp_net_plan.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.pp_round_bf16.argtypes = [vp, vp, sz]
     lib.pp_jit_library.argtypes = [vp, sz, i32, i32, i32, i32, i32]
     lib.pp_project_patterns.argtypes = [vp, i32, i32, vp, i32, vp, vp]
     lib.pp_project_connectivity.argtypes = [vp, i32, i32, ctypes.c_int64, vp]
@@ -343,74 +346,65 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
 # networks: a flat op list over activation slots (pp_net_fwd)
 # ---------------------------------------------------------------------------
 
-def _bf16_bits(a: np.ndarray) -> np.ndarray:
-    """fp32 -> bf16 bit patterns, round to nearest even (offline weight prep)."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    return (((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF).astype(np.uint16)
+def round_bf16(a) -> np.ndarray:
+    """fp32 -> bf16 bit patterns (uint16), rounded by the library
+    (pp_round_bf16: nearest, ties to even) -- the dense weights of a bf16
+    network."""
+    src = np.ascontiguousarray(a, dtype=np.float32)
+    dst = np.empty(src.shape, np.uint16)
+    _check(load_library().pp_round_bf16(src.ctypes.data, dst.ctypes.data, src.size), "pp_round_bf16")
+    return dst
 
 
-def _dead_after(ops, slot, j0) -> bool:
-    for o in ops[j0:]:
-        if o["src"] == slot or (o["op"] == "add" and o.get("src2") == slot):
-            return False
-        if o["dst"] == slot:
-            return True
-    return True
+def _op_array(ops, params, wd, device_tensors):
+    """The pp_net_op array of a network spec.  device_tensors(op, prm, blob)
+    returns the device buffers of a layer (None for a host-only plan query),
+    kept alive by the caller: (d_blob,) for a pruned conv, (d_w, d_b) for a
+    dense one.  Returns the array and the host objects it points into."""
+    arr = (NetOp * len(ops))()
+    keep = []
+    for i, (op, prm) in enumerate(zip(ops, params)):
+        kind = Net._KIND[op["op"]]
+        e = arr[i]
+        e.kind = kind
+        e.src, e.dst = op["src"], op["dst"]
+        e.src2 = op.get("src2", 0)
+        e.flags = PP_RELU if op.get("relu") else 0
+        if kind == OP_CONV_PP:
+            blob = pack(prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"], op["stride"], op["pad"], op["dil"], wd)
+            dev = device_tensors(op, prm, blob)
+            keep.append((blob, dev))
+            e.h_blob = blob.ctypes.data
+            e.blob_bytes = blob.nbytes
+            e.d_blob = dev[0].data_ptr() if dev else None
+        elif kind in (OP_CONV_DENSE, OP_DECONV):
+            dev = device_tensors(op, prm, None)
+            keep.append(dev)
+            e.k, e.stride, e.pad, e.dilation = op["k"], op["stride"], op["pad"], op.get("dil", 1)
+            e.c_in, e.c_out = op["c_in"], op["c_out"]
+            e.d_w = dev[0].data_ptr() if dev else None
+            e.d_b = dev[1].data_ptr() if dev else None
+    return arr, keep
 
 
-def fused_ops(ops) -> dict:
-    """The ops that pp_net_fwd does not launch on their own, as {index:
-    "up2" | "maxpool2" | "pshuf2" | "add"}: an x2 upsample taken by the pruned
-    conv right after it ("up2"), or a max pool, pixel shuffle or add taken by
-    the pruned conv right before it.  The conv is a canonical / all-ones layer
-    with padding equal to its dilation.  Upsample: the conv reads its output
-    slot, which is not slot 1 and is dead after the conv (no later op reads
-    it before one rewrites it); a conv that writes the upsample's input slot
-    needs it in the workspace (slot >= 2).  Pool / shuffle / add: the op
-    reads the conv's output slot, the conv does not write slot 1, the conv's
-    output is dead after the op; a pool or shuffle that writes the slot the
-    conv reads has it in the workspace; an add's other operand and its dst
-    are workspace slots, that operand is not the slot the conv reads and is
-    dead after the add too; a conv that reads an upsample's input and writes
-    that slot takes no op after it.  ops: the op dicts of a network spec."""
-    def conv_ok(cv):
-        return cv["op"] == "conv3" and cv["pad"] == cv["dil"] and cv.get("lib") in ("canon8", "dense9")
-
-    out, up_in = {}, set()
-    i = 0
-    while i + 1 < len(ops):
-        us, cv = ops[i], ops[i + 1]
-        if us["op"] == "up2" and conv_ok(cv) and cv["src"] == us["dst"] and us["dst"] != 1 and \
-                not (cv["dst"] == us["src"] and cv["dst"] < 2) and _dead_after(ops, us["dst"], i + 2):
-            out[i] = "up2"
-            up_in.add(i + 1)
-            i += 2
-        else:
-            i += 1
-    i = 1
-    while i < len(ops):
-        cv, nx = ops[i - 1], ops[i]
-        f = None
-        cs = ops[i - 2]["src"] if (i - 1) in up_in else cv.get("src")
-        if conv_ok(cv) and cv["dst"] != 1 and cs != cv["dst"]:
-            if nx["op"] in ("maxpool2", "pshuf2") and nx["src"] == cv["dst"] and not (nx["dst"] == cs and cs < 2):
-                if nx["op"] == "maxpool2" or cv["c_out"] % 4 == 0:
-                    f = nx["op"]
-            elif nx["op"] == "add" and (nx["src"] == cv["dst"]) != (nx["src2"] == cv["dst"]):
-                r = nx["src2"] if nx["src"] == cv["dst"] else nx["src"]
-                if r >= 2 and nx["dst"] >= 2 and r != cs and _dead_after(ops, r, i + 1):
-                    f = "add"
-        if f is not None and _dead_after(ops, cv["dst"], i + 1):
-            out[i] = f
-            i += 2
-        else:
-            i += 1
-    return out
+def _read_plan(ops, arr, n_ops, n, c, h, w, wd) -> dict:
+    lib = load_library()
+    flags = (ctypes.c_uint32 * n_ops)()
+    recipe = (ctypes.c_int32 * n_ops)()
+    _check(lib.pp_net_plan(arr, n_ops, n, c, h, w, wd, flags, recipe), "pp_net_plan")
+    fused = {i: ops[i]["op"] for i in range(n_ops) if flags[i] & PP_NET_TAKEN}
+    return dict(flags=list(flags), recipe=list(recipe), fused=fused)
 
 
-def fused_pools(ops) -> set:
-    """Indices of the max-pool ops fused into the conv before them."""
-    return {i for i, k in fused_ops(ops).items() if k == "maxpool2"}
+def net_plan(ops, params, n, c, h, w, dtype="f32") -> dict:
+    """How pp_net_fwd runs a network spec (ops, params as for Net) on an
+    n x c x h x w input, as the library plans it (pp_net_plan; host-only):
+    ``flags`` per op (a pruned conv's fusion flags, PP_NET_TAKEN for an op
+    run inside a conv's launch), ``recipe`` per op (the pruned convs'
+    tiling ids, else -1) and ``fused`` = {index: op kind} of the taken ops."""
+    wd = PP_BF16 if dtype == "bf16" else PP_F32
+    arr, keep = _op_array(ops, params, wd, lambda op, prm, blob: None)
+    return _read_plan(ops, arr, len(ops), n, c, h, w, wd)
 
 
 class Net:
@@ -430,36 +424,23 @@ class Net:
         self.dtype = dtype
         self.wd = PP_BF16 if dtype == "bf16" else PP_F32
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
-        self.layers = []     # keeps device buffers alive
         self.pruned = []     # the PackedLayer of every pruned conv, in op order
-        arr = (NetOp * len(ops))()
-        for i, (op, prm) in enumerate(zip(ops, params)):
-            kind = self._KIND[op["op"]]
-            e = arr[i]
-            e.kind = kind
-            e.src, e.dst = op["src"], op["dst"]
-            e.src2 = op.get("src2", 0)
-            e.flags = PP_RELU if op.get("relu") else 0
-            if kind == OP_CONV_PP:
-                L = PackedLayer.from_weights(prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"],
-                                             op["stride"], op["pad"], op["dil"], self.wd, device)
-                self.layers.append(L)
+
+        def device_tensors(op, prm, blob):
+            if blob is not None:
+                L = PackedLayer(blob, device)
                 self.pruned.append(L)
-                e.h_blob = L.h_blob.ctypes.data
-                e.blob_bytes = L.h_blob.nbytes
-                e.d_blob = L.d_blob.data_ptr()
-            elif kind in (OP_CONV_DENSE, OP_DECONV):
-                w = np.ascontiguousarray(prm["w"], dtype=np.float32)
-                if self.wd == PP_BF16:
-                    dw = torch.from_numpy(_bf16_bits(w).view(np.int16)).to(device)
-                else:
-                    dw = torch.from_numpy(w).to(device)
-                db = torch.from_numpy(np.ascontiguousarray(prm["b"], dtype=np.float32)).to(device)
-                self.layers.append((dw, db))
-                e.k, e.stride, e.pad, e.dilation = op["k"], op["stride"], op["pad"], op.get("dil", 1)
-                e.c_in, e.c_out = op["c_in"], op["c_out"]
-                e.d_w = dw.data_ptr()
-                e.d_b = db.data_ptr()
+                return (L.d_blob, L)
+            w = np.ascontiguousarray(prm["w"], dtype=np.float32)
+            if self.wd == PP_BF16:
+                dw = torch.from_numpy(round_bf16(w).view(np.int16)).to(device)
+            else:
+                dw = torch.from_numpy(w).to(device)
+            db = torch.from_numpy(np.ascontiguousarray(prm["b"], dtype=np.float32)).to(device)
+            return (dw, db)
+
+        arr, self.layers = _op_array(ops, params, self.wd, device_tensors)   # layers: keeps buffers alive
+        self.spec_ops = list(ops)
         self.ops = arr
         self.n_ops = len(ops)
         self._ws = None
@@ -471,6 +452,10 @@ class Net:
         _check(lib.pp_net_workspace(self.ops, self.n_ops, n, c, h, w, self.wd, ctypes.byref(nb), ctypes.byref(oc),
                                     ctypes.byref(oh), ctypes.byref(ow)), "pp_net_workspace")
         return nb.value, (n, oc.value, oh.value, ow.value)
+
+    def launch_plan(self, n, c, h, w) -> dict:
+        """net_plan for this network's own op array (pp_net_plan)."""
+        return _read_plan(self.spec_ops, self.ops, self.n_ops, n, c, h, w, self.wd)
 
     def forward(self, x, out=None, workspace=None, stream=None):
         torch = _torch()

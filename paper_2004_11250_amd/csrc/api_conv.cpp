@@ -58,6 +58,22 @@ pp_status conv_check(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t
 
 ConvParams layer_params(const BlobView& v, int32_t n, int32_t h, int32_t w, int ho, int wo);
 
+ConvPlan plan_with_scratch(const ConvParams& p, int kind, bool bf16, size_t scratch_bytes, bool no_lean) {
+  ConvPlan pl = plan_conv(p, kind, bf16, scratch_bytes > 0, no_lean);
+  if (split_bytes(pl, p) > scratch_bytes) pl = plan_conv(p, kind, bf16, false, no_lean);   // no room: no split
+  return pl;
+}
+
+int conv_recipe(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
+                size_t scratch_bytes) {
+  const bool up = (flags & PP_UPSAMPLE2) != 0;
+  int ho = 0, wo = 0;
+  if (conv_check(v, n, up ? 2 * h : h, up ? 2 * w : w, act_dtype, &ho, &wo) != PP_OK) return -1;
+  ConvParams p = layer_params(v, n, up ? 2 * h : h, up ? 2 * w : w, ho, wo);
+  p.flags = flags;
+  return plan_with_scratch(p, library_kind(v), act_dtype == PP_BF16, scratch_bytes, false).recipe;
+}
+
 pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
                        int32_t w, int32_t act_dtype, uint32_t flags, void* scratch, size_t scratch_bytes,
                        hipStream_t st) {
@@ -95,15 +111,11 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   p.flags = flags;
   const int lib = library_kind(v);
   const bool bf = act_dtype == PP_BF16;
+  const size_t usable = reinterpret_cast<uintptr_t>(scratch) % 256 ? 0 : scratch_bytes;
   // the plan for library kind `kind`; a split only with enough scratch
   auto make_plan = [&](int kind, ConvParams* pp_, bool no_lean) {
-    ConvPlan pl = plan_conv(*pp_, kind, bf, scratch != nullptr, no_lean);
-    if (split_bytes(pl, *pp_) > 0) {
-      if (split_bytes(pl, *pp_) > scratch_bytes || reinterpret_cast<uintptr_t>(scratch) % 256)
-        pl = plan_conv(*pp_, kind, bf, false, no_lean);   // not enough scratch: no split
-      else
-        pp_->part = static_cast<float*>(scratch);
-    }
+    ConvPlan pl = plan_with_scratch(*pp_, kind, bf, scratch != nullptr ? usable : 0, no_lean);
+    if (split_bytes(pl, *pp_) > 0) pp_->part = static_cast<float*>(scratch);
     return pl;
   };
   if (lib == kLibGeneric && jit_library4(v)) {

@@ -37,6 +37,15 @@ pp_status jit_prepare(const BlobView& v, const ConvPlan& plan, bool bf16);
 bool jit_ready(const BlobView& v, const ConvPlan& plan, bool bf16);
 bool jit_launch(const BlobView& v, const ConvPlan& plan, ConvParams p, bool bf16, hipStream_t st, hipError_t* err);
 
+// the plan of a layer whose channel split may use scratch_bytes of scratch
+// (a plan whose split needs more runs unsplit)
+ConvPlan plan_with_scratch(const ConvParams& p, int kind, bool bf16, size_t scratch_bytes, bool no_lean);
+
+// the tiling pp_conv2d_fwd runs for this layer (flags as there; h, w: the
+// stored input size) with scratch_bytes of split scratch; -1 if none
+int conv_recipe(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
+                size_t scratch_bytes);
+
 // scratch bytes pp_conv2d_fwd can use for this layer and input (0: none)
 size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype);
 

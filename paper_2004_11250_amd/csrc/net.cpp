@@ -53,7 +53,10 @@ struct Plan {
 
 pp_status bad(int i, const std::string& msg) { return fail(PP_EINVAL, "op " + std::to_string(i) + ": " + msg); }
 
-pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w, int act, Plan* pl) {
+// device: the op list is for a launch (device pointers must be set); a plan
+// query reads host memory only
+pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w, int act, Plan* pl,
+                    bool device = true) {
   if (!ops || n_ops < 1) return fail(PP_EINVAL, "empty op list");
   if (n < 1 || c < 1 || h < 1 || w < 1) return fail(PP_EINVAL, "bad input shape");
   if (act != PP_F32 && act != PP_BF16) return fail(PP_EINVAL, "bad activation dtype");
@@ -79,7 +82,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
       case PP_OP_CONV_PP: {
         pp_status st = parse_blob(op.h_blob, op.blob_bytes, &pl->views[i], /*full=*/false);
         if (st != PP_OK) return st;
-        if (!op.d_blob) return bad(i, "d_blob is NULL");
+        if (device && !op.d_blob) return bad(i, "d_blob is NULL");
         const BlobView& v = pl->views[i];
         if (v.c_in != s.c) return bad(i, "input channels do not match the blob");
         {
@@ -98,7 +101,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
         if (op.stride != 1 || op.dilation != 1) return fail(PP_EUNSUPPORTED, "dense conv: stride and dilation 1 only");
         if (op.pad < 0 || op.pad > op.k) return bad(i, "bad pad");
         if (op.c_in != s.c || op.c_out < 1) return bad(i, "channel mismatch");
-        if (!op.d_w) return bad(i, "d_w is NULL");
+        if (device && !op.d_w) return bad(i, "d_w is NULL");
         const int ho = s.h + 2 * op.pad - op.k + 1, wo = s.w + 2 * op.pad - op.k + 1;
         if (ho < 1 || wo < 1) return bad(i, "input smaller than the kernel");
         o = Shape{op.c_out, ho, wo, true};
@@ -108,7 +111,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
         if (op.k != 4 || op.stride != 2 || op.pad != 1)
           return fail(PP_EUNSUPPORTED, "transposed conv: kernel 4, stride 2, pad 1 only");
         if (op.c_in != s.c || op.c_out < 1) return bad(i, "channel mismatch");
-        if (!op.d_w) return bad(i, "d_w is NULL");
+        if (device && !op.d_w) return bad(i, "d_w is NULL");
         o = Shape{op.c_out, 2 * s.h, 2 * s.w, true};
         break;
       }
@@ -276,6 +279,32 @@ extern "C" pp_status pp_net_workspace(const pp_net_op* ops, int32_t n_ops, int32
   if (out_c) *out_c = pl.final_shape.c;
   if (out_h) *out_h = pl.final_shape.h;
   if (out_w) *out_w = pl.final_shape.w;
+  return PP_OK;
+}
+
+extern "C" pp_status pp_net_plan(const pp_net_op* ops, int32_t n_ops, int32_t n, int32_t c, int32_t h, int32_t w,
+                                 int32_t act_dtype, uint32_t* op_flags, int32_t* recipe) {
+  clear_error();
+  if (!op_flags) return fail(PP_EINVAL, "NULL op_flags");
+  Plan pl;
+  pp_status st = make_plan(ops, n_ops, n, c, h, w, act_dtype, &pl, /*device=*/false);
+  if (st != PP_OK) return st;
+  for (int i = 0; i < n_ops; ++i) {
+    op_flags[i] = 0;
+    if (recipe) recipe[i] = -1;
+  }
+  for (int i = 0; i < n_ops; ++i) {
+    if (ops[i].kind != PP_OP_CONV_PP) continue;
+    const uint32_t f = pl.fuse[i] | (pl.up_in[i] ? PP_UPSAMPLE2 : 0u);
+    op_flags[i] = f;
+    if (pl.up_in[i]) op_flags[i - 1] = PP_NET_TAKEN;
+    if (pl.fuse[i]) op_flags[i + 1] = PP_NET_TAKEN;
+    if (recipe) {
+      // the conv reads the stored (not upsampled) input of a taken upsample
+      const Shape& s = pl.up_in[i] ? pl.in[i - 1] : pl.in[i];
+      recipe[i] = conv_recipe(pl.views[i], n, s.h, s.w, act_dtype, ops[i].flags | f, pl.scratch_bytes);
+    }
+  }
   return PP_OK;
 }
 

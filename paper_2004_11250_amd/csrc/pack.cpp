@@ -322,6 +322,19 @@ extern "C" pp_status pp_blob_info(const void* h_blob, size_t bytes, pp_layer_des
   return PP_OK;
 }
 
+extern "C" pp_status pp_round_bf16(const float* src, uint16_t* dst, size_t count) {
+  clear_error();
+  if (count && (!src || !dst)) return fail(PP_EINVAL, "NULL src or dst");
+  for (size_t i = 0; i < count; ++i) {
+    uint32_t u;
+    std::memcpy(&u, src + i, 4);
+    // a NaN keeps its sign and top payload bits, made quiet (rounding could
+    // carry it into infinity)
+    dst[i] = (u & 0x7FFFFFFFu) > 0x7F800000u ? static_cast<uint16_t>((u >> 16) | 0x40u) : to_bf16(src[i]);
+  }
+  return PP_OK;
+}
+
 extern "C" const char* pp_status_str(pp_status s) {
   switch (s) {
     case PP_OK: return "ok";

@@ -203,3 +203,22 @@ def test_net_rejects_bad_op_lists(lib):
     hn.arr[1].dst = 3
     hn.arr[0].kind = 42
     assert status() == pp.PP_EINVAL
+
+
+def test_round_bf16_matches_the_oracle_rounding(lib):
+    from oracle import bf16 as obf16
+    rng = np.random.default_rng(7)
+    x = np.concatenate([rng.standard_normal(4096).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 4096),
+                        np.array([0.0, -0.0, 1e-40, -1e-40], np.float32)]).astype(np.float32)
+    assert np.array_equal(pp.round_bf16(x), obf16.round_bits(x))
+    # ties to even, carry into the exponent, overflow to infinity, infinities
+    u = np.array([0x3F808000, 0x3F818000, 0x3F80FFFF, 0x3FFF8000, 0x7F7FFFFF, 0x7F800000, 0xFF800000],
+                 np.uint32)
+    want = np.array([0x3F80, 0x3F82, 0x3F81, 0x4000, 0x7F80, 0x7F80, 0xFF80], np.uint16)
+    assert np.array_equal(pp.round_bf16(u.view(np.float32)), want)
+    # a NaN stays a NaN, also one whose payload sits in the dropped bits
+    nan = np.array([0x7FC00000, 0x7F800001, 0xFFFFFFFF], np.uint32).view(np.float32)
+    r = pp.round_bf16(nan)
+    assert np.all((r & 0x7F80) == 0x7F80) and np.all(r & 0x007F)
+    assert lib.pp_round_bf16(None, None, 1) == pp.PP_EINVAL
+    assert lib.pp_round_bf16(None, None, 0) == pp.PP_OK

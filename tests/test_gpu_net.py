@@ -90,7 +90,7 @@ def teacher_forced(cfg, dtype, n_keep=6):
     spec = workloads.net_spec(cfg)
     params = workloads.net_params(cfg)
     net = pp.Net(spec["ops"], params, dtype)
-    fused = pp.fused_ops(spec["ops"])
+    fused = net.launch_plan(spec["batch"], spec["c"], spec["h"], spec["w"])["fused"]
     x_np, x = _input(cfg, dtype)
     slots = {0: x_np}
     worst = 0.0
@@ -151,7 +151,7 @@ def test_vgg16_net_equals_chained_layer_calls():
     _say("vgg16 pp_net_fwd vs chained pp_conv2d_fwd (pool fused where the net fuses it) + maxpool")
     y_net = _np(net.forward(x))
     ops = spec["ops"]
-    fused = pp.fused_ops(ops)
+    fused = net.launch_plan(spec["batch"], spec["c"], spec["h"], spec["w"])["fused"]
     cur = x
     li = 0
     for i, (op, prm) in enumerate(zip(ops, params)):
@@ -174,7 +174,7 @@ def test_net_fused_equals_unfused(cfg, dtype):
     spec = workloads.net_spec(cfg)
     params = workloads.net_params(cfg)
     ops = spec["ops"]
-    fused = pp.fused_ops(ops)
+    fused = pp.net_plan(ops, params, spec["batch"], spec["c"], spec["h"], spec["w"], dtype)["fused"]
     assert any(k == "add" for k in fused.values()), "the network has fusable residual adds"
     if cfg == 4:
         assert sum(k == "pshuf2" for k in fused.values()) == 2
