@@ -170,13 +170,20 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   const uint8_t* blob = a.blob;
   const u32x4 brs = make_rsrc_below(blob, a.blob_bytes, kDmaShift);
   u32x4 cr = make_rsrc_below(xi + static_cast<size_t>(c0) * sh * sw, chan_bytes, kDmaShift);
-  auto dma_patch = [&](uint32_t sb) __attribute__((always_inline)) {
+  // one channel's DMAs into ring slot sb (LDS byte address).  A channel past
+  // the wave's range is staged all the same through descriptors of range 0
+  // (every lane out of range: no memory is read, zeros land in a slot nobody
+  // reads), so that the number of DMAs in flight never depends on where the
+  // range ends and every wait below is one constant count.
+  auto dma_patch = [&](uint32_t sb, bool live) __attribute__((always_inline)) {
+    u32x4 d = cr;
+    d.z = live ? cr.z : 0u;
     static_for<0, NQ>([&](auto ti) __attribute__((always_inline)) {
       constexpr int T = decltype(ti)::value;
       if constexpr (V4)
-        dma_b128_at<1024u * T, 1024u * (T - 1), T == 0>(cr, qoff[T], sb);
+        dma_b128_at<1024u * T, 1024u * (T - 1), T == 0>(d, qoff[T], sb);
       else
-        dma_b32_at<256u * T, 256u * (T - 1), T == 0>(cr, qoff[T], sb);
+        dma_b32_at<256u * T, 256u * (T - 1), T == 0>(d, qoff[T], sb);
     });
     cr = next_channel(cr, chan_bytes);
   };
@@ -186,21 +193,23 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   const uint32_t wlow = lane < 32 ? (1u << wslot) - 1u : 0u;
   const uint32_t wbit = lane < 32 ? 1u << wslot : 0u;
   const uint32_t wbase = a.off_w + 4u * (lane & 3) + kDmaShift - (LW0 & 4095u);
-  auto dma_weights = [&](uint32_t wo, uint32_t sb) __attribute__((always_inline)) {
+  auto dma_weights = [&](uint32_t wo, uint32_t sb, bool live) __attribute__((always_inline)) {
+    u32x4 d = brs;
+    d.z = live ? brs.z : 0u;
     const uint32_t kept = wo >> 24;
     const uint32_t o = wbase + 4u * ((wo & 0xFFFFFFu) + 4u * __builtin_popcount(kept & wlow));
-    dma_b32_at<LW0, 4u * G::EPD * (NQ - 1), false>(brs, (kept & wbit) ? o : 0x80000000u, sb);
+    dma_b32_at<LW0, 4u * G::EPD * (NQ - 1), false>(d, (kept & wbit) ? o : 0x80000000u, sb);
   };
-  auto slot_b = [&](int c) { return ring_b + 4u * ((static_cast<uint32_t>(c - c0) % NS) * SLOT); };
 
   // metadata: woff word (weight offset | kept-slot mask << 24) and the 8
-  // pattern codes of (group, channel); channels past the layer's last read
-  // its last entry again (not used)
-  const uint32_t e_base = grp * a.c_in;
-  const uint32_t woff_last = a.off_woff + 4u * (e_base + a.c_in - 1);
-  const uint32_t code_last = a.off_codes + 8u * (e_base + a.c_in - 1);
-  auto woff_at = [&](int c) { return min(a.off_woff + 4u * (e_base + c), woff_last); };
-  auto code_at = [&](int c) { return min(a.off_codes + 8u * (e_base + c), code_last); };
+  // pattern codes of (group, channel), read by scalar loads at byte offsets
+  // that move on by one entry per channel.  Reads for channels past the
+  // layer's last (at most NS entries past the end of the woff array, one
+  // past the end of the codes) land in the sections that follow them in the
+  // blob (woff, weights, bias: the blob validation enforces that order) and
+  // feed only the staging of channels nobody reads.
+  uint32_t wo_at = a.off_woff + 4u * (grp * a.c_in + c0);
+  uint32_t cd_at = a.off_codes + 8u * (grp * a.c_in + c0);
 
   // the slot group's output channels and biases for the epilogue, lane s <
   // 8 holding slot s's (loaded before the first DMA: in-order completion
@@ -220,45 +229,44 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   if (c0 < c1) {
     constexpr int QV = NQ + 1;   // DMAs per lane and channel
     constexpr int DPF = NS - 1;  // channels DMA'd ahead
+    constexpr uint32_t SLOTB = 4u * SLOT;
+    // ring slots (LDS byte addresses): rd holds channel c, and channel c +
+    // DPF goes to the slot channel c - 1 used (its reads are done by then)
+    const uint32_t ring_end = ring_b + NS * SLOTB;
+    uint32_t rd = ring_b;
+    uint32_t wr = ring_b + DPF * SLOTB;
     // prologue: channel c0's halo before anything else, then channels up
     // to c0 + DPF - 1
-    dma_patch(slot_b(c0));
+    dma_patch(ring_b, true);
     __builtin_amdgcn_sched_barrier(0);
     uint32_t wo_pre[DPF + 1];
 #pragma unroll
-    for (int i = 0; i <= DPF; ++i) wo_pre[i] = kern::sload<uint32_t>(blob, woff_at(c0 + i));
-    uint2 code_c = kern::sload<uint2>(blob, code_at(c0));
+    for (int i = 0; i <= DPF; ++i) wo_pre[i] = kern::sload<uint32_t>(blob, wo_at + 4u * i);
+    uint2 code_c = kern::sload<uint2>(blob, cd_at);
     wait_lgkm();
-    dma_weights(wo_pre[0], slot_b(c0));
+    dma_weights(wo_pre[0], ring_b, true);
 #pragma unroll
-    for (int i = 1; i < DPF; ++i)
-      if (c0 + i < c1) {
-        dma_patch(slot_b(c0 + i));
-        dma_weights(wo_pre[i], slot_b(c0 + i));
-      }
+    for (int i = 1; i < DPF; ++i) {
+      const bool live = c0 + i < c1;
+      dma_patch(ring_b + i * SLOTB, live);
+      dma_weights(wo_pre[i], ring_b + i * SLOTB, live);
+    }
     uint32_t kept_c = wo_pre[0] >> 24;
     uint32_t wo_n = wo_pre[DPF];   // woff word of channel c + DPF
-    const int lane_off = (ly * R) * LSTR + lx * CC;
+    const uint32_t lane_b = 4u * ((ly * R) * LSTR + lx * CC);
 
 #pragma unroll 1
     for (int c = c0; c < c1; ++c) {
-      // channel c has landed once at most min(DPF - 1, c1 - 1 - c) later
-      // channels are in flight
-      {
-        const int later = min(DPF - 1, c1 - 1 - c);
-        asm volatile("" ::: "memory");
-        static_for<0, DPF>([&](auto ni) __attribute__((always_inline)) {
-          constexpr int n = decltype(ni)::value;
-          if (later == n) __builtin_amdgcn_s_waitcnt(vmcnt_imm(n * QV));
-        });
-        asm volatile("" ::: "memory");
-      }
+      // channel c has landed once the DMAs of the DPF - 1 channels after it
+      // are the only ones in flight
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm((DPF - 1) * QV));
+      asm volatile("" ::: "memory");
       // the patch and the 8 slots' expanded weights of channel c
-      const float* cur = ring + (static_cast<uint32_t>(c - c0) % NS) * SLOT;
+      const float* cur = ring + (rd - ring_b) / 4u;
       float w[8][4];
       float p[PR][PC];
-      const uint32_t kept = kept_c;
-      if (kept != 0) {
+      {
         const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
@@ -266,26 +274,30 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
           w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
         }
 #pragma unroll
-        for (int r = 0; r < PR; ++r) read_row<G::SH, G::SH, PC, G::VWL, false>(p[r], cur + lane_off + r * LSTR);
+        for (int r = 0; r < PR; ++r)
+          read_row<G::SH, G::SH, PC, G::VWL, false>(p[r], cur + lane_b / 4u + r * LSTR);
       }
       // channel c's reads, and the scalar loads of the previous step
       wait_lgkm();
       __builtin_amdgcn_sched_barrier(0);
       // channel c + DPF into the slot channel c - 1 used (its reads are done)
-      if (c + DPF < c1) {
-        const uint32_t sb = slot_b(c + DPF);
-        dma_patch(sb);
-        dma_weights(wo_n, sb);
+      {
+        const bool live = c + DPF < c1;
+        dma_patch(wr, live);
+        dma_weights(wo_n, wr, live);
       }
       // metadata for the next step: waited for there, while this channel's
       // FMAs run
-      const uint32_t wo_nn = kern::sload<uint32_t>(blob, woff_at(c + DPF + 1));
-      const uint32_t wo_c1 = kern::sload<uint32_t>(blob, woff_at(c + 1));
-      const uint2 code_c1 = kern::sload<uint2>(blob, code_at(c + 1));
+      wo_at += 4u;
+      cd_at += 8u;
+      const uint32_t wo_nn = kern::sload<uint32_t>(blob, wo_at + 4u * DPF);
+      const uint32_t wo_c1 = kern::sload<uint32_t>(blob, wo_at);
+      const uint2 code_c1 = kern::sload<uint2>(blob, cd_at);
       __builtin_amdgcn_sched_barrier(0);
+      const uint32_t kept = kept_c;
       uint32_t kc = kept;
       asm volatile("" : "+s"(kc));   // fresh slot tests
-      if (kc != 0) {
+      {
         const uint32_t cx = code_c.x, cy = code_c.y;
         static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
           constexpr int s = decltype(si)::value;
@@ -296,6 +308,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       kept_c = wo_c1 >> 24;
       code_c = code_c1;
       wo_n = wo_nn;
+      wr = rd;
+      rd = rd + SLOTB == ring_end ? ring_b : rd + SLOTB;
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // no DMA may land in the exchange area below
   }
