@@ -68,32 +68,35 @@ def load_library(path: str = LIB_PATH):
                            "(or __graft_entry__.build())")
     lib = ctypes.CDLL(path)
     vp, sz, i32, u32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_uint32
-    lib.pp_pack.argtypes = [ctypes.POINTER(LayerDesc), vp, vp, vp, vp, vp, i32, vp, ctypes.POINTER(sz)]
-    lib.pp_blob_info.argtypes = [vp, sz, ctypes.POINTER(LayerDesc), ctypes.POINTER(i32),
-                                 ctypes.POINTER(ctypes.c_int64)]
-    lib.pp_conv2d_fwd.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp, sz, vp]
-    lib.pp_conv2d_fwd_noalloc.argtypes = [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp]
-    lib.pp_conv2d_workspace.argtypes = [vp, sz, i32, i32, i32, i32, ctypes.POINTER(sz)]
-    lib.pp_conv2d_out_size.argtypes = [vp, sz, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
-    lib.pp_conv2d_recipe.argtypes = [vp, sz, i32, i32, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
-    lib.pp_net_workspace.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
-                                     ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
-    lib.pp_net_fwd.argtypes = [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp]
-    lib.pp_net_plan.argtypes = [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, vp, vp]
-    lib.pp_round_bf16.argtypes = [vp, vp, sz]
-    lib.pp_jit_library.argtypes = [vp, sz, i32, i32, i32, i32, i32]
-    lib.pp_project_patterns.argtypes = [vp, i32, i32, vp, i32, vp, vp]
-    lib.pp_project_connectivity.argtypes = [vp, i32, i32, ctypes.c_int64, vp]
-    lib.pp_project_columns.argtypes = [vp, i32, i32, ctypes.c_int64, vp]
-    lib.pp_column_library.argtypes = [vp, i32, i32, vp, ctypes.POINTER(i32), vp, vp]
-    lib.pp_fold_bn.argtypes = [vp, vp, i32, i32, vp, vp, vp, vp, ctypes.c_float]
-    lib.pp_status_str.argtypes = [i32]
-    lib.pp_status_str.restype = ctypes.c_char_p
-    lib.pp_last_error.argtypes = []
-    lib.pp_last_error.restype = ctypes.c_char_p
-    for name in SYMBOLS:
-        if name not in ("pp_status_str", "pp_last_error"):
-            getattr(lib, name).restype = i32
+    argtypes = {
+        "pp_pack": [ctypes.POINTER(LayerDesc), vp, vp, vp, vp, vp, i32, vp, ctypes.POINTER(sz)],
+        "pp_blob_info": [vp, sz, ctypes.POINTER(LayerDesc), ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_int64)],
+        "pp_conv2d_fwd": [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp, sz, vp],
+        "pp_conv2d_fwd_noalloc": [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp],
+        "pp_conv2d_workspace": [vp, sz, i32, i32, i32, i32, ctypes.POINTER(sz)],
+        "pp_conv2d_out_size": [vp, sz, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "pp_conv2d_recipe": [vp, sz, i32, i32, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "pp_net_workspace": [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
+                             ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "pp_net_fwd": [ctypes.POINTER(NetOp), i32, vp, vp, i32, i32, i32, i32, i32, vp, sz, vp],
+        "pp_net_plan": [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, vp, vp],
+        "pp_round_bf16": [vp, vp, sz],
+        "pp_jit_library": [vp, sz, i32, i32, i32, i32, i32],
+        "pp_project_patterns": [vp, i32, i32, vp, i32, vp, vp],
+        "pp_project_connectivity": [vp, i32, i32, ctypes.c_int64, vp],
+        "pp_project_columns": [vp, i32, i32, ctypes.c_int64, vp],
+        "pp_column_library": [vp, i32, i32, vp, ctypes.POINTER(i32), vp, vp],
+        "pp_fold_bn": [vp, vp, i32, i32, vp, vp, vp, vp, ctypes.c_float],
+        "pp_status_str": [i32],
+        "pp_last_error": [],
+    }
+    # (the host-only packer library, libppconv_host.so, has the host entry
+    # points only)
+    for name, at in argtypes.items():
+        if hasattr(lib, name):
+            fn = getattr(lib, name)
+            fn.argtypes = at
+            fn.restype = ctypes.c_char_p if name in ("pp_status_str", "pp_last_error") else i32
     _lib = lib
     return lib
 

@@ -211,6 +211,27 @@ def test_vgg16_full_size_layer_sampled(idx):
     check(y, ref, bound, "f32", f"vgg layer {i}")
 
 
+# the 28 x 28 and 14 x 14 VGG-16 layers at full size and full width: every
+# filter against the oracle, in the plan the network runs (the 14 x 14
+# layers split their channels over workgroups; the last layer of each block
+# with the max pool the network fuses into it)
+@pytest.mark.parametrize("idx,pool", [(8, False), (9, True), (10, False), (12, True)])
+def test_vgg16_full_width_small_maps(idx, pool):
+    i, op, h = _vgg_layers()[idx]
+    L = workloads.layer_params(2, i, op)
+    x = workloads.random_input(600 + i, (1, op["c_in"], h, h), 0.0, 1.0)
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+    plan = pp.conv2d_plan(layer.h_blob, 1, h, h, pp.PP_F32)
+    _say("vgg16 layer", i, op["c_in"], "->", op["c_out"], f"{h}x{h}", "pool", pool, "plan", plan, "all filters")
+    y = _from_dev(pp.conv2d_fwd(layer, _to_dev(x, "f32"), relu=True, maxpool2=pool))
+    args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+    ref = oconv.conv3x3_pruned(*args, 1, 1, 1, True)
+    bound = oconv.conv3x3_bound(*args, 1, 1, 1)
+    if pool:
+        ref, bound = oconv.maxpool2(ref), oconv.maxpool2(bound)
+    check(y, ref, bound, "f32", f"vgg layer {i} full width")
+
+
 # every compiled tiling, forced through the PP_RECIPE override of the planner
 RECIPES = list(range(40))
 

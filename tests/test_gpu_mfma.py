@@ -73,6 +73,14 @@ CASES = [  # library, (stride, pad, dilation), (n, c_out, c_in, h, w), keep, rel
     ("mixed", (1, 2, 2), (1, 33, 32, 18, 40), 0.3, False),
     ("dense9", (1, 1, 1), (2, 64, 32, 17, 19), 1.0, True),
     ("dense9", (2, 1, 1), (1, 130, 64, 31, 29), 1.0, False),
+    # k steps of 64 (reductions 9 c_in >= 1152); with c_in an odd multiple
+    # of 32 the last step is a half step
+    ("canon8", (1, 1, 1), (1, 40, 160, 20, 22), 0.4, True),     # half step, 64-filter tiles
+    ("canon8", (1, 1, 1), (1, 100, 128, 18, 21), 0.4, True),    # whole steps, 128-filter tiles
+    ("canon8", (1, 2, 2), (2, 136, 224, 15, 17), 0.3, False),   # half step, 128-filter tiles, ragged second tile
+    # more than 256 tiles: one wave group per tile
+    ("canon8", (1, 1, 1), (1, 48, 160, 200, 172), 0.3, True),   # 269 tiles, long k with a half step
+    ("canon8", (1, 1, 1), (1, 130, 64, 130, 128), 0.5, True),   # 260 tiles of 128 filters, short k
 ]
 
 
@@ -85,6 +93,12 @@ def test_mfma_against_oracle(case, monkeypatch):
     x = obf16.round_f32(workloads.random_input(seed, (n, c_in, h, w)))
     _say("mfma", lib, (s, p, d), (n, c_out, c_in, h, w), "keep", keep, "relu", relu, "seed", seed)
     assert pp.conv2d_recipe(layer.h_blob, n, h, w, pp.PP_BF16) == MFMA
+    ho = (h + 2 * p - 2 * d - 1) // s + 1
+    wo = (w + 2 * p - 2 * d - 1) // s + 1
+    bm = 128 if c_out > 64 else 64
+    tiles = -(-n * ho * wo // 128) * -(-c_out // bm)
+    _say("  k step", 64 if 9 * c_in >= 1152 else 32, "half last step", (9 * c_in) % 64 == 32 and 9 * c_in >= 1152,
+         "tiles", tiles, "wave groups per tile", 2 if tiles <= 256 else 1)
     y = _host(pp.conv2d_fwd(layer, _dev(x), relu=relu))
     ref, bound = _oracle(L, x, s, p, d, relu)
     check(y, ref, bound, "bf16", f"mfma {lib} {(s, p, d)} {(n, c_out, c_in, h, w)}")
@@ -177,3 +191,20 @@ def test_planner_takes_mfma_for_large_bf16_layers():
     sel = np.array([0, 17, 38, 63])
     ref, bound = _oracle(L, x, 1, 1, 1, True, sel)
     check(y[:, sel], ref, bound, "bf16", "mfma sr 270x480 sampled filters")
+
+
+def test_mfma_full_colourization_layer():
+    # a whole 512 -> 512 dilated layer of the colourization network (batch 8,
+    # 32 x 32, bf16), the form and launch the network runs, every filter
+    spec = workloads.net_spec(5)
+    i = next(j for j, op in enumerate(spec["ops"]) if op["op"] == "conv3" and op["c_in"] == 512 and op["dil"] == 2)
+    op = spec["ops"][i]
+    L = workloads.layer_params(5, i, op)
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], op["stride"], op["pad"],
+                                        op["dil"], pp.PP_BF16)
+    x = obf16.round_f32(workloads.random_input(1300 + i, (8, 512, 32, 32), 0.0, 1.0))
+    _say("colourization layer", i, "512 -> 512 dilation 2, 8 x 32 x 32 bf16, all filters")
+    assert pp.conv2d_recipe(layer.h_blob, 8, 32, 32, pp.PP_BF16) == MFMA
+    y = _host(pp.conv2d_fwd(layer, _dev(x), relu=True))
+    ref, bound = _oracle(L, x, op["stride"], op["pad"], op["dil"], True)
+    check(y, ref, bound, "bf16", f"colourization layer {i}")
