@@ -57,8 +57,12 @@ typedef enum { PP_F32 = 0, PP_BF16 = 1 } pp_dtype;
  * the nearest x2 upsampling of x; PP_MAXPOOL2 stores the 2 x 2, stride 2 max
  * pool of the activated output instead of the output itself; PP_ACCUMULATE
  * adds the activated output to what y holds (a residual connection);
- * PP_PIXSHUF2 stores the activated output through PixelShuffle(2). */
-enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u, PP_ACCUMULATE = 4u, PP_PIXSHUF2 = 8u, PP_UPSAMPLE2 = 16u };
+ * PP_PIXSHUF2 stores the activated output through PixelShuffle(2).
+ * PP_PREPARED (pp_conv2d_fwd only): the workspace already holds this
+ * layer's matrix-core weights, written by pp_conv2d_prepare, and is not
+ * rewritten (see there). */
+enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u, PP_ACCUMULATE = 4u, PP_PIXSHUF2 = 8u, PP_UPSAMPLE2 = 16u,
+       PP_PREPARED = 32u };
 
 /* Shape and storage of one pruned 3x3 layer. */
 typedef struct {
@@ -257,6 +261,29 @@ pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes, const voi
                                 int32_t act_dtype, uint32_t flags, void* hip_stream);
 
 /*
+ * pp_conv2d_prepare -- write, once, the weights a bf16 layer run in its
+ * matrix-core form reads (the layer as the masked dense contraction of
+ * Sec. 2's pruning structure: bf16 [c_out][9][c_in] in original filter
+ * order, zeros for taps off a kernel's pattern and for pruned kernels, then
+ * the fp32 bias), which pp_conv2d_fwd otherwise re-derives from the blob on
+ * every call.  The weights never change, so a caller that keeps the buffer
+ * passes it as the workspace of later calls with PP_PREPARED (or as
+ * pp_net_op.d_w of the layer in pp_net_fwd), and the per-call expansion is
+ * skipped.  A call whose plan is not the matrix-core form ignores the
+ * buffer and runs without a workspace.
+ *   h_blob, blob_bytes, d_blob  as pp_conv2d_fwd
+ *   prepared     device buffer, 256-byte aligned, or NULL to query the size
+ *   inout_bytes  in: capacity of prepared; out: bytes required
+ *   hip_stream   stream the expansion is enqueued on (NULL: default)
+ * Errors: PP_EBLOB, PP_EINVAL (NULL pointers, misaligned buffers),
+ * PP_EUNSUPPORTED (c_in not a multiple of 32 or a layer too large for the
+ * matrix-core form), PP_ESIZE (capacity too small; *inout_bytes then holds
+ * the required size), PP_EHIP.
+ */
+pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, const void* d_blob, void* prepared,
+                            size_t* inout_bytes, void* hip_stream);
+
+/*
  * pp_conv2d_workspace -- device scratch bytes pp_conv2d_fwd can use for this
  * layer and input (0: it would not use any); h, w are the conv's input size
  * (for a PP_UPSAMPLE2 call the upsampled size 2h x 2w; a call with fused
@@ -334,7 +361,10 @@ typedef struct {
   const void* h_blob;        /* PP_OP_CONV_PP: host blob                        */
   size_t blob_bytes;
   const void* d_blob;        /* PP_OP_CONV_PP: device blob                      */
-  const void* d_w;           /* dense ops: device weights in the act dtype      */
+  const void* d_w;           /* dense ops: device weights in the act dtype;     */
+                             /* PP_OP_CONV_PP: NULL, or the layer's prepared    */
+                             /* weights (pp_conv2d_prepare), read when the net  */
+                             /* runs the layer in its matrix-core form          */
   const float* d_b;          /* dense ops: device fp32 bias, or NULL            */
 } pp_net_op;
 

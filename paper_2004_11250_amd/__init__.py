@@ -25,6 +25,7 @@ PP_MAXPOOL2 = 2
 PP_ACCUMULATE = 4
 PP_PIXSHUF2 = 8
 PP_UPSAMPLE2 = 16
+PP_PREPARED = 32
 PP_NET_TAKEN = 0x80000000
 (OP_CONV_PP, OP_CONV_DENSE, OP_DECONV, OP_MAXPOOL2, OP_UPSAMPLE2, OP_PIXSHUF2, OP_ADD) = range(7)
 
@@ -32,7 +33,8 @@ PP_NET_TAKEN = 0x80000000
 SYMBOLS = ("pp_pack", "pp_blob_info", "pp_conv2d_fwd", "pp_conv2d_workspace", "pp_conv2d_recipe",
            "pp_conv2d_out_size", "pp_net_workspace", "pp_net_fwd", "pp_status_str", "pp_last_error",
            "pp_project_patterns", "pp_project_connectivity", "pp_project_columns", "pp_column_library",
-           "pp_fold_bn", "pp_jit_library", "pp_conv2d_fwd_noalloc", "pp_net_plan", "pp_round_bf16")
+           "pp_fold_bn", "pp_jit_library", "pp_conv2d_fwd_noalloc", "pp_net_plan", "pp_round_bf16",
+           "pp_conv2d_prepare")
 
 
 class PPError(RuntimeError):
@@ -74,6 +76,7 @@ def load_library(path: str = LIB_PATH):
         "pp_conv2d_fwd": [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp, sz, vp],
         "pp_conv2d_fwd_noalloc": [vp, sz, vp, vp, vp, i32, i32, i32, i32, u32, vp],
         "pp_conv2d_workspace": [vp, sz, i32, i32, i32, i32, ctypes.POINTER(sz)],
+        "pp_conv2d_prepare": [vp, sz, vp, vp, ctypes.POINTER(sz), vp],
         "pp_conv2d_out_size": [vp, sz, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "pp_conv2d_recipe": [vp, sz, i32, i32, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "pp_net_workspace": [ctypes.POINTER(NetOp), i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz),
@@ -287,6 +290,28 @@ class PackedLayer:
         if self.d_blob.data_ptr() % 256:
             raise RuntimeError("device blob allocation is not 256-byte aligned")
         self.scratch = {}   # conv2d_fwd workspaces by input shape
+        self.prepared = None   # matrix-core weights (prepare())
+
+    def prepare(self, stream=None):
+        """pp_conv2d_prepare: write this layer's matrix-core weights once
+        into a device buffer kept on the layer (for bf16 calls that run the
+        matrix-core form; conv2d_fwd(..., prepared=True) then skips the
+        per-call expansion).  Returns the buffer, or None for a layer the
+        form cannot run (c_in not a multiple of 32)."""
+        torch = _torch()
+        lib = load_library()
+        nb = ctypes.c_size_t(0)
+        st = lib.pp_conv2d_prepare(_ptr(self.h_blob), self.h_blob.nbytes, None, None, ctypes.byref(nb), None)
+        if st == PP_EUNSUPPORTED:
+            return None
+        _check(st, "pp_conv2d_prepare(size)")
+        buf = torch.empty(nb.value, dtype=torch.uint8, device=self.d_blob.device)
+        if buf.data_ptr() % 256:
+            raise RuntimeError("prepared-weights allocation is not 256-byte aligned")
+        _check(lib.pp_conv2d_prepare(_ptr(self.h_blob), self.h_blob.nbytes, self.d_blob.data_ptr(), buf.data_ptr(),
+                                     ctypes.byref(nb), _stream_ptr(stream)), "pp_conv2d_prepare")
+        self.prepared = buf
+        return buf
 
     @classmethod
     def from_weights(cls, w, b, pattern_id, conn, lib_masks, stride=1, pad=1, dilation=1, wdtype=PP_F32,
@@ -295,7 +320,7 @@ class PackedLayer:
 
 
 def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspace="auto", maxpool2=False,
-               accumulate=False, pixshuf2=False, upsample2=False):
+               accumulate=False, pixshuf2=False, upsample2=False, prepared=False):
     """pp_conv2d_fwd on torch tensors; returns y (allocated when out is None).
     workspace: "auto" (a scratch tensor of pp_conv2d_workspace bytes, kept on
     the layer per input shape), None (no scratch) or a uint8 device tensor.
@@ -303,9 +328,14 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     accumulate: add the activated output to ``out`` in place (PP_ACCUMULATE;
     out is required).  pixshuf2: store through PixelShuffle(2)
     (PP_PIXSHUF2).  upsample2: convolve the nearest x2 upsampling of x
-    (PP_UPSAMPLE2)."""
+    (PP_UPSAMPLE2).  prepared: pass the layer's prepared matrix-core weights
+    (layer.prepare()) as the workspace with PP_PREPARED."""
     torch = _torch()
     lib = load_library()
+    if prepared:
+        if layer.prepared is None:
+            raise ValueError("the layer has no prepared weights (call layer.prepare() first)")
+        workspace = layer.prepared
     if not x.is_contiguous():
         raise ValueError("x must be contiguous NCHW")
     n, c, h, w = x.shape
@@ -339,7 +369,7 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
                            out.data_ptr(), n, h, w, _dtype_code(x),
                            (PP_RELU if relu else 0) | (PP_MAXPOOL2 if maxpool2 else 0) |
                            (PP_ACCUMULATE if accumulate else 0) | (PP_PIXSHUF2 if pixshuf2 else 0) |
-                           (PP_UPSAMPLE2 if upsample2 else 0), ws_ptr, ws_bytes,
+                           (PP_UPSAMPLE2 if upsample2 else 0) | (PP_PREPARED if prepared else 0), ws_ptr, ws_bytes,
                            _stream_ptr(stream))
     _check(st, "pp_conv2d_fwd")
     return out
@@ -380,6 +410,8 @@ def _op_array(ops, params, wd, device_tensors):
             e.h_blob = blob.ctypes.data
             e.blob_bytes = blob.nbytes
             e.d_blob = dev[0].data_ptr() if dev else None
+            prep = dev[1].prepared if dev else None
+            e.d_w = prep.data_ptr() if prep is not None else None
         elif kind in (OP_CONV_DENSE, OP_DECONV):
             dev = device_tensors(op, prm, None)
             keep.append(dev)
@@ -422,7 +454,11 @@ class Net:
     _KIND = {"conv3": OP_CONV_PP, "conv": OP_CONV_DENSE, "deconv": OP_DECONV, "maxpool2": OP_MAXPOOL2,
              "up2": OP_UPSAMPLE2, "pshuf2": OP_PIXSHUF2, "add": OP_ADD}
 
-    def __init__(self, ops, params, dtype="f32", device="cuda"):
+    def __init__(self, ops, params, dtype="f32", device="cuda", prepare=True):
+        """prepare: (bf16) write each pruned layer's matrix-core weights once
+        (PackedLayer.prepare) and hand them to pp_net_fwd (pp_net_op.d_w),
+        which reads them for the layers it runs in that form instead of
+        expanding the blob on every call."""
         torch = _torch()
         self.dtype = dtype
         self.wd = PP_BF16 if dtype == "bf16" else PP_F32
@@ -433,6 +469,8 @@ class Net:
             if blob is not None:
                 L = PackedLayer(blob, device)
                 self.pruned.append(L)
+                if prepare and self.wd == PP_BF16:
+                    L.prepare()
                 return (L.d_blob, L)
             w = np.ascontiguousarray(prm["w"], dtype=np.float32)
             if self.wd == PP_BF16:

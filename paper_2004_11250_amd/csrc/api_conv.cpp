@@ -89,8 +89,14 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const size_t esz = act_dtype == PP_BF16 ? 2 : 4;
   if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % esz)
     return fail(PP_EINVAL, "activation pointers misaligned");
-  if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2))
+  if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2 | PP_PREPARED))
     return fail(PP_EINVAL, "unknown flags");
+  // PP_PREPARED: the scratch holds the layer's matrix-core weights; it is
+  // used only by that form and never as split scratch
+  const bool prepared = (flags & PP_PREPARED) != 0;
+  flags &= ~static_cast<uint32_t>(PP_PREPARED);
+  if (prepared && (!scratch || reinterpret_cast<uintptr_t>(scratch) % 256))
+    return fail(PP_EINVAL, "PP_PREPARED needs the prepared weights (256-byte aligned) as the workspace");
   {
     const uint32_t f = flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2);
     if (f & (f - 1)) return fail(PP_EINVAL, "more than one of PP_MAXPOOL2, PP_ACCUMULATE, PP_PIXSHUF2");
@@ -111,6 +117,21 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   p.flags = flags;
   const int lib = library_kind(v);
   const bool bf = act_dtype == PP_BF16;
+  if (prepared) {
+    // the prepared weights serve the matrix-core form only; any other plan
+    // runs without a workspace
+    ConvParams q = p;
+    const ConvPlan mp = plan_with_scratch(q, lib, bf, scratch_bytes, false);
+    if (mp.recipe == kRecipeMfma) {
+      q.part = static_cast<float*>(scratch);
+      q.flags |= PP_PREPARED;   // the expansion is skipped
+      const hipError_t e = launch_conv(lib, mp, q, bf, st);
+      if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
+      return PP_OK;
+    }
+    scratch = nullptr;
+    scratch_bytes = 0;
+  }
   const size_t usable = reinterpret_cast<uintptr_t>(scratch) % 256 ? 0 : scratch_bytes;
   // the plan for library kind `kind`; a split only with enough scratch
   auto make_plan = [&](int kind, ConvParams* pp_, bool no_lean) {
@@ -265,6 +286,37 @@ extern "C" pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, 
     const size_t b = split_bytes(plan_conv(p, kLibCanon8, act_dtype == PP_BF16, true, true), p);
     if (b > *bytes) *bytes = b;
   }
+  return PP_OK;
+}
+
+namespace pp {
+size_t prepared_bytes(const BlobView& v) { return mfma_bytes(layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1)); }
+}  // namespace pp
+
+extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, const void* d_blob, void* prepared,
+                                       size_t* inout_bytes, void* hip_stream) {
+  clear_error();
+  BlobView v;
+  pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
+  if (s != PP_OK) return s;
+  if (!inout_bytes) return fail(PP_EINVAL, "inout_bytes is NULL");
+  // the expansion does not depend on the input size: one pixel stands in
+  ConvParams p = layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1);
+  if (!mfma_eligible(p)) return fail(PP_EUNSUPPORTED, "the matrix-core form needs c_in a multiple of 32");
+  const size_t need = prepared_bytes(v);
+  if (!prepared) {
+    *inout_bytes = need;
+    return PP_OK;
+  }
+  if (*inout_bytes < need) {
+    *inout_bytes = need;
+    return fail(PP_ESIZE, "prepared buffer too small");
+  }
+  if (!d_blob || reinterpret_cast<uintptr_t>(d_blob) % 256 || reinterpret_cast<uintptr_t>(prepared) % 256)
+    return fail(PP_EINVAL, "d_blob and prepared must be 256-byte aligned device pointers");
+  p.blob = static_cast<const uint8_t*>(d_blob);
+  const hipError_t e = launch_mfma_expand(p, prepared, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(PP_EHIP, std::string("expansion launch: ") + hipGetErrorString(e));
   return PP_OK;
 }
 

@@ -174,7 +174,8 @@ bool mfma_eligible(const ConvParams& p);
 size_t mfma_bytes(const ConvParams& p);
 bool mfma_long_k(const ConvParams& p);   // k steps of 64 (else 32)
 int mfma_groups(const ConvParams& p);    // wave groups per tile splitting its k steps (1 or 2)
-hipError_t launch_mfma_conv(const ConvParams& p, hipStream_t st);
+hipError_t launch_mfma_conv(const ConvParams& p, hipStream_t st);   // PP_PREPARED in p.flags: no expansion
+hipError_t launch_mfma_expand(const ConvParams& p, void* out, hipStream_t st);   // the weights into out
 
 // allow_split: the caller can provide scratch (a channel split's partial
 // sums, or the matrix-core form's expanded weights: kRecipeMfma).  With

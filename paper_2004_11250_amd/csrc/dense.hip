@@ -376,6 +376,223 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
   }
 }
 
+// The same implicit GEMMs for bf16 activations and weights on the bf16
+// matrix cores (v_mfma_f32_32x32x16_bf16, 16x the fp32 rate): operands stay
+// bf16 through LDS, stored row-major per filter / pixel with k fastest
+// ([row][k], a pitch of kMK + 8 elements: one 16-byte read gives a lane its
+// 8 k of a 32 x 32 x 16 step), products are exact in fp32 and sums fp32, and
+// the store rounds once to bf16.  The gathers are those of the fp32 kernel.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+template <int MODE, int KD, int WM, int TM, int TN>
+__global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int n_tiles, int m_tiles) {
+  constexpr int WN = 4 / WM, BM = 32 * TM * WM, BN = 32 * TN * WN;
+  constexpr int JA = kMK * BM / 256, JB = kMK * BN / 256;   // A / B elements per thread per step
+  constexpr int AR = 256 / kMK;                             // A rows per load pass
+  constexpr int KK = MODE == 0 ? KD * KD : 4;               // k per input channel
+  constexpr int kPitch = kMK + 8;
+  static_assert(JB % 8 == 0, "a thread's B elements of a step are whole 16-byte pieces");
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][kPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][kPitch];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wv % WM, wn = wv / WM;
+  int t = blockIdx.x;
+  const int nt = t % n_tiles;
+  t /= n_tiles;
+  const int mt = t % m_tiles;
+  const int cls = t / m_tiles;   // parity class of the transposed conv (0 for a conv)
+  const int py = cls >> 1, px = cls & 1;
+  const int K = p.c_in * KK;
+  const int gh = MODE == 0 ? p.ho : p.h, gw = MODE == 0 ? p.wo : p.w;
+  const long np = static_cast<long>(p.n) * gh * gw;
+  const uint16_t* __restrict__ wt = static_cast<const uint16_t*>(p.wt);
+  const uint16_t* __restrict__ x = static_cast<const uint16_t*>(p.x);
+
+  const int ak = tid % kMK, am0 = tid / kMK;
+  const int bn = tid % BN, bk0 = (tid / BN) * JB;
+  const long bp = static_cast<long>(nt) * BN + bn;
+  const bool bvalid = bp < np;
+  int by = 0, bx = 0;
+  long bimg = 0;
+  if (bvalid) {
+    bx = static_cast<int>(bp % gw);
+    const long q = bp / gw;
+    by = static_cast<int>(q % gh);
+    bimg = q / gh;
+  }
+  const uint32_t ximg = static_cast<uint32_t>(bimg) * p.c_in * p.h * p.w;
+  constexpr uint32_t kOut = 0x80000000u;
+  const size_t x_elems = static_cast<size_t>(p.n) * p.c_in * p.h * p.w;
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(x), static_cast<short>(0), static_cast<int>(x_elems * 2), 0x00020000);
+  const size_t n_w = static_cast<size_t>(p.c_out) * p.c_in * (MODE == 0 ? KK : 16);
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(wt), static_cast<short>(0), static_cast<int>(n_w * 2), 0x00020000);
+  auto bload_b = [&](__amdgpu_buffer_rsrc_t r, uint32_t off) __attribute__((always_inline)) {
+    return static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+  };
+  auto bload = [&](__amdgpu_buffer_rsrc_t r, uint32_t el) __attribute__((always_inline)) {
+    return bload_b(r, el == kOut ? kOut : el * 2u);
+  };
+  uint32_t ra[JA], rb[JB];
+  auto fetch_any = [&](int k0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < JA; ++j) {
+      const int kk = k0 + ak, ao = mt * BM + am0 + AR * j;
+      uint32_t el = kOut;
+      if (ao < p.c_out && kk < K) {
+        if constexpr (MODE == 0) {
+          el = static_cast<uint32_t>(ao) * K + kk;
+        } else {
+          const int c = kk >> 2, a = (kk >> 1) & 1, b = kk & 1;
+          const int ky = 1 - py + 2 * a, kx = 1 - px + 2 * b;
+          el = ((static_cast<uint32_t>(c) * p.c_out + ao) * 4 + ky) * 4 + kx;
+        }
+      }
+      ra[j] = bload(wr, el);
+    }
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int kk = k0 + bk0 + j;
+      uint32_t el = kOut;
+      if (bvalid && kk < K) {
+        int c, iy, ix;
+        if constexpr (MODE == 0) {
+          c = kk / KK;
+          const int r = kk - c * KK, ky = r / KD, kx = r - ky * KD;
+          iy = by + ky - p.pad;
+          ix = bx + kx - p.pad;
+        } else {
+          c = kk >> 2;
+          iy = by + py - ((kk >> 1) & 1);
+          ix = bx + px - (kk & 1);
+        }
+        if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) el = ximg + (static_cast<uint32_t>(c) * p.h + iy) * p.w + ix;
+      }
+      rb[j] = bload(xr, el);
+    }
+  };
+  constexpr bool STEPPED = MODE == 1 || KD == 1;
+  uint32_t aoff[STEPPED ? JA : 1], boff[STEPPED ? JB : 1];
+  if constexpr (STEPPED) {
+#pragma unroll
+    for (int j = 0; j < JA; ++j) {
+      const int ao = mt * BM + am0 + AR * j;
+      uint32_t el = kOut;
+      if (ao < p.c_out) {
+        if constexpr (MODE == 0) {
+          el = static_cast<uint32_t>(ao) * K + ak;
+        } else {
+          const int c = ak >> 2, ky = 1 - py + 2 * ((ak >> 1) & 1), kx = 1 - px + 2 * (ak & 1);
+          el = ((static_cast<uint32_t>(c) * p.c_out + ao) * 4 + ky) * 4 + kx;
+        }
+      }
+      aoff[j] = el == kOut ? kOut : el * 2u;
+    }
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int kk = bk0 + j;
+      uint32_t el = kOut;
+      if (bvalid) {
+        const int c = MODE == 0 ? kk : kk >> 2;
+        const int iy = MODE == 0 ? by : by + py - ((kk >> 1) & 1);
+        const int ix = MODE == 0 ? bx : bx + px - (kk & 1);
+        if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) el = ximg + (static_cast<uint32_t>(c) * p.h + iy) * p.w + ix;
+      }
+      boff[j] = el == kOut ? kOut : el * 2u;
+    }
+  }
+  const size_t a_step = MODE == 0 ? kMK : static_cast<size_t>(kMK / 4) * p.c_out * 16;
+  const size_t b_step = static_cast<size_t>(MODE == 0 ? kMK : kMK / 4) * p.h * p.w;
+  auto fetch = [&](int s) __attribute__((always_inline)) {
+    const int k0 = s * kMK;
+    if constexpr (STEPPED) {
+      if (k0 + kMK <= K) {
+        const size_t ao0 = s * a_step, bo0 = s * b_step;
+        const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(wt + ao0), static_cast<short>(0), static_cast<int>((n_w - min(n_w, ao0)) * 2),
+            0x00020000);
+        const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(x + bo0), static_cast<short>(0), static_cast<int>((x_elems - min(x_elems, bo0)) * 2),
+            0x00020000);
+#pragma unroll
+        for (int j = 0; j < JA; ++j) ra[j] = bload_b(wrs, aoff[j]);
+#pragma unroll
+        for (int j = 0; j < JB; ++j) rb[j] = bload_b(xrs, boff[j]);
+        return;
+      }
+    }
+    fetch_any(k0);
+  };
+  auto put = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < JA; ++j) As[buf][am0 + AR * j][ak] = static_cast<uint16_t>(ra[j]);
+#pragma unroll
+    for (int q = 0; q < JB / 8; ++q)
+      *reinterpret_cast<uint4*>(&Bs[buf][bn][bk0 + 8 * q]) =
+          make_uint4(rb[8 * q] | (rb[8 * q + 1] << 16), rb[8 * q + 2] | (rb[8 * q + 3] << 16),
+                     rb[8 * q + 4] | (rb[8 * q + 5] << 16), rb[8 * q + 6] | (rb[8 * q + 7] << 16));
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+  const int steps = (K + kMK - 1) / kMK;
+  fetch(0);
+  put(0);
+  __syncthreads();
+  for (int s = 0; s < steps; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < steps) fetch(s + 1);
+    // a 32 x 32 x 16 MFMA takes row l % 32 of A and column l % 32 of B, k
+    // 8 (l / 32) .. 8 (l / 32) + 7 of its 16, in lane l
+#pragma unroll
+    for (int h = 0; h < kMK; h += 16) {
+      bf16x8 av[TM], bv[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        av[i] = *reinterpret_cast<const bf16x8*>(&As[buf][(wm * TM + i) * 32 + (lane & 31)][h + 8 * (lane >> 5)]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bv[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][(wn * TN + j) * 32 + (lane & 31)][h + 8 * (lane >> 5)]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+    if (s + 1 < steps) put(buf ^ 1);   // that buffer's last readers passed the barrier below one step ago
+    __syncthreads();
+  }
+
+  // accumulator r of block (i, j), lane l, is C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] of the block
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const long gp = static_cast<long>(nt) * BN + (wn * TN + j) * 32 + (lane & 31);
+    if (gp >= np) continue;
+    const int ex = static_cast<int>(gp % gw);
+    const long q = gp / gw;
+    const int ey = static_cast<int>(q % gh);
+    const long eimg = q / gh;
+    const int oy = MODE == 0 ? ey : 2 * ey + py, ox = MODE == 0 ? ex : 2 * ex + px;
+    uint16_t* __restrict__ y = static_cast<uint16_t*>(p.y) + static_cast<size_t>(eimg) * p.c_out * p.ho * p.wo;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int o = mt * BM + (wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (o < p.c_out) {
+          float v = acc[i][j][r] + (p.bias ? p.bias[o] : 0.0f);
+          if (p.relu) v = fmaxf(v, 0.0f);
+          st(y, (static_cast<size_t>(o) * p.ho + oy) * p.wo + ox, v);
+        }
+      }
+  }
+}
+
 template <int MODE, int KD, class TA>
 hipError_t launch_mfma(const DenseParams& p, hipStream_t st) {
   const int gh = MODE == 0 ? p.ho : p.h, gw = MODE == 0 ? p.wo : p.w;
@@ -400,12 +617,21 @@ hipError_t launch_mfma(const DenseParams& p, hipStream_t st) {
   if (blocks < 1 || blocks > 0x7FFFFFFFL) return hipErrorInvalidConfiguration;
   const dim3 grid(static_cast<uint32_t>(blocks));
   const int nt = static_cast<int>(n_tiles), mt = static_cast<int>(m_tiles);
-  if (shape == 0)
-    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 1, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
-  else if (shape == 2)
-    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 2, 2, TA>), grid, dim3(256), 0, st, p, nt, mt);
-  else
-    hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
+  if constexpr (sizeof(TA) == 2) {
+    if (shape == 0)
+      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 1, 1, 1>), grid, dim3(256), 0, st, p, nt, mt);
+    else if (shape == 2)
+      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 2, 2, 2>), grid, dim3(256), 0, st, p, nt, mt);
+    else
+      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 2, 1, 1>), grid, dim3(256), 0, st, p, nt, mt);
+  } else {
+    if (shape == 0)
+      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 1, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
+    else if (shape == 2)
+      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 2, 2, TA>), grid, dim3(256), 0, st, p, nt, mt);
+    else
+      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
+  }
   return hipGetLastError();
 }
 

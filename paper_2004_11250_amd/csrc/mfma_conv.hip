@@ -341,14 +341,24 @@ int mfma_groups(const ConvParams& p) {
 
 size_t mfma_bytes(const ConvParams& p) { return a_bytes(p) + static_cast<size_t>(p.c_out) * sizeof(float); }
 
-hipError_t launch_mfma_conv(const ConvParams& p, hipStream_t st) {
-  if (!mfma_eligible(p) || !p.part || reinterpret_cast<uintptr_t>(p.part) % 256) return hipErrorInvalidValue;
-  uint16_t* am = reinterpret_cast<uint16_t*>(p.part);
-  float* bo = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(p.part) + a_bytes(p));
+hipError_t launch_mfma_expand(const ConvParams& p, void* out, hipStream_t st) {
+  if (!out || reinterpret_cast<uintptr_t>(out) % 256) return hipErrorInvalidValue;
+  uint16_t* am = static_cast<uint16_t*>(out);
+  float* bo = reinterpret_cast<float*>(static_cast<uint8_t*>(out) + a_bytes(p));
   const long ex = static_cast<long>(p.n_groups) * 8 * p.c_in;
   hipLaunchKernelGGL(pp_mfma_expand_kernel, dim3(static_cast<uint32_t>((ex + 255) / 256)), dim3(256), 0, st, p, am, bo);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_mfma_conv(const ConvParams& p, hipStream_t st) {
+  if (!mfma_eligible(p) || !p.part || reinterpret_cast<uintptr_t>(p.part) % 256) return hipErrorInvalidValue;
+  const uint16_t* am = reinterpret_cast<const uint16_t*>(p.part);
+  const float* bo = reinterpret_cast<const float*>(reinterpret_cast<const uint8_t*>(p.part) + a_bytes(p));
+  // PP_PREPARED: the workspace already holds the expansion (pp_conv2d_prepare)
+  if (!(p.flags & PP_PREPARED)) {
+    const hipError_t e = launch_mfma_expand(p, p.part, st);
+    if (e != hipSuccess) return e;
+  }
   const bool up = (p.flags & PP_UPSAMPLE2) != 0;
   // 128 x 128 tiles for more than 64 filters, else 64 x 128; k steps of 64
   // for reductions of 1152+ (fewer, longer steps: better where each tile's

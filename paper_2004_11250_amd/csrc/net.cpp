@@ -340,8 +340,16 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
         // with the upsample before it (PP_UPSAMPLE2) and / or the pool, add or
         // shuffle after it (then op i + 1 is taken too)
         const uint32_t fl = op.flags | pl.fuse[i] | (pl.up_in[i] ? PP_UPSAMPLE2 : 0u);
-        st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl, scratch, pl.scratch_bytes,
-                          stream);
+        // a layer the net runs in its matrix-core form reads the caller's
+        // prepared weights (d_w) instead of expanding the blob into the
+        // scratch
+        if (op.d_w && conv_recipe(pl.views[i], n, si.h, si.w, act_dtype, fl, pl.scratch_bytes) == kRecipeMfma) {
+          st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl | PP_PREPARED,
+                            const_cast<void*>(op.d_w), prepared_bytes(pl.views[i]), stream);
+        } else {
+          st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl, scratch, pl.scratch_bytes,
+                            stream);
+        }
         if (st != PP_OK) return st;
         if (pl.fuse[i]) ++i;
         break;

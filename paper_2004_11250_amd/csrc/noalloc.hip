@@ -53,6 +53,7 @@ extern "C" pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes
   BlobView v;
   pp_status s = parse_blob(h_blob, blob_bytes, &v, /*full=*/false);
   if (s != PP_OK) return s;
+  if (flags & PP_PREPARED) return fail(PP_EINVAL, "PP_PREPARED needs the prepared weights as a workspace");
   // the scratch pp_conv2d_fwd would use with a pp_conv2d_workspace()-sized
   // workspace (that call sizes a PP_UPSAMPLE2 conv by its upsampled input)
   const bool up = (flags & PP_UPSAMPLE2) != 0;

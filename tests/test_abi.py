@@ -222,3 +222,28 @@ def test_round_bf16_matches_the_oracle_rounding(lib):
     assert np.all((r & 0x7F80) == 0x7F80) and np.all(r & 0x007F)
     assert lib.pp_round_bf16(None, None, 1) == pp.PP_EINVAL
     assert lib.pp_round_bf16(None, None, 0) == pp.PP_OK
+
+
+def test_prepare_host_checks(lib):
+    # host-side outcomes of pp_conv2d_prepare: the size query, a layer the
+    # matrix-core form cannot run, a short buffer, NULL and misaligned
+    # pointers -- all before any device work
+    L = workloads.random_layer(31, 40, 64, keep=0.5)
+    blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+    nb = ctypes.c_size_t(0)
+    assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_OK
+    assert nb.value == -(-40 * 9 * 64 * 2 // 256) * 256 + 40 * 4
+    small = ctypes.c_size_t(nb.value - 1)
+    assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, 0x100000, 0x200000, ctypes.byref(small),
+                                 None) == pp.PP_ESIZE
+    assert small.value == nb.value
+    assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, 0x100000, 0x200010, ctypes.byref(nb),
+                                 None) == pp.PP_EINVAL
+    assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, None, None, None, None) == pp.PP_EINVAL
+    L2 = workloads.random_layer(32, 40, 48, keep=0.5)   # c_in not a multiple of 32
+    blob2 = pp.pack(L2["w"], L2["b"], L2["pid"], L2["conn"], L2["lib"], 1, 1, 1, pp.PP_BF16)
+    assert lib.pp_conv2d_prepare(blob2.ctypes.data, blob2.nbytes, None, None, ctypes.byref(nb),
+                                 None) == pp.PP_EUNSUPPORTED
+    # the allocation-free call has no prepared buffer to read
+    assert lib.pp_conv2d_fwd_noalloc(blob.ctypes.data, blob.nbytes, 0x100000, 0x200000, 0x300000, 1, 8, 8,
+                                     pp.PP_BF16, pp.PP_PREPARED, None) == pp.PP_EINVAL

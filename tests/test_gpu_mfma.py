@@ -208,3 +208,40 @@ def test_mfma_full_colourization_layer():
     y = _host(pp.conv2d_fwd(layer, _dev(x), relu=True))
     ref, bound = _oracle(L, x, op["stride"], op["pad"], op["dil"], True)
     check(y, ref, bound, "bf16", f"colourization layer {i}")
+
+
+@pytest.mark.parametrize("case", [0, 2, 12, 15])
+def test_prepared_weights_equal_per_call_expansion(case, monkeypatch):
+    # the weights written once by pp_conv2d_prepare and passed with
+    # PP_PREPARED give bitwise the output of the call that expands them
+    monkeypatch.setenv("PP_RECIPE", str(MFMA))
+    lib, (s, p, d), (n, c_out, c_in, h, w), keep, relu = CASES[case]
+    seed = 1400 + case
+    L, layer = _layer(seed, c_out, c_in, lib, keep, s, p, d)
+    x = _dev(obf16.round_f32(workloads.random_input(seed, (n, c_in, h, w))))
+    _say("prepared", lib, (s, p, d), (n, c_out, c_in, h, w), "seed", seed)
+    assert pp.conv2d_recipe(layer.h_blob, n, h, w, pp.PP_BF16) == MFMA
+    want = _host(pp.conv2d_fwd(layer, x, relu=relu))
+    assert layer.prepare() is not None
+    for _ in range(2):
+        got = _host(pp.conv2d_fwd(layer, x, relu=relu, prepared=True))
+        assert np.array_equal(got, want)
+
+
+def test_prepared_weights_ignored_off_the_matrix_cores():
+    # a layer the planner keeps on the vector ALUs: with PP_PREPARED the call
+    # runs without a workspace (the prepared buffer is left untouched)
+    spec = workloads.net_spec(2)
+    i = next(j for j, op in enumerate(spec["ops"]) if op["op"] == "conv3" and op["c_in"] == 512)
+    op = spec["ops"][i]
+    L = workloads.layer_params(2, i, op)
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+    x = _dev(obf16.round_f32(workloads.random_input(1500, (1, 512, 14, 14), 0.0, 1.0)))
+    _say("prepared off the matrix cores: VGG-16 layer", i, "bf16 14 x 14")
+    assert pp.conv2d_recipe(layer.h_blob, 1, 14, 14, pp.PP_BF16) != MFMA
+    buf = layer.prepare()
+    before = buf.clone()
+    want = _host(pp.conv2d_fwd(layer, x, relu=True, workspace=None))
+    got = _host(pp.conv2d_fwd(layer, x, relu=True, prepared=True))
+    assert np.array_equal(got, want)
+    assert torch.equal(buf, before)

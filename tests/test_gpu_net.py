@@ -234,3 +234,19 @@ def test_vgg16_end_to_end_vs_oracle_chain():
     rel = np.max(np.abs(y - ref)) / np.max(np.abs(ref))
     _say(f"vgg16 end-to-end max|err|/max|ref| = {rel:.3e}")
     assert rel < 1e-4
+
+
+@pytest.mark.parametrize("cfg", [4, 5])
+def test_prepared_net_equals_per_call_expansion(cfg):
+    # bf16 networks: prepared matrix-core weights (pp_net_op.d_w) give
+    # bitwise the frame that expands them on every call
+    spec = workloads.net_spec(cfg)
+    params = workloads.net_params(cfg)
+    _, x = _input(cfg, "bf16")
+    _say(f"cfg {cfg} bf16: prepared vs per-call expansion")
+    a = pp.Net(spec["ops"], params, "bf16", prepare=False)
+    b = pp.Net(spec["ops"], params, "bf16", prepare=True)
+    assert sum(L.prepared is not None for L in b.pruned) > 0
+    ya = _np(a.forward(x))
+    for _ in range(2):
+        assert np.array_equal(_np(b.forward(x)), ya)
