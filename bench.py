@@ -163,7 +163,7 @@ def summarize_profile(root, cfg=2):
                     return out
                 e = dict(ds[j], c=dict(ds[j]["c"]))
                 j += 1
-                if j < len(ds) and "pp_split_reduce" in ds[j]["name"]:
+                if j < len(ds) and ("pp_split_reduce" in ds[j]["name"] or "pp_lean_reduce" in ds[j]["name"]):
                     e["dur_ns"] += ds[j]["dur_ns"]
                     for k, v in ds[j]["c"].items():
                         e["c"][k] = e["c"].get(k, 0.0) + v
@@ -479,12 +479,24 @@ def main():
         for _ in range(5):
             pp.conv2d_fwd(L, xin, out=yo, **kw)
         torch.cuda.synchronize()
+        # the launches recorded in a graph and replayed: the layer's GPU time
+        # (a host loop of calls would be bound by the calls themselves for
+        # the shortest layers)
+        gr = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(gr, stream=side):
+                for _ in range(args.layer_steps):
+                    pp.conv2d_fwd(L, xin, out=yo, **kw)
+        gr.replay()
+        torch.cuda.synchronize()
         a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a0.record(stream)
-        for _ in range(args.layer_steps):
-            pp.conv2d_fwd(L, xin, out=yo, **kw)
+        gr.replay()
         a1.record(stream)
         torch.cuda.synchronize()
+        del gr
         us = a0.elapsed_time(a1) * 1e3 / args.layer_steps
         macs = surviving_macs(op, prm, shapes[i][3], batch)
         # the form the planner runs: the vector-ALU kernels, or (bf16) the
