@@ -119,15 +119,20 @@ static int choose_split(int id, const ConvParams& p) {
   return ks;
 }
 
-// channel split of a lean tiling: the one-row-per-lane 16-wave tiling on
-// maps of at most 16 x 16 outputs runs split two ways (measured on MI355X at
-// 14 x 14, 512 -> 512: 21 us against 27 unsplit); none otherwise
+// channel split of a lean tiling: the 16-wave tilings on maps of at most
+// 16 x 16 outputs run split, the one-row-per-lane ones two ways and the 2 x 2
+// ones four ways, keeping at least 8 channels per wave (measured on MI355X
+// at 14 x 14, 512 -> 512: 2 x 2 split four ways 18 us, one row split two
+// ways 19 us, unsplit 26-28 us); none on larger maps, where the grid already
+// holds four waves per SIMD and a split only adds partial sums
 static int choose_split_lean(int id, const ConvParams& p) {
   const int forced = env_int("PP_KSPLIT");
   if (forced >= 1) return forced < p.c_in ? forced : p.c_in;
   const RecipeInfo r = recipe_info(id);
-  if (r.r == 1 && r.ws == 16 && static_cast<long>(p.ho) * p.wo <= 16L * 16 && p.c_in >= 64) return 2;
-  return 1;
+  if (r.ws != 16 || static_cast<long>(p.ho) * p.wo > 16L * 16) return 1;
+  int ks = r.r == 1 ? 2 : 4;
+  while (ks > 1 && p.c_in / (ks * r.ws) < 8) ks /= 2;
+  return ks;
 }
 
 static ConvPlan finish_plan(int id, const ConvParams& p, bool allow_split) {
@@ -209,8 +214,8 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
     // fp32, stride 1, one image: the lean tilings that timed fastest on the
     // VGG-16 layer shapes (MI355X), by output size: 4 x 4 outputs per lane on
     // the 224 x 224 maps (4 channel-split waves) and 112 x 112 (8), 2 x 4 on
-    // 56 x 56, 2 x 2 with 16 waves on 28 x 28, and one row of 2 outputs per
-    // lane with 16 waves on smaller maps.  Each 16-byte staging tiling has a
+    // 56 x 56, 2 x 2 with 16 waves on 28 x 28 and, with 4-byte staging and a
+    // channel split, on smaller maps (else one row of 2 outputs per lane).  Each 16-byte staging tiling has a
     // 4-byte staging twin of the same tiling (widths not a multiple of 4, a
     // fused x2 upsample): same accumulation order, so a conv fused with the
     // upsample before it gives bitwise what the unfused conv gives.
@@ -224,7 +229,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
     } else if (pix >= 20L * 20L) {
       lp[0] = 48; lp[1] = 51;
     } else {
-      lp[0] = 54;
+      lp[0] = 51; lp[1] = 54;
     }
     if (forced < 0)
       for (int id : lp)

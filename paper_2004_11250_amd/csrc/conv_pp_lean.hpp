@@ -466,7 +466,10 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
 // Second pass of a channel split: y = act(sum over the ksplit partial-sum
 // blocks of a tile, in split order, + bias), stored through perm; with
 // PP_MAXPOOL2 the 2 x 2 max of the activated sums (windows wholly inside the
-// output).  One workgroup per (image, tile, slot group).
+// output).  One workgroup per (image, tile, slot group).  A thread first
+// works out where each of its outputs (or pooled windows) sits in a partial
+// block, then issues the loads of one split for all of them at once, so the
+// pass costs about one memory round trip per split, not one per output.
 template <int R, int CC, int LW>
 __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
   constexpr int LH = 64 / LW, TH = LH * R, TW = LW * CC;
@@ -481,44 +484,88 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
   const uint32_t img = t;
   const float* pb = a.part + static_cast<size_t>(item) * a.ksplit * BLK;
   const bool relu = (a.flags & PP_RELU) != 0;
-  const uint32_t* perm = reinterpret_cast<const uint32_t*>(a.blob + a.off_perm);
-  const float* biasv = reinterpret_cast<const float*>(a.blob + a.off_bias);
-  auto sum_at = [&](int s, int yl, int xl) {
-    const int ln = (yl / R) * LW + xl / CC;
-    const int e = (s * R + yl % R) * CC + xl % CC;
-    float v = 0.0f;
-    for (uint32_t k = 0; k < a.ksplit; ++k) v += pb[static_cast<size_t>(k) * BLK + e * 64 + ln];
-    v += biasv[grp * 8 + s];
+  uint32_t perm[8];
+  float biasv[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    perm[s] = sload<uint32_t>(a.blob, a.off_perm + 4u * (grp * 8u + s));
+    biasv[s] = sload<float>(a.blob, a.off_bias + 4u * (grp * 8u + s));
+  }
+  // offset of output (s, yl, xl) of the tile in a partial block
+  auto at = [](int s, int yl, int xl) {
+    return ((s * R + yl % R) * CC + xl % CC) * 64 + (yl / R) * LW + xl / CC;
+  };
+  auto act = [&](float v, int s) {
+    v += biasv[s];
     return relu ? fmaxf(v, 0.0f) : v;
   };
   if (a.flags & PP_MAXPOOL2) {
     const uint32_t pho = a.ho / 2, pwo = a.wo / 2;
     float* yp = a.y + static_cast<size_t>(img) * a.c_out * pho * pwo;
-    constexpr int PH = TH / 2, PW = TW / 2;
-    for (int i = threadIdx.x; i < 8 * PH * PW; i += 256) {
+    constexpr int PH = TH / 2, PW = TW / 2, NW = 8 * PH * PW, PER = (NW + 255) / 256;
+    int off[PER][4];
+    float v[PER][4];
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      const int i = min(static_cast<int>(threadIdx.x) + 256 * m, NW - 1);
+      const int s = i / (PH * PW), px = i % PW, py = (i / PW) % PH;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        off[m][j] = at(s, 2 * py + (j >> 1), 2 * px + (j & 1));
+        v[m][j] = 0.0f;
+      }
+    }
+    for (uint32_t k = 0; k < a.ksplit; ++k) {
+      const float* pk = pb + static_cast<size_t>(k) * BLK;
+#pragma unroll
+      for (int m = 0; m < PER; ++m)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[m][j] += pk[off[m][j]];
+    }
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      const int i = static_cast<int>(threadIdx.x) + 256 * m;
+      if (i >= NW) continue;
       const int s = i / (PH * PW), px = i % PW, py = (i / PW) % PH;
       const uint32_t oy = ty * TH + 2 * py, ox = tx * TW + 2 * px;
       if (oy + 1 >= a.ho || ox + 1 >= a.wo) continue;
-      const uint32_t o = perm[grp * 8 + s];
+      const uint32_t o = perm[s];
       if (o >= a.c_out) continue;
-      const float m = fmaxf(fmaxf(sum_at(s, 2 * py, 2 * px), sum_at(s, 2 * py, 2 * px + 1)),
-                            fmaxf(sum_at(s, 2 * py + 1, 2 * px), sum_at(s, 2 * py + 1, 2 * px + 1)));
-      yp[(static_cast<size_t>(o) * pho + oy / 2) * pwo + ox / 2] = m;
+      const float r = fmaxf(fmaxf(act(v[m][0], s), act(v[m][1], s)), fmaxf(act(v[m][2], s), act(v[m][3], s)));
+      yp[(static_cast<size_t>(o) * pho + oy / 2) * pwo + ox / 2] = r;
     }
     return;
   }
   float* y = a.y + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
-  for (int i = threadIdx.x; i < 8 * TH * TW; i += 256) {
+  constexpr int NO = 8 * TH * TW, PER = (NO + 255) / 256;
+  int off[PER];
+  float v[PER];
+#pragma unroll
+  for (int m = 0; m < PER; ++m) {
+    const int i = min(static_cast<int>(threadIdx.x) + 256 * m, NO - 1);
+    const int s = i / (TH * TW), xl = i % TW, yl = (i / TW) % TH;
+    off[m] = at(s, yl, xl);
+    v[m] = 0.0f;
+  }
+  for (uint32_t k = 0; k < a.ksplit; ++k) {
+    const float* pk = pb + static_cast<size_t>(k) * BLK;
+#pragma unroll
+    for (int m = 0; m < PER; ++m) v[m] += pk[off[m]];
+  }
+#pragma unroll
+  for (int m = 0; m < PER; ++m) {
+    const int i = static_cast<int>(threadIdx.x) + 256 * m;
+    if (i >= NO) continue;
     const int s = i / (TH * TW), xl = i % TW, yl = (i / TW) % TH;
     const uint32_t oy = ty * TH + yl, ox = tx * TW + xl;
     if (oy >= a.ho || ox >= a.wo) continue;
-    const uint32_t o = perm[grp * 8 + s];
+    const uint32_t o = perm[s];
     if (o >= a.c_out) continue;
-    const size_t at = (a.flags & PP_PIXSHUF2)
-                          ? (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + 2 * ox + (o & 1)
-                          : (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
-    const float v = sum_at(s, yl, xl);
-    y[at] = (a.flags & PP_ACCUMULATE) ? y[at] + v : v;
+    const size_t at_y = (a.flags & PP_PIXSHUF2)
+                            ? (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + 2 * ox + (o & 1)
+                            : (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
+    const float r = act(v[m], s);
+    y[at_y] = (a.flags & PP_ACCUMULATE) ? y[at_y] + r : r;
   }
 }
 
