@@ -213,9 +213,10 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
   if (!bf16 && lib == kLibCanon8 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.n == 1 && p.c_in > 8 && !no_lean) {
     // fp32, stride 1, one image: the lean tilings that timed fastest on the
     // VGG-16 layer shapes (MI355X), by output size: 4 x 4 outputs per lane on
-    // the 224 x 224 maps (4 channel-split waves) and 112 x 112 (8), 2 x 4 on
-    // 56 x 56, 2 x 2 with 16 waves on 28 x 28 and, with 4-byte staging and a
-    // channel split, on smaller maps (else one row of 2 outputs per lane).  Each 16-byte staging tiling has a
+    // the 224 x 224 maps (4 channel-split waves), 2 x 4 on 112 x 112 (8
+    // waves) and 56 x 56 (16 waves, two-channel rings), 2 x 2 with 16 waves
+    // on 28 x 28 and, with 4-byte staging and a channel split, on smaller
+    // maps (else one row of 2 outputs per lane).  Each 16-byte staging tiling has a
     // 4-byte staging twin of the same tiling (widths not a multiple of 4, a
     // fused x2 upsample): same accumulation order, so a conv fused with the
     // upsample before it gives bitwise what the unfused conv gives.
@@ -223,9 +224,9 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
     if (pix >= 160L * 160L) {
       lp[0] = 40; lp[1] = 56;
     } else if (pix >= 80L * 80L) {
-      lp[0] = 42; lp[1] = 57;
-    } else if (pix >= 40L * 40L) {
       lp[0] = 46; lp[1] = 55;
+    } else if (pix >= 40L * 40L) {
+      lp[0] = 58; lp[1] = 59;
     } else if (pix >= 20L * 20L) {
       lp[0] = 48; lp[1] = 51;
     } else {

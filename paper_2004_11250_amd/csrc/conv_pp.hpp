@@ -104,10 +104,12 @@ constexpr int kFirstWaveRecipe = 20;
   X(54, 1, 2, 8, 16, 0) \
   X(55, 2, 4, 8, 8, 0)  \
   X(56, 4, 4, 8, 4, 0)  \
-  X(57, 4, 4, 8, 8, 0)
+  X(57, 4, 4, 8, 8, 0)  \
+  X(58, 2, 4, 8, 16, 1) \
+  X(59, 2, 4, 8, 16, 0)
 
 constexpr int kFirstLeanRecipe = 40;
-constexpr int kEndLeanRecipe = 58;
+constexpr int kEndLeanRecipe = 60;
 
 // LDS row stride (floats) of the wave-pipeline kernel's staged tile: the
 // smallest multiple of 4 >= n, up to n + 12, for which lane rows rstep tile

@@ -89,9 +89,10 @@ struct LGeo {
   static constexpr int PATCH = NQ * EPD;
   static constexpr int SLOT = PATCH + 64;                // + 8 slots x 4 expanded weights (padded)
   // ring of NS channels (a channel's DMA is issued NS - 1 channels ahead);
-  // the smaller ring when four slots would leave a CU fewer than two
-  // workgroups of 8 waves
-  static constexpr int NS = (WS * 4 * SLOT * 4 <= 80 * 1024) ? 4 : 3;
+  // the smaller rings when four slots would leave a CU fewer than two
+  // workgroups of 8 waves, and two slots when three would not fit one
+  // workgroup's LDS
+  static constexpr int NS = (WS * 4 * SLOT * 4 <= 80 * 1024) ? 4 : (WS * 3 * SLOT * 4 <= 160 * 1024) ? 3 : 2;
   static constexpr int RING = NS * SLOT;
   static constexpr int NACC = 8 * R * CC;
   // partial-sum exchange: SPP slots per pass, as many as fit the LDS that
@@ -262,14 +263,17 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       asm volatile("" ::: "memory");
       __builtin_amdgcn_s_waitcnt(vmcnt_imm((DPF - 1) * QV));
       asm volatile("" ::: "memory");
-      // the patch and the 8 slots' expanded weights of channel c
+      // the patch and the expanded weights of slots 0-3 of channel c (those
+      // of slots 4-7 are read into the same registers once slots 0-3 are
+      // done: 16 fewer registers, which lets the 2 x 4 tilings hold four
+      // waves per SIMD)
       const float* cur = ring + (rd - ring_b) / 4u;
-      float w[8][4];
+      const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
+      float w[4][4];
       float p[PR][PC];
       {
-        const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
+        for (int s = 0; s < 4; ++s) {
           const float4 v = wc[s];
           w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
         }
@@ -299,10 +303,20 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       asm volatile("" : "+s"(kc));   // fresh slot tests
       {
         const uint32_t cx = code_c.x, cy = code_c.y;
-        static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
+        static_for<0, 4>([&](auto si) __attribute__((always_inline)) {
           constexpr int s = decltype(si)::value;
           if (!((kc >> s) & 1u)) return;
-          apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+          apply_canon8_bits<8 * s, 1, 1>(cx, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+        });
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const float4 v = wc[4 + s];
+          w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+        }
+        static_for<4, 8>([&](auto si) __attribute__((always_inline)) {
+          constexpr int s = decltype(si)::value;
+          if (!((kc >> s) & 1u)) return;
+          apply_canon8_bits<8 * (s - 4), 1, 1>(cy, acc[s], p, w[s - 4][0], w[s - 4][1], w[s - 4][2], w[s - 4][3]);
         });
       }
       kept_c = wo_c1 >> 24;

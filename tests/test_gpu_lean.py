@@ -17,10 +17,10 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 pp = pytest.importorskip("paper_2004_11250_amd")
 
-# tilings 40-50 stage the halo by 16-byte DMAs (image width a multiple of
-# 4), 51-57 by 4-byte DMAs (any width)
-LEAN = list(range(40, 58))
-V4 = set(range(40, 51))
+# tilings 40-50 and 58 stage the halo by 16-byte DMAs (image width a
+# multiple of 4), 51-57 and 59 by 4-byte DMAs (any width)
+LEAN = list(range(40, 60))
+V4 = set(range(40, 51)) | {58}
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -95,7 +95,7 @@ def test_lean_fused_maxpool(recipe, monkeypatch):
 
 
 @pytest.mark.parametrize("recipe,ksplit", [(40, 2), (45, 3), (47, 4), (48, 2), (49, 5), (42, 2), (51, 2), (52, 4),
-                                           (54, 3), (55, 2)])
+                                           (54, 3), (55, 2), (58, 2), (59, 3)])
 def test_lean_channel_split(recipe, ksplit, monkeypatch):
     monkeypatch.setenv("PP_RECIPE", str(recipe))
     monkeypatch.setenv("PP_KSPLIT", str(ksplit))
