@@ -204,10 +204,15 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
   mfma.recipe = kRecipeMfma;
   const bool mfma_ok = bf16 && allow_split && mfma_eligible(p);
   if (forced == kRecipeMfma && mfma_ok) return mfma;
+  ConvPlan cin;
+  cin.recipe = kRecipeCin;
+  const bool cin_ok = !no_lean && cin_eligible(p, bf16);
+  if (forced == kRecipeCin && cin_ok) return cin;
   if (forced >= 0 && (forced < kNumRecipes || is_lean_recipe(forced))) {
     const ConvPlan pl = try_plan(forced);
     if (pl.recipe >= 0) return pl;
   }
+  if (cin_ok && forced < 0) return cin;
   if (mfma_ok && forced < 0 && mfma_pays(p)) return mfma;
   const long pix = static_cast<long>(p.ho) * p.wo;
   if (!bf16 && lib == kLibCanon8 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.n == 1 && p.c_in > 8 && !no_lean) {
@@ -360,6 +365,7 @@ static hipError_t launch_wave(int id, const ConvParams& p, hipStream_t st) {
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p0, bool bf16_act, hipStream_t st) {
   ConvParams p = p0;
   if (plan.recipe == kRecipeMfma) return bf16_act ? launch_mfma_conv(p, st) : hipErrorInvalidConfiguration;
+  if (plan.recipe == kRecipeCin) return cin_eligible(p, bf16_act) ? launch_cin_conv(p, st) : hipErrorInvalidConfiguration;
   p.ksplit = plan.ksplit;
   if (plan.ksplit > 1 && !is_wave_recipe(plan.recipe) && !is_lean_recipe(plan.recipe))
     return hipErrorInvalidConfiguration;

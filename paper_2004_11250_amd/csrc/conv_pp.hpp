@@ -172,6 +172,14 @@ struct ConvPlan {
 // multiple of 32, no fused max pool, offsets within 32 bits), the scratch it
 // needs (the expanded weights and bias) and its launch (p.part = scratch).
 constexpr int kRecipeMfma = 64;
+
+// fp32 layers with at most four input channels (a network's first layer) as
+// dense 3 x 3 taps expanded in LDS (conv_pp_cin.hip): the plan's recipe id,
+// whether a layer can run so (stride 1, dilation 1, pad 1, no fused epilogue
+// other than ReLU, any pattern library) and its launch
+constexpr int kRecipeCin = 60;
+bool cin_eligible(const ConvParams& p, bool bf16_act);
+hipError_t launch_cin_conv(const ConvParams& p, hipStream_t st);
 bool mfma_eligible(const ConvParams& p);
 size_t mfma_bytes(const ConvParams& p);
 bool mfma_long_k(const ConvParams& p);   // k steps of 64 (else 32)
