@@ -180,6 +180,16 @@ constexpr int kRecipeMfma = 64;
 constexpr int kRecipeCin = 60;
 bool cin_eligible(const ConvParams& p, bool bf16_act);
 hipError_t launch_cin_conv(const ConvParams& p, hipStream_t st);
+
+// layers with at most 8 output channels (one slot group: a network's
+// image-producing last layer), fp32 or bf16, stride 1, dilation 1, pad 1,
+// width a multiple of 4, no fused epilogue other than ReLU, the expanded
+// weights within 60 KB of LDS (conv_pp_fewout.hip): dense taps over every
+// channel with no dispatch, so the planner takes it for bf16 layers of the
+// all-ones library
+constexpr int kRecipeFewOut = 61;
+bool fewout_eligible(const ConvParams& p);
+hipError_t launch_fewout_conv(const ConvParams& p, bool bf16_act, hipStream_t st);
 bool mfma_eligible(const ConvParams& p);
 size_t mfma_bytes(const ConvParams& p);
 bool mfma_long_k(const ConvParams& p);   // k steps of 64 (else 32)
