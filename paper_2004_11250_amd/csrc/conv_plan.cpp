@@ -40,7 +40,7 @@ static bool wave_recipe_fits(const RecipeInfo& r, int s, int d, int lib, bool bf
 bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
   const RecipeInfo r = recipe_info(id);
   if (r.r == 0) return false;
-  if (is_lean_recipe(id)) return lib == kLibCanon8 && !bf16 && s == 1 && d == 1 && lean_lds_bytes(id) > 0;
+  if (is_lean_recipe(id)) return lib == kLibCanon8 && s == 1 && d == 1 && lean_lds_bytes(id, bf16) > 0;
   if (is_wave_recipe(id)) return (lib == kLibCanon8 || lib == kLibDense9) && wave_recipe_fits(r, s, d, lib, bf16);
   const int lh = 64 / r.lw;
   const int th = lh * r.r, tw = r.lw * r.cc;
@@ -71,8 +71,10 @@ bool recipe_compiled(int lib, int id) {
 // and (register-pipelined tilings) fp32 with the canonical library
 static bool recipe_usable(int id, const ConvParams& p, int lib, bool bf16) {
   if (!recipe_compiled(lib, id) || !recipe_fits(id, p.stride, p.dil, bf16, lib)) return false;
-  if (is_lean_recipe(id))
-    return p.pad == 1 && (!lean_v4(id) || (p.w % 4 == 0 && !(p.flags & PP_UPSAMPLE2)));
+  if (is_lean_recipe(id)) {
+    if (bf16 && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_ACCUMULATE | PP_PIXSHUF2)))) return false;
+    return p.pad == 1 && (!lean_v4(id) || (p.w % (bf16 ? 8 : 4) == 0 && !(p.flags & PP_UPSAMPLE2)));
+  }
   if (recipe_info(id).pipe && (bf16 || lib != kLibCanon8)) return false;
   return !is_wave_recipe(id) || p.pad == p.dil;
 }
@@ -221,7 +223,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
   if (few_any && lib == kLibDense9 && bf16 && forced < 0) return few;
   if (mfma_ok && forced < 0 && mfma_pays(p)) return mfma;
   const long pix = static_cast<long>(p.ho) * p.wo;
-  if (!bf16 && lib == kLibCanon8 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.c_in > 8 && !no_lean) {
+  if (lib == kLibCanon8 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.c_in > 8 && !no_lean) {
     // fp32, stride 1: the lean tilings that timed fastest on the
     // VGG-16 layer shapes (MI355X), by output size: 4 x 4 outputs per lane on
     // the 224 x 224 maps (4 channel-split waves), 2 x 4 on 112 x 112 (8
@@ -234,7 +236,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
     // Batches (timed on the colourization layer shapes, 8 images): 2 x 4
     // outputs per lane with 8 waves up to 8 x 64 x 64 outputs (512 -> 512 at
     // 32 x 32: 162 us against 220 on the wave kernel), 4 x 4 beyond.
-    int lp[3] = {-1, -1, -1};
+    int lp[4] = {-1, -1, -1, -1};
     if (p.n > 1) {
       if (static_cast<long>(p.n) * pix >= 65536L) {
         lp[0] = 40; lp[1] = 56;
@@ -246,7 +248,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
     } else if (pix >= 80L * 80L) {
       lp[0] = 46; lp[1] = 55;
     } else if (pix >= 40L * 40L) {
-      lp[0] = 58; lp[1] = 59;
+      lp[0] = 58; lp[1] = 59; lp[2] = 46; lp[3] = 55;   // (the last two: bf16)
     } else if (pix >= 20L * 20L) {
       lp[0] = 48; lp[1] = 51;
     } else {
@@ -387,7 +389,7 @@ hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p0, bool
   if (plan.ksplit > 1 && !is_wave_recipe(plan.recipe) && !is_lean_recipe(plan.recipe))
     return hipErrorInvalidConfiguration;
   if (!recipe_usable(plan.recipe, p, lib, bf16_act)) return hipErrorInvalidConfiguration;
-  if (is_lean_recipe(plan.recipe)) return launch_lean_recipe(plan.recipe, p, st);
+  if (is_lean_recipe(plan.recipe)) return launch_lean_recipe(plan.recipe, p, bf16_act, st);
   if (is_wave_recipe(plan.recipe)) {
     if (lib == kLibDense9)
       return bf16_act ? launch_wave<kLibDense9, uint16_t>(plan.recipe, p, st) : launch_wave<kLibDense9, float>(plan.recipe, p, st);

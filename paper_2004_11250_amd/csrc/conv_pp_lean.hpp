@@ -23,6 +23,12 @@
 //     load;
 //   * the epilogue sums the WS partial blocks with one LDS exchange per pass
 //     of slots (two barriers) and stores 16-byte rows.
+//
+// bf16 activations (BF): the DMAs stage raw bf16 rows (half the bytes), a
+// lane reads its patch rows as aligned 4- and 8-byte pieces and widens them
+// to fp32 in registers; the weights (bf16 in the blob) are staged as pairs
+// and widened per kept slot; accumulation is fp32 and the store rounds once
+// to bf16 (round to nearest even).
 #pragma once
 
 #include "conv_pp_wave.hpp"
@@ -49,8 +55,8 @@ inline FastDiv make_fastdiv(uint32_t d) {
 
 struct LeanParams {
   const uint8_t* blob = nullptr;
-  const float* x = nullptr;
-  float* y = nullptr;
+  const void* x = nullptr;   // float or bf16 (uint16_t) activations
+  void* y = nullptr;
   float* part = nullptr;         // channel split over workgroups: partial-sum blocks
   uint32_t h = 0, w = 0, ho = 0, wo = 0;
   uint32_t c_in = 0, c_out = 0;
@@ -67,26 +73,32 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
 }
 
 // V4: the halo tile is staged by 16-byte DMAs (image width a multiple of
-// 4), else by 4-byte DMAs (any width)
-template <int R, int CC, int LW, int WS, bool V4>
+// 4 fp32 / 8 bf16 elements), else by 4-byte DMAs (any width for fp32, even
+// for bf16).  Sizes below are in elements unless named otherwise.
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false>
 struct LGeo {
+  static constexpr int ES = BF ? 2 : 4;                 // element bytes
   static constexpr int LH = 64 / LW;
   static constexpr int TH = LH * R, TW = LW * CC;       // output tile
   static constexpr int PR = R + 2, PC = CC + 2;         // patch of a lane
   static constexpr int TIH = TH + 2;                    // staged rows
-  // 16-byte staging: the staged columns start at the tile's first input
-  // column moved down to a multiple of 4 (3 columns in front for pad 1);
-  // 4-byte staging: at the tile's first input column
-  static constexpr int SH = V4 ? 3 : 0;
-  static constexpr int SWID = (TW + 2 + SH + 3) / 4 * 4;
-  // a lane's patch rows are read with aligned loads of up to VWL floats (the
-  // alignment its row start allows)
+  // the staged columns start SH columns before the tile's first input
+  // column: fp32 16-byte staging at a multiple of 4 (SH 3), fp32 4-byte
+  // staging at that column (SH 0); bf16 at a multiple of 8 (SH 7) or of 2
+  // (SH 3), so that a lane's first input element sits one after a dword
+  // boundary and its row reads are aligned pieces
+  static constexpr int SH = V4 ? (BF ? 7 : 3) : (BF ? 3 : 0);
+  static constexpr int SALIGN = BF ? 8 : 4;
+  static constexpr int SWID = (TW + 2 + SH + SALIGN - 1) / SALIGN * SALIGN;
+  // fp32: a lane's patch rows are read with aligned loads of up to VWL
+  // floats (the alignment its row start allows)
   static constexpr int VWL = CC % 4 == 0 ? 4 : (CC % 2 == 0 ? 2 : 1);
-  static constexpr int LSTR = wave_row_stride(SWID, R);
+  static constexpr int LSTR = BF ? SWID : wave_row_stride(SWID, R);
   static constexpr int AREA = TIH * LSTR;
-  static constexpr int EPD = V4 ? 256 : 64;              // floats per DMA instruction
+  static constexpr int DPB = V4 ? 1024 : 256;            // LDS bytes of one DMA instruction
+  static constexpr int EPD = DPB / ES;                   // elements per DMA instruction
   static constexpr int NQ = (AREA + EPD - 1) / EPD;      // DMAs per lane and channel
-  static constexpr int PATCH = NQ * EPD;
+  static constexpr int PATCH = NQ * DPB / 4;             // 4-byte words of a staged channel
   static constexpr int SLOT = PATCH + 64;                // + 8 slots x 4 expanded weights (padded)
   // ring of NS channels (a channel's DMA is issued NS - 1 channels ahead);
   // the smaller rings when four slots would leave a CU fewer than two
@@ -102,12 +114,49 @@ struct LGeo {
   static constexpr int SPP = WS == 1 ? 8 : (SPP0 >= 8 ? 8 : (SPP0 >= 4 ? 4 : (SPP0 >= 2 ? 2 : 1)));
   static constexpr int XCH = WS == 1 ? 0 : WS * SPP * XPS;
   static constexpr int LDS_FLOATS = WS * RING > XCH ? WS * RING : XCH;
-  static constexpr bool fits = LDS_FLOATS * 4 <= 160 * 1024 && WS >= 1 && WS <= 16 && LW * LH == 64 && TW % 4 == 0;
+  static constexpr bool fits = LDS_FLOATS * 4 <= 160 * 1024 && WS >= 1 && WS <= 16 && LW * LH == 64 && TW % 4 == 0 &&
+                               (!BF || (CC % 2 == 0 && (!V4 || TW % 8 == 0)));
 };
 
-template <int R, int CC, int LW, int WS, bool V4>
+// bf16 bits to fp32
+__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+__device__ __forceinline__ uint32_t bf_rne(float f) {   // fp32 to bf16 bits, round to nearest even (finite)
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// one bf16 patch row of a lane: elements [0, PC) of the lane's row, which
+// starts at element index st of the staged row (st odd: it sits one after a
+// dword boundary) at LDS byte address rb + 2 st.  Read as the dword holding
+// (st - 1, st), then 8-byte pieces while they fit (st + 1 is a multiple of 4
+// when CC is a multiple of 4), then dwords.
+template <int PC, bool Q8>
+__device__ __forceinline__ void read_row_bf(float (&d)[PC], const uint8_t* rb) {
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(__builtin_assume_aligned(rb, 4));
+  const uint32_t u0 = w[0];
+  d[0] = bf_hi(u0);
+  int j = 1;
+  if constexpr (Q8) {
+#pragma unroll
+    for (; j + 3 < PC; j += 4) {
+      const uint2 u = *reinterpret_cast<const uint2*>(__builtin_assume_aligned(rb + 2 * j + 2, 8));
+      d[j] = bf_lo(u.x); d[j + 1] = bf_hi(u.x); d[j + 2] = bf_lo(u.y); d[j + 3] = bf_hi(u.y);
+    }
+  }
+#pragma unroll
+  for (; j < PC; j += 2) {
+    const uint32_t u = w[(j + 1) / 2];
+    d[j] = bf_lo(u);
+    if (j + 1 < PC) d[j + 1] = bf_hi(u);
+  }
+}
+
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false>
 __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) {
-  using G = LGeo<R, CC, LW, WS, V4>;
+  using G = LGeo<R, CC, LW, WS, V4, BF>;
+  constexpr uint32_t ES = G::ES;
   constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT, NS = G::NS;
   static_assert(G::fits, "tiling does not fit");
   __shared__ __attribute__((aligned(16))) float lds[G::LDS_FLOATS];
@@ -141,36 +190,37 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   // with PP_UPSAMPLE2 (4-byte staging only) the conv's input is the nearest
   // x2 upsampling of x: a.h x a.w is the upsampled size and element (gy, gx)
   // is read from x[gy / 2][gx / 2]
-  const bool up = !V4 && (a.flags & PP_UPSAMPLE2) != 0;
+  const bool up = !V4 && !BF && (a.flags & PP_UPSAMPLE2) != 0;
   const uint32_t sh = up ? a.h >> 1 : a.h, sw = up ? a.w >> 1 : a.w;   // stored input size
-  const uint32_t chan_bytes = sh * sw * 4;
-  const float* xi = a.x + static_cast<size_t>(img) * a.c_in * sh * sw;
+  const uint32_t chan_bytes = sh * sw * ES;
+  const uint8_t* xi = static_cast<const uint8_t*>(a.x) + static_cast<size_t>(img) * a.c_in * sh * sw * ES;
 
   float* const ring = lds + wk * G::RING;
   const uint32_t ring_b = lds_addr(ring);
   constexpr uint32_t LW0 = 4u * G::PATCH;   // weights' byte offset in a ring slot
 
   // ---- per-lane staging offsets (bytes in one channel, + the DMA shift).
-  // 16-byte staging: load t of a lane stages elements 4 (64 t + lane) .. + 3
-  // of the tile, all in one tile row (LSTR is a multiple of 4) and all inside
-  // or all outside the image (the row starts at a multiple of 4, w is a
-  // multiple of 4); 4-byte staging: element 64 t + lane.  A DMA's LDS bytes
-  // start at 4 EPD t within the channel's slot.
+  // A load t of a lane stages the PE = 16 / ES (16-byte staging) or 4 / ES
+  // (4-byte staging) elements PE (64 t + lane) .. + PE - 1 of the tile, all in
+  // one tile row (LSTR is a multiple of PE) and all inside or all outside the
+  // image (the row starts at a multiple of PE, w is a multiple of PE).  A
+  // DMA's LDS bytes start at DPB t within the channel's slot.
+  constexpr uint32_t PE = (V4 ? 16u : 4u) / ES;
   uint32_t qoff[NQ];
 #pragma unroll
   for (int t = 0; t < NQ; ++t) {
-    const uint32_t e = V4 ? 4u * (64u * t + lane) : 64u * t + lane;
+    const uint32_t e = PE * (64u * t + lane);
     const uint32_t row = e / LSTR, col = e % LSTR;
     const uint32_t gy = static_cast<uint32_t>(iy0 + static_cast<int>(row));
     const uint32_t gx = static_cast<uint32_t>(ixa + static_cast<int>(col));
     const bool ok = e < static_cast<uint32_t>(G::AREA) && gy < a.h && gx < a.w;
     const uint32_t el = up ? (gy >> 1) * sw + (gx >> 1) : gy * a.w + gx;
-    qoff[t] = ok ? el * 4u + kDmaShift - ((4u * G::EPD * t) & 4095u) : 0x80000000u;
+    qoff[t] = ok ? el * ES + kDmaShift - ((static_cast<uint32_t>(G::DPB) * t) & 4095u) : 0x80000000u;
   }
 
   const uint8_t* blob = a.blob;
   const u32x4 brs = make_rsrc_below(blob, a.blob_bytes, kDmaShift);
-  u32x4 cr = make_rsrc_below(xi + static_cast<size_t>(c0) * sh * sw, chan_bytes, kDmaShift);
+  u32x4 cr = make_rsrc_below(xi + static_cast<size_t>(c0) * chan_bytes, chan_bytes, kDmaShift);
   // one channel's DMAs into ring slot sb (LDS byte address).  A channel past
   // the wave's range is staged all the same through descriptors of range 0
   // (every lane out of range: no memory is read, zeros land in a slot nobody
@@ -188,18 +238,22 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
     });
     cr = next_channel(cr, chan_bytes);
   };
-  // expanded weights of a channel: lane j < 32 loads tap j % 4 of slot j / 4
-  // (its compact index: woff + 4 * rank of the slot among the kept ones + tap)
-  const uint32_t wslot = static_cast<uint32_t>(lane) >> 2;
-  const uint32_t wlow = lane < 32 ? (1u << wslot) - 1u : 0u;
-  const uint32_t wbit = lane < 32 ? 1u << wslot : 0u;
-  const uint32_t wbase = a.off_w + 4u * (lane & 3) + kDmaShift - (LW0 & 4095u);
+  // expanded weights of a channel (its compact index: woff + 4 * rank of the
+  // slot among the kept ones + tap).  fp32: lane j < 32 loads tap j % 4 of
+  // slot j / 4; bf16: lane j < 16 loads the dword of taps 2 (j % 2), + 1 of
+  // slot j / 2 (4-tap kernels: no padding, dword-aligned)
+  constexpr uint32_t WPL = BF ? 2u : 1u;   // taps per lane
+  const uint32_t wslot = static_cast<uint32_t>(lane) / (4u / WPL);
+  const bool wlane = lane < static_cast<int>(32u / WPL);
+  const uint32_t wlow = wlane ? (1u << wslot) - 1u : 0u;
+  const uint32_t wbit = wlane ? 1u << wslot : 0u;
+  const uint32_t wbase = a.off_w + 4u * (lane & (4 / WPL - 1)) + kDmaShift - (LW0 & 4095u);
   auto dma_weights = [&](uint32_t wo, uint32_t sb, bool live) __attribute__((always_inline)) {
     u32x4 d = brs;
     d.z = live ? brs.z : 0u;
     const uint32_t kept = wo >> 24;
-    const uint32_t o = wbase + 4u * ((wo & 0xFFFFFFu) + 4u * __builtin_popcount(kept & wlow));
-    dma_b32_at<LW0, 4u * G::EPD * (NQ - 1), false>(d, (kept & wbit) ? o : 0x80000000u, sb);
+    const uint32_t o = wbase + ES * ((wo & 0xFFFFFFu) + 4u * __builtin_popcount(kept & wlow));
+    dma_b32_at<LW0, static_cast<uint32_t>(G::DPB) * (NQ - 1), false>(d, (kept & wbit) ? o : 0x80000000u, sb);
   };
 
   // metadata: woff word (weight offset | kept-slot mask << 24) and the 8
@@ -254,7 +308,9 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
     }
     uint32_t kept_c = wo_pre[0] >> 24;
     uint32_t wo_n = wo_pre[DPF];   // woff word of channel c + DPF
-    const uint32_t lane_b = 4u * ((ly * R) * LSTR + lx * CC);
+    // the lane's patch in a slot: fp32 from element lx CC of its first row;
+    // bf16 from the dword holding element lx CC + SH - 1 (read_row_bf)
+    const uint32_t lane_b = BF ? ES * ((ly * R) * LSTR + lx * CC + G::SH - 1) : 4u * ((ly * R) * LSTR + lx * CC);
 
 #pragma unroll 1
     for (int c = c0; c < c1; ++c) {
@@ -270,16 +326,29 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       const float* cur = ring + (rd - ring_b) / 4u;
       const float4* wc = reinterpret_cast<const float4*>(cur + G::PATCH);
       float w[4][4];
+      uint32_t wq[16];   // bf16: the 8 slots' taps as pairs
       float p[PR][PC];
       {
+        if constexpr (BF) {
+          const uint4* wu = reinterpret_cast<const uint4*>(cur + G::PATCH);
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const float4 v = wc[s];
-          w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+          for (int k = 0; k < 4; ++k) {
+            const uint4 v = wu[k];
+            wq[4 * k] = v.x; wq[4 * k + 1] = v.y; wq[4 * k + 2] = v.z; wq[4 * k + 3] = v.w;
+          }
+          const uint8_t* pb = reinterpret_cast<const uint8_t*>(cur) + lane_b;
+#pragma unroll
+          for (int r = 0; r < PR; ++r) read_row_bf<PC, CC % 4 == 0>(p[r], pb + r * LSTR * ES);
+        } else {
+#pragma unroll
+          for (int s = 0; s < 4; ++s) {
+            const float4 v = wc[s];
+            w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+          }
+#pragma unroll
+          for (int r = 0; r < PR; ++r)
+            read_row<G::SH, G::SH, PC, G::VWL, false>(p[r], cur + lane_b / 4u + r * LSTR);
         }
-#pragma unroll
-        for (int r = 0; r < PR; ++r)
-          read_row<G::SH, G::SH, PC, G::VWL, false>(p[r], cur + lane_b / 4u + r * LSTR);
       }
       // channel c's reads, and the scalar loads of the previous step
       wait_lgkm();
@@ -303,21 +372,31 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       asm volatile("" : "+s"(kc));   // fresh slot tests
       {
         const uint32_t cx = code_c.x, cy = code_c.y;
-        static_for<0, 4>([&](auto si) __attribute__((always_inline)) {
-          constexpr int s = decltype(si)::value;
-          if (!((kc >> s) & 1u)) return;
-          apply_canon8_bits<8 * s, 1, 1>(cx, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
-        });
+        if constexpr (BF) {
+          // a kept slot's 4 taps widened from its two dwords
+          static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
+            constexpr int s = decltype(si)::value;
+            if (!((kc >> s) & 1u)) return;
+            const uint32_t u0 = wq[2 * s], u1 = wq[2 * s + 1];
+            apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
+          });
+        } else {
+          static_for<0, 4>([&](auto si) __attribute__((always_inline)) {
+            constexpr int s = decltype(si)::value;
+            if (!((kc >> s) & 1u)) return;
+            apply_canon8_bits<8 * s, 1, 1>(cx, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+          });
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const float4 v = wc[4 + s];
-          w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+          for (int s = 0; s < 4; ++s) {
+            const float4 v = wc[4 + s];
+            w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+          }
+          static_for<4, 8>([&](auto si) __attribute__((always_inline)) {
+            constexpr int s = decltype(si)::value;
+            if (!((kc >> s) & 1u)) return;
+            apply_canon8_bits<8 * (s - 4), 1, 1>(cy, acc[s], p, w[s - 4][0], w[s - 4][1], w[s - 4][2], w[s - 4][3]);
+          });
         }
-        static_for<4, 8>([&](auto si) __attribute__((always_inline)) {
-          constexpr int s = decltype(si)::value;
-          if (!((kc >> s) & 1u)) return;
-          apply_canon8_bits<8 * (s - 4), 1, 1>(cy, acc[s], p, w[s - 4][0], w[s - 4][1], w[s - 4][2], w[s - 4][3]);
-        });
       }
       kept_c = wo_c1 >> 24;
       code_c = code_c1;
@@ -338,7 +417,9 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   const bool accum = (a.flags & PP_ACCUMULATE) != 0;
   const bool shuf = (a.flags & PP_PIXSHUF2) != 0;
   const uint32_t pho = a.ho / 2, pwo = a.wo / 2;
-  float* __restrict__ y = a.y + static_cast<size_t>(img) * a.c_out * (pool ? pho * pwo : a.ho * a.wo);
+  const size_t yoff = static_cast<size_t>(img) * a.c_out * (pool ? pho * pwo : a.ho * a.wo);
+  float* __restrict__ y = static_cast<float*>(a.y) + yoff;
+  uint16_t* __restrict__ yb = static_cast<uint16_t*>(a.y) + yoff;   // bf16 output
   const int oxl = ox0 + lx * CC;
   const bool vec = (CC % 4 == 0) && (a.wo % 4 == 0);
   // a row r of slot s: finish (bias, activation, store through perm) or,
@@ -361,6 +442,21 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
     for (int qq = 0; qq < CC; ++qq) {
       v[qq] += bias;
       if (relu) v[qq] = fmaxf(v[qq], 0.0f);
+    }
+    if constexpr (BF) {
+      // one rounding to bf16; CC (even) outputs as dword pairs when the row
+      // and the lane's first column are even
+      uint16_t* row = yb + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
+      if (a.wo % 2 == 0 && oxl + CC <= static_cast<int>(a.wo)) {
+#pragma unroll
+        for (int qq = 0; qq < CC; qq += 2)
+          *reinterpret_cast<uint32_t*>(row + oxl + qq) = bf_rne(v[qq]) | (bf_rne(v[qq + 1]) << 16);
+      } else {
+#pragma unroll
+        for (int qq = 0; qq < CC; ++qq)
+          if (oxl + qq < static_cast<int>(a.wo)) row[oxl + qq] = static_cast<uint16_t>(bf_rne(v[qq]));
+      }
+      return;
     }
     if (shuf) {
       float* row2 = y + (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + (o & 1);
@@ -404,6 +500,13 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
         t0 = fmaxf(t0, 0.0f); t1 = fmaxf(t1, 0.0f); t2 = fmaxf(t2, 0.0f); t3 = fmaxf(t3, 0.0f);
       }
       m[j] = fmaxf(fmaxf(t0, t1), fmaxf(t2, t3));
+    }
+    if constexpr (BF) {
+      uint16_t* rowb = yb + (static_cast<size_t>(o) * pho + oy / 2) * pwo;
+#pragma unroll
+      for (int j = 0; j < CC / 2; ++j)
+        if (oxl + 2 * j + 1 < static_cast<int>(a.wo)) rowb[oxl / 2 + j] = static_cast<uint16_t>(bf_rne(m[j]));
+      return;
     }
 #pragma unroll
     for (int j = 0; j < CC / 2; ++j)
@@ -484,7 +587,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
 // works out where each of its outputs (or pooled windows) sits in a partial
 // block, then issues the loads of one split for all of them at once, so the
 // pass costs about one memory round trip per split, not one per output.
-template <int R, int CC, int LW>
+template <int R, int CC, int LW, bool BF = false>
 __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
   constexpr int LH = 64 / LW, TH = LH * R, TW = LW * CC;
   constexpr int BLK = 8 * R * CC * 64;
@@ -515,7 +618,7 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
   };
   if (a.flags & PP_MAXPOOL2) {
     const uint32_t pho = a.ho / 2, pwo = a.wo / 2;
-    float* yp = a.y + static_cast<size_t>(img) * a.c_out * pho * pwo;
+    const size_t ypo = static_cast<size_t>(img) * a.c_out * pho * pwo;
     constexpr int PH = TH / 2, PW = TW / 2, NW = 8 * PH * PW, PER = (NW + 255) / 256;
     int off[PER][4];
     float v[PER][4];
@@ -546,11 +649,15 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
       const uint32_t o = perm[s];
       if (o >= a.c_out) continue;
       const float r = fmaxf(fmaxf(act(v[m][0], s), act(v[m][1], s)), fmaxf(act(v[m][2], s), act(v[m][3], s)));
-      yp[(static_cast<size_t>(o) * pho + oy / 2) * pwo + ox / 2] = r;
+      const size_t at_p = ypo + (static_cast<size_t>(o) * pho + oy / 2) * pwo + ox / 2;
+      if constexpr (BF)
+        static_cast<uint16_t*>(a.y)[at_p] = static_cast<uint16_t>(bf_rne(r));
+      else
+        static_cast<float*>(a.y)[at_p] = r;
     }
     return;
   }
-  float* y = a.y + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  const size_t yo = static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
   constexpr int NO = 8 * TH * TW, PER = (NO + 255) / 256;
   int off[PER];
   float v[PER];
@@ -579,18 +686,25 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
                             ? (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * oy + ((o >> 1) & 1)) * 2 * a.wo + 2 * ox + (o & 1)
                             : (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
     const float r = act(v[m], s);
-    y[at_y] = (a.flags & PP_ACCUMULATE) ? y[at_y] + r : r;
+    if constexpr (BF) {
+      static_cast<uint16_t*>(a.y)[yo + at_y] = static_cast<uint16_t>(bf_rne(r));   // (no accumulate / shuffle)
+    } else {
+      float* y = static_cast<float*>(a.y) + yo;
+      y[at_y] = (a.flags & PP_ACCUMULATE) ? y[at_y] + r : r;
+    }
   }
 }
 
 #ifndef __HIPCC_RTC__   // host side
-template <int R, int CC, int LW, int WS, bool V4>
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false>
 hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
-  using G = LGeo<R, CC, LW, WS, V4>;
+  using G = LGeo<R, CC, LW, WS, V4, BF>;
   if constexpr (!G::fits) {
     return hipErrorInvalidConfiguration;
   } else {
-    if (V4 && (p.w % 4 != 0 || (p.flags & PP_UPSAMPLE2))) return hipErrorInvalidConfiguration;
+    if (V4 && (p.w % (BF ? 8 : 4) != 0 || (p.flags & PP_UPSAMPLE2))) return hipErrorInvalidConfiguration;
+    if (BF && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_ACCUMULATE | PP_PIXSHUF2))))
+      return hipErrorInvalidConfiguration;
     const uint32_t tx = (p.wo + G::TW - 1) / G::TW, ty = (p.ho + G::TH - 1) / G::TH;
     const uint32_t ng = p.groups.d;
     if (p.ksplit < 1 || p.ksplit > p.c_in || (p.ksplit > 1 && !p.part)) return hipErrorInvalidValue;
@@ -600,12 +714,12 @@ hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
     p.splits = make_fastdiv(p.ksplit);
     const size_t nb = static_cast<size_t>(ng) * p.ksplit * tx * ty * n;
     if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4>), dim3(static_cast<uint32_t>(nb)), dim3(WS * 64), 0, st,
-                       p);
+    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4, BF>), dim3(static_cast<uint32_t>(nb)), dim3(WS * 64), 0,
+                       st, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.ksplit == 1) return e;
-    hipLaunchKernelGGL((pp_lean_reduce_kernel<R, CC, LW>), dim3(static_cast<uint32_t>(nb / p.ksplit)), dim3(256), 0, st,
-                       p);
+    hipLaunchKernelGGL((pp_lean_reduce_kernel<R, CC, LW, BF>), dim3(static_cast<uint32_t>(nb / p.ksplit)), dim3(256), 0,
+                       st, p);
     return hipGetLastError();
   }
 }

@@ -214,3 +214,83 @@ def test_lean_fused_upsample(mode, recipe, ksplit, monkeypatch):
             want = y
         torch.cuda.synchronize()
         assert torch.equal(yd.cpu(), want.cpu()), f"lean {recipe}: fused upsample ({mode}) differs"
+
+
+# ---- bf16 activations (the tilings built for bf16: 16-byte staging needs a
+# width that is a multiple of 8, 4-byte staging an even width).  Inputs and
+# weights are rounded to bf16 for the oracle too; the output is rounded once.
+LEAN_BF = [40, 56, 46, 55, 48, 51, 54]
+V4_BF = {40, 46, 48}
+
+
+def _run_bf16(L, x, relu=True, maxpool2=False):
+    from oracle import bf16 as obf16
+    xr = obf16.round_f32(x)
+    wr = obf16.round_f32(L["w"])
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+    xd = torch.from_numpy(np.ascontiguousarray(xr, np.float32)).cuda().to(torch.bfloat16)
+    y = pp.conv2d_fwd(layer, xd, relu=relu, maxpool2=maxpool2)
+    torch.cuda.synchronize()
+    args = (xr, wr, L["b"], L["pid"], L["conn"], L["lib"])
+    return layer, xd, y, args
+
+
+@pytest.mark.parametrize("recipe", LEAN_BF)
+def test_lean_bf16_tiling(recipe, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    shapes = [(19, 21, 37, 48), (16, 64, 32, 32), (24, 5, 20, 40), (8, 40, 70, 64)]
+    if recipe not in V4_BF:
+        shapes += [(19, 21, 37, 46), (16, 64, 14, 14), (24, 5, 21, 30), (8, 40, 33, 18)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 8000 + 10 * recipe + si
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+        used = pp.conv2d_recipe(blob, 2, h, w, pp.PP_BF16)
+        _say("lean bf16 tiling", recipe, "runs as", used, "seed", seed, (c_out, c_in, h, w))
+        assert used == recipe
+        for relu in (True, False):
+            _, _, y, args = _run_bf16(L, x, relu=relu)
+            ref = oconv.conv3x3_pruned(*args, 1, 1, 1, relu)
+            bound = oconv.conv3x3_bound(*args, 1, 1, 1)
+            check(y.float().cpu().numpy().astype(np.float64), ref, bound, "bf16",
+                  f"lean bf16 {recipe} {(c_out, c_in, h, w)} relu={relu}")
+
+
+@pytest.mark.parametrize("recipe,ksplit", [(r, 0) for r in LEAN_BF if r != 54] + [(48, 2), (51, 4), (54, 2), (46, 3)])
+def test_lean_bf16_pool_and_split(recipe, ksplit, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    shapes = [(19, 21, 36, 48), (16, 64, 32, 32)]
+    if recipe not in V4_BF:
+        shapes += [(16, 64, 14, 14), (8, 19, 29, 30)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 8500 + 10 * recipe + si + ksplit
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.4)
+        x = workloads.random_input(seed, (1, c_in, h, w))
+        blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+        plan = pp.conv2d_plan(blob, 1, h, w, pp.PP_BF16)
+        _say("lean bf16 pool/split", recipe, ksplit, "seed", seed, (c_out, c_in, h, w), "runs as", plan)
+        assert plan[0] == recipe and (not ksplit or plan[1] == ksplit)
+        for pool in ((False, True) if ksplit else (True,)):
+            layer, xd, y, args = _run_bf16(L, x, maxpool2=pool)
+            ref = oconv.conv3x3_pruned(*args, 1, 1, 1, True)
+            bound = oconv.conv3x3_bound(*args, 1, 1, 1)
+            if pool:
+                ref, bound = oconv.maxpool2(ref), oconv.maxpool2(bound)
+            check(y.float().cpu().numpy().astype(np.float64), ref, bound, "bf16",
+                  f"lean bf16 {recipe}/{ksplit} pool={pool}")
+            if pool:
+                yu = pp.conv2d_fwd(layer, xd, relu=True)
+                pooled = torch.nn.functional.max_pool2d(yu.float().cpu(), 2)
+                assert torch.equal(y.float().cpu(), pooled), f"lean bf16 {recipe}: fused pool differs"
+
+
+def test_lean_bf16_not_for_other_epilogues():
+    # the bf16 lean tilings take ReLU and the max pool only: a fused add,
+    # pixel shuffle or upsample runs on the wave-pipeline kernel
+    L = workloads.random_layer(8900, 16, 32, keep=0.5)
+    blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+    assert pp.conv2d_recipe(blob, 1, 56, 56, pp.PP_BF16) in LEAN_BF
+    assert pp.conv2d_recipe(blob, 1, 56, 55, pp.PP_BF16) not in range(40, 60)   # odd width
