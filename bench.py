@@ -451,8 +451,9 @@ def main():
     value = total_macs / (ms * 1e-3) / 1e9
 
     # ---- per-layer timing of the pruned-conv kernel (same launches as in the
-    # frame: a conv whose next op pp_net_fwd fuses runs with that op's flag;
-    # an accumulating conv adds into the same tensor every call)
+    # frame: a conv whose next op pp_net_fwd fuses runs with that op's flag,
+    # and with the prepared weights the net reads; an accumulating conv adds
+    # into the same tensor every call)
     layers = []
     li = 0
     esz = 2 if dtype == "bf16" else 4
@@ -472,8 +473,10 @@ def main():
             o = (o[0] // 4, 2 * o[1], 2 * o[2])
         if up:
             ishape = (ishape[0], ishape[1] // 2, ishape[2] // 2)   # read as stored, upsampled on load
+        # with the layer's prepared weights when the net has them (it passes
+        # them to pp_net_fwd), and split scratch behind them
         kw = dict(relu=op["relu"], maxpool2=f == "maxpool2", accumulate=f == "add", pixshuf2=f == "pshuf2",
-                  upsample2=up)
+                  upsample2=up, prepared=L.prepared is not None)
         xin = torch.rand((batch,) + ishape, device=dev).to(tdt)
         yo = torch.zeros((batch,) + o, device=dev, dtype=tdt)
         for _ in range(5):

@@ -58,9 +58,10 @@ typedef enum { PP_F32 = 0, PP_BF16 = 1 } pp_dtype;
  * pool of the activated output instead of the output itself; PP_ACCUMULATE
  * adds the activated output to what y holds (a residual connection);
  * PP_PIXSHUF2 stores the activated output through PixelShuffle(2).
- * PP_PREPARED (pp_conv2d_fwd only): the workspace already holds this
- * layer's matrix-core weights, written by pp_conv2d_prepare, and is not
- * rewritten (see there). */
+ * PP_PREPARED (pp_conv2d_fwd only): the workspace starts with this
+ * layer's prepared weights, written by pp_conv2d_prepare, which are read
+ * and not rewritten (see there); bytes past them, from the next 256-byte
+ * boundary, serve as the workspace a call without the flag would get. */
 enum { PP_RELU = 1u, PP_MAXPOOL2 = 2u, PP_ACCUMULATE = 4u, PP_PIXSHUF2 = 8u, PP_UPSAMPLE2 = 16u,
        PP_PREPARED = 32u };
 
@@ -261,23 +262,29 @@ pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes, const voi
                                 int32_t act_dtype, uint32_t flags, void* hip_stream);
 
 /*
- * pp_conv2d_prepare -- write, once, the weights a bf16 layer run in its
- * matrix-core form reads (the layer as the masked dense contraction of
- * Sec. 2's pruning structure: bf16 [c_out][9][c_in] in original filter
- * order, zeros for taps off a kernel's pattern and for pruned kernels, then
- * the fp32 bias), which pp_conv2d_fwd otherwise re-derives from the blob on
- * every call.  The weights never change, so a caller that keeps the buffer
- * passes it as the workspace of later calls with PP_PREPARED (or as
- * pp_net_op.d_w of the layer in pp_net_fwd), and the per-call expansion is
- * skipped.  A call whose plan is not the matrix-core form ignores the
- * buffer and runs without a workspace.
+ * pp_conv2d_prepare -- write, once, a layer's weights in the form its
+ * kernels read them, which pp_conv2d_fwd otherwise re-derives from the blob
+ * on every call.  bf16 layers: the weights of the matrix-core form (the
+ * layer as the masked dense contraction of Sec. 2's pruning structure: bf16
+ * [c_out][9][c_in] in original filter order, zeros for taps off a kernel's
+ * pattern and for pruned kernels, then the fp32 bias).  fp32 layers of the
+ * canonical library, stride 1, dilation 1, pad 1: each (slot group, input
+ * channel)'s 8 slots x 4 taps of the compact storage (Sec. 3) expanded,
+ * zeros for pruned slots, fp32 [ceil(c_out/8)][c_in][32], which the lean
+ * kernel reads by scalar loads instead of staging them through LDS.  The
+ * weights never change, so a caller that keeps the buffer passes it as the
+ * workspace of later calls with PP_PREPARED (or as pp_net_op.d_w of the
+ * layer in pp_net_fwd), and the per-call expansion is skipped.  A call whose
+ * plan does not read them ignores the buffer and runs without a workspace
+ * (pp_conv2d_fwd; pp_net_fwd keeps its own scratch for splits).
  *   h_blob, blob_bytes, d_blob  as pp_conv2d_fwd
  *   prepared     device buffer, 256-byte aligned, or NULL to query the size
  *   inout_bytes  in: capacity of prepared; out: bytes required
  *   hip_stream   stream the expansion is enqueued on (NULL: default)
  * Errors: PP_EBLOB, PP_EINVAL (NULL pointers, misaligned buffers),
- * PP_EUNSUPPORTED (c_in not a multiple of 32 or a layer too large for the
- * matrix-core form), PP_ESIZE (capacity too small; *inout_bytes then holds
+ * PP_EUNSUPPORTED (bf16: c_in not a multiple of 32 or a layer too large for
+ * the matrix-core form; fp32: another library, stride, dilation or pad),
+ * PP_ESIZE (capacity too small; *inout_bytes then holds
  * the required size), PP_EHIP.
  */
 pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, const void* d_blob, void* prepared,
@@ -364,7 +371,7 @@ typedef struct {
   const void* d_w;           /* dense ops: device weights in the act dtype;     */
                              /* PP_OP_CONV_PP: NULL, or the layer's prepared    */
                              /* weights (pp_conv2d_prepare), read when the net  */
-                             /* runs the layer in its matrix-core form          */
+                             /* runs the layer in the form they are for         */
   const float* d_b;          /* dense ops: device fp32 bias, or NULL            */
 } pp_net_op;
 

@@ -293,11 +293,12 @@ class PackedLayer:
         self.prepared = None   # matrix-core weights (prepare())
 
     def prepare(self, stream=None):
-        """pp_conv2d_prepare: write this layer's matrix-core weights once
-        into a device buffer kept on the layer (for bf16 calls that run the
-        matrix-core form; conv2d_fwd(..., prepared=True) then skips the
-        per-call expansion).  Returns the buffer, or None for a layer the
-        form cannot run (c_in not a multiple of 32)."""
+        """pp_conv2d_prepare: write this layer's prepared weights once into a
+        device buffer kept on the layer (bf16: the matrix-core form's; fp32
+        canonical-library stride-1 layers: the lean kernel's expanded
+        weights; conv2d_fwd(..., prepared=True) then skips the per-call
+        expansion).  Returns the buffer, or None for a layer none of those
+        forms runs."""
         torch = _torch()
         lib = load_library()
         nb = ctypes.c_size_t(0)
@@ -328,14 +329,14 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
     accumulate: add the activated output to ``out`` in place (PP_ACCUMULATE;
     out is required).  pixshuf2: store through PixelShuffle(2)
     (PP_PIXSHUF2).  upsample2: convolve the nearest x2 upsampling of x
-    (PP_UPSAMPLE2).  prepared: pass the layer's prepared matrix-core weights
-    (layer.prepare()) as the workspace with PP_PREPARED."""
+    (PP_UPSAMPLE2).  prepared: pass the layer's prepared weights
+    (layer.prepare()) at the head of the workspace with PP_PREPARED; when
+    the layer can also use split scratch, a copy of them is kept (per input
+    shape) at the head of a buffer whose tail is that scratch."""
     torch = _torch()
     lib = load_library()
-    if prepared:
-        if layer.prepared is None:
-            raise ValueError("the layer has no prepared weights (call layer.prepare() first)")
-        workspace = layer.prepared
+    if prepared and layer.prepared is None:
+        raise ValueError("the layer has no prepared weights (call layer.prepare() first)")
     if not x.is_contiguous():
         raise ValueError("x must be contiguous NCHW")
     n, c, h, w = x.shape
@@ -355,7 +356,18 @@ def conv2d_fwd(layer: PackedLayer, x, relu=False, out=None, stream=None, workspa
         out = torch.empty(shape, dtype=x.dtype, device=x.device)
     elif tuple(out.shape) != shape or out.dtype != x.dtype or not out.is_contiguous():
         raise ValueError(f"out must be a contiguous {x.dtype} tensor of shape {shape}")
-    if isinstance(workspace, str) and workspace == "auto":
+    if prepared:
+        nb = conv2d_workspace(layer.h_blob, n, hc, wc, _dtype_code(x))
+        workspace = layer.prepared
+        if nb:
+            key = ("prepared", n, hc, wc, _dtype_code(x), x.device.index)
+            head = -(-layer.prepared.numel() // 256) * 256
+            workspace = layer.scratch.get(key)
+            if workspace is None:
+                workspace = torch.empty(head + nb, dtype=torch.uint8, device=x.device)
+                workspace[:layer.prepared.numel()].copy_(layer.prepared)
+                layer.scratch[key] = workspace
+    elif isinstance(workspace, str) and workspace == "auto":
         nb = conv2d_workspace(layer.h_blob, n, hc, wc, _dtype_code(x))
         key = (n, hc, wc, _dtype_code(x), x.device.index)
         workspace = layer.scratch.get(key)
@@ -455,10 +467,11 @@ class Net:
              "up2": OP_UPSAMPLE2, "pshuf2": OP_PIXSHUF2, "add": OP_ADD}
 
     def __init__(self, ops, params, dtype="f32", device="cuda", prepare=True):
-        """prepare: (bf16) write each pruned layer's matrix-core weights once
-        (PackedLayer.prepare) and hand them to pp_net_fwd (pp_net_op.d_w),
-        which reads them for the layers it runs in that form instead of
-        expanding the blob on every call."""
+        """prepare: write each pruned layer's prepared weights once
+        (PackedLayer.prepare: bf16 matrix-core weights, fp32 lean-kernel
+        weights) and hand them to pp_net_fwd (pp_net_op.d_w), which reads
+        them for the layers it runs in the form they are for instead of
+        re-deriving them from the blob on every call."""
         torch = _torch()
         self.dtype = dtype
         self.wd = PP_BF16 if dtype == "bf16" else PP_F32
@@ -469,7 +482,7 @@ class Net:
             if blob is not None:
                 L = PackedLayer(blob, device)
                 self.pruned.append(L)
-                if prepare and self.wd == PP_BF16:
+                if prepare:
                     L.prepare()
                 return (L.d_blob, L)
             w = np.ascontiguousarray(prm["w"], dtype=np.float32)

@@ -74,9 +74,11 @@ int conv_recipe(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_
   return plan_with_scratch(p, library_kind(v), act_dtype == PP_BF16, scratch_bytes, false).recipe;
 }
 
+static size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
 pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
                        int32_t w, int32_t act_dtype, uint32_t flags, void* scratch, size_t scratch_bytes,
-                       hipStream_t st) {
+                       hipStream_t st, const void* wprep) {
   // with PP_UPSAMPLE2 the conv's input is x upsampled to 2h x 2w
   const bool up = (flags & PP_UPSAMPLE2) != 0;
   if (up && (h < 1 || w < 1 || h > (1 << 29) || w > (1 << 29))) return fail(PP_EINVAL, "bad h, w");
@@ -91,12 +93,16 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
     return fail(PP_EINVAL, "activation pointers misaligned");
   if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2 | PP_PREPARED))
     return fail(PP_EINVAL, "unknown flags");
-  // PP_PREPARED: the scratch holds the layer's matrix-core weights; it is
-  // used only by that form and never as split scratch
+  // PP_PREPARED: the scratch holds the layer's prepared weights (bf16: the
+  // matrix-core form's; fp32: the lean kernel's); it is used only by the
+  // plan they are for and never as split scratch
   const bool prepared = (flags & PP_PREPARED) != 0;
   flags &= ~static_cast<uint32_t>(PP_PREPARED);
   if (prepared && (!scratch || reinterpret_cast<uintptr_t>(scratch) % 256))
     return fail(PP_EINVAL, "PP_PREPARED needs the prepared weights (256-byte aligned) as the workspace");
+  if (prepared && scratch_bytes < prepared_bytes(v))
+    return fail(PP_ESIZE, "prepared weights smaller than pp_conv2d_prepare writes");
+  if (wprep && reinterpret_cast<uintptr_t>(wprep) % 256) return fail(PP_EINVAL, "prepared weights misaligned");
   {
     const uint32_t f = flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2);
     if (f & (f - 1)) return fail(PP_EINVAL, "more than one of PP_MAXPOOL2, PP_ACCUMULATE, PP_PIXSHUF2");
@@ -118,19 +124,28 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   const int lib = library_kind(v);
   const bool bf = act_dtype == PP_BF16;
   if (prepared) {
-    // the prepared weights serve the matrix-core form only; any other plan
-    // runs without a workspace
-    ConvParams q = p;
-    const ConvPlan mp = plan_with_scratch(q, lib, bf, scratch_bytes, false);
-    if (mp.recipe == kRecipeMfma) {
-      q.part = static_cast<float*>(scratch);
-      q.flags |= PP_PREPARED;   // the expansion is skipped
-      const hipError_t e = launch_conv(lib, mp, q, bf, st);
-      if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
-      return PP_OK;
+    // the workspace starts with the prepared weights; bytes past them
+    // (from the next 256-byte boundary) serve as split scratch
+    void* const pw = scratch;
+    const size_t head = align256(prepared_bytes(v));
+    void* const tail = scratch_bytes > head ? static_cast<uint8_t*>(scratch) + head : nullptr;
+    const size_t tail_bytes = tail ? scratch_bytes - head : 0;
+    if (act_dtype == PP_F32) {
+      wprep = pw;   // the lean kernel's weights
+    } else {
+      // bf16: the matrix-core form's weights; any other plan ignores them
+      ConvParams q = p;
+      const ConvPlan mp = plan_with_scratch(q, lib, bf, scratch_bytes, false);
+      if (mp.recipe == kRecipeMfma) {
+        q.part = static_cast<float*>(pw);
+        q.flags |= PP_PREPARED;   // the expansion is skipped
+        const hipError_t e = launch_conv(lib, mp, q, bf, st);
+        if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
+        return PP_OK;
+      }
     }
-    scratch = nullptr;
-    scratch_bytes = 0;
+    scratch = tail;
+    scratch_bytes = tail_bytes;
   }
   const size_t usable = reinterpret_cast<uintptr_t>(scratch) % 256 ? 0 : scratch_bytes;
   // the plan for library kind `kind`; a split only with enough scratch
@@ -152,6 +167,8 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   }
   ConvPlan plan = make_plan(lib, &p, false);
   if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the upsampling / max pool / accumulation / pixel shuffle for this layer");
+  // prepared fp32 weights: read by the lean tilings built for them, ignored by any other plan
+  if (wprep && act_dtype == PP_F32 && is_lean_recipe(plan.recipe) && lean_pw_tiling(plan.recipe)) p.wprep = wprep;
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;
@@ -290,7 +307,18 @@ extern "C" pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, 
 }
 
 namespace pp {
-size_t prepared_bytes(const BlobView& v) { return mfma_bytes(layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1)); }
+size_t prepared_bytes(const BlobView& v) {
+  const ConvParams p = layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1);
+  return v.wdtype == PP_BF16 ? mfma_bytes(p) : lean_prepared_bytes(p);
+}
+
+// a layer pp_conv2d_prepare serves: bf16 in the matrix-core form (c_in a
+// multiple of 32), fp32 on the lean kernel (canonical library, stride 1,
+// dilation 1, pad 1)
+static bool preparable(const BlobView& v, const ConvParams& p) {
+  if (v.wdtype == PP_BF16) return mfma_eligible(p);
+  return library_kind(v) == kLibCanon8 && v.stride == 1 && v.dil == 1 && v.pad == 1;
+}
 }  // namespace pp
 
 extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, const void* d_blob, void* prepared,
@@ -302,7 +330,10 @@ extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, co
   if (!inout_bytes) return fail(PP_EINVAL, "inout_bytes is NULL");
   // the expansion does not depend on the input size: one pixel stands in
   ConvParams p = layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1);
-  if (!mfma_eligible(p)) return fail(PP_EUNSUPPORTED, "the matrix-core form needs c_in a multiple of 32");
+  if (!preparable(v, p))
+    return fail(PP_EUNSUPPORTED, v.wdtype == PP_BF16 ? "the matrix-core form needs c_in a multiple of 32"
+                                                     : "fp32 prepared weights need the canonical library, stride 1, "
+                                                       "dilation 1 and pad 1");
   const size_t need = prepared_bytes(v);
   if (!prepared) {
     *inout_bytes = need;
@@ -315,7 +346,8 @@ extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, co
   if (!d_blob || reinterpret_cast<uintptr_t>(d_blob) % 256 || reinterpret_cast<uintptr_t>(prepared) % 256)
     return fail(PP_EINVAL, "d_blob and prepared must be 256-byte aligned device pointers");
   p.blob = static_cast<const uint8_t*>(d_blob);
-  const hipError_t e = launch_mfma_expand(p, prepared, static_cast<hipStream_t>(hip_stream));
+  const hipError_t e = v.wdtype == PP_BF16 ? launch_mfma_expand(p, prepared, static_cast<hipStream_t>(hip_stream))
+                                            : launch_lean_expand(p, prepared, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(PP_EHIP, std::string("expansion launch: ") + hipGetErrorString(e));
   return PP_OK;
 }

@@ -17,9 +17,11 @@ pp_status conv_check(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t
 // validate pointers and enqueue one pruned conv on `st`.  scratch (may be
 // NULL) of scratch_bytes lets the planner split the input channels over
 // workgroups (partial sums there, added by a second kernel)
+// wprep: an fp32 layer's prepared lean weights (or null), read when the plan
+// is a lean tiling built for them; the scratch then still serves a split
 pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, void* y, int32_t n, int32_t h,
                        int32_t w, int32_t act_dtype, uint32_t flags, void* scratch, size_t scratch_bytes,
-                       hipStream_t st);
+                       hipStream_t st, const void* wprep = nullptr);
 
 // whether pp_conv2d_fwd can fuse the ops before / after the conv (flags:
 // PP_UPSAMPLE2 and one of PP_MAXPOOL2, PP_ACCUMULATE, PP_PIXSHUF2) for this

@@ -30,6 +30,11 @@ struct ConvParams {
   // blocks per output tile in `part`, added by a second kernel
   int ksplit = 1;
   float* part = nullptr;
+  // the lean kernel's prepared weights (fp32 canonical library): every
+  // (slot group, channel)'s 8 slots x 4 taps expanded, zeros for pruned
+  // slots, [n_groups][c_in][32] floats; null: the kernel stages them from
+  // the blob itself
+  const void* wprep = nullptr;
 };
 
 // The compiled tilings ("recipes"):
@@ -226,6 +231,11 @@ hipError_t launch_lean_recipe(int id, const ConvParams& p, bool bf16_act, hipStr
 // for that dtype, or does not fit); whether it stages by 16-byte DMAs (image
 // width a multiple of 4 fp32 / 8 bf16 elements)
 long lean_lds_bytes(int id, bool bf16 = false);
+// the fp32 tilings also built to read prepared weights (ConvParams::wprep)
+bool lean_pw_tiling(int id);
+// bytes of a layer's prepared lean weights, and their expansion from the blob
+size_t lean_prepared_bytes(const ConvParams& p);
+hipError_t launch_lean_expand(const ConvParams& p, void* out, hipStream_t st);
 bool lean_v4(int id);
 
 #endif

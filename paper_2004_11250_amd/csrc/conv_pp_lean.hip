@@ -3,12 +3,19 @@
 
 namespace pp {
 
+// the fp32 tilings also built to read prepared weights (those the planner picks)
+constexpr bool lean_pw_id(int id) {
+  return id == 40 || id == 56 || id == 46 || id == 55 || id == 58 || id == 59 || id == 48 || id == 51 || id == 54;
+}
+
 // the tilings also built for bf16 activations (those the planner picks for
 // bf16 layers, and their 4-byte staging twins; the 16-wave 2 x 4 tilings
 // would spill at bf16's register count)
 constexpr bool lean_bf_tiling(int id) {
   return id == 40 || id == 56 || id == 46 || id == 55 || id == 48 || id == 51 || id == 54;
 }
+
+bool lean_pw_tiling(int id) { return lean_pw_id(id); }
 
 hipError_t launch_lean_recipe(int id, const ConvParams& c, bool bf16, hipStream_t st) {
   LeanParams p;
@@ -30,15 +37,22 @@ hipError_t launch_lean_recipe(int id, const ConvParams& c, bool bf16, hipStream_
   p.blob_bytes = c.blob_bytes;
   p.flags = c.flags;
   p.ksplit = c.ksplit;
+  p.wprep = static_cast<const uint8_t*>(c.wprep);
+  const bool pw = !bf16 && c.wprep != nullptr;
   p.groups = make_fastdiv(c.n_groups);
   switch (id) {
-#define PP_L(ID, R, CC, LW, WS, V4)                                                   \
-  case ID:                                                                            \
-    if constexpr (lean_bf_tiling(ID)) {                                               \
+#define PP_L(ID, R, CC, LW, WS, V4)                                                          \
+  case ID:                                                                                   \
+    if constexpr (lean_bf_tiling(ID)) {                                                      \
       if (bf16) return kern::launch_lean_tiling<R, CC, LW, WS, (V4 != 0), true>(p, c.n, st); \
-    } else {                                                                          \
-      if (bf16) return hipErrorInvalidConfiguration;                                  \
-    }                                                                                 \
+    } else {                                                                                 \
+      if (bf16) return hipErrorInvalidConfiguration;                                         \
+    }                                                                                        \
+    if constexpr (lean_pw_id(ID)) {                                                          \
+      if (pw) return kern::launch_lean_tiling<R, CC, LW, WS, (V4 != 0), false, true>(p, c.n, st); \
+    } else {                                                                                 \
+      if (pw) return hipErrorInvalidConfiguration;                                           \
+    }                                                                                        \
     return kern::launch_lean_tiling<R, CC, LW, WS, (V4 != 0)>(p, c.n, st);
     PP_LRECIPES(PP_L)
 #undef PP_L
@@ -73,6 +87,36 @@ long lean_lds_bytes(int id, bool bf16) {
     default:
       return 0;
   }
+}
+
+// the prepared weights of a layer: entry (group, channel) holds its 8 slots'
+// 4 taps (pattern tap order, as stored), zeros for pruned slots; one thread
+// per float.  Every offset read from the blob is clamped to the weights it
+// holds.
+__global__ __launch_bounds__(256) void pp_lean_expand_kernel(const uint8_t* blob, uint32_t off_woff, uint32_t off_w,
+                                                             uint32_t n_wt, uint32_t n_entries, float* out) {
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= n_entries * 32u) return;
+  const uint32_t e = i >> 5, j = i & 31u, s = j >> 2, t = j & 3u;
+  const uint32_t wo = reinterpret_cast<const uint32_t*>(blob + off_woff)[e];
+  const uint32_t kept = wo >> 24;
+  float v = 0.0f;
+  if ((kept >> s) & 1u) {
+    const uint32_t k = (wo & 0xFFFFFFu) + 4u * __builtin_popcount(kept & ((1u << s) - 1u)) + t;
+    v = reinterpret_cast<const float*>(blob + off_w)[min(k, n_wt ? n_wt - 1 : 0u)];
+  }
+  out[i] = v;
+}
+
+size_t lean_prepared_bytes(const ConvParams& p) { return static_cast<size_t>(p.n_groups) * p.c_in * 32u * sizeof(float); }
+
+hipError_t launch_lean_expand(const ConvParams& p, void* out, hipStream_t st) {
+  const size_t n = static_cast<size_t>(p.n_groups) * p.c_in;
+  if (n == 0 || n * 32 > 0xFFFFFFFFull) return hipErrorInvalidValue;
+  const uint32_t blocks = static_cast<uint32_t>((n * 32 + 255) / 256);
+  hipLaunchKernelGGL(pp_lean_expand_kernel, dim3(blocks), dim3(256), 0, st, p.blob, p.off_woff, p.off_w, p.n_wt,
+                     static_cast<uint32_t>(n), static_cast<float*>(out));
+  return hipGetLastError();
 }
 
 }  // namespace pp

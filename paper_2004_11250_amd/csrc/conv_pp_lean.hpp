@@ -63,6 +63,7 @@ struct LeanParams {
   uint32_t off_codes = 0, off_woff = 0, off_w = 0, off_bias = 0, off_perm = 0, blob_bytes = 0;
   uint32_t flags = 0;
   uint32_t ksplit = 1;
+  const uint8_t* wprep = nullptr;   // prepared weights (PW): [groups][c_in][32] fp32
   FastDiv groups, tiles_x, tiles_y, splits;   // block decode
 };
 
@@ -153,8 +154,13 @@ __device__ __forceinline__ void read_row_bf(float (&d)[PC], const uint8_t* rb) {
   }
 }
 
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false>
+// PW (fp32 only): the weights come from a prepared expanded copy by scalar
+// loads into SGPRs (one channel's 32 at the end of the step before it), each
+// kept slot's 4 copied to VGPRs for its FMAs: no weight DMA and no LDS reads of
+// weights, which relieves the LDS path the patch DMAs and reads share
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false>
 __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) {
+  static_assert(!(BF && PW), "prepared weights are fp32");
   using G = LGeo<R, CC, LW, WS, V4, BF>;
   constexpr uint32_t ES = G::ES;
   constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT, NS = G::NS;
@@ -282,7 +288,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
 #pragma unroll
       for (int qq = 0; qq < CC; ++qq) acc[s][r][qq] = 0.0f;
   if (c0 < c1) {
-    constexpr int QV = NQ + 1;   // DMAs per lane and channel
+    constexpr int QV = NQ + (PW ? 0 : 1);   // DMAs per lane and channel
     constexpr int DPF = NS - 1;  // channels DMA'd ahead
     constexpr uint32_t SLOTB = 4u * SLOT;
     // ring slots (LDS byte addresses): rd holds channel c, and channel c +
@@ -298,13 +304,20 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
 #pragma unroll
     for (int i = 0; i <= DPF; ++i) wo_pre[i] = kern::sload<uint32_t>(blob, wo_at + 4u * i);
     uint2 code_c = kern::sload<uint2>(blob, cd_at);
+    // PW: the prepared weights of (group, channel) e at byte 128 e
+    const uint32_t wp_at0 = 128u * (grp * a.c_in);
+    float4 wsc[8];
+    if constexpr (PW) {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) wsc[s] = kern::sload<float4>(a.wprep, wp_at0 + 128u * c0 + 16u * s);
+    }
     wait_lgkm();
-    dma_weights(wo_pre[0], ring_b, true);
+    if constexpr (!PW) dma_weights(wo_pre[0], ring_b, true);
 #pragma unroll
     for (int i = 1; i < DPF; ++i) {
       const bool live = c0 + i < c1;
       dma_patch(ring_b + i * SLOTB, live);
-      dma_weights(wo_pre[i], ring_b + i * SLOTB, live);
+      if constexpr (!PW) dma_weights(wo_pre[i], ring_b + i * SLOTB, live);
     }
     uint32_t kept_c = wo_pre[0] >> 24;
     uint32_t wo_n = wo_pre[DPF];   // woff word of channel c + DPF
@@ -340,10 +353,12 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
 #pragma unroll
           for (int r = 0; r < PR; ++r) read_row_bf<PC, CC % 4 == 0>(p[r], pb + r * LSTR * ES);
         } else {
+          if constexpr (!PW) {
 #pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            const float4 v = wc[s];
-            w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+            for (int s = 0; s < 4; ++s) {
+              const float4 v = wc[s];
+              w[s][0] = v.x; w[s][1] = v.y; w[s][2] = v.z; w[s][3] = v.w;
+            }
           }
 #pragma unroll
           for (int r = 0; r < PR; ++r)
@@ -357,7 +372,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       {
         const bool live = c + DPF < c1;
         dma_patch(wr, live);
-        dma_weights(wo_n, wr, live);
+        if constexpr (!PW) dma_weights(wo_n, wr, live);
       }
       // metadata for the next step: waited for there, while this channel's
       // FMAs run
@@ -366,6 +381,15 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       const uint32_t wo_nn = kern::sload<uint32_t>(blob, wo_at + 4u * DPF);
       const uint32_t wo_c1 = kern::sload<uint32_t>(blob, wo_at);
       const uint2 code_c1 = kern::sload<uint2>(blob, cd_at);
+      uint32_t warm0 = 0, warm1 = 0;
+      if constexpr (PW) {
+        // the weights of two channels ahead brought into the scalar cache
+        // (one dword of each of their two 64-byte lines), so that the loads
+        // of the next channel at the end of this step hit it
+        const uint32_t cw = c + 2 < c1 ? c + 2 : c1 - 1;
+        warm0 = kern::sload<uint32_t>(a.wprep, wp_at0 + 128u * cw);
+        warm1 = kern::sload<uint32_t>(a.wprep, wp_at0 + 128u * cw + 64u);
+      }
       __builtin_amdgcn_sched_barrier(0);
       const uint32_t kept = kept_c;
       uint32_t kc = kept;
@@ -379,6 +403,18 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
             if (!((kc >> s) & 1u)) return;
             const uint32_t u0 = wq[2 * s], u1 = wq[2 * s + 1];
             apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
+          });
+        } else if constexpr (PW) {
+          (void)w;
+          static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
+            constexpr int s = decltype(si)::value;
+            if (!((kc >> s) & 1u)) return;
+            // the slot's 4 weights into VGPRs (an SGPR operand would halve the FMA rate)
+            float w0, w1, w2, w3;
+            asm volatile("v_mov_b32 %0, %4\n v_mov_b32 %1, %5\n v_mov_b32 %2, %6\n v_mov_b32 %3, %7"
+                         : "=v"(w0), "=v"(w1), "=v"(w2), "=v"(w3)
+                         : "s"(wsc[s].x), "s"(wsc[s].y), "s"(wsc[s].z), "s"(wsc[s].w));
+            apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, w0, w1, w2, w3);
           });
         } else {
           static_for<0, 4>([&](auto si) __attribute__((always_inline)) {
@@ -401,9 +437,18 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       kept_c = wo_c1 >> 24;
       code_c = code_c1;
       wo_n = wo_nn;
+      if constexpr (PW) {
+        asm volatile("" ::"s"(warm0), "s"(warm1));
+        // the next channel's weights (the last channel reloads its own:
+        // nothing past the wave's range is read), waited for with the next
+        // step's LDS reads
+        const uint32_t cn = c + 1 < c1 ? c + 1 : c;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) wsc[s] = kern::sload<float4>(a.wprep, wp_at0 + 128u * cn + 16u * s);
+      }
       wr = rd;
       rd = rd + SLOTB == ring_end ? ring_b : rd + SLOTB;
-    }
+        }
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // no DMA may land in the exchange area below
   }
 
@@ -696,7 +741,7 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
 }
 
 #ifndef __HIPCC_RTC__   // host side
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false>
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false>
 hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
   using G = LGeo<R, CC, LW, WS, V4, BF>;
   if constexpr (!G::fits) {
@@ -714,8 +759,9 @@ hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
     p.splits = make_fastdiv(p.ksplit);
     const size_t nb = static_cast<size_t>(ng) * p.ksplit * tx * ty * n;
     if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4, BF>), dim3(static_cast<uint32_t>(nb)), dim3(WS * 64), 0,
-                       st, p);
+    if (PW && !p.wprep) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4, BF, PW>), dim3(static_cast<uint32_t>(nb)),
+                       dim3(WS * 64), 0, st, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.ksplit == 1) return e;
     hipLaunchKernelGGL((pp_lean_reduce_kernel<R, CC, LW, BF>), dim3(static_cast<uint32_t>(nb / p.ksplit)), dim3(256), 0,

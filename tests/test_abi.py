@@ -244,6 +244,16 @@ def test_prepare_host_checks(lib):
     blob2 = pp.pack(L2["w"], L2["b"], L2["pid"], L2["conn"], L2["lib"], 1, 1, 1, pp.PP_BF16)
     assert lib.pp_conv2d_prepare(blob2.ctypes.data, blob2.nbytes, None, None, ctypes.byref(nb),
                                  None) == pp.PP_EUNSUPPORTED
+    # fp32: the lean kernel's expanded weights, [ceil(c_out / 8)][c_in][32]
+    # floats, for the canonical library at stride 1 only
+    b32 = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+    assert lib.pp_conv2d_prepare(b32.ctypes.data, b32.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_OK
+    assert nb.value == 5 * 64 * 32 * 4
+    s2 = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 2, 1, 1, pp.PP_F32)
+    assert lib.pp_conv2d_prepare(s2.ctypes.data, s2.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_EUNSUPPORTED
+    d9 = pp.pack(L["w"], L["b"], np.zeros_like(L["pid"]), L["conn"], np.array(workloads.DENSE9, np.uint16),
+                 1, 1, 1, pp.PP_F32)
+    assert lib.pp_conv2d_prepare(d9.ctypes.data, d9.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_EUNSUPPORTED
     # the allocation-free call has no prepared buffer to read
     assert lib.pp_conv2d_fwd_noalloc(blob.ctypes.data, blob.nbytes, 0x100000, 0x200000, 0x300000, 1, 8, 8,
                                      pp.PP_BF16, pp.PP_PREPARED, None) == pp.PP_EINVAL

@@ -294,3 +294,40 @@ def test_lean_bf16_not_for_other_epilogues():
     blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
     assert pp.conv2d_recipe(blob, 1, 56, 56, pp.PP_BF16) in LEAN_BF
     assert pp.conv2d_recipe(blob, 1, 56, 55, pp.PP_BF16) not in range(40, 60)   # odd width
+
+
+# fp32 prepared weights (pp_conv2d_prepare; PP_PREPARED): the tilings built
+# for them read the expanded weights by scalar loads and give bitwise what
+# the same tiling gives staging them from the blob, with and without a
+# channel split (whose scratch follows the prepared weights)
+PW = [40, 56, 46, 55, 58, 59, 48, 51, 54]
+
+
+@pytest.mark.parametrize("recipe", PW)
+def test_lean_prepared_weights_bitwise(recipe, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    shapes = [(19, 21, 37, 44), (16, 64, 32, 32), (8, 40, 20, 40)]
+    if recipe not in V4:
+        shapes += [(19, 21, 37, 45), (16, 64, 14, 14)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 9000 + 10 * recipe + si
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.4)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
+        _say("lean prepared", recipe, "seed", seed, (c_out, c_in, h, w))
+        assert layer.prepare() is not None
+        xd = torch.from_numpy(x).cuda()
+        for relu, pool in ((True, False), (False, False), (True, True)):
+            if pool and (recipe == 54 or h % 2 or w % 2):
+                continue
+            # the same plan both ways (a split gets its scratch behind the
+            # prepared weights)
+            ya = pp.conv2d_fwd(layer, xd, relu=relu, maxpool2=pool)
+            yb = pp.conv2d_fwd(layer, xd, relu=relu, maxpool2=pool, prepared=True)
+            torch.cuda.synchronize()
+            assert torch.equal(ya, yb), f"prepared {recipe} relu={relu} pool={pool}"
+        args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        check(yb.cpu().numpy().astype(np.float64) if not pool else
+              pp.conv2d_fwd(layer, xd, relu=True, prepared=True).cpu().numpy().astype(np.float64),
+              oconv.conv3x3_pruned(*args, 1, 1, 1, True), oconv.conv3x3_bound(*args, 1, 1, 1), "f32",
+              f"lean prepared {recipe}")

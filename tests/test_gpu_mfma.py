@@ -230,7 +230,8 @@ def test_prepared_weights_equal_per_call_expansion(case, monkeypatch):
 
 def test_prepared_weights_ignored_off_the_matrix_cores():
     # a layer the planner keeps on the vector ALUs: with PP_PREPARED the call
-    # runs without a workspace (the prepared buffer is left untouched)
+    # ignores the prepared weights (left untouched) and runs the plan a call
+    # without the flag runs (its split scratch behind them)
     spec = workloads.net_spec(2)
     i = next(j for j, op in enumerate(spec["ops"]) if op["op"] == "conv3" and op["c_in"] == 512)
     op = spec["ops"][i]
@@ -241,7 +242,7 @@ def test_prepared_weights_ignored_off_the_matrix_cores():
     assert pp.conv2d_recipe(layer.h_blob, 1, 14, 14, pp.PP_BF16) != MFMA
     buf = layer.prepare()
     before = buf.clone()
-    want = _host(pp.conv2d_fwd(layer, x, relu=True, workspace=None))
+    want = _host(pp.conv2d_fwd(layer, x, relu=True))
     got = _host(pp.conv2d_fwd(layer, x, relu=True, prepared=True))
     assert np.array_equal(got, want)
     assert torch.equal(buf, before)

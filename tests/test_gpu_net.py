@@ -236,6 +236,22 @@ def test_vgg16_end_to_end_vs_oracle_chain():
     assert rel < 1e-4
 
 
+@pytest.mark.parametrize("cfg", [1, 2, 3, 5])
+def test_prepared_fp32_net_is_bitwise_the_same(cfg):
+    # fp32 networks: the lean kernel's prepared weights (pp_net_op.d_w, read
+    # by scalar loads) give bitwise the frame that stages them from the blob
+    spec = workloads.net_spec(cfg)
+    params = workloads.net_params(cfg)
+    _, x = _input(cfg, "f32")
+    _say(f"cfg {cfg} f32: prepared vs blob-staged weights")
+    a = pp.Net(spec["ops"], params, "f32", prepare=False)
+    b = pp.Net(spec["ops"], params, "f32", prepare=True)
+    assert sum(L.prepared is not None for L in b.pruned) > 0
+    ya = _np(a.forward(x))
+    for _ in range(2):
+        assert np.array_equal(_np(b.forward(x)), ya)
+
+
 @pytest.mark.parametrize("cfg", [4, 5])
 def test_prepared_net_equals_per_call_expansion(cfg):
     # bf16 networks: prepared matrix-core weights (pp_net_op.d_w) give
