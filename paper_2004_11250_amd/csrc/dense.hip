@@ -6,8 +6,9 @@
 //
 // The dense convs and the transposed conv are dense contractions and run on
 // the matrix cores (implicit GEMM, below), except dense convs with few
-// filters or a short reduction (vector kernel); the glue ops are one
-// elementwise kernel.
+// filters or a short reduction (vector kernels: a tiled one for 9 x 9 with
+// pad 4 and a width that is a multiple of 4, a per-row one otherwise); the
+// glue ops are one elementwise kernel.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -672,6 +673,201 @@ __global__ __launch_bounds__(256) void glue_kernel(GlueParams p) {
   }
 }
 
+// Dense 9 x 9 convolution, stride 1, pad 4 (same size), width a multiple of
+// 4, on the vector ALUs: the style network's 9 x 9 layers (3 -> 32, 32 -> 3),
+// whose few filters or short reduction leave GEMM tiles mostly padding.
+// A wave computes F filters x one output row x 64 CC columns (CC adjacent
+// columns per lane); S waves of a workgroup share that tile and take
+// consecutive channel ranges, summed through LDS at the end, so a layer with
+// few output tiles still fills the chip.  The workgroup's weights are staged
+// once in LDS as fp32, [c][ky][f][12] (9 taps padded to 12 floats): a
+// wave-uniform address, so each tap row is three broadcast 16-byte reads.
+// Per (channel, ky) step a lane reads its CC + 8 input columns as aligned
+// 4-element pieces through a raw-buffer descriptor of that input row: a row
+// outside the image gets a zero-length descriptor and a piece outside the
+// row an out-of-range offset, both read as zero (the padding) with no
+// branch; the next step's pieces load while this step's FMAs run.
+template <int F, int CC, int NW, int S, class TA>
+__global__ __launch_bounds__(64 * NW) void dense9_tile_kernel(DenseParams p, int col_tiles, int n_tiles) {
+  static_assert(NW % S == 0 && CC % 4 == 0, "tile shape");
+  constexpr int T = NW / S;            // output tiles per workgroup
+  constexpr int NP = (CC + 8) / 4;     // 4-element pieces per input row segment
+  constexpr int WR = 12;               // LDS floats per (channel, ky, filter)
+  constexpr uint32_t ES = sizeof(TA);
+  constexpr uint32_t kOut = 0x80000000u;
+  extern __shared__ float lds[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+  const int sp = wave % S, tl = wave / S;
+  const int f0 = static_cast<int>(blockIdx.y) * F;
+
+  // ---- weights of filters [f0, f0 + F), every channel, fp32: the group's
+  // weights are one contiguous block of the OIHW tensor, read in batches of
+  // 8 independent coalesced loads per thread (the 3 pad floats of a tap row
+  // are never read; a filter past c_out is zero)
+  {
+    const int fl = min(F, p.c_out - f0);
+    const int n_g = fl * p.c_in * 81;
+    const TA* wg = static_cast<const TA*>(p.wt) + static_cast<size_t>(f0) * p.c_in * 81;
+    for (int i0 = threadIdx.x; i0 < n_g; i0 += 8 * 64 * NW) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = i0 + u * 64 * NW;
+        v[u] = e < n_g ? ld(wg, e) : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = i0 + u * 64 * NW;
+        if (e < n_g) {
+          const int kx = e % 9, t9 = e / 9, ky = t9 % 9, t81 = t9 / 9, c = t81 % p.c_in, f = t81 / p.c_in;
+          lds[((c * 9 + ky) * F + f) * WR + kx] = v[u];
+        }
+      }
+    }
+    for (int i = threadIdx.x; i < (F - fl) * p.c_in * 81; i += 64 * NW) {
+      const int kx = i % 9, t9 = i / 9, ky = t9 % 9, t81 = t9 / 9, c = t81 % p.c_in, f = fl + t81 / p.c_in;
+      lds[((c * 9 + ky) * F + f) * WR + kx] = 0.0f;
+    }
+  }
+  __syncthreads();
+
+  // ---- this wave's tile and channel range
+  const int t = static_cast<int>(blockIdx.x) * T + tl;
+  const bool live = t < n_tiles;
+  const int ct = live ? t % col_tiles : 0;
+  const int r = live ? t / col_tiles : 0;
+  const int oy = r % p.ho, img = r / p.ho;
+  const int cps = (p.c_in + S - 1) / S;
+  const int c0 = min(sp * cps, p.c_in), c1 = min(c0 + cps, p.c_in);
+  const int n_steps = live ? 9 * (c1 - c0) : 0;
+  const int ox0 = ct * 64 * CC + lane * CC;
+  uint32_t off[NP];
+#pragma unroll
+  for (int j = 0; j < NP; ++j) {
+    const int ix = ox0 - 4 + 4 * j;
+    off[j] = ix >= 0 && ix < p.w ? static_cast<uint32_t>(ix) * ES : kOut;
+  }
+  const TA* xi = static_cast<const TA*>(p.x) + static_cast<size_t>(img) * p.c_in * p.h * p.w;
+  const int row_bytes = static_cast<int>(p.w * ES);
+
+  auto load = [&](int c, int ky, float (&xs)[CC + 8]) __attribute__((always_inline)) {
+    const int iy = oy + ky - 4;
+    const bool rv = iy >= 0 && iy < p.h;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<TA*>(xi + (static_cast<size_t>(c) * p.h + (rv ? iy : 0)) * p.w), static_cast<short>(0),
+        rv ? row_bytes : 0, 0x00020000);
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      if constexpr (ES == 2) {
+        const uint2 u = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(xr, off[j], 0, 0));
+        xs[4 * j + 0] = __uint_as_float(u.x << 16);
+        xs[4 * j + 1] = __uint_as_float(u.x & 0xFFFF0000u);
+        xs[4 * j + 2] = __uint_as_float(u.y << 16);
+        xs[4 * j + 3] = __uint_as_float(u.y & 0xFFFF0000u);
+      } else {
+        const float4 u = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(xr, off[j], 0, 0));
+        xs[4 * j + 0] = u.x;
+        xs[4 * j + 1] = u.y;
+        xs[4 * j + 2] = u.z;
+        xs[4 * j + 3] = u.w;
+      }
+    }
+  };
+
+  float acc[F][CC];
+#pragma unroll
+  for (int f = 0; f < F; ++f)
+#pragma unroll
+    for (int q = 0; q < CC; ++q) acc[f][q] = 0.0f;
+
+  auto fmas = [&](int c, int ky, const float (&xs)[CC + 8]) __attribute__((always_inline)) {
+    const float* wr = lds + (c * 9 + ky) * F * WR;
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+      const float4 wa = *reinterpret_cast<const float4*>(wr + f * WR);
+      const float4 wb = *reinterpret_cast<const float4*>(wr + f * WR + 4);
+      const float wc = wr[f * WR + 8];
+      const float wk[9] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w, wc};
+#pragma unroll
+      for (int kx = 0; kx < 9; ++kx)
+#pragma unroll
+        for (int q = 0; q < CC; ++q) acc[f][q] = __builtin_fmaf(wk[kx], xs[q + kx], acc[f][q]);
+    }
+  };
+
+  // steps (c, ky) in order; the step after the last reloads the last one
+  // (unconditional loads stay ahead of the FMAs)
+  float xa[CC + 8], xb[CC + 8];
+  int c = c0, ky = 0;
+  if (n_steps > 0) load(c, ky, xa);
+#pragma unroll 1
+  for (int i = 0; i < n_steps; i += 2) {
+    int cn = ky == 8 ? c + 1 : c, kn = ky == 8 ? 0 : ky + 1;
+    if (i + 1 >= n_steps) cn = c, kn = ky;
+    load(cn, kn, xb);
+    fmas(c, ky, xa);
+    if (i + 1 >= n_steps) break;
+    c = cn, ky = kn;
+    cn = ky == 8 ? c + 1 : c, kn = ky == 8 ? 0 : ky + 1;
+    if (i + 2 >= n_steps) cn = c, kn = ky;
+    load(cn, kn, xa);
+    fmas(c, ky, xb);
+    c = cn, ky = kn;
+  }
+
+  // ---- channel-split partial sums through LDS (the weights are done with)
+  if constexpr (S > 1) {
+    __syncthreads();
+    if (sp != 0) {
+#pragma unroll
+      for (int f = 0; f < F; ++f)
+#pragma unroll
+        for (int q = 0; q < CC; ++q) lds[((wave * F + f) * CC + q) * 64 + lane] = acc[f][q];
+    }
+    __syncthreads();
+    if (sp == 0) {
+#pragma unroll 1
+      for (int s2 = 1; s2 < S; ++s2)
+#pragma unroll
+        for (int f = 0; f < F; ++f)
+#pragma unroll
+          for (int q = 0; q < CC; ++q) acc[f][q] += lds[(((wave + s2) * F + f) * CC + q) * 64 + lane];
+    }
+  }
+  if (!live || sp != 0) return;
+  TA* y = static_cast<TA*>(p.y) + static_cast<size_t>(img) * p.c_out * p.ho * p.wo;
+#pragma unroll
+  for (int f = 0; f < F; ++f) {
+    const int fo = f0 + f;
+    if (fo >= p.c_out) break;
+    const float b = p.bias ? p.bias[fo] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < CC / 4; ++j) {
+      const int ox = ox0 + 4 * j;
+      if (ox >= p.wo) break;
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[q] = acc[f][4 * j + q] + b;
+        if (p.relu) v[q] = fmaxf(v[q], 0.0f);
+      }
+      const size_t at = (static_cast<size_t>(fo) * p.ho + oy) * p.wo + ox;
+      if constexpr (ES == 2) {
+        uint32_t u[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          u[q] = __float_as_uint(v[q]);
+          u[q] = (u[q] + 0x7FFFu + ((u[q] >> 16) & 1u)) >> 16;
+        }
+        *reinterpret_cast<uint2*>(y + at) = make_uint2(u[0] | (u[1] << 16), u[2] | (u[3] << 16));
+      } else {
+        *reinterpret_cast<float4*>(y + at) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    }
+  }
+}
+
 }  // namespace
 
 template <int K, int F, class TA>
@@ -684,13 +880,61 @@ hipError_t launch_vec(const DenseParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int F, int CC, int NW, int S, class TA>
+hipError_t launch_d9(const DenseParams& p, hipStream_t st) {
+  constexpr int T = NW / S;
+  const int col_tiles = (p.wo + 64 * CC - 1) / (64 * CC);
+  const long tiles = static_cast<long>(p.n) * p.ho * col_tiles;
+  const long bx = (tiles + T - 1) / T;
+  const int fgs = (p.c_out + F - 1) / F;
+  const size_t lw = static_cast<size_t>(p.c_in) * 9 * F * 12 * sizeof(float);
+  const size_t red = S > 1 ? static_cast<size_t>(NW) * F * CC * 64 * sizeof(float) : 0;
+  const size_t lds = lw > red ? lw : red;
+  if (lds > 65536 || bx < 1 || tiles > 0x7FFFFFFFL || fgs > 65535) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((dense9_tile_kernel<F, CC, NW, S, TA>), dim3(static_cast<uint32_t>(bx), fgs), dim3(64 * NW),
+                     lds, st, p, col_tiles, static_cast<int>(tiles));
+  return hipGetLastError();
+}
+
+// F = 3 filters per wave for layers with at most 3 (the 32 -> 3 output
+// layer), else 4; channels split S ways (1, 4 or 8: the smallest that puts
+// 8192+ waves on the chip, at most c_in), S = 8 with two tiles per 16-wave
+// workgroup (each staged weight set serves both), else 8-wave workgroups.
+// Timed on the style network's layers at 512 x 512: 32 -> 3 at F 3, S 8 and
+// 3 -> 32 at F 4, S 1 (F 8 and 8 columns per lane were slower).
+template <int F>
+int dense9_split(const DenseParams& p) {
+  const long waves = static_cast<long>(p.n) * p.ho * ((p.wo + 255) / 256) * ((p.c_out + F - 1) / F);
+  int s = 1;
+  while (s < 8 && waves * s < 8192 && (s == 1 ? 4 : 8) <= p.c_in) s = s == 1 ? 4 : 8;
+  return s;
+}
+
+template <int F, class TA>
+hipError_t launch_dense9_f(const DenseParams& p, hipStream_t st) {
+  const int s = dense9_split<F>(p);
+  if (s == 8) return launch_d9<F, 4, 16, 8, TA>(p, st);
+  if (s == 4) return launch_d9<F, 4, 8, 4, TA>(p, st);
+  return launch_d9<F, 4, 8, 1, TA>(p, st);
+}
+
+template <class TA>
+bool dense9_fits(const DenseParams& p) {
+  const int f = p.c_out <= 3 ? 3 : 4;
+  return p.k == 9 && p.pad == 4 && p.stride == 1 && p.w % 4 == 0 && p.ho == p.h && p.wo == p.w &&
+         static_cast<size_t>(p.c_in) * 9 * f * 12 * sizeof(float) <= 65536;
+}
+
 template <int K, class TA>
 hipError_t launch_conv_k(const DenseParams& p, hipStream_t st) {
   // the matrix cores once a tile has 16+ filters and the reduction is at
   // least 256 long (timed on the evaluated layers: the 9 x 9 convs 3 -> 32
   // and 32 -> 3 run faster on the vector ALUs, the 1 x 1 conv 256 -> 313
-  // several times faster on the matrix cores)
+  // several times faster on the matrix cores); then the tiled 9 x 9 kernel
+  // where its shape rules and LDS allow
   if (p.c_out >= 16 && static_cast<long>(p.c_in) * K * K >= 256) return launch_mfma<0, K, TA>(p, st);
+  if (K == 9 && dense9_fits<TA>(p))
+    return p.c_out <= 3 ? launch_dense9_f<3, TA>(p, st) : launch_dense9_f<4, TA>(p, st);
   return p.c_out <= 4 ? launch_vec<K, 4, TA>(p, st) : launch_vec<K, 8, TA>(p, st);
 }
 
