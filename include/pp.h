@@ -264,14 +264,17 @@ pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes, const voi
 /*
  * pp_conv2d_prepare -- write, once, a layer's weights in the form its
  * kernels read them, which pp_conv2d_fwd otherwise re-derives from the blob
- * on every call.  bf16 layers: the weights of the matrix-core form (the
- * layer as the masked dense contraction of Sec. 2's pruning structure: bf16
- * [c_out][9][c_in] in original filter order, zeros for taps off a kernel's
- * pattern and for pruned kernels, then the fp32 bias).  fp32 layers of the
- * canonical library, stride 1, dilation 1, pad 1: each (slot group, input
- * channel)'s 8 slots x 4 taps of the compact storage (Sec. 3) expanded,
- * zeros for pruned slots, fp32 [ceil(c_out/8)][c_in][32], which the lean
- * kernel reads by scalar loads instead of staging them through LDS.  The
+ * on every call, in up to two parts.  The matrix-core part (bf16 layers
+ * with c_in a multiple of 32): the layer as the masked dense contraction of
+ * Sec. 2's pruning structure, bf16 [c_out][9][c_in] in original filter
+ * order, zeros for taps off a kernel's pattern and for pruned kernels, then
+ * the fp32 bias.  The lean part (layers of the canonical library, stride 1,
+ * dilation 1, pad 1, fp32 or bf16), from the next 256-byte boundary after
+ * the matrix-core part (at the start when there is none): each (slot group,
+ * input channel)'s 8 slots x 4 taps of the compact storage (Sec. 3)
+ * expanded, zeros for pruned slots, fp32 [ceil(c_out/8)][c_in][32] (bf16
+ * weights widened, exact), which the lean kernel reads by scalar loads
+ * instead of staging them through LDS.  The
  * weights never change, so a caller that keeps the buffer passes it as the
  * workspace of later calls with PP_PREPARED (or as pp_net_op.d_w of the
  * layer in pp_net_fwd), and the per-call expansion is skipped.  A call whose
@@ -282,8 +285,10 @@ pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes, const voi
  *   inout_bytes  in: capacity of prepared; out: bytes required
  *   hip_stream   stream the expansion is enqueued on (NULL: default)
  * Errors: PP_EBLOB, PP_EINVAL (NULL pointers, misaligned buffers),
- * PP_EUNSUPPORTED (bf16: c_in not a multiple of 32 or a layer too large for
- * the matrix-core form; fp32: another library, stride, dilation or pad),
+ * PP_EUNSUPPORTED (a layer with neither part: bf16 with c_in not a multiple
+ * of 32 or too large for the matrix-core form and another library, stride,
+ * dilation or pad than the lean part's; fp32 with another library, stride,
+ * dilation or pad),
  * PP_ESIZE (capacity too small; *inout_bytes then holds
  * the required size), PP_EHIP.
  */

@@ -93,9 +93,9 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
     return fail(PP_EINVAL, "activation pointers misaligned");
   if (flags & ~static_cast<uint32_t>(PP_RELU | PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2 | PP_PREPARED))
     return fail(PP_EINVAL, "unknown flags");
-  // PP_PREPARED: the scratch holds the layer's prepared weights (bf16: the
-  // matrix-core form's; fp32: the lean kernel's); it is used only by the
-  // plan they are for and never as split scratch
+  // PP_PREPARED: the workspace starts with the layer's prepared weights (the
+  // matrix-core form's and / or the lean kernel's), read only by the plans
+  // they are for
   const bool prepared = (flags & PP_PREPARED) != 0;
   flags &= ~static_cast<uint32_t>(PP_PREPARED);
   if (prepared && (!scratch || reinterpret_cast<uintptr_t>(scratch) % 256))
@@ -130,10 +130,9 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
     const size_t head = align256(prepared_bytes(v));
     void* const tail = scratch_bytes > head ? static_cast<uint8_t*>(scratch) + head : nullptr;
     const size_t tail_bytes = tail ? scratch_bytes - head : 0;
-    if (act_dtype == PP_F32) {
-      wprep = pw;   // the lean kernel's weights
-    } else {
-      // bf16: the matrix-core form's weights; any other plan ignores them
+    wprep = lean_prepared(v, pw);   // the lean kernel's weights (when it runs)
+    if (bf) {
+      // the matrix-core form's weights; any other plan ignores them
       ConvParams q = p;
       const ConvPlan mp = plan_with_scratch(q, lib, bf, scratch_bytes, false);
       if (mp.recipe == kRecipeMfma) {
@@ -167,8 +166,8 @@ pp_status conv_enqueue(const BlobView& v, const void* d_blob, const void* x, voi
   }
   ConvPlan plan = make_plan(lib, &p, false);
   if (plan.recipe < 0) return fail(PP_EUNSUPPORTED, "no tiling fuses the upsampling / max pool / accumulation / pixel shuffle for this layer");
-  // prepared fp32 weights: read by the lean tilings built for them, ignored by any other plan
-  if (wprep && act_dtype == PP_F32 && is_lean_recipe(plan.recipe) && lean_pw_tiling(plan.recipe)) p.wprep = wprep;
+  // prepared lean weights: read by the lean tilings built for them, ignored by any other plan
+  if (wprep && is_lean_recipe(plan.recipe) && lean_pw_tiling(plan.recipe)) p.wprep = wprep;
   hipError_t e = launch_conv(lib, plan, p, bf, st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("conv launch: ") + hipGetErrorString(e));
   return PP_OK;
@@ -183,7 +182,18 @@ bool conv_fusable(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t ac
   if ((flags & PP_UPSAMPLE2) && (h % 2 || w % 2)) return false;
   ConvParams p = layer_params(v, n, h, w, ho, wo);
   p.flags = flags;
-  return plan_conv(p, library_kind(v), act_dtype == PP_BF16, with_scratch).recipe >= 0;
+  const int lib = library_kind(v);
+  const bool bf = act_dtype == PP_BF16;
+  if (plan_conv(p, lib, bf, with_scratch).recipe < 0) return false;
+  // a bf16 conv that runs on the lean kernel unfused is not fused with an
+  // upsample or a pixel shuffle, which that kernel does not take: the fused
+  // conv would run on another kernel, whose sums round differently
+  if (bf && (flags & (PP_UPSAMPLE2 | PP_PIXSHUF2))) {
+    ConvParams q = p;
+    q.flags = flags & ~static_cast<uint32_t>(PP_UPSAMPLE2 | PP_PIXSHUF2);
+    if (is_lean_recipe(plan_conv(q, lib, bf, with_scratch).recipe)) return false;
+  }
+  return true;
 }
 
 size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype) {
@@ -307,18 +317,31 @@ extern "C" pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, 
 }
 
 namespace pp {
-size_t prepared_bytes(const BlobView& v) {
-  const ConvParams p = layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1);
-  return v.wdtype == PP_BF16 ? mfma_bytes(p) : lean_prepared_bytes(p);
-}
-
-// a layer pp_conv2d_prepare serves: bf16 in the matrix-core form (c_in a
-// multiple of 32), fp32 on the lean kernel (canonical library, stride 1,
-// dilation 1, pad 1)
-static bool preparable(const BlobView& v, const ConvParams& p) {
-  if (v.wdtype == PP_BF16) return mfma_eligible(p);
+// a layer's prepared weights: the bf16 matrix-core form's (bf16 layers it
+// serves: c_in a multiple of 32), then, from the next 256-byte boundary, the
+// lean kernel's fp32 expansion (canonical library, stride 1, dilation 1, pad
+// 1; fp32 or bf16 weights); either part may be absent
+static bool mfma_part(const BlobView& v, const ConvParams& p) { return v.wdtype == PP_BF16 && mfma_eligible(p); }
+static bool lean_part(const BlobView& v) {
   return library_kind(v) == kLibCanon8 && v.stride == 1 && v.dil == 1 && v.pad == 1;
 }
+static size_t lean_part_offset(const BlobView& v, const ConvParams& p) {
+  return mfma_part(v, p) ? align256(mfma_bytes(p)) : 0;
+}
+
+size_t prepared_bytes(const BlobView& v) {
+  const ConvParams p = layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1);
+  if (!lean_part(v)) return mfma_part(v, p) ? mfma_bytes(p) : 0;
+  return lean_part_offset(v, p) + lean_prepared_bytes(p);
+}
+
+const void* lean_prepared(const BlobView& v, const void* prepared) {
+  if (!prepared || !lean_part(v)) return nullptr;
+  const ConvParams p = layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1);
+  return static_cast<const uint8_t*>(prepared) + lean_part_offset(v, p);
+}
+
+static bool preparable(const BlobView& v, const ConvParams& p) { return mfma_part(v, p) || lean_part(v); }
 }  // namespace pp
 
 extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, const void* d_blob, void* prepared,
@@ -331,7 +354,9 @@ extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, co
   // the expansion does not depend on the input size: one pixel stands in
   ConvParams p = layer_params(v, 1, 3 * v.dil, 3 * v.dil, 1, 1);
   if (!preparable(v, p))
-    return fail(PP_EUNSUPPORTED, v.wdtype == PP_BF16 ? "the matrix-core form needs c_in a multiple of 32"
+    return fail(PP_EUNSUPPORTED, v.wdtype == PP_BF16 ? "bf16 prepared weights need c_in a multiple of 32 (the "
+                                                       "matrix-core form) or the canonical library with stride 1, "
+                                                       "dilation 1 and pad 1 (the lean kernel)"
                                                      : "fp32 prepared weights need the canonical library, stride 1, "
                                                        "dilation 1 and pad 1");
   const size_t need = prepared_bytes(v);
@@ -346,8 +371,11 @@ extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, co
   if (!d_blob || reinterpret_cast<uintptr_t>(d_blob) % 256 || reinterpret_cast<uintptr_t>(prepared) % 256)
     return fail(PP_EINVAL, "d_blob and prepared must be 256-byte aligned device pointers");
   p.blob = static_cast<const uint8_t*>(d_blob);
-  const hipError_t e = v.wdtype == PP_BF16 ? launch_mfma_expand(p, prepared, static_cast<hipStream_t>(hip_stream))
-                                            : launch_lean_expand(p, prepared, static_cast<hipStream_t>(hip_stream));
+  const hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  hipError_t e = hipSuccess;
+  if (mfma_part(v, p)) e = launch_mfma_expand(p, prepared, st);
+  if (e == hipSuccess && lean_part(v))
+    e = launch_lean_expand(p, v.wdtype == PP_BF16, static_cast<uint8_t*>(prepared) + lean_part_offset(v, p), st);
   if (e != hipSuccess) return fail(PP_EHIP, std::string("expansion launch: ") + hipGetErrorString(e));
   return PP_OK;
 }

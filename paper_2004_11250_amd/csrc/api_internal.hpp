@@ -48,8 +48,10 @@ ConvPlan plan_with_scratch(const ConvParams& p, int kind, bool bf16, size_t scra
 int conv_recipe(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype, uint32_t flags,
                 size_t scratch_bytes);
 
-// bytes of a layer's prepared matrix-core weights (pp_conv2d_prepare)
+// bytes of a layer's prepared weights (pp_conv2d_prepare), and where in them
+// the lean kernel's part starts (NULL: the layer has none)
 size_t prepared_bytes(const BlobView& v);
+const void* lean_prepared(const BlobView& v, const void* prepared);
 
 // scratch bytes pp_conv2d_fwd can use for this layer and input (0: none)
 size_t conv_scratch_bytes(const BlobView& v, int32_t n, int32_t h, int32_t w, int32_t act_dtype);

@@ -72,7 +72,7 @@ bool recipe_compiled(int lib, int id) {
 static bool recipe_usable(int id, const ConvParams& p, int lib, bool bf16) {
   if (!recipe_compiled(lib, id) || !recipe_fits(id, p.stride, p.dil, bf16, lib)) return false;
   if (is_lean_recipe(id)) {
-    if (bf16 && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_ACCUMULATE | PP_PIXSHUF2)))) return false;
+    if (bf16 && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_PIXSHUF2)))) return false;
     return p.pad == 1 && (!lean_v4(id) || (p.w % (bf16 ? 8 : 4) == 0 && !(p.flags & PP_UPSAMPLE2)));
   }
   if (recipe_info(id).pipe && (bf16 || lib != kLibCanon8)) return false;
@@ -164,16 +164,28 @@ static bool pool_fits(int id) {
 
 // whether the matrix-core form of a bf16 layer beats the vector kernels: a
 // time model of each, its constants fitted to the bf16 layers of the five
-// workloads on MI355X.  The vector kernels do n_wt MACs per output pixel
-// (n_wt: stored weights, about the surviving taps) at about 12 T MAC/s (half
-// that at stride 2).  The matrix-core form is latency-bound while the chip
+// workloads on MI355X.  The wave-pipeline kernel does n_wt MACs per output
+// pixel (n_wt: stored weights, about the surviving taps) at about 12 T MAC/s
+// (half that at stride 2); the lean kernel (lean: it can run the layer) costs
+// about one step per (output pixel, input channel, slot group), pruned slots
+// all but free, plus 5 us, at a rate set by the tiling the lean table picks:
+// about 1.0 T steps/s for the 4 x 4 tilings (maps of 160 x 160 and more, or
+// batches of 64 K outputs and more), 1.5 T for 2 x 4 on maps from 80 x 80,
+// 1.1 T below (with prepared weights: VGG-16's layers 14-28 us, the style
+// network's 128 -> 128 at 128 x 128 25.6 us).  The matrix-core form is
+// latency-bound while the chip
 // holds all its workgroups (about 1.4-1.5 us per k step, each waiting for
 // its own loads), else bound by workgroup steps (about 880 / 390 per us for
 // 64 / 128-filter tiles); plus about 8 us for the weight expansion and its
 // launch.
-static bool mfma_pays(const ConvParams& p) {
+static bool mfma_pays(const ConvParams& p, bool lean) {
   const double pix = static_cast<double>(p.n) * p.ho * p.wo;
-  const double t_vec = pix * p.n_wt * (p.stride == 2 ? 2.2 : 1.0) / 12e12 + 8e-6;
+  const double map = static_cast<double>(p.ho) * p.wo;
+  const double lean_rate = (p.n > 1 ? pix >= 65536.0 : map >= 160.0 * 160.0) ? 1.0e12
+                           : (p.n > 1 || map >= 80.0 * 80.0)                 ? 1.5e12
+                                                                              : 1.1e12;
+  const double t_vec = lean ? pix * p.c_in * p.n_groups / lean_rate + 5e-6
+                            : pix * p.n_wt * (p.stride == 2 ? 2.2 : 1.0) / 12e12 + 8e-6;
   const bool long_k = mfma_long_k(p);
   const int km = long_k ? 64 : 32;
   const double steps = (9.0 * p.c_in + km - 1) / km;
@@ -221,9 +233,12 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
   if (cin_ok && forced < 0) return cin;
   // (bf16: 64 -> 3 at 1080 x 1920 228 -> 135 us; fp32 stays on the wave kernel, 173 against 186 here)
   if (few_any && lib == kLibDense9 && bf16 && forced < 0) return few;
-  if (mfma_ok && forced < 0 && mfma_pays(p)) return mfma;
+  const bool lean_layer = lib == kLibCanon8 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.c_in > 8 && !no_lean;
+  if (mfma_ok && forced < 0 &&
+      mfma_pays(p, lean_layer && bf16 && p.w % 2 == 0 && !(p.flags & (PP_UPSAMPLE2 | PP_PIXSHUF2))))
+    return mfma;
   const long pix = static_cast<long>(p.ho) * p.wo;
-  if (lib == kLibCanon8 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.c_in > 8 && !no_lean) {
+  if (lean_layer) {
     // fp32, stride 1: the lean tilings that timed fastest on the
     // VGG-16 layer shapes (MI355X), by output size: 4 x 4 outputs per lane on
     // the 224 x 224 maps (4 channel-split waves), 2 x 4 on 112 x 112 (8

@@ -231,11 +231,13 @@ hipError_t launch_lean_recipe(int id, const ConvParams& p, bool bf16_act, hipStr
 // for that dtype, or does not fit); whether it stages by 16-byte DMAs (image
 // width a multiple of 4 fp32 / 8 bf16 elements)
 long lean_lds_bytes(int id, bool bf16 = false);
-// the fp32 tilings also built to read prepared weights (ConvParams::wprep)
+// the tilings also built to read prepared weights (ConvParams::wprep; for
+// bf16 activations those of them lean_lds_bytes(id, true) admits)
 bool lean_pw_tiling(int id);
-// bytes of a layer's prepared lean weights, and their expansion from the blob
+// bytes of a layer's prepared lean weights (fp32), and their expansion from
+// the blob's fp32 or bf16 weights
 size_t lean_prepared_bytes(const ConvParams& p);
-hipError_t launch_lean_expand(const ConvParams& p, void* out, hipStream_t st);
+hipError_t launch_lean_expand(const ConvParams& p, bool bf16_w, void* out, hipStream_t st);
 bool lean_v4(int id);
 
 #endif

@@ -38,12 +38,13 @@ hipError_t launch_lean_recipe(int id, const ConvParams& c, bool bf16, hipStream_
   p.flags = c.flags;
   p.ksplit = c.ksplit;
   p.wprep = static_cast<const uint8_t*>(c.wprep);
-  const bool pw = !bf16 && c.wprep != nullptr;
+  const bool pw = c.wprep != nullptr;
   p.groups = make_fastdiv(c.n_groups);
   switch (id) {
 #define PP_L(ID, R, CC, LW, WS, V4)                                                          \
   case ID:                                                                                   \
     if constexpr (lean_bf_tiling(ID)) {                                                      \
+      if (bf16 && pw) return kern::launch_lean_tiling<R, CC, LW, WS, (V4 != 0), true, true>(p, c.n, st); \
       if (bf16) return kern::launch_lean_tiling<R, CC, LW, WS, (V4 != 0), true>(p, c.n, st); \
     } else {                                                                                 \
       if (bf16) return hipErrorInvalidConfiguration;                                         \
@@ -94,7 +95,8 @@ long lean_lds_bytes(int id, bool bf16) {
 // per float.  Every offset read from the blob is clamped to the weights it
 // holds.
 __global__ __launch_bounds__(256) void pp_lean_expand_kernel(const uint8_t* blob, uint32_t off_woff, uint32_t off_w,
-                                                             uint32_t n_wt, uint32_t n_entries, float* out) {
+                                                             uint32_t n_wt, uint32_t n_entries, int bf16_w,
+                                                             float* out) {
   const uint32_t i = blockIdx.x * 256u + threadIdx.x;
   if (i >= n_entries * 32u) return;
   const uint32_t e = i >> 5, j = i & 31u, s = j >> 2, t = j & 3u;
@@ -102,20 +104,23 @@ __global__ __launch_bounds__(256) void pp_lean_expand_kernel(const uint8_t* blob
   const uint32_t kept = wo >> 24;
   float v = 0.0f;
   if ((kept >> s) & 1u) {
-    const uint32_t k = (wo & 0xFFFFFFu) + 4u * __builtin_popcount(kept & ((1u << s) - 1u)) + t;
-    v = reinterpret_cast<const float*>(blob + off_w)[min(k, n_wt ? n_wt - 1 : 0u)];
+    const uint32_t k = min((wo & 0xFFFFFFu) + 4u * __builtin_popcount(kept & ((1u << s) - 1u)) + t,
+                           n_wt ? n_wt - 1 : 0u);
+    // bf16 weights widen exactly
+    v = bf16_w ? __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(blob + off_w)[k]) << 16)
+               : reinterpret_cast<const float*>(blob + off_w)[k];
   }
   out[i] = v;
 }
 
 size_t lean_prepared_bytes(const ConvParams& p) { return static_cast<size_t>(p.n_groups) * p.c_in * 32u * sizeof(float); }
 
-hipError_t launch_lean_expand(const ConvParams& p, void* out, hipStream_t st) {
+hipError_t launch_lean_expand(const ConvParams& p, bool bf16_w, void* out, hipStream_t st) {
   const size_t n = static_cast<size_t>(p.n_groups) * p.c_in;
   if (n == 0 || n * 32 > 0xFFFFFFFFull) return hipErrorInvalidValue;
   const uint32_t blocks = static_cast<uint32_t>((n * 32 + 255) / 256);
   hipLaunchKernelGGL(pp_lean_expand_kernel, dim3(blocks), dim3(256), 0, st, p.blob, p.off_woff, p.off_w, p.n_wt,
-                     static_cast<uint32_t>(n), static_cast<float*>(out));
+                     static_cast<uint32_t>(n), bf16_w ? 1 : 0, static_cast<float*>(out));
   return hipGetLastError();
 }
 

@@ -154,13 +154,13 @@ __device__ __forceinline__ void read_row_bf(float (&d)[PC], const uint8_t* rb) {
   }
 }
 
-// PW (fp32 only): the weights come from a prepared expanded copy by scalar
-// loads into SGPRs (one channel's 32 at the end of the step before it), each
-// kept slot's 4 copied to VGPRs for its FMAs: no weight DMA and no LDS reads of
-// weights, which relieves the LDS path the patch DMAs and reads share
+// PW: the weights come from a prepared expanded fp32 copy (for bf16 layers
+// the bf16 weights widened, exact) by scalar loads into SGPRs (one channel's
+// 32 at the end of the step before it), each kept slot's 4 copied to VGPRs
+// for its FMAs: no weight DMA and no LDS reads of weights, which relieves the
+// LDS path the patch DMAs and reads share
 template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false>
 __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) {
-  static_assert(!(BF && PW), "prepared weights are fp32");
   using G = LGeo<R, CC, LW, WS, V4, BF>;
   constexpr uint32_t ES = G::ES;
   constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT, NS = G::NS;
@@ -343,11 +343,13 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       float p[PR][PC];
       {
         if constexpr (BF) {
-          const uint4* wu = reinterpret_cast<const uint4*>(cur + G::PATCH);
+          if constexpr (!PW) {
+            const uint4* wu = reinterpret_cast<const uint4*>(cur + G::PATCH);
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const uint4 v = wu[k];
-            wq[4 * k] = v.x; wq[4 * k + 1] = v.y; wq[4 * k + 2] = v.z; wq[4 * k + 3] = v.w;
+            for (int k = 0; k < 4; ++k) {
+              const uint4 v = wu[k];
+              wq[4 * k] = v.x; wq[4 * k + 1] = v.y; wq[4 * k + 2] = v.z; wq[4 * k + 3] = v.w;
+            }
           }
           const uint8_t* pb = reinterpret_cast<const uint8_t*>(cur) + lane_b;
 #pragma unroll
@@ -396,16 +398,9 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       asm volatile("" : "+s"(kc));   // fresh slot tests
       {
         const uint32_t cx = code_c.x, cy = code_c.y;
-        if constexpr (BF) {
-          // a kept slot's 4 taps widened from its two dwords
-          static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
-            constexpr int s = decltype(si)::value;
-            if (!((kc >> s) & 1u)) return;
-            const uint32_t u0 = wq[2 * s], u1 = wq[2 * s + 1];
-            apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
-          });
-        } else if constexpr (PW) {
+        if constexpr (PW) {
           (void)w;
+          (void)wq;
           static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
             constexpr int s = decltype(si)::value;
             if (!((kc >> s) & 1u)) return;
@@ -415,6 +410,14 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
                          : "=v"(w0), "=v"(w1), "=v"(w2), "=v"(w3)
                          : "s"(wsc[s].x), "s"(wsc[s].y), "s"(wsc[s].z), "s"(wsc[s].w));
             apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, w0, w1, w2, w3);
+          });
+        } else if constexpr (BF) {
+          // a kept slot's 4 taps widened from its two dwords
+          static_for<0, 8>([&](auto si) __attribute__((always_inline)) {
+            constexpr int s = decltype(si)::value;
+            if (!((kc >> s) & 1u)) return;
+            const uint32_t u0 = wq[2 * s], u1 = wq[2 * s + 1];
+            apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
           });
         } else {
           static_for<0, 4>([&](auto si) __attribute__((always_inline)) {
@@ -489,17 +492,30 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
       if (relu) v[qq] = fmaxf(v[qq], 0.0f);
     }
     if constexpr (BF) {
-      // one rounding to bf16; CC (even) outputs as dword pairs when the row
-      // and the lane's first column are even
+      // one rounding to bf16 (PP_ACCUMULATE: the stored residual plus the
+      // rounded activated value, rounded again); CC (even) outputs as dword
+      // pairs when the row and the lane's first column are even
       uint16_t* row = yb + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
       if (a.wo % 2 == 0 && oxl + CC <= static_cast<int>(a.wo)) {
 #pragma unroll
-        for (int qq = 0; qq < CC; qq += 2)
-          *reinterpret_cast<uint32_t*>(row + oxl + qq) = bf_rne(v[qq]) | (bf_rne(v[qq + 1]) << 16);
+        for (int qq = 0; qq < CC; qq += 2) {
+          uint32_t* pr = reinterpret_cast<uint32_t*>(row + oxl + qq);
+          uint32_t lo = bf_rne(v[qq]), hi = bf_rne(v[qq + 1]);
+          if (accum) {
+            const uint32_t old = *pr;
+            lo = bf_rne(bf_lo(old) + bf_lo(lo));
+            hi = bf_rne(bf_hi(old) + bf_lo(hi));
+          }
+          *pr = lo | (hi << 16);
+        }
       } else {
 #pragma unroll
         for (int qq = 0; qq < CC; ++qq)
-          if (oxl + qq < static_cast<int>(a.wo)) row[oxl + qq] = static_cast<uint16_t>(bf_rne(v[qq]));
+          if (oxl + qq < static_cast<int>(a.wo)) {
+            uint32_t b = bf_rne(v[qq]);
+            if (accum) b = bf_rne(bf_lo(row[oxl + qq]) + bf_lo(b));
+            row[oxl + qq] = static_cast<uint16_t>(b);
+          }
       }
       return;
     }
@@ -732,7 +748,11 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
                             : (static_cast<size_t>(o) * a.ho + oy) * a.wo + ox;
     const float r = act(v[m], s);
     if constexpr (BF) {
-      static_cast<uint16_t*>(a.y)[yo + at_y] = static_cast<uint16_t>(bf_rne(r));   // (no accumulate / shuffle)
+      // (no shuffle in bf16; accumulate as in the first pass)
+      uint16_t* y = static_cast<uint16_t*>(a.y) + yo;
+      uint32_t b = bf_rne(r);
+      if (a.flags & PP_ACCUMULATE) b = bf_rne(bf_lo(y[at_y]) + bf_lo(b));
+      y[at_y] = static_cast<uint16_t>(b);
     } else {
       float* y = static_cast<float*>(a.y) + yo;
       y[at_y] = (a.flags & PP_ACCUMULATE) ? y[at_y] + r : r;
@@ -748,7 +768,7 @@ hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
     return hipErrorInvalidConfiguration;
   } else {
     if (V4 && (p.w % (BF ? 8 : 4) != 0 || (p.flags & PP_UPSAMPLE2))) return hipErrorInvalidConfiguration;
-    if (BF && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_ACCUMULATE | PP_PIXSHUF2))))
+    if (BF && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_PIXSHUF2))))
       return hipErrorInvalidConfiguration;
     const uint32_t tx = (p.wo + G::TW - 1) / G::TW, ty = (p.ho + G::TH - 1) / G::TH;
     const uint32_t ng = p.groups.d;

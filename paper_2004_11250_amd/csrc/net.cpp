@@ -347,10 +347,11 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
             conv_recipe(pl.views[i], n, si.h, si.w, act_dtype, fl, pl.scratch_bytes) == kRecipeMfma) {
           st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl | PP_PREPARED,
                             const_cast<void*>(op.d_w), prepared_bytes(pl.views[i]), stream);
-        } else if (op.d_w && act_dtype == PP_F32) {
-          // fp32: the lean kernel's prepared weights, with the net's scratch for a split
+        } else if (op.d_w) {
+          // the lean kernel's part of the prepared weights (if the layer has
+          // one), with the net's scratch for a split
           st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl, scratch, pl.scratch_bytes,
-                            stream, op.d_w);
+                            stream, lean_prepared(pl.views[i], op.d_w));
         } else {
           st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl, scratch, pl.scratch_bytes,
                             stream);

@@ -232,7 +232,10 @@ def test_prepare_host_checks(lib):
     blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
     nb = ctypes.c_size_t(0)
     assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_OK
-    assert nb.value == -(-40 * 9 * 64 * 2 // 256) * 256 + 40 * 4
+    # bf16, canonical library, stride 1: the matrix-core part (bf16 weights,
+    # then the bias), then from the next 256-byte boundary the lean part
+    mfma = -(-40 * 9 * 64 * 2 // 256) * 256 + 40 * 4
+    assert nb.value == -(-mfma // 256) * 256 + 5 * 64 * 32 * 4
     small = ctypes.c_size_t(nb.value - 1)
     assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, 0x100000, 0x200000, ctypes.byref(small),
                                  None) == pp.PP_ESIZE
@@ -240,9 +243,18 @@ def test_prepare_host_checks(lib):
     assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, 0x100000, 0x200010, ctypes.byref(nb),
                                  None) == pp.PP_EINVAL
     assert lib.pp_conv2d_prepare(blob.ctypes.data, blob.nbytes, None, None, None, None) == pp.PP_EINVAL
-    L2 = workloads.random_layer(32, 40, 48, keep=0.5)   # c_in not a multiple of 32
+    L2 = workloads.random_layer(32, 40, 48, keep=0.5)   # c_in not a multiple of 32: the lean part only
     blob2 = pp.pack(L2["w"], L2["b"], L2["pid"], L2["conn"], L2["lib"], 1, 1, 1, pp.PP_BF16)
     assert lib.pp_conv2d_prepare(blob2.ctypes.data, blob2.nbytes, None, None, ctypes.byref(nb),
+                                 None) == pp.PP_OK
+    assert nb.value == 5 * 48 * 32 * 4
+    # the matrix-core part only (stride 2)
+    b2s = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 2, 1, 1, pp.PP_BF16)
+    assert lib.pp_conv2d_prepare(b2s.ctypes.data, b2s.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_OK
+    assert nb.value == mfma
+    # neither part: c_in 48 at stride 2
+    blob3 = pp.pack(L2["w"], L2["b"], L2["pid"], L2["conn"], L2["lib"], 2, 1, 1, pp.PP_BF16)
+    assert lib.pp_conv2d_prepare(blob3.ctypes.data, blob3.nbytes, None, None, ctypes.byref(nb),
                                  None) == pp.PP_EUNSUPPORTED
     # fp32: the lean kernel's expanded weights, [ceil(c_out / 8)][c_in][32]
     # floats, for the canonical library at stride 1 only

@@ -288,8 +288,8 @@ def test_lean_bf16_pool_and_split(recipe, ksplit, monkeypatch):
 
 
 def test_lean_bf16_not_for_other_epilogues():
-    # the bf16 lean tilings take ReLU and the max pool only: a fused add,
-    # pixel shuffle or upsample runs on the wave-pipeline kernel
+    # the bf16 lean tilings take ReLU, the max pool and the residual add: a
+    # fused pixel shuffle or upsample, or an odd width, runs on another kernel
     L = workloads.random_layer(8900, 16, 32, keep=0.5)
     blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
     assert pp.conv2d_recipe(blob, 1, 56, 56, pp.PP_BF16) in LEAN_BF
@@ -331,3 +331,80 @@ def test_lean_prepared_weights_bitwise(recipe, monkeypatch):
               pp.conv2d_fwd(layer, xd, relu=True, prepared=True).cpu().numpy().astype(np.float64),
               oconv.conv3x3_pruned(*args, 1, 1, 1, True), oconv.conv3x3_bound(*args, 1, 1, 1), "f32",
               f"lean prepared {recipe}")
+
+
+# bf16 layers' prepared lean weights (the fp32 widening of the bf16 weights,
+# after the matrix-core part when c_in is a multiple of 32): every bf16
+# tiling, bitwise what the blob-staged weights give, with the pool and a
+# channel split
+@pytest.mark.parametrize("recipe,ksplit", [(r, 0) for r in LEAN_BF] + [(51, 4), (46, 3)])
+def test_lean_bf16_prepared_weights_bitwise(recipe, ksplit, monkeypatch):
+    from oracle import bf16 as obf16
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    shapes = [(19, 21, 36, 48), (16, 64, 32, 32), (8, 40, 20, 40)]
+    if recipe not in V4_BF:
+        shapes += [(19, 21, 37, 46), (16, 64, 14, 14)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 9500 + 10 * recipe + si + ksplit
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.4)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, pp.PP_BF16)
+        _say("lean bf16 prepared", recipe, ksplit, "seed", seed, (c_out, c_in, h, w), "runs as", plan)
+        assert plan[0] == recipe and (not ksplit or plan[1] == ksplit)
+        assert layer.prepare() is not None
+        xr = obf16.round_f32(x)
+        xd = torch.from_numpy(np.ascontiguousarray(xr, np.float32)).cuda().to(torch.bfloat16)
+        for relu, pool in ((True, False), (False, False), (True, True)):
+            if pool and (recipe == 54 or h % 2 or w % 2):
+                continue
+            ya = pp.conv2d_fwd(layer, xd, relu=relu, maxpool2=pool)
+            yb = pp.conv2d_fwd(layer, xd, relu=relu, maxpool2=pool, prepared=True)
+            torch.cuda.synchronize()
+            assert torch.equal(ya, yb), f"bf16 prepared {recipe}/{ksplit} relu={relu} pool={pool}"
+        args = (xr, obf16.round_f32(L["w"]), L["b"], L["pid"], L["conn"], L["lib"])
+        y = pp.conv2d_fwd(layer, xd, relu=False, prepared=True)
+        check(y.float().cpu().numpy().astype(np.float64), oconv.conv3x3_pruned(*args, 1, 1, 1, False),
+              oconv.conv3x3_bound(*args, 1, 1, 1), "bf16", f"lean bf16 prepared {recipe}/{ksplit}")
+
+
+# bf16 conv fused with a residual add (PP_ACCUMULATE): the activated value
+# rounded to bf16, added to the stored residual and rounded again -- bitwise
+# the same plan's plain store followed by a bf16 add in torch -- with and
+# without prepared weights, on every bf16 tiling and through the split's
+# second pass
+@pytest.mark.parametrize("recipe,ksplit", [(r, 0) for r in LEAN_BF] + [(46, 3), (51, 4), (54, 2)])
+def test_lean_bf16_fused_add(recipe, ksplit, monkeypatch):
+    from oracle import bf16 as obf16
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    shapes = [(20, 21, 36, 48, True), (16, 64, 32, 32, False)]
+    if recipe not in V4_BF:
+        shapes += [(8, 13, 29, 34, True), (16, 64, 14, 14, False)]
+    for si, (c_out, c_in, h, w, relu) in enumerate(shapes):
+        seed = 9700 + 10 * recipe + si + ksplit
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = obf16.round_f32(workloads.random_input(seed, (2, c_in, h, w)))
+        r = obf16.round_f32(workloads.random_input(seed + 1, (2, c_out, h, w)))
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, pp.PP_BF16)
+        _say("lean bf16 fused add", recipe, ksplit, "seed", seed, (c_out, c_in, h, w), "relu", relu, "runs as", plan)
+        assert plan[0] == recipe and (not ksplit or plan[1] == ksplit)
+        assert layer.prepare() is not None
+        xd = torch.from_numpy(np.ascontiguousarray(x, np.float32)).cuda().to(torch.bfloat16)
+        rd = torch.from_numpy(np.ascontiguousarray(r, np.float32)).cuda().to(torch.bfloat16)
+        y_plain = pp.conv2d_fwd(layer, xd, relu=relu)
+        ya = rd.clone()
+        pp.conv2d_fwd(layer, xd, relu=relu, out=ya, accumulate=True)
+        yb = rd.clone()
+        pp.conv2d_fwd(layer, xd, relu=relu, out=yb, accumulate=True, prepared=True)
+        torch.cuda.synchronize()
+        assert torch.equal(ya, rd + y_plain), f"bf16 fused add {recipe}/{ksplit} differs from the add after the conv"
+        assert torch.equal(ya, yb), f"bf16 fused add {recipe}/{ksplit}: prepared weights differ"
+        args = (x, obf16.round_f32(L["w"]), L["b"], L["pid"], L["conn"], L["lib"])
+        ref = oconv.conv3x3_pruned(*args, 1, 1, 1, relu) + r.astype(np.float64)
+        bound = oconv.conv3x3_bound(*args, 1, 1, 1) + np.abs(r.astype(np.float64))
+        check(ya.float().cpu().numpy().astype(np.float64), ref, bound, "bf16", f"lean bf16 add {recipe}/{ksplit}")

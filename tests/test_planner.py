@@ -24,7 +24,9 @@ def _no_forced_plan(monkeypatch):
 def test_large_bf16_layers_take_the_matrix_cores():
     assert pp.conv2d_recipe(_blob(1, 64, 64, pp.PP_BF16), 1, 270, 480, pp.PP_BF16) == MFMA      # super-resolution body
     assert pp.conv2d_recipe(_blob(2, 512, 512, pp.PP_BF16), 8, 32, 32, pp.PP_BF16) == MFMA     # colourization
-    assert pp.conv2d_recipe(_blob(3, 128, 128, pp.PP_BF16), 1, 128, 128, pp.PP_BF16) == MFMA   # style transfer
+    # the style network's 128 -> 128 at 128 x 128: the lean kernel (25.6 us
+    # with prepared weights against 29.3 on the matrix cores)
+    assert pp.conv2d_recipe(_blob(3, 128, 128, pp.PP_BF16), 1, 128, 128, pp.PP_BF16) == 46
     # any library: the form reads the blob's own masks
     other = [0x00F, 0x0B2, 0x1C8, 0x055, 0x113, 0x0A9]
     assert pp.conv2d_recipe(_blob(4, 64, 64, pp.PP_BF16, lib=other), 1, 270, 480, pp.PP_BF16) == MFMA
