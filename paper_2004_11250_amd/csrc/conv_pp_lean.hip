@@ -40,6 +40,8 @@ hipError_t launch_lean_recipe(int id, const ConvParams& c, bool bf16, hipStream_
   p.wprep = static_cast<const uint8_t*>(c.wprep);
   const bool pw = c.wprep != nullptr;
   p.groups = make_fastdiv(c.n_groups);
+  if (c.stride != 1 || c.pad != c.dil || (c.dil != 1 && (c.dil != 2 || bf16))) return hipErrorInvalidValue;
+  if (c.dil == 2) return launch_lean_d2(id, p, c.n, pw, st);
   switch (id) {
 #define PP_L(ID, R, CC, LW, WS, V4)                                                          \
   case ID:                                                                                   \
@@ -74,7 +76,9 @@ bool lean_v4(int id) {
   }
 }
 
-long lean_lds_bytes(int id, bool bf16) {
+long lean_lds_bytes(int id, bool bf16, int dil) {
+  if (dil == 2) return bf16 ? 0L : lean_lds_bytes_d2(id);
+  if (dil != 1) return 0L;
   switch (id) {
 #define PP_L(ID, R, CC, LW, WS, V4)                                                                     \
   case ID:                                                                                              \

@@ -76,21 +76,23 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
 // V4: the halo tile is staged by 16-byte DMAs (image width a multiple of
 // 4 fp32 / 8 bf16 elements), else by 4-byte DMAs (any width for fp32, even
 // for bf16).  Sizes below are in elements unless named otherwise.
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false>
+// D: the dilation (= the padding): 1, or 2 for fp32.
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, int D = 1>
 struct LGeo {
+  static_assert(D == 1 || (D == 2 && !BF), "dilation 2: fp32 only");
   static constexpr int ES = BF ? 2 : 4;                 // element bytes
   static constexpr int LH = 64 / LW;
   static constexpr int TH = LH * R, TW = LW * CC;       // output tile
-  static constexpr int PR = R + 2, PC = CC + 2;         // patch of a lane
-  static constexpr int TIH = TH + 2;                    // staged rows
+  static constexpr int PR = R + 2 * D, PC = CC + 2 * D;   // patch of a lane
+  static constexpr int TIH = TH + 2 * D;                // staged rows
   // the staged columns start SH columns before the tile's first input
-  // column: fp32 16-byte staging at a multiple of 4 (SH 3), fp32 4-byte
+  // column: fp32 16-byte staging at a multiple of 4 (SH 4 - D), fp32 4-byte
   // staging at that column (SH 0); bf16 at a multiple of 8 (SH 7) or of 2
   // (SH 3), so that a lane's first input element sits one after a dword
   // boundary and its row reads are aligned pieces
-  static constexpr int SH = V4 ? (BF ? 7 : 3) : (BF ? 3 : 0);
+  static constexpr int SH = V4 ? (BF ? 7 : 4 - D) : (BF ? 3 : 0);
   static constexpr int SALIGN = BF ? 8 : 4;
-  static constexpr int SWID = (TW + 2 + SH + SALIGN - 1) / SALIGN * SALIGN;
+  static constexpr int SWID = (TW + 2 * D + SH + SALIGN - 1) / SALIGN * SALIGN;
   // fp32: a lane's patch rows are read with aligned loads of up to VWL
   // floats (the alignment its row start allows)
   static constexpr int VWL = CC % 4 == 0 ? 4 : (CC % 2 == 0 ? 2 : 1);
@@ -159,9 +161,9 @@ __device__ __forceinline__ void read_row_bf(float (&d)[PC], const uint8_t* rb) {
 // 32 at the end of the step before it), each kept slot's 4 copied to VGPRs
 // for its FMAs: no weight DMA and no LDS reads of weights, which relieves the
 // LDS path the patch DMAs and reads share
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false>
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false, int D = 1>
 __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) {
-  using G = LGeo<R, CC, LW, WS, V4, BF>;
+  using G = LGeo<R, CC, LW, WS, V4, BF, D>;
   constexpr uint32_t ES = G::ES;
   constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT, NS = G::NS;
   static_assert(G::fits, "tiling does not fit");
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   const uint32_t img = q;
 
   const int oy0 = ty * G::TH, ox0 = tx * G::TW;
-  const int iy0 = oy0 - 1, ixa = ox0 - 1 - G::SH;   // staged origin
+  const int iy0 = oy0 - D, ixa = ox0 - D - G::SH;   // staged origin
 
   // ---- this wave's channels: split ks of ksplit, then the wave's part
   const uint32_t kc0 = fdiv(ks * a.c_in, a.splits), kc1 = fdiv((ks + 1) * a.c_in, a.splits);
@@ -196,7 +198,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   // with PP_UPSAMPLE2 (4-byte staging only) the conv's input is the nearest
   // x2 upsampling of x: a.h x a.w is the upsampled size and element (gy, gx)
   // is read from x[gy / 2][gx / 2]
-  const bool up = !V4 && !BF && (a.flags & PP_UPSAMPLE2) != 0;
+  const bool up = !V4 && !BF && D == 1 && (a.flags & PP_UPSAMPLE2) != 0;
   const uint32_t sh = up ? a.h >> 1 : a.h, sw = up ? a.w >> 1 : a.w;   // stored input size
   const uint32_t chan_bytes = sh * sw * ES;
   const uint8_t* xi = static_cast<const uint8_t*>(a.x) + static_cast<size_t>(img) * a.c_in * sh * sw * ES;
@@ -409,7 +411,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
             asm volatile("v_mov_b32 %0, %4\n v_mov_b32 %1, %5\n v_mov_b32 %2, %6\n v_mov_b32 %3, %7"
                          : "=v"(w0), "=v"(w1), "=v"(w2), "=v"(w3)
                          : "s"(wsc[s].x), "s"(wsc[s].y), "s"(wsc[s].z), "s"(wsc[s].w));
-            apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, w0, w1, w2, w3);
+            apply_canon8_bits<8 * (s & 3), 1, D>(s < 4 ? cx : cy, acc[s], p, w0, w1, w2, w3);
           });
         } else if constexpr (BF) {
           // a kept slot's 4 taps widened from its two dwords
@@ -417,13 +419,13 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
             constexpr int s = decltype(si)::value;
             if (!((kc >> s) & 1u)) return;
             const uint32_t u0 = wq[2 * s], u1 = wq[2 * s + 1];
-            apply_canon8_bits<8 * (s & 3), 1, 1>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
+            apply_canon8_bits<8 * (s & 3), 1, D>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
           });
         } else {
           static_for<0, 4>([&](auto si) __attribute__((always_inline)) {
             constexpr int s = decltype(si)::value;
             if (!((kc >> s) & 1u)) return;
-            apply_canon8_bits<8 * s, 1, 1>(cx, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+            apply_canon8_bits<8 * s, 1, D>(cx, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
           });
 #pragma unroll
           for (int s = 0; s < 4; ++s) {
@@ -433,7 +435,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
           static_for<4, 8>([&](auto si) __attribute__((always_inline)) {
             constexpr int s = decltype(si)::value;
             if (!((kc >> s) & 1u)) return;
-            apply_canon8_bits<8 * (s - 4), 1, 1>(cy, acc[s], p, w[s - 4][0], w[s - 4][1], w[s - 4][2], w[s - 4][3]);
+            apply_canon8_bits<8 * (s - 4), 1, D>(cy, acc[s], p, w[s - 4][0], w[s - 4][1], w[s - 4][2], w[s - 4][3]);
           });
         }
       }
@@ -761,15 +763,16 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
 }
 
 #ifndef __HIPCC_RTC__   // host side
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false>
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false, int D = 1>
 hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
-  using G = LGeo<R, CC, LW, WS, V4, BF>;
+  using G = LGeo<R, CC, LW, WS, V4, BF, D>;
   if constexpr (!G::fits) {
     return hipErrorInvalidConfiguration;
   } else {
     if (V4 && (p.w % (BF ? 8 : 4) != 0 || (p.flags & PP_UPSAMPLE2))) return hipErrorInvalidConfiguration;
     if (BF && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_PIXSHUF2))))
       return hipErrorInvalidConfiguration;
+    if (D != 1 && (p.flags & PP_UPSAMPLE2)) return hipErrorInvalidConfiguration;
     const uint32_t tx = (p.wo + G::TW - 1) / G::TW, ty = (p.ho + G::TH - 1) / G::TH;
     const uint32_t ng = p.groups.d;
     if (p.ksplit < 1 || p.ksplit > p.c_in || (p.ksplit > 1 && !p.part)) return hipErrorInvalidValue;
@@ -780,7 +783,7 @@ hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
     const size_t nb = static_cast<size_t>(ng) * p.ksplit * tx * ty * n;
     if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
     if (PW && !p.wprep) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4, BF, PW>), dim3(static_cast<uint32_t>(nb)),
+    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4, BF, PW, D>), dim3(static_cast<uint32_t>(nb)),
                        dim3(WS * 64), 0, st, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.ksplit == 1) return e;
@@ -792,4 +795,11 @@ hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
 #endif
 
 }  // namespace kern
+
+#ifndef __HIPCC_RTC__
+// the dilation-2 tilings (conv_pp_lean_d2.hip): launch, and LDS bytes (0:
+// not built at dilation 2, or does not fit)
+hipError_t launch_lean_d2(int id, const LeanParams& p, int n, bool pw, hipStream_t st);
+long lean_lds_bytes_d2(int id);
+#endif
 }  // namespace pp

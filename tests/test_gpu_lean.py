@@ -408,3 +408,41 @@ def test_lean_bf16_fused_add(recipe, ksplit, monkeypatch):
         ref = oconv.conv3x3_pruned(*args, 1, 1, 1, relu) + r.astype(np.float64)
         bound = oconv.conv3x3_bound(*args, 1, 1, 1) + np.abs(r.astype(np.float64))
         check(ya.float().cpu().numpy().astype(np.float64), ref, bound, "bf16", f"lean bf16 add {recipe}/{ksplit}")
+
+
+# dilation 2 (pad 2, fp32): every tiling built for it against the oracle,
+# with the fused max pool, channel splits, and prepared weights (bitwise the
+# blob-staged ones)
+LEAN_D2 = [40, 56, 46, 55, 48, 51, 54]
+
+
+@pytest.mark.parametrize("recipe,ksplit", [(r, 0) for r in LEAN_D2] + [(46, 3), (51, 4), (54, 2)])
+def test_lean_dilation2(recipe, ksplit, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    shapes = [(19, 21, 36, 44), (16, 64, 32, 32), (8, 40, 20, 40)]
+    if recipe not in V4:
+        shapes += [(19, 21, 37, 45), (16, 64, 14, 14), (8, 13, 5, 7)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 9900 + 10 * recipe + si + ksplit
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 2, 2, pp.PP_F32)
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, pp.PP_F32)
+        _say("lean dilation 2", recipe, ksplit, "seed", seed, (c_out, c_in, h, w), "runs as", plan)
+        assert plan[0] == recipe and (not ksplit or plan[1] == ksplit)
+        assert layer.prepare() is not None
+        xd = torch.from_numpy(x).cuda()
+        args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        ref = oconv.conv3x3_pruned(*args, 1, 2, 2, True)
+        bound = oconv.conv3x3_bound(*args, 1, 2, 2)
+        for pool in (False, True):
+            if pool and (h % 2 or w % 2 or (recipe == 54 and not ksplit)):
+                continue
+            y = pp.conv2d_fwd(layer, xd, relu=True, maxpool2=pool)
+            yp = pp.conv2d_fwd(layer, xd, relu=True, maxpool2=pool, prepared=True)
+            torch.cuda.synchronize()
+            assert torch.equal(y, yp), f"dilation 2 {recipe}/{ksplit} pool={pool}: prepared weights differ"
+            r, b = (oconv.maxpool2(ref), oconv.maxpool2(bound)) if pool else (ref, bound)
+            check(y.cpu().numpy().astype(np.float64), r, b, "f32", f"lean d2 {recipe}/{ksplit} pool={pool}")
