@@ -171,8 +171,8 @@ static bool pool_fits(int id) {
 // about one step per (output pixel, input channel, slot group), pruned slots
 // all but free, plus 5 us, at a rate set by the tiling the lean table picks:
 // about 1.0 T steps/s for the 4 x 4 tilings (maps from 160 x 160 up to
-// 256 x 256, or batches of 64 K outputs and more), 1.25 T for 2 x 4 on maps
-// from 256 x 256, 1.5 T on maps from 80 x 80, 1.1 T below (with prepared weights: VGG-16's layers 14-28 us, the style
+// 256 x 256 and from 512 x 512, or batches of 64 K outputs and more), 1.25 T
+// for 2 x 4 on maps in between, 1.5 T on maps from 80 x 80, 1.1 T below (with prepared weights: VGG-16's layers 14-28 us, the style
 // network's 128 -> 128 at 128 x 128 25.6 us).  The matrix-core form is
 // latency-bound while the chip
 // holds all its workgroups (about 1.4-1.5 us per k step, each waiting for
@@ -182,7 +182,7 @@ static bool pool_fits(int id) {
 static bool mfma_pays(const ConvParams& p, bool lean) {
   const double pix = static_cast<double>(p.n) * p.ho * p.wo;
   const double map = static_cast<double>(p.ho) * p.wo;
-  const double lean_rate = p.n == 1 && map >= 256.0 * 256.0                    ? 1.25e12
+  const double lean_rate = p.n == 1 && map >= 256.0 * 256.0 && map < 512.0 * 512.0 ? 1.25e12
                            : (p.n > 1 ? pix >= 65536.0 : map >= 160.0 * 160.0) ? 1.0e12
                            : (p.n > 1 || map >= 80.0 * 80.0)                 ? 1.5e12
                                                                               : 1.1e12;
@@ -268,9 +268,9 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
       } else {
         lp[0] = 46; lp[1] = 55;
       }
-    } else if (pix >= 256L * 256L) {
+    } else if (pix >= 256L * 256L && pix < 512L * 512L) {
       // (super-resolution 64 -> 64 at 270 x 480: 2 x 4 58.6 us against 74
-      // for 4 x 4; style 64 -> 32 at 512 x 512: equal)
+      // for 4 x 4; its 64 -> 256 at 540 x 960: 4 x 4 874 us against 949)
       lp[0] = 46; lp[1] = 55;
     } else if (pix >= 160L * 160L) {
       lp[0] = 40; lp[1] = 56;
