@@ -268,9 +268,9 @@ pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes, const voi
  * with c_in a multiple of 32): the layer as the masked dense contraction of
  * Sec. 2's pruning structure, bf16 [c_out][9][c_in] in original filter
  * order, zeros for taps off a kernel's pattern and for pruned kernels, then
- * the fp32 bias.  The lean part (layers of the canonical library, stride 1,
- * dilation 1 and pad 1 (fp32 or bf16) or dilation 2 and pad 2 (fp32)), from
- * the next 256-byte boundary after
+ * the fp32 bias.  The lean part (layers of the canonical library with pad =
+ * dilation: stride and dilation 1 (fp32 or bf16), or stride 1 and dilation
+ * 2, or stride 2 and dilation 1 (fp32)), from the next 256-byte boundary after
  * the matrix-core part (at the start when there is none): each (slot group,
  * input channel)'s 8 slots x 4 taps of the compact storage (Sec. 3)
  * expanded, zeros for pruned slots, fp32 [ceil(c_out/8)][c_in][32] (bf16
@@ -288,8 +288,8 @@ pp_status pp_conv2d_fwd_noalloc(const void* h_blob, size_t blob_bytes, const voi
  * Errors: PP_EBLOB, PP_EINVAL (NULL pointers, misaligned buffers),
  * PP_EUNSUPPORTED (a layer with neither part: bf16 with c_in not a multiple
  * of 32 or too large for the matrix-core form and another library, stride,
- * dilation or pad than the lean part's; fp32 with another library or stride,
- * or a dilation and pad other than both 1 or both 2),
+ * dilation or pad than the lean part's; fp32 with another library, pad not
+ * equal to the dilation, or both stride and dilation 2 or either above 2),
  * PP_ESIZE (capacity too small; *inout_bytes then holds
  * the required size), PP_EHIP.
  */

@@ -319,12 +319,14 @@ extern "C" pp_status pp_conv2d_workspace(const void* h_blob, size_t blob_bytes, 
 namespace pp {
 // a layer's prepared weights: the bf16 matrix-core form's (bf16 layers it
 // serves: c_in a multiple of 32), then, from the next 256-byte boundary, the
-// lean kernel's fp32 expansion (canonical library, stride 1, dilation = pad
-// = 1, or 2 for fp32; fp32 or bf16 weights); either part may be absent
+// lean kernel's fp32 expansion (canonical library, pad = dilation, stride
+// and dilation 1; fp32 also stride 1 with dilation 2 and stride 2 with
+// dilation 1; fp32 or bf16 weights); either part may be absent
 static bool mfma_part(const BlobView& v, const ConvParams& p) { return v.wdtype == PP_BF16 && mfma_eligible(p); }
 static bool lean_part(const BlobView& v) {
-  return library_kind(v) == kLibCanon8 && v.stride == 1 && v.pad == v.dil &&
-         (v.dil == 1 || (v.dil == 2 && v.wdtype == PP_F32));
+  const bool f32 = v.wdtype == PP_F32;
+  return library_kind(v) == kLibCanon8 && v.pad == v.dil &&
+         ((v.stride == 1 && v.dil == 1) || (f32 && ((v.stride == 1 && v.dil == 2) || (v.stride == 2 && v.dil == 1))));
 }
 static size_t lean_part_offset(const BlobView& v, const ConvParams& p) {
   return mfma_part(v, p) ? align256(mfma_bytes(p)) : 0;
@@ -358,8 +360,8 @@ extern "C" pp_status pp_conv2d_prepare(const void* h_blob, size_t blob_bytes, co
     return fail(PP_EUNSUPPORTED, v.wdtype == PP_BF16 ? "bf16 prepared weights need c_in a multiple of 32 (the "
                                                        "matrix-core form) or the canonical library with stride 1, "
                                                        "dilation 1 and pad 1 (the lean kernel)"
-                                                     : "fp32 prepared weights need the canonical library, stride 1, "
-                                                       "and dilation and pad both 1 or both 2");
+                                                     : "fp32 prepared weights need the canonical library, pad = "
+                                                       "dilation, and stride and dilation 1, or one of them 2");
   const size_t need = prepared_bytes(v);
   if (!prepared) {
     *inout_bytes = need;

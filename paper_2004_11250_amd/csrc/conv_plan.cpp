@@ -40,7 +40,7 @@ static bool wave_recipe_fits(const RecipeInfo& r, int s, int d, int lib, bool bf
 bool recipe_fits(int id, int s, int d, bool bf16, int lib) {
   const RecipeInfo r = recipe_info(id);
   if (r.r == 0) return false;
-  if (is_lean_recipe(id)) return lib == kLibCanon8 && s == 1 && lean_lds_bytes(id, bf16, d) > 0;
+  if (is_lean_recipe(id)) return lib == kLibCanon8 && lean_lds_bytes(id, bf16, d, s) > 0;
   if (is_wave_recipe(id)) return (lib == kLibCanon8 || lib == kLibDense9) && wave_recipe_fits(r, s, d, lib, bf16);
   const int lh = 64 / r.lw;
   const int th = lh * r.r, tw = r.lw * r.cc;
@@ -73,7 +73,7 @@ static bool recipe_usable(int id, const ConvParams& p, int lib, bool bf16) {
   if (!recipe_compiled(lib, id) || !recipe_fits(id, p.stride, p.dil, bf16, lib)) return false;
   if (is_lean_recipe(id)) {
     if (bf16 && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_PIXSHUF2)))) return false;
-    if (p.dil != 1 && (p.flags & PP_UPSAMPLE2)) return false;
+    if ((p.dil != 1 || p.stride != 1) && (p.flags & PP_UPSAMPLE2)) return false;
     return p.pad == p.dil && (!lean_v4(id) || (p.w % (bf16 ? 8 : 4) == 0 && !(p.flags & PP_UPSAMPLE2)));
   }
   if (recipe_info(id).pipe && (bf16 || lib != kLibCanon8)) return false;
@@ -235,8 +235,10 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
   if (cin_ok && forced < 0) return cin;
   // (bf16: 64 -> 3 at 1080 x 1920 228 -> 135 us; fp32 stays on the wave kernel, 173 against 186 here)
   if (few_any && lib == kLibDense9 && bf16 && forced < 0) return few;
-  // (dilation 2 = pad 2: fp32 only)
-  const bool lean_layer = lib == kLibCanon8 && p.stride == 1 && p.pad == p.dil && (p.dil == 1 || (p.dil == 2 && !bf16)) &&
+  // (dilation 2 = pad 2, or stride 2: fp32 only)
+  const bool lean_layer = lib == kLibCanon8 && p.pad == p.dil &&
+                          ((p.stride == 1 && p.dil == 1) ||
+                           (!bf16 && ((p.stride == 1 && p.dil == 2) || (p.stride == 2 && p.dil == 1)))) &&
                           p.c_in > 8 && !no_lean;
   if (mfma_ok && forced < 0 &&
       mfma_pays(p, lean_layer && bf16 && p.w % 2 == 0 && !(p.flags & (PP_UPSAMPLE2 | PP_PIXSHUF2))))
@@ -260,7 +262,9 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
     // LDS tile fits two workgroups per CU (130 us against 186 for 2 x 4 and
     // 192 on the wave kernel).
     int lp[4] = {-1, -1, -1, -1};
-    if (p.dil == 2) {
+    if (p.stride == 2) {
+      lp[0] = 49; lp[1] = 53;
+    } else if (p.dil == 2) {
       lp[0] = 56; lp[1] = 55;
     } else if (p.n > 1) {
       if (static_cast<long>(p.n) * pix >= 65536L) {

@@ -227,11 +227,11 @@ hipError_t launch_wave_recipe(int id, const ConvParams& p, hipStream_t st);
 // lean kernel (conv_pp_lean.hip)
 inline bool is_lean_recipe(int id) { return id >= kFirstLeanRecipe && id < kEndLeanRecipe; }
 hipError_t launch_lean_recipe(int id, const ConvParams& p, bool bf16_act, hipStream_t st);
-// LDS bytes of a lean tiling for fp32 or bf16 activations at dilation (=
-// pad) 1, or fp32 at 2 (0: not compiled for that case, or does not fit);
-// whether it stages by 16-byte DMAs (image width a multiple of 4 fp32 / 8
-// bf16 elements)
-long lean_lds_bytes(int id, bool bf16 = false, int dil = 1);
+// LDS bytes of a lean tiling for fp32 or bf16 activations at stride 1 and
+// dilation (= pad) 1, or fp32 at dilation 2 or stride 2 (0: not compiled
+// for that case, or does not fit); whether it stages by 16-byte DMAs (image
+// width a multiple of 4 fp32 / 8 bf16 elements)
+long lean_lds_bytes(int id, bool bf16 = false, int dil = 1, int stride = 1);
 // the tilings also built to read prepared weights (ConvParams::wprep; for
 // bf16 activations those of them lean_lds_bytes(id, true) admits)
 bool lean_pw_tiling(int id);

@@ -40,8 +40,12 @@ hipError_t launch_lean_recipe(int id, const ConvParams& c, bool bf16, hipStream_
   p.wprep = static_cast<const uint8_t*>(c.wprep);
   const bool pw = c.wprep != nullptr;
   p.groups = make_fastdiv(c.n_groups);
-  if (c.stride != 1 || c.pad != c.dil || (c.dil != 1 && (c.dil != 2 || bf16))) return hipErrorInvalidValue;
+  // (stride, dilation = pad): (1, 1); fp32 also (1, 2) and (2, 1)
+  const bool ok = c.pad == c.dil && ((c.stride == 1 && c.dil == 1) ||
+                                     (!bf16 && ((c.stride == 1 && c.dil == 2) || (c.stride == 2 && c.dil == 1))));
+  if (!ok) return hipErrorInvalidValue;
   if (c.dil == 2) return launch_lean_d2(id, p, c.n, pw, st);
+  if (c.stride == 2) return launch_lean_s2(id, p, c.n, pw, st);
   switch (id) {
 #define PP_L(ID, R, CC, LW, WS, V4)                                                          \
   case ID:                                                                                   \
@@ -76,9 +80,10 @@ bool lean_v4(int id) {
   }
 }
 
-long lean_lds_bytes(int id, bool bf16, int dil) {
-  if (dil == 2) return bf16 ? 0L : lean_lds_bytes_d2(id);
-  if (dil != 1) return 0L;
+long lean_lds_bytes(int id, bool bf16, int dil, int stride) {
+  if (stride == 2) return bf16 || dil != 1 ? 0L : lean_lds_bytes_s2(id);
+  if (dil == 2) return bf16 || stride != 1 ? 0L : lean_lds_bytes_d2(id);
+  if (dil != 1 || stride != 1) return 0L;
   switch (id) {
 #define PP_L(ID, R, CC, LW, WS, V4)                                                                     \
   case ID:                                                                                              \

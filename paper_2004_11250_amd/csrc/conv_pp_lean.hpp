@@ -76,15 +76,17 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
 // V4: the halo tile is staged by 16-byte DMAs (image width a multiple of
 // 4 fp32 / 8 bf16 elements), else by 4-byte DMAs (any width for fp32, even
 // for bf16).  Sizes below are in elements unless named otherwise.
-// D: the dilation (= the padding): 1, or 2 for fp32.
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false, int D = 1>
+// D: the dilation (= the padding): 1, or 2 for fp32; S: the stride: 1, or 2
+// for fp32 at dilation 1.
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, int D = 1, int S = 1>
 struct LGeo {
   static_assert(D == 1 || (D == 2 && !BF), "dilation 2: fp32 only");
+  static_assert(S == 1 || (S == 2 && !BF && D == 1), "stride 2: fp32 at dilation 1 only");
   static constexpr int ES = BF ? 2 : 4;                 // element bytes
   static constexpr int LH = 64 / LW;
   static constexpr int TH = LH * R, TW = LW * CC;       // output tile
-  static constexpr int PR = R + 2 * D, PC = CC + 2 * D;   // patch of a lane
-  static constexpr int TIH = TH + 2 * D;                // staged rows
+  static constexpr int PR = (R - 1) * S + 2 * D + 1, PC = (CC - 1) * S + 2 * D + 1;   // patch of a lane
+  static constexpr int TIH = (TH - 1) * S + 2 * D + 1;  // staged rows
   // the staged columns start SH columns before the tile's first input
   // column: fp32 16-byte staging at a multiple of 4 (SH 4 - D), fp32 4-byte
   // staging at that column (SH 0); bf16 at a multiple of 8 (SH 7) or of 2
@@ -92,11 +94,11 @@ struct LGeo {
   // boundary and its row reads are aligned pieces
   static constexpr int SH = V4 ? (BF ? 7 : 4 - D) : (BF ? 3 : 0);
   static constexpr int SALIGN = BF ? 8 : 4;
-  static constexpr int SWID = (TW + 2 * D + SH + SALIGN - 1) / SALIGN * SALIGN;
+  static constexpr int SWID = ((TW - 1) * S + 2 * D + 1 + SH + SALIGN - 1) / SALIGN * SALIGN;
   // fp32: a lane's patch rows are read with aligned loads of up to VWL
   // floats (the alignment its row start allows)
-  static constexpr int VWL = CC % 4 == 0 ? 4 : (CC % 2 == 0 ? 2 : 1);
-  static constexpr int LSTR = BF ? SWID : wave_row_stride(SWID, R);
+  static constexpr int VWL = (CC * S) % 4 == 0 ? 4 : ((CC * S) % 2 == 0 ? 2 : 1);
+  static constexpr int LSTR = BF ? SWID : wave_row_stride(SWID, R * S);
   static constexpr int AREA = TIH * LSTR;
   static constexpr int DPB = V4 ? 1024 : 256;            // LDS bytes of one DMA instruction
   static constexpr int EPD = DPB / ES;                   // elements per DMA instruction
@@ -161,9 +163,9 @@ __device__ __forceinline__ void read_row_bf(float (&d)[PC], const uint8_t* rb) {
 // 32 at the end of the step before it), each kept slot's 4 copied to VGPRs
 // for its FMAs: no weight DMA and no LDS reads of weights, which relieves the
 // LDS path the patch DMAs and reads share
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false, int D = 1>
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false, int D = 1, int S = 1>
 __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) {
-  using G = LGeo<R, CC, LW, WS, V4, BF, D>;
+  using G = LGeo<R, CC, LW, WS, V4, BF, D, S>;
   constexpr uint32_t ES = G::ES;
   constexpr int PR = G::PR, PC = G::PC, LSTR = G::LSTR, NQ = G::NQ, SLOT = G::SLOT, NS = G::NS;
   static_assert(G::fits, "tiling does not fit");
@@ -189,7 +191,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   const uint32_t img = q;
 
   const int oy0 = ty * G::TH, ox0 = tx * G::TW;
-  const int iy0 = oy0 - D, ixa = ox0 - D - G::SH;   // staged origin
+  const int iy0 = oy0 * S - D, ixa = ox0 * S - D - G::SH;   // staged origin
 
   // ---- this wave's channels: split ks of ksplit, then the wave's part
   const uint32_t kc0 = fdiv(ks * a.c_in, a.splits), kc1 = fdiv((ks + 1) * a.c_in, a.splits);
@@ -198,7 +200,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
   // with PP_UPSAMPLE2 (4-byte staging only) the conv's input is the nearest
   // x2 upsampling of x: a.h x a.w is the upsampled size and element (gy, gx)
   // is read from x[gy / 2][gx / 2]
-  const bool up = !V4 && !BF && D == 1 && (a.flags & PP_UPSAMPLE2) != 0;
+  const bool up = !V4 && !BF && D == 1 && S == 1 && (a.flags & PP_UPSAMPLE2) != 0;
   const uint32_t sh = up ? a.h >> 1 : a.h, sw = up ? a.w >> 1 : a.w;   // stored input size
   const uint32_t chan_bytes = sh * sw * ES;
   const uint8_t* xi = static_cast<const uint8_t*>(a.x) + static_cast<size_t>(img) * a.c_in * sh * sw * ES;
@@ -325,7 +327,8 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
     uint32_t wo_n = wo_pre[DPF];   // woff word of channel c + DPF
     // the lane's patch in a slot: fp32 from element lx CC of its first row;
     // bf16 from the dword holding element lx CC + SH - 1 (read_row_bf)
-    const uint32_t lane_b = BF ? ES * ((ly * R) * LSTR + lx * CC + G::SH - 1) : 4u * ((ly * R) * LSTR + lx * CC);
+    const uint32_t lane_b =
+        BF ? ES * ((ly * R) * LSTR + lx * CC + G::SH - 1) : 4u * ((ly * R * S) * LSTR + lx * CC * S);
 
 #pragma unroll 1
     for (int c = c0; c < c1; ++c) {
@@ -411,7 +414,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
             asm volatile("v_mov_b32 %0, %4\n v_mov_b32 %1, %5\n v_mov_b32 %2, %6\n v_mov_b32 %3, %7"
                          : "=v"(w0), "=v"(w1), "=v"(w2), "=v"(w3)
                          : "s"(wsc[s].x), "s"(wsc[s].y), "s"(wsc[s].z), "s"(wsc[s].w));
-            apply_canon8_bits<8 * (s & 3), 1, D>(s < 4 ? cx : cy, acc[s], p, w0, w1, w2, w3);
+            apply_canon8_bits<8 * (s & 3), S, D>(s < 4 ? cx : cy, acc[s], p, w0, w1, w2, w3);
           });
         } else if constexpr (BF) {
           // a kept slot's 4 taps widened from its two dwords
@@ -419,13 +422,13 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
             constexpr int s = decltype(si)::value;
             if (!((kc >> s) & 1u)) return;
             const uint32_t u0 = wq[2 * s], u1 = wq[2 * s + 1];
-            apply_canon8_bits<8 * (s & 3), 1, D>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
+            apply_canon8_bits<8 * (s & 3), S, D>(s < 4 ? cx : cy, acc[s], p, bf_lo(u0), bf_hi(u0), bf_lo(u1), bf_hi(u1));
           });
         } else {
           static_for<0, 4>([&](auto si) __attribute__((always_inline)) {
             constexpr int s = decltype(si)::value;
             if (!((kc >> s) & 1u)) return;
-            apply_canon8_bits<8 * s, 1, D>(cx, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
+            apply_canon8_bits<8 * s, S, D>(cx, acc[s], p, w[s][0], w[s][1], w[s][2], w[s][3]);
           });
 #pragma unroll
           for (int s = 0; s < 4; ++s) {
@@ -435,7 +438,7 @@ __global__ __launch_bounds__(WS * 64) void pp_conv3x3_lean_kernel(LeanParams a) 
           static_for<4, 8>([&](auto si) __attribute__((always_inline)) {
             constexpr int s = decltype(si)::value;
             if (!((kc >> s) & 1u)) return;
-            apply_canon8_bits<8 * (s - 4), 1, D>(cy, acc[s], p, w[s - 4][0], w[s - 4][1], w[s - 4][2], w[s - 4][3]);
+            apply_canon8_bits<8 * (s - 4), S, D>(cy, acc[s], p, w[s - 4][0], w[s - 4][1], w[s - 4][2], w[s - 4][3]);
           });
         }
       }
@@ -763,16 +766,16 @@ __global__ __launch_bounds__(256) void pp_lean_reduce_kernel(LeanParams a) {
 }
 
 #ifndef __HIPCC_RTC__   // host side
-template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false, int D = 1>
+template <int R, int CC, int LW, int WS, bool V4, bool BF = false, bool PW = false, int D = 1, int S = 1>
 hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
-  using G = LGeo<R, CC, LW, WS, V4, BF, D>;
+  using G = LGeo<R, CC, LW, WS, V4, BF, D, S>;
   if constexpr (!G::fits) {
     return hipErrorInvalidConfiguration;
   } else {
     if (V4 && (p.w % (BF ? 8 : 4) != 0 || (p.flags & PP_UPSAMPLE2))) return hipErrorInvalidConfiguration;
     if (BF && (p.w % 2 != 0 || (p.flags & (PP_UPSAMPLE2 | PP_PIXSHUF2))))
       return hipErrorInvalidConfiguration;
-    if (D != 1 && (p.flags & PP_UPSAMPLE2)) return hipErrorInvalidConfiguration;
+    if ((D != 1 || S != 1) && (p.flags & PP_UPSAMPLE2)) return hipErrorInvalidConfiguration;
     const uint32_t tx = (p.wo + G::TW - 1) / G::TW, ty = (p.ho + G::TH - 1) / G::TH;
     const uint32_t ng = p.groups.d;
     if (p.ksplit < 1 || p.ksplit > p.c_in || (p.ksplit > 1 && !p.part)) return hipErrorInvalidValue;
@@ -783,7 +786,7 @@ hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
     const size_t nb = static_cast<size_t>(ng) * p.ksplit * tx * ty * n;
     if (nb == 0 || nb > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
     if (PW && !p.wprep) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4, BF, PW, D>), dim3(static_cast<uint32_t>(nb)),
+    hipLaunchKernelGGL((pp_conv3x3_lean_kernel<R, CC, LW, WS, V4, BF, PW, D, S>), dim3(static_cast<uint32_t>(nb)),
                        dim3(WS * 64), 0, st, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.ksplit == 1) return e;
@@ -797,9 +800,12 @@ hipError_t launch_lean_tiling(LeanParams p, int n, hipStream_t st) {
 }  // namespace kern
 
 #ifndef __HIPCC_RTC__
-// the dilation-2 tilings (conv_pp_lean_d2.hip): launch, and LDS bytes (0:
-// not built at dilation 2, or does not fit)
+// the dilation-2 tilings (conv_pp_lean_d2.hip) and the stride-2 ones
+// (conv_pp_lean_s2.hip): launch, and LDS bytes (0: not built for that case,
+// or does not fit)
 hipError_t launch_lean_d2(int id, const LeanParams& p, int n, bool pw, hipStream_t st);
 long lean_lds_bytes_d2(int id);
+hipError_t launch_lean_s2(int id, const LeanParams& p, int n, bool pw, hipStream_t st);
+long lean_lds_bytes_s2(int id);
 #endif
 }  // namespace pp

@@ -257,12 +257,17 @@ def test_prepare_host_checks(lib):
     assert lib.pp_conv2d_prepare(blob3.ctypes.data, blob3.nbytes, None, None, ctypes.byref(nb),
                                  None) == pp.PP_EUNSUPPORTED
     # fp32: the lean kernel's expanded weights, [ceil(c_out / 8)][c_in][32]
-    # floats, for the canonical library at stride 1 only
+    # floats, for the canonical library (pad = dilation; stride and dilation
+    # not both 2)
     b32 = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
     assert lib.pp_conv2d_prepare(b32.ctypes.data, b32.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_OK
     assert nb.value == 5 * 64 * 32 * 4
-    s2 = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 2, 1, 1, pp.PP_F32)
-    assert lib.pp_conv2d_prepare(s2.ctypes.data, s2.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_EUNSUPPORTED
+    s2 = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 2, 1, 1, pp.PP_F32)     # stride 2: the lean part
+    assert lib.pp_conv2d_prepare(s2.ctypes.data, s2.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_OK
+    assert nb.value == 5 * 64 * 32 * 4
+    s2d2 = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 2, 2, 2, pp.PP_F32)   # stride and dilation 2
+    assert lib.pp_conv2d_prepare(s2d2.ctypes.data, s2d2.nbytes, None, None, ctypes.byref(nb),
+                                 None) == pp.PP_EUNSUPPORTED
     d9 = pp.pack(L["w"], L["b"], np.zeros_like(L["pid"]), L["conn"], np.array(workloads.DENSE9, np.uint16),
                  1, 1, 1, pp.PP_F32)
     assert lib.pp_conv2d_prepare(d9.ctypes.data, d9.nbytes, None, None, ctypes.byref(nb), None) == pp.PP_EUNSUPPORTED

@@ -446,3 +446,42 @@ def test_lean_dilation2(recipe, ksplit, monkeypatch):
             assert torch.equal(y, yp), f"dilation 2 {recipe}/{ksplit} pool={pool}: prepared weights differ"
             r, b = (oconv.maxpool2(ref), oconv.maxpool2(bound)) if pool else (ref, bound)
             check(y.cpu().numpy().astype(np.float64), r, b, "f32", f"lean d2 {recipe}/{ksplit} pool={pool}")
+
+
+# stride 2 (pad 1, fp32): every tiling built for it against the oracle, with
+# the fused max pool, channel splits, and prepared weights (bitwise the
+# blob-staged ones); odd input sizes give ragged output tiles
+LEAN_S2 = [45, 47, 49, 50, 52, 53, 54]
+
+
+@pytest.mark.parametrize("recipe,ksplit", [(r, 0) for r in LEAN_S2] + [(49, 2), (53, 4), (54, 3)])
+def test_lean_stride2(recipe, ksplit, monkeypatch):
+    monkeypatch.setenv("PP_RECIPE", str(recipe))
+    if ksplit:
+        monkeypatch.setenv("PP_KSPLIT", str(ksplit))
+    shapes = [(19, 21, 36, 44), (16, 64, 64, 64), (8, 40, 20, 40)]
+    if recipe not in V4:
+        shapes += [(19, 21, 37, 45), (16, 64, 29, 14), (8, 13, 5, 7)]
+    for si, (c_out, c_in, h, w) in enumerate(shapes):
+        seed = 9950 + 10 * recipe + si + ksplit
+        L = workloads.random_layer(seed, c_out, c_in, keep=0.5)
+        x = workloads.random_input(seed, (2, c_in, h, w))
+        layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 2, 1, 1, pp.PP_F32)
+        plan = pp.conv2d_plan(layer.h_blob, 2, h, w, pp.PP_F32)
+        _say("lean stride 2", recipe, ksplit, "seed", seed, (c_out, c_in, h, w), "runs as", plan)
+        assert plan[0] == recipe and (not ksplit or plan[1] == ksplit)
+        assert layer.prepare() is not None
+        xd = torch.from_numpy(x).cuda()
+        args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        ref = oconv.conv3x3_pruned(*args, 2, 1, 1, True)
+        bound = oconv.conv3x3_bound(*args, 2, 1, 1)
+        ho, wo = ref.shape[2], ref.shape[3]
+        for pool in (False, True):
+            if pool and (ho % 2 or wo % 2 or (recipe == 54 and not ksplit)):
+                continue
+            y = pp.conv2d_fwd(layer, xd, relu=True, maxpool2=pool)
+            yp = pp.conv2d_fwd(layer, xd, relu=True, maxpool2=pool, prepared=True)
+            torch.cuda.synchronize()
+            assert torch.equal(y, yp), f"stride 2 {recipe}/{ksplit} pool={pool}: prepared weights differ"
+            r, b = (oconv.maxpool2(ref), oconv.maxpool2(bound)) if pool else (ref, bound)
+            check(y.cpu().numpy().astype(np.float64), r, b, "f32", f"lean s2 {recipe}/{ksplit} pool={pool}")
