@@ -415,7 +415,7 @@ static hipError_t launch_wave(int id, const ConvParams& p, hipStream_t st) {
 hipError_t launch_conv(int lib, const ConvPlan& plan, const ConvParams& p0, bool bf16_act, hipStream_t st) {
   ConvParams p = p0;
   if (plan.recipe == kRecipeMfma) return bf16_act ? launch_mfma_conv(p, st) : hipErrorInvalidConfiguration;
-  if (plan.recipe == kRecipeCin) return cin_eligible(p, bf16_act) ? launch_cin_conv(p, st) : hipErrorInvalidConfiguration;
+  if (plan.recipe == kRecipeCin) return cin_eligible(p, bf16_act) ? launch_cin_conv(p, bf16_act, st) : hipErrorInvalidConfiguration;
   if (plan.recipe == kRecipeFewOut)
     return fewout_eligible(p) ? launch_fewout_conv(p, bf16_act, st) : hipErrorInvalidConfiguration;
   p.ksplit = plan.ksplit;

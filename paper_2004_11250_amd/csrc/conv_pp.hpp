@@ -178,13 +178,13 @@ struct ConvPlan {
 // needs (the expanded weights and bias) and its launch (p.part = scratch).
 constexpr int kRecipeMfma = 64;
 
-// fp32 layers with at most four input channels (a network's first layer) as
-// dense 3 x 3 taps expanded in LDS (conv_pp_cin.hip): the plan's recipe id,
-// whether a layer can run so (stride 1, dilation 1, pad 1, no fused epilogue
-// other than ReLU, any pattern library) and its launch
+// layers with at most four input channels (a network's first layer; fp32 or
+// bf16) as dense 3 x 3 taps expanded in LDS (conv_pp_cin.hip): the plan's
+// recipe id, whether a layer can run so (stride 1, dilation 1, pad 1, no
+// fused epilogue other than ReLU, any pattern library) and its launch
 constexpr int kRecipeCin = 60;
 bool cin_eligible(const ConvParams& p, bool bf16_act);
-hipError_t launch_cin_conv(const ConvParams& p, hipStream_t st);
+hipError_t launch_cin_conv(const ConvParams& p, bool bf16_act, hipStream_t st);
 
 // layers with at most 8 output channels (one slot group: a network's
 // image-producing last layer), fp32 or bf16, stride 1, dilation 1, pad 1,

@@ -1,6 +1,6 @@
 // conv_pp_cin.hip -- pattern/connectivity-pruned 3x3 convolution of a layer
 // with at most four input channels (a network's first layer: an RGB or
-// one-channel image), fp32, stride 1, dilation 1, pad 1, any pattern library.
+// one-channel image), fp32 or bf16, stride 1, dilation 1, pad 1, any pattern library.
 //
 // Same result as the other kernels (pattern + connectivity pruning, Sec. 2;
 // compact storage, Sec. 3; conv fused with bias and activation, Sec. 3).
@@ -33,7 +33,9 @@ constexpr int kCinSPW = 4;               // slots (filters) per wave
 constexpr int kCinGPG = kCinWPG * kCinSPW / 8;   // slot groups per workgroup
 constexpr int kCinLS = 36;               // staged row stride (floats): >= 34, a multiple of 4
 
-template <int CIN>
+// BF: bf16 activations and weights, widened to fp32 on their way into LDS
+// (exact), fp32 sums, one rounding at the store.
+template <int CIN, bool BF>
 __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams a) {
   constexpr int WPS = (CIN * 9 + 3) / 4 * 4;   // expanded taps of one slot, padded to 16 bytes
   constexpr int SR = kCinTH + 2, SC = kCinTW + 2;
@@ -58,7 +60,9 @@ __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams
 
   // ---- the input tile of every channel (pad 1: zeros outside the image);
   // staged column j holds input column ox0 - 1 + j
-  const float* x = static_cast<const float*>(a.x) + static_cast<size_t>(img) * CIN * a.h * a.w;
+  const size_t xoff = static_cast<size_t>(img) * CIN * a.h * a.w;
+  const float* x = static_cast<const float*>(a.x) + xoff;
+  const uint16_t* xb = static_cast<const uint16_t*>(a.x) + xoff;
   {
     // every load first, then every store: one memory round trip
     constexpr int NT = 64 * kCinWPG, NST = (CIN * SR * SC + NT - 1) / NT;
@@ -69,8 +73,10 @@ __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams
       const int c = i / (SR * SC), r = (i / SC) % SR, j = i % SC;
       const int gy = oy0 - 1 + r, gx = ox0 - 1 + j;
       v[k] = 0.0f;
-      if (i < CIN * SR * SC && gy >= 0 && gy < a.h && gx >= 0 && gx < a.w)
-        v[k] = x[(static_cast<size_t>(c) * a.h + gy) * a.w + gx];
+      if (i < CIN * SR * SC && gy >= 0 && gy < a.h && gx >= 0 && gx < a.w) {
+        const size_t at = (static_cast<size_t>(c) * a.h + gy) * a.w + gx;
+        v[k] = BF ? __uint_as_float(static_cast<uint32_t>(xb[at]) << 16) : x[at];
+      }
     }
 #pragma unroll
     for (int k = 0; k < NST; ++k) {
@@ -100,6 +106,7 @@ __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams
     const uint32_t wo = reinterpret_cast<const uint32_t*>(a.blob + a.off_woff)[e];
     const uint2 cw = *reinterpret_cast<const uint2*>(a.blob + a.off_codes + 8u * e);
     const float* wts = reinterpret_cast<const float*>(a.blob + a.off_w);
+    const uint16_t* wtb = reinterpret_cast<const uint16_t*>(a.blob + a.off_w);
     const uint32_t last = a.n_wt ? a.n_wt - 1 : 0u;
     uint32_t mk[8];
 #pragma unroll
@@ -113,13 +120,17 @@ __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       const uint32_t kt = ((kept >> t) & 1u) ? mk[t] : 0u;
-      if (t < s) off += __builtin_popcount(kt);
+      // (bf16 kernels are padded to an even element count)
+      if (t < s) off += BF ? (__builtin_popcount(kt) + 1u) & ~1u : __builtin_popcount(kt);
       if (t == s) m = kt;
     }
 #pragma unroll
     for (int t = 0; t < 9; ++t) {
       float v = 0.0f;
-      if ((m >> t) & 1u) v = wts[min(off + __builtin_popcount(m & ((1u << t) - 1u)), last)];
+      if ((m >> t) & 1u) {
+        const uint32_t k = min(off + __builtin_popcount(m & ((1u << t) - 1u)), last);
+        v = BF ? __uint_as_float(static_cast<uint32_t>(wtb[k]) << 16) : wts[k];
+      }
       ws[wk][j][9 * c + t] = v;
     }
     if (c == 0) {
@@ -148,7 +159,9 @@ __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams
   const bool relu = (a.flags & PP_RELU) != 0;
   const int oy = oy0 + ly, ox = ox0 + 4 * lx;
   const bool vec = (a.wo % 4 == 0) && ox + 3 < a.wo;
-  float* y = static_cast<float*>(a.y) + static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  const size_t yoff = static_cast<size_t>(img) * a.c_out * a.ho * a.wo;
+  float* y = static_cast<float*>(a.y) + yoff;
+  uint16_t* yb = static_cast<uint16_t*>(a.y) + yoff;
   // the wave's filters one after the other, each slot's taps read from LDS
   // while the slot before it computes
   constexpr int NW4 = WPS / 4;
@@ -183,13 +196,32 @@ __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams
         acc[q] += b;
         if (relu) acc[q] = fmaxf(acc[q], 0.0f);
       }
-      float* row = y + (static_cast<size_t>(o) * a.ho + oy) * a.wo;
-      if (vec) {
-        *reinterpret_cast<float4*>(row + ox) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-      } else {
+      const size_t ro = (static_cast<size_t>(o) * a.ho + oy) * a.wo;
+      if constexpr (BF) {
+        // round to nearest even (finite values)
+        uint32_t u[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (ox + q < a.wo) row[ox + q] = acc[q];
+        for (int q = 0; q < 4; ++q) {
+          u[q] = __float_as_uint(acc[q]);
+          u[q] = (u[q] + 0x7FFFu + ((u[q] >> 16) & 1u)) >> 16;
+        }
+        uint16_t* row = yb + ro;
+        if (vec) {
+          *reinterpret_cast<uint2*>(row + ox) = make_uint2(u[0] | (u[1] << 16), u[2] | (u[3] << 16));
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (ox + q < a.wo) row[ox + q] = static_cast<uint16_t>(u[q]);
+        }
+      } else {
+        float* row = y + ro;
+        if (vec) {
+          *reinterpret_cast<float4*>(row + ox) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (ox + q < a.wo) row[ox + q] = acc[q];
+        }
       }
     }
     if (s + 1 < kCinSPW) {
@@ -202,12 +234,13 @@ __global__ __launch_bounds__(64 * kCinWPG) void pp_conv3x3_cin_kernel(ConvParams
 }  // namespace kern
 
 bool cin_eligible(const ConvParams& p, bool bf16_act) {
-  return !bf16_act && p.c_in >= 1 && p.c_in <= 4 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.ho == p.h &&
+  (void)bf16_act;
+  return p.c_in >= 1 && p.c_in <= 4 && p.stride == 1 && p.dil == 1 && p.pad == 1 && p.ho == p.h &&
          p.wo == p.w && (p.flags & (PP_MAXPOOL2 | PP_ACCUMULATE | PP_PIXSHUF2 | PP_UPSAMPLE2)) == 0;
 }
 
-hipError_t launch_cin_conv(const ConvParams& p0, hipStream_t st) {
-  if (!cin_eligible(p0, false) || p0.n < 1 || p0.n_groups < 1) return hipErrorInvalidConfiguration;
+hipError_t launch_cin_conv(const ConvParams& p0, bool bf16, hipStream_t st) {
+  if (!cin_eligible(p0, bf16) || p0.n < 1 || p0.n_groups < 1) return hipErrorInvalidConfiguration;
   ConvParams p = p0;
   p.tiles_x = (p.wo + kern::kCinTW - 1) / kern::kCinTW;
   p.tiles_y = (p.ho + kern::kCinTH - 1) / kern::kCinTH;
@@ -215,12 +248,16 @@ hipError_t launch_cin_conv(const ConvParams& p0, hipStream_t st) {
   const long nb = static_cast<long>(p.n) * p.tiles_y * p.tiles_x * gchunks;
   if (nb < 1 || nb > 0x7FFFFFFFL) return hipErrorInvalidConfiguration;
   const dim3 grid(static_cast<uint32_t>(nb)), block(64 * kern::kCinWPG);
+#define PP_CIN(C)                                                                               \
+  if (bf16) hipLaunchKernelGGL((kern::pp_conv3x3_cin_kernel<C, true>), grid, block, 0, st, p);  \
+  else hipLaunchKernelGGL((kern::pp_conv3x3_cin_kernel<C, false>), grid, block, 0, st, p);
   switch (p.c_in) {
-    case 1: hipLaunchKernelGGL(kern::pp_conv3x3_cin_kernel<1>, grid, block, 0, st, p); break;
-    case 2: hipLaunchKernelGGL(kern::pp_conv3x3_cin_kernel<2>, grid, block, 0, st, p); break;
-    case 3: hipLaunchKernelGGL(kern::pp_conv3x3_cin_kernel<3>, grid, block, 0, st, p); break;
-    default: hipLaunchKernelGGL(kern::pp_conv3x3_cin_kernel<4>, grid, block, 0, st, p); break;
+    case 1: PP_CIN(1) break;
+    case 2: PP_CIN(2) break;
+    case 3: PP_CIN(3) break;
+    default: PP_CIN(4) break;
   }
+#undef PP_CIN
   return hipGetLastError();
 }
 

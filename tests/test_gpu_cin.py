@@ -1,5 +1,5 @@
-"""GPU parity of the few-input-channel kernel (recipe 60: fp32, at most four
-input channels, stride 1, pad 1, any pattern library) against the CPU oracle,
+"""GPU parity of the few-input-channel kernel (recipe 60: fp32 or bf16, at most
+four input channels, stride 1, pad 1, any pattern library) against the CPU oracle,
 element by element, every filter: one to four channels, ragged tiles in both
 directions, widths that are not a multiple of 4, c_out not a multiple of 8,
 more slot groups than one workgroup holds, two images, the canonical,
@@ -41,30 +41,39 @@ SHAPES = [(64, 3, 1, 40, 72), (19, 1, 2, 9, 33), (40, 2, 1, 17, 30), (72, 4, 2, 
           (5, 4, 1, 23, 5)]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("libname", sorted(LIBS))
 @pytest.mark.parametrize("si", range(len(SHAPES)))
-def test_cin_kernel(libname, si):
+def test_cin_kernel(libname, si, dtype):
+    from oracle import bf16 as obf16
     c_out, c_in, n, h, w = SHAPES[si]
-    seed = 6000 + 37 * si + len(libname)
+    seed = 6000 + 37 * si + len(libname) + (500 if dtype == "bf16" else 0)
     keep = 1.0 if libname == "dense9" and si % 2 == 0 else 0.6
     L = workloads.random_layer(seed, c_out, c_in, lib=LIBS[libname], keep=keep)
     x = workloads.random_input(seed, (n, c_in, h, w))
-    blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
-    used = pp.conv2d_recipe(blob, n, h, w, pp.PP_F32)
-    _say("cin kernel", libname, "seed", seed, (c_out, c_in, n, h, w), "runs as", used)
+    wd = pp.PP_BF16 if dtype == "bf16" else pp.PP_F32
+    blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, wd)
+    used = pp.conv2d_recipe(blob, n, h, w, wd)
+    _say("cin kernel", libname, dtype, "seed", seed, (c_out, c_in, n, h, w), "runs as", used)
     assert used == CIN
-    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
-    xd = torch.from_numpy(x).cuda()
-    args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+    layer = pp.PackedLayer.from_weights(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, wd)
+    if dtype == "bf16":
+        x = obf16.round_f32(x)
+        args = (x, obf16.round_f32(L["w"]), L["b"], L["pid"], L["conn"], L["lib"])
+        xd = torch.from_numpy(x).cuda().to(torch.bfloat16)
+    else:
+        args = (x, L["w"], L["b"], L["pid"], L["conn"], L["lib"])
+        xd = torch.from_numpy(x).cuda()
     bound = oconv.conv3x3_bound(*args, 1, 1, 1)
     for relu in (True, False):
         y = pp.conv2d_fwd(layer, xd, relu=relu)
         torch.cuda.synchronize()
         ref = oconv.conv3x3_pruned(*args, 1, 1, 1, relu)
-        check(y.cpu().numpy().astype(np.float64), ref, bound, "f32", f"cin {libname} {SHAPES[si]} relu={relu}")
+        check(y.float().cpu().numpy().astype(np.float64), ref, bound, dtype,
+              f"cin {libname} {dtype} {SHAPES[si]} relu={relu}")
 
 
-def test_cin_not_taken_for_strides_or_bf16_or_more_channels():
+def test_cin_not_taken_for_strides_or_more_channels():
     L = workloads.random_layer(6100, 16, 3)
     blob = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_F32)
     assert pp.conv2d_recipe(blob, 1, 32, 32, pp.PP_F32) == CIN
@@ -74,7 +83,7 @@ def test_cin_not_taken_for_strides_or_bf16_or_more_channels():
     b5 = pp.pack(L5["w"], L5["b"], L5["pid"], L5["conn"], L5["lib"], 1, 1, 1, pp.PP_F32)
     assert pp.conv2d_recipe(b5, 1, 32, 32, pp.PP_F32) != CIN
     bb = pp.pack(L["w"], L["b"], L["pid"], L["conn"], L["lib"], 1, 1, 1, pp.PP_BF16)
-    assert pp.conv2d_recipe(bb, 1, 32, 32, pp.PP_BF16) != CIN
+    assert pp.conv2d_recipe(bb, 1, 32, 32, pp.PP_BF16) == CIN   # bf16 too
 
 
 def test_cin_layer_with_fused_pool_runs_elsewhere():
