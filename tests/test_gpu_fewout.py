@@ -62,9 +62,11 @@ SHAPES = [(3, 64, 1, 40, 132), (1, 5, 2, 9, 12), (4, 17, 1, 33, 68), (6, 70, 1, 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("si", range(len(SHAPES)))
 def test_fewout_dense9(si, dtype, monkeypatch):
-    if dtype == "f32":
-        monkeypatch.setenv("PP_RECIPE", str(FEW))
     c_out, c_in, n, h, w = SHAPES[si]
+    # (fp32, and layers of at most 4 input channels, which the planner gives
+    # the few-input-channel kernel: forced)
+    if dtype == "f32" or c_in <= 4:
+        monkeypatch.setenv("PP_RECIPE", str(FEW))
     seed = 7000 + 31 * si + (dtype == "bf16")
     keep = 1.0 if si % 2 == 0 else 0.7
     L = workloads.random_layer(seed, c_out, c_in, lib=workloads.DENSE9, keep=keep)
@@ -116,6 +118,9 @@ def test_fewout_not_taken():
     Lc = workloads.random_layer(7202, 3, 16, keep=0.5)
     bc = pp.pack(Lc["w"], Lc["b"], Lc["pid"], Lc["conn"], Lc["lib"], 1, 1, 1, B)
     assert pp.conv2d_recipe(bc, 1, 32, 32, B) != FEW                    # pruned canonical library
+    L3 = workloads.random_layer(7203, 3, 3, lib=workloads.DENSE9, keep=1.0)
+    b3 = pp.pack(L3["w"], L3["b"], L3["pid"], L3["conn"], L3["lib"], 1, 1, 1, B)
+    assert pp.conv2d_recipe(b3, 1, 32, 32, B) == 60                     # 3 input channels: that kernel first
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
