@@ -485,3 +485,26 @@ def test_lean_stride2(recipe, ksplit, monkeypatch):
             assert torch.equal(y, yp), f"stride 2 {recipe}/{ksplit} pool={pool}: prepared weights differ"
             r, b = (oconv.maxpool2(ref), oconv.maxpool2(bound)) if pool else (ref, bound)
             check(y.cpu().numpy().astype(np.float64), r, b, "f32", f"lean s2 {recipe}/{ksplit} pool={pool}")
+
+
+# the colourization network's dilated and strided layers at full size and
+# full width (8 images, every output channel): the dilation-2 and stride-2
+# lean paths as the network runs them, with prepared weights
+@pytest.mark.parametrize("opi,hw", [(10, 32), (6, 64), (3, 128), (1, 256)])
+def test_colourization_dilated_and_strided_layers_full_width(opi, hw):
+    spec = workloads.net_spec(5)
+    params = workloads.net_params(5)
+    op, prm = spec["ops"][opi], params[opi]
+    layer = pp.PackedLayer.from_weights(prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"], op["stride"],
+                                        op["pad"], op["dil"], pp.PP_F32)
+    assert layer.prepare() is not None
+    x = workloads.random_input(5000 + opi, (8, op["c_in"], hw, hw), 0.0, 1.0)
+    plan = pp.conv2d_plan(layer.h_blob, 8, hw, hw, pp.PP_F32)
+    _say("colourization layer", opi, op["c_in"], "->", op["c_out"], f"{hw}x{hw}", "stride", op["stride"], "dil",
+         op["dil"], "plan", plan, "all filters")
+    assert plan[0] in range(40, 60)
+    y = pp.conv2d_fwd(layer, torch.from_numpy(x).cuda(), relu=op["relu"], prepared=True)
+    torch.cuda.synchronize()
+    args = (x, prm["w"], prm["b"], prm["pid"], prm["conn"], prm["lib"], op["stride"], op["pad"], op["dil"])
+    check(y.cpu().numpy().astype(np.float64), oconv.conv3x3_pruned(*args, op["relu"]), oconv.conv3x3_bound(*args),
+          "f32", f"colourization layer {opi} full width")
