@@ -11,6 +11,7 @@
 // glue ops are one elementwise kernel.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "dense.hpp"
@@ -385,8 +386,14 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
 // the store rounds once to bf16.  The gathers are those of the fp32 kernel.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-template <int MODE, int KD, int WM, int TM, int TN>
+// AP (transposed conv): the weights come laid out per parity class,
+// [class][filter][k] (deconv_relayout_kernel), so a thread loads 8
+// consecutive k of a filter as one 16-byte piece; read as given (IOHW),
+// consecutive k of a filter are 8 KB apart for 512 filters and a 64-lane load
+// touches 16 cache lines for 128 useful bytes.
+template <int MODE, int KD, int WM, int TM, int TN, bool AP = false>
 __global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int n_tiles, int m_tiles) {
+  static_assert(!AP || MODE == 1, "laid-out weights: transposed conv only");
   constexpr int WN = 4 / WM, BM = 32 * TM * WM, BN = 32 * TN * WN;
   constexpr int JA = kMK * BM / 256, JB = kMK * BN / 256;   // A / B elements per thread per step
   constexpr int AR = 256 / kMK;                             // A rows per load pass
@@ -437,7 +444,7 @@ __global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int
     return bload_b(r, el == kOut ? kOut : el * 2u);
   };
   uint32_t ra[JA], rb[JB];
-  auto fetch_any = [&](int k0) __attribute__((always_inline)) {
+  auto fetch_any_a = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < JA; ++j) {
       const int kk = k0 + ak, ao = mt * BM + am0 + AR * j;
@@ -453,6 +460,8 @@ __global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int
       }
       ra[j] = bload(wr, el);
     }
+  };
+  auto fetch_any_b = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
       const int kk = k0 + bk0 + j;
@@ -504,10 +513,32 @@ __global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int
       boff[j] = el == kOut ? kOut : el * 2u;
     }
   }
+  // AP: pieces (row ar + (256 / APR) j, k 8 aq .. 8 aq + 7) of the step; K is
+  // a multiple of 8 (c_in even), so a piece is wholly inside or past K
+  constexpr int APR = kMK / 8, JP = (BM * APR + 255) / 256;   // (a 32-row tile: half the threads)
+  const int par = tid / APR, paq = tid % APR;
+  uint32_t poff[AP ? JP : 1];
+  uint4 pa[AP ? JP : 1];
+  const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(p.scratch), static_cast<short>(0),
+      AP ? static_cast<int>(static_cast<size_t>(16) * p.c_in * p.c_out * 2) : 0, 0x00020000);
+  if constexpr (AP) {
+#pragma unroll
+    for (int j = 0; j < JP; ++j) {
+      const int lr = par + (256 / APR) * j, ao = mt * BM + lr;
+      poff[j] = lr < BM && ao < p.c_out ? ((static_cast<uint32_t>(cls) * p.c_out + ao) * K + 8 * paq) * 2u : kOut;
+    }
+  }
   const size_t a_step = MODE == 0 ? kMK : static_cast<size_t>(kMK / 4) * p.c_out * 16;
   const size_t b_step = static_cast<size_t>(MODE == 0 ? kMK : kMK / 4) * p.h * p.w;
   auto fetch = [&](int s) __attribute__((always_inline)) {
     const int k0 = s * kMK;
+    if constexpr (AP) {
+#pragma unroll
+      for (int j = 0; j < JP; ++j)
+        pa[j] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              pr, poff[j] == kOut || k0 + 8 * paq >= K ? kOut : poff[j] + 2u * k0, 0, 0));
+    }
     if constexpr (STEPPED) {
       if (k0 + kMK <= K) {
         const size_t ao0 = s * a_step, bo0 = s * b_step;
@@ -517,18 +548,27 @@ __global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int
         const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<uint16_t*>(x + bo0), static_cast<short>(0), static_cast<int>((x_elems - min(x_elems, bo0)) * 2),
             0x00020000);
+        if constexpr (!AP) {
 #pragma unroll
-        for (int j = 0; j < JA; ++j) ra[j] = bload_b(wrs, aoff[j]);
+          for (int j = 0; j < JA; ++j) ra[j] = bload_b(wrs, aoff[j]);
+        }
 #pragma unroll
         for (int j = 0; j < JB; ++j) rb[j] = bload_b(xrs, boff[j]);
         return;
       }
     }
-    fetch_any(k0);
+    if constexpr (!AP) fetch_any_a(k0);
+    fetch_any_b(k0);
   };
   auto put = [&](int buf) __attribute__((always_inline)) {
+    if constexpr (AP) {
 #pragma unroll
-    for (int j = 0; j < JA; ++j) As[buf][am0 + AR * j][ak] = static_cast<uint16_t>(ra[j]);
+      for (int j = 0; j < JP; ++j)
+        if (par + (256 / APR) * j < BM) *reinterpret_cast<uint4*>(&As[buf][par + (256 / APR) * j][8 * paq]) = pa[j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < JA; ++j) As[buf][am0 + AR * j][ak] = static_cast<uint16_t>(ra[j]);
+    }
 #pragma unroll
     for (int q = 0; q < JB / 8; ++q)
       *reinterpret_cast<uint4*>(&Bs[buf][bn][bk0 + 8 * q]) =
@@ -594,7 +634,24 @@ __global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int
   }
 }
 
-template <int MODE, int KD, class TA>
+// The transposed conv's weights w[c][o][ky][kx] laid out for the GEMM of
+// parity class (py, px): row (class, o) holds k = 4 c + 2 a + b, the tap
+// (ky, kx) = (1 - py + 2 a, 1 - px + 2 b) -- the k order the kernel contracts
+// in, so the sums are the same as when it reads w directly.
+__global__ __launch_bounds__(256) void deconv_relayout_kernel(const uint16_t* __restrict__ w,
+                                                              uint16_t* __restrict__ out, int c_in, int c_out) {
+  const size_t n = static_cast<size_t>(16) * c_in * c_out;
+  const int K = 4 * c_in;
+  for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += static_cast<size_t>(gridDim.x) * 256) {
+    const int k = static_cast<int>(i % K);
+    const size_t r = i / K;
+    const int o = static_cast<int>(r % c_out), cls = static_cast<int>(r / c_out);
+    const int c = k >> 2, ky = 1 - (cls >> 1) + 2 * ((k >> 1) & 1), kx = 1 - (cls & 1) + 2 * (k & 1);
+    out[i] = w[((static_cast<size_t>(c) * c_out + o) * 4 + ky) * 4 + kx];
+  }
+}
+
+template <int MODE, int KD, class TA, bool AP = false>
 hipError_t launch_mfma(const DenseParams& p, hipStream_t st) {
   const int gh = MODE == 0 ? p.ho : p.h, gw = MODE == 0 ? p.wo : p.w;
   const long np = static_cast<long>(p.n) * gh * gw;
@@ -620,11 +677,11 @@ hipError_t launch_mfma(const DenseParams& p, hipStream_t st) {
   const int nt = static_cast<int>(n_tiles), mt = static_cast<int>(m_tiles);
   if constexpr (sizeof(TA) == 2) {
     if (shape == 0)
-      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 1, 1, 1>), grid, dim3(256), 0, st, p, nt, mt);
+      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 1, 1, 1, AP>), grid, dim3(256), 0, st, p, nt, mt);
     else if (shape == 2)
-      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 2, 2, 2>), grid, dim3(256), 0, st, p, nt, mt);
+      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 2, 2, 2, AP>), grid, dim3(256), 0, st, p, nt, mt);
     else
-      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 2, 1, 1>), grid, dim3(256), 0, st, p, nt, mt);
+      hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 2, 1, 1, AP>), grid, dim3(256), 0, st, p, nt, mt);
   } else {
     if (shape == 0)
       hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 1, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
@@ -952,9 +1009,27 @@ hipError_t launch_dense_conv(const DenseParams& p, bool bf16, hipStream_t st) {
   }
 }
 
+size_t deconv_scratch_bytes(int c_in, int c_out, bool bf16) {
+  return bf16 && c_in % 2 == 0 ? static_cast<size_t>(16) * c_in * c_out * sizeof(uint16_t) : 0;
+}
+
 hipError_t launch_deconv(const DenseParams& p, bool bf16, hipStream_t st) {
   if (p.k != 4 || p.stride != 2 || p.pad != 1 || p.ho != 2 * p.h || p.wo != 2 * p.w) return hipErrorInvalidValue;
-  return bf16 ? launch_mfma<1, 2, uint16_t>(p, st) : launch_mfma<1, 2, float>(p, st);
+  if (!bf16) return launch_mfma<1, 2, float>(p, st);
+  // bf16 with scratch (c_in even: whole 16-byte pieces of k): the weights
+  // laid out per parity class first (timed on the colourization 512 -> 256
+  // layer: the direct reads of the IOHW weights bound it)
+  const size_t nb = deconv_scratch_bytes(p.c_in, p.c_out, true);
+  if (p.scratch && nb && reinterpret_cast<uintptr_t>(p.scratch) % 16 == 0 && nb < (size_t{1} << 31)) {
+    const size_t n = nb / 2;
+    const uint32_t blocks = static_cast<uint32_t>(std::min<size_t>((n + 255) / 256, 4096));
+    hipLaunchKernelGGL(deconv_relayout_kernel, dim3(blocks), dim3(256), 0, st, static_cast<const uint16_t*>(p.wt),
+                       static_cast<uint16_t*>(p.scratch), p.c_in, p.c_out);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_mfma<1, 2, uint16_t, true>(p, st);
+  }
+  return launch_mfma<1, 2, uint16_t>(p, st);
 }
 
 hipError_t launch_glue(const GlueParams& p, bool bf16, hipStream_t st) {

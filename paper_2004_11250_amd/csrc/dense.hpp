@@ -15,6 +15,9 @@ struct DenseParams {
   int n = 0, c_in = 0, h = 0, w = 0, c_out = 0, ho = 0, wo = 0;
   int k = 0, stride = 1, pad = 0;
   int relu = 0;
+  // bf16 transposed conv: device scratch of deconv_scratch_bytes() for the
+  // weights laid out per parity class (or NULL: read them as given)
+  void* scratch = nullptr;
 };
 
 enum { kGlueMaxPool2 = 0, kGlueUp2 = 1, kGluePixShuf2 = 2, kGlueAdd = 3 };
@@ -29,6 +32,7 @@ struct GlueParams {
 
 hipError_t launch_dense_conv(const DenseParams& p, bool bf16, hipStream_t st);
 hipError_t launch_deconv(const DenseParams& p, bool bf16, hipStream_t st);
+size_t deconv_scratch_bytes(int c_in, int c_out, bool bf16);
 hipError_t launch_glue(const GlueParams& p, bool bf16, hipStream_t st);
 
 }  // namespace pp

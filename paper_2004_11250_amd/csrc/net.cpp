@@ -113,6 +113,11 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
         if (op.c_in != s.c || op.c_out < 1) return bad(i, "channel mismatch");
         if (device && !op.d_w) return bad(i, "d_w is NULL");
         o = Shape{op.c_out, 2 * s.h, 2 * s.w, true};
+        {
+          // (bf16: the weights laid out per parity class, in the scratch)
+          const size_t db = deconv_scratch_bytes(op.c_in, op.c_out, act == PP_BF16);
+          if (db > part_max) part_max = db;
+        }
         break;
       }
       case PP_OP_MAXPOOL2:
@@ -378,6 +383,7 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
         p.stride = op.stride;
         p.pad = op.pad;
         p.relu = (op.flags & PP_RELU) ? 1 : 0;
+        if (op.kind == PP_OP_DECONV && pl.scratch_bytes >= deconv_scratch_bytes(si.c, so.c, bf)) p.scratch = scratch;
         e = op.kind == PP_OP_CONV_DENSE ? launch_dense_conv(p, bf, stream) : launch_deconv(p, bf, stream);
         break;
       }
