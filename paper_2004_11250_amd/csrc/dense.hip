@@ -150,8 +150,11 @@ __global__ __launch_bounds__(256) void dense_conv_vec_kernel(DenseParams p) {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kMK = 32;
 
-template <int MODE, int KD, int WM, int TM, int TN, class TA>
+// AP (fp32 transposed conv): the weights laid out per parity class as in the
+// bf16 kernel, read as 16-byte pieces of 4 consecutive k.
+template <int MODE, int KD, int WM, int TM, int TN, class TA, bool AP = false>
 __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_tiles, int m_tiles) {
+  static_assert(!AP || (MODE == 1 && sizeof(TA) == 4), "laid-out weights: fp32 transposed conv only");
   constexpr int WN = 4 / WM, BM = 32 * TM * WM, BN = 32 * TN * WN;
   constexpr int JA = kMK * BM / 256, JB = kMK * BN / 256;   // A / B elements per thread per step
   constexpr int AR = 256 / kMK;                             // A rows per load pass
@@ -213,7 +216,7 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
   };
   float ra[JA], rb[JB];
   // the general gather: every element's offset from (k, filter / pixel)
-  auto fetch_any = [&](int k0) __attribute__((always_inline)) {
+  auto fetch_any_a = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < JA; ++j) {
       const int kk = k0 + ak, ao = mt * BM + am0 + AR * j;
@@ -229,6 +232,8 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
       }
       ra[j] = bload(wr, el);
     }
+  };
+  auto fetch_any_b = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < JB; ++j) {
       const int kk = k0 + bk0 + j;
@@ -287,10 +292,32 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
       boff[j] = el == kOut ? kOut : el * kES;
     }
   }
+  // AP: pieces (row par + 32 j, k 4 paq .. 4 paq + 3) of the step (K = 4
+  // c_in: a piece is wholly inside or past K)
+  constexpr int APR = kMK / 4, JP = (BM * APR + 255) / 256;
+  const int par = tid / APR, paq = tid % APR;
+  uint32_t poff[AP ? JP : 1];
+  float4 pa[AP ? JP : 1];
+  const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(p.scratch), static_cast<short>(0),
+      AP ? static_cast<int>(static_cast<size_t>(16) * p.c_in * p.c_out * 4) : 0, 0x00020000);
+  if constexpr (AP) {
+#pragma unroll
+    for (int j = 0; j < JP; ++j) {
+      const int lr = par + (256 / APR) * j, ao = mt * BM + lr;
+      poff[j] = lr < BM && ao < p.c_out ? ((static_cast<uint32_t>(cls) * p.c_out + ao) * K + 4 * paq) * 4u : kOut;
+    }
+  }
   const size_t a_step = MODE == 0 ? kMK : static_cast<size_t>(kMK / 4) * p.c_out * 16;      // elements per K step
   const size_t b_step = static_cast<size_t>(MODE == 0 ? kMK : kMK / 4) * p.h * p.w;
   auto fetch = [&](int s) __attribute__((always_inline)) {
     const int k0 = s * kMK;
+    if constexpr (AP) {
+#pragma unroll
+      for (int j = 0; j < JP; ++j)
+        pa[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                               pr, poff[j] == kOut || k0 + 4 * paq >= K ? kOut : poff[j] + 4u * k0, 0, 0));
+    }
     if constexpr (STEPPED) {
       if (k0 + kMK <= K) {
         const size_t ao0 = s * a_step, bo0 = s * b_step;
@@ -299,18 +326,34 @@ __global__ __launch_bounds__(256) void dense_mfma_kernel(DenseParams p, int n_ti
         const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<TA*>(x + bo0), static_cast<short>(0), static_cast<int>((x_elems - min(x_elems, bo0)) * kES),
             0x00020000);
+        if constexpr (!AP) {
 #pragma unroll
-        for (int j = 0; j < JA; ++j) ra[j] = bload_b(wrs, aoff[j]);
+          for (int j = 0; j < JA; ++j) ra[j] = bload_b(wrs, aoff[j]);
+        }
 #pragma unroll
         for (int j = 0; j < JB; ++j) rb[j] = bload_b(xrs, boff[j]);
         return;
       }
     }
-    fetch_any(k0);
+    if constexpr (!AP) fetch_any_a(k0);
+    fetch_any_b(k0);
   };
   auto put = [&](int buf) __attribute__((always_inline)) {
+    if constexpr (AP) {
 #pragma unroll
-    for (int j = 0; j < JA; ++j) As[buf][ak][am0 + AR * j] = ra[j];
+      for (int j = 0; j < JP; ++j) {
+        const int lr = par + (256 / APR) * j;
+        if (lr < BM) {
+          As[buf][4 * paq][lr] = pa[j].x;
+          As[buf][4 * paq + 1][lr] = pa[j].y;
+          As[buf][4 * paq + 2][lr] = pa[j].z;
+          As[buf][4 * paq + 3][lr] = pa[j].w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < JA; ++j) As[buf][ak][am0 + AR * j] = ra[j];
+    }
 #pragma unroll
     for (int j = 0; j < JB; ++j) Bs[buf][bk0 + j][bn] = rb[j];
   };
@@ -638,8 +681,9 @@ __global__ __launch_bounds__(256) void dense_mfma_bf16_kernel(DenseParams p, int
 // parity class (py, px): row (class, o) holds k = 4 c + 2 a + b, the tap
 // (ky, kx) = (1 - py + 2 a, 1 - px + 2 b) -- the k order the kernel contracts
 // in, so the sums are the same as when it reads w directly.
-__global__ __launch_bounds__(256) void deconv_relayout_kernel(const uint16_t* __restrict__ w,
-                                                              uint16_t* __restrict__ out, int c_in, int c_out) {
+template <class T>
+__global__ __launch_bounds__(256) void deconv_relayout_kernel(const T* __restrict__ w, T* __restrict__ out, int c_in,
+                                                              int c_out) {
   const size_t n = static_cast<size_t>(16) * c_in * c_out;
   const int K = 4 * c_in;
   for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += static_cast<size_t>(gridDim.x) * 256) {
@@ -684,11 +728,11 @@ hipError_t launch_mfma(const DenseParams& p, hipStream_t st) {
       hipLaunchKernelGGL((dense_mfma_bf16_kernel<MODE, KD, 2, 1, 1, AP>), grid, dim3(256), 0, st, p, nt, mt);
   } else {
     if (shape == 0)
-      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 1, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
+      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 1, 1, 1, TA, AP>), grid, dim3(256), 0, st, p, nt, mt);
     else if (shape == 2)
-      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 2, 2, TA>), grid, dim3(256), 0, st, p, nt, mt);
+      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 2, 2, TA, AP>), grid, dim3(256), 0, st, p, nt, mt);
     else
-      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 1, 1, TA>), grid, dim3(256), 0, st, p, nt, mt);
+      hipLaunchKernelGGL((dense_mfma_kernel<MODE, KD, 2, 1, 1, TA, AP>), grid, dim3(256), 0, st, p, nt, mt);
   }
   return hipGetLastError();
 }
@@ -1010,26 +1054,32 @@ hipError_t launch_dense_conv(const DenseParams& p, bool bf16, hipStream_t st) {
 }
 
 size_t deconv_scratch_bytes(int c_in, int c_out, bool bf16) {
-  return bf16 && c_in % 2 == 0 ? static_cast<size_t>(16) * c_in * c_out * sizeof(uint16_t) : 0;
+  // (bf16: c_in even, so that k comes in whole 16-byte pieces of 8)
+  if (bf16) return c_in % 2 == 0 ? static_cast<size_t>(16) * c_in * c_out * sizeof(uint16_t) : 0;
+  return static_cast<size_t>(16) * c_in * c_out * sizeof(float);
+}
+
+// With scratch: the weights laid out per parity class first (timed on the
+// colourization 512 -> 256 layer: the direct reads of the IOHW weights bound
+// the bf16 form), then the GEMM reads them as 16-byte pieces.
+template <class T>
+hipError_t launch_deconv_t(const DenseParams& p, hipStream_t st) {
+  const size_t nb = deconv_scratch_bytes(p.c_in, p.c_out, sizeof(T) == 2);
+  if (p.scratch && nb && reinterpret_cast<uintptr_t>(p.scratch) % 16 == 0 && nb < (size_t{1} << 31)) {
+    const size_t n = nb / sizeof(T);
+    const uint32_t blocks = static_cast<uint32_t>(std::min<size_t>((n + 255) / 256, 4096));
+    hipLaunchKernelGGL(deconv_relayout_kernel<T>, dim3(blocks), dim3(256), 0, st, static_cast<const T*>(p.wt),
+                       static_cast<T*>(p.scratch), p.c_in, p.c_out);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_mfma<1, 2, T, true>(p, st);
+  }
+  return launch_mfma<1, 2, T>(p, st);
 }
 
 hipError_t launch_deconv(const DenseParams& p, bool bf16, hipStream_t st) {
   if (p.k != 4 || p.stride != 2 || p.pad != 1 || p.ho != 2 * p.h || p.wo != 2 * p.w) return hipErrorInvalidValue;
-  if (!bf16) return launch_mfma<1, 2, float>(p, st);
-  // bf16 with scratch (c_in even: whole 16-byte pieces of k): the weights
-  // laid out per parity class first (timed on the colourization 512 -> 256
-  // layer: the direct reads of the IOHW weights bound it)
-  const size_t nb = deconv_scratch_bytes(p.c_in, p.c_out, true);
-  if (p.scratch && nb && reinterpret_cast<uintptr_t>(p.scratch) % 16 == 0 && nb < (size_t{1} << 31)) {
-    const size_t n = nb / 2;
-    const uint32_t blocks = static_cast<uint32_t>(std::min<size_t>((n + 255) / 256, 4096));
-    hipLaunchKernelGGL(deconv_relayout_kernel, dim3(blocks), dim3(256), 0, st, static_cast<const uint16_t*>(p.wt),
-                       static_cast<uint16_t*>(p.scratch), p.c_in, p.c_out);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_mfma<1, 2, uint16_t, true>(p, st);
-  }
-  return launch_mfma<1, 2, uint16_t>(p, st);
+  return bf16 ? launch_deconv_t<uint16_t>(p, st) : launch_deconv_t<float>(p, st);
 }
 
 hipError_t launch_glue(const GlueParams& p, bool bf16, hipStream_t st) {

@@ -15,7 +15,7 @@ struct DenseParams {
   int n = 0, c_in = 0, h = 0, w = 0, c_out = 0, ho = 0, wo = 0;
   int k = 0, stride = 1, pad = 0;
   int relu = 0;
-  // bf16 transposed conv: device scratch of deconv_scratch_bytes() for the
+  // transposed conv: device scratch of deconv_scratch_bytes() for the
   // weights laid out per parity class (or NULL: read them as given)
   void* scratch = nullptr;
 };

@@ -114,7 +114,7 @@ pp_status make_plan(const pp_net_op* ops, int n_ops, int n, int c, int h, int w,
         if (device && !op.d_w) return bad(i, "d_w is NULL");
         o = Shape{op.c_out, 2 * s.h, 2 * s.w, true};
         {
-          // (bf16: the weights laid out per parity class, in the scratch)
+          // (the weights laid out per parity class, in the scratch)
           const size_t db = deconv_scratch_bytes(op.c_in, op.c_out, act == PP_BF16);
           if (db > part_max) part_max = db;
         }
