@@ -400,7 +400,11 @@ pp_status pp_net_workspace(const pp_net_op* ops, int32_t n_ops, int32_t n, int32
  * shuffle, or an add whose other operand is dead afterwards too -- runs
  * fused with that op in one launch (pp_conv2d_fwd's PP_MAXPOOL2,
  * PP_PIXSHUF2, PP_ACCUMULATE); the result is the same.  The workspace is
- * only valid for the op list and shape it was sized for.
+ * only valid for the op list and shape it was sized for.  With the
+ * environment variable PP_TRACE set (and not "0") when the library first
+ * runs a net, each op's (or fused pair's) launches sit in a named roctx
+ * range, "pp op <index> <kind>", for rocprofv3 --marker-trace; the roctx
+ * library is loaded at run time, and without it there are no ranges.
  * Errors: as pp_net_workspace, PP_ESIZE (ws_bytes too small),
  * PP_EUNSUPPORTED, PP_EHIP.
  */

@@ -15,7 +15,11 @@
 //     accumulates into src's buffer in place, which becomes dst's;
 //   - a conv that reads an upsample's input slot and writes that slot
 //     writes the upsample's unused output buffer instead.
+#include <dlfcn.h>
 #include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
 
 #include <string>
 #include <vector>
@@ -313,6 +317,43 @@ extern "C" pp_status pp_net_plan(const pp_net_op* ops, int32_t n_ops, int32_t n,
   return PP_OK;
 }
 
+// PP_TRACE (environment, read once per process; set and not "0"): the
+// launches of each op, or fused pair, inside a named roctx range ("pp op <i>
+// <kind>"), for rocprofv3 --marker-trace.  The roctx library is loaded at run
+// time (none is linked in); when it is not found there are no ranges.
+namespace {
+struct Tracer {
+  int (*push)(const char*) = nullptr;
+  int (*pop)() = nullptr;
+  Tracer() {
+    const char* e = std::getenv("PP_TRACE");
+    if (!e || !*e || (e[0] == '0' && !e[1])) return;
+    void* h = dlopen("librocprofiler-sdk-roctx.so.1", RTLD_NOW | RTLD_LOCAL);
+    if (!h) h = dlopen("libroctx64.so.4", RTLD_NOW | RTLD_LOCAL);
+    if (!h) return;
+    push = reinterpret_cast<int (*)(const char*)>(dlsym(h, "roctxRangePushA"));
+    pop = reinterpret_cast<int (*)()>(dlsym(h, "roctxRangePop"));
+    if (!push || !pop) push = nullptr, pop = nullptr;
+  }
+};
+const Tracer& tracer() {
+  static const Tracer t;
+  return t;
+}
+const char* op_kind_name(int kind) {
+  switch (kind) {
+    case PP_OP_CONV_PP: return "conv3 (pruned)";
+    case PP_OP_CONV_DENSE: return "conv (dense)";
+    case PP_OP_DECONV: return "deconv";
+    case PP_OP_MAXPOOL2: return "maxpool2";
+    case PP_OP_UPSAMPLE2: return "upsample2";
+    case PP_OP_PIXSHUF2: return "pixshuf2";
+    case PP_OP_ADD: return "add";
+    default: return "op";
+  }
+}
+}  // namespace
+
 extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void* x, void* y, int32_t n, int32_t c,
                                 int32_t h, int32_t w, int32_t act_dtype, void* workspace, size_t ws_bytes,
                                 void* hip_stream) {
@@ -340,6 +381,13 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
     void* dst = buf_ptr(pl.b_dst[i]);
     const void* src = buf_ptr(pl.b_src[i]);
     hipError_t e = hipSuccess;
+    const Tracer& tr = tracer();
+    if (tr.push) {
+      char name[96];
+      std::snprintf(name, sizeof(name), "pp op %d %s%s%s%s", i, pl.up_in[i] ? "upsample2 + " : "", op_kind_name(op.kind),
+                    pl.fuse[i] ? " + " : "", pl.fuse[i] && i + 1 < n_ops ? op_kind_name(ops[i + 1].kind) : "");
+      tr.push(name);
+    }
     switch (op.kind) {
       case PP_OP_CONV_PP: {
         // with the upsample before it (PP_UPSAMPLE2) and / or the pool, add or
@@ -361,7 +409,10 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
           st = conv_enqueue(pl.views[i], op.d_blob, src, dst, n, si.h, si.w, act_dtype, fl, scratch, pl.scratch_bytes,
                             stream);
         }
-        if (st != PP_OK) return st;
+        if (st != PP_OK) {
+          if (tr.push) tr.pop();
+          return st;
+        }
         if (pl.fuse[i]) ++i;
         break;
       }
@@ -406,6 +457,7 @@ extern "C" pp_status pp_net_fwd(const pp_net_op* ops, int32_t n_ops, const void*
         break;
       }
     }
+    if (tr.push) tr.pop();
     if (e != hipSuccess) return fail(PP_EHIP, "op " + std::to_string(i) + ": " + hipGetErrorString(e));
   }
   return PP_OK;

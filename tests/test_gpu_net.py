@@ -266,3 +266,27 @@ def test_prepared_net_equals_per_call_expansion(cfg):
     ya = _np(a.forward(x))
     for _ in range(2):
         assert np.array_equal(_np(b.forward(x)), ya)
+
+
+def test_trace_ranges_change_nothing(tmp_path):
+    # PP_TRACE (read once per process): the same VGG-16 frame, bitwise, in a
+    # child process that traces every op
+    import os
+    import subprocess
+    import sys
+    spec = workloads.net_spec(2)
+    params = workloads.net_params(2)
+    net = pp.Net(spec["ops"], params, "f32")
+    _, x = _input(2, "f32")
+    want = _np(net.forward(x))
+    out = tmp_path / "traced.npy"
+    code = ("import numpy as np, torch, workloads, paper_2004_11250_amd as pp\n"
+            "spec = workloads.net_spec(2); params = workloads.net_params(2)\n"
+            "net = pp.Net(spec['ops'], params, 'f32')\n"
+            "x = torch.from_numpy(workloads.net_input(2)).cuda()\n"
+            f"np.save({str(out)!r}, net.forward(x).cpu().numpy())\n")
+    env = dict(os.environ, PP_TRACE="1")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    _say("traced VGG-16 frame in a child process")
+    subprocess.run([sys.executable, "-c", code], env=env, cwd=root, check=True, timeout=300)
+    assert np.array_equal(np.load(out), want)
