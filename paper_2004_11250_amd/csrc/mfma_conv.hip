@@ -273,6 +273,27 @@ __global__ __launch_bounds__(256 * G) void pp_mfma_conv_kernel(ConvParams a, con
     const int ey = static_cast<int>(q % a.ho);
     const long eimg = q / a.ho;
     uint16_t* __restrict__ y = static_cast<uint16_t*>(a.y) + static_cast<size_t>(eimg) * a.c_out * a.ho * a.wo;
+    if (shuf && !accum) {
+      // PixelShuffle(2): filters o, o + 1 (o even; accumulators r, r + 1)
+      // land in adjacent columns 2 ex, 2 ex + 1 of one output row: one
+      // aligned 4-byte store per pair (c_out is a multiple of 4)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          const int o = mt * BM + (wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (o < a.c_out) {
+            float v0 = acc[i][j][r] + bias[o], v1 = acc[i][j][r + 1] + bias[o + 1];
+            if (relu) {
+              v0 = fmaxf(v0, 0.0f);
+              v1 = fmaxf(v1, 0.0f);
+            }
+            const size_t at = (static_cast<size_t>(o >> 2) * 2 * a.ho + 2 * ey + ((o >> 1) & 1)) * 2 * a.wo + 2 * ex;
+            *reinterpret_cast<uint32_t*>(y + at) = rne_bf16(v0) | (rne_bf16(v1) << 16);
+          }
+        }
+      continue;
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
