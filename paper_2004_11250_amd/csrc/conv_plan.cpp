@@ -281,7 +281,7 @@ ConvPlan plan_conv(const ConvParams& p, int lib, bool bf16, bool allow_split, bo
     } else if (pix >= 80L * 80L) {
       lp[0] = 46; lp[1] = 55;
     } else if (pix >= 40L * 40L) {
-      lp[0] = 58; lp[1] = 59; lp[2] = 46; lp[3] = 55;   // (the last two: bf16)
+      lp[0] = 58; lp[1] = 59;
     } else if (pix >= 20L * 20L) {
       lp[0] = 48; lp[1] = 51;
     } else {

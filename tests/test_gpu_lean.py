@@ -219,8 +219,8 @@ def test_lean_fused_upsample(mode, recipe, ksplit, monkeypatch):
 # ---- bf16 activations (the tilings built for bf16: 16-byte staging needs a
 # width that is a multiple of 8, 4-byte staging an even width).  Inputs and
 # weights are rounded to bf16 for the oracle too; the output is rounded once.
-LEAN_BF = [40, 56, 46, 55, 48, 51, 54]
-V4_BF = {40, 46, 48}
+LEAN_BF = [40, 56, 46, 55, 58, 59, 48, 51, 54]
+V4_BF = {40, 46, 58, 48}
 
 
 def _run_bf16(L, x, relu=True, maxpool2=False):
