@@ -289,17 +289,24 @@ def other_workloads(dev, no_dense, steps=10, warmup=3):
             ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
             y = torch.empty(oshape, dtype=tdt, device=dev)
 
-            def timed(fn):
+            def timed(fn, min_ms=50.0):
+                # at least `steps` frames and about min_ms of them, so that
+                # short frames are not timed over a handful of calls
                 for _ in range(warmup):
                     fn()
                 torch.cuda.synchronize()
                 a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a0.record(stream)
-                for _ in range(steps):
+                fn()
+                a1.record(stream)
+                torch.cuda.synchronize()
+                k = max(steps, min(1000, int(min_ms / max(a0.elapsed_time(a1), 1e-3)) + 1))
+                a0.record(stream)
+                for _ in range(k):
                     fn()
                 a1.record(stream)
                 torch.cuda.synchronize()
-                return a0.elapsed_time(a1) / steps
+                return a0.elapsed_time(a1) / k
 
             ms = timed(lambda: net.forward(x, y, ws))
             macs = sum(surviving_macs(op, prm, o, spec["batch"]) for (i, op, _, o), prm in zip(shapes, params))
